@@ -1,0 +1,246 @@
+/*
+ * xmix.h - C ABI of the per-layer, multi-tenant MI hook step on one MI355X
+ * (gfx950), after xMIx (arXiv 2607.22595).
+ *
+ * The paper's contract for an MI function (Sec. 4.2, "Executable units"):
+ * it consumes the activation slice at a hook plus the runtime parameters of
+ * one app, and yields a derived signal, an update of the activation, or
+ * both.  Read results go to buffers that later GPU work or the CPU consume
+ * (Sec. 4.2, "State and dataflow").  Apps are deployed once and toggled per
+ * request, and a request that does not use an app must not pay for it
+ * (Sec. 4.2, "Toggling semantics"; Sec. 4.3, "Graph-level toggling and
+ * continuous batching").  Graph replay needs a fixed structure whose
+ * arguments can change between launches (Sec. 4.3, "CUDA-graph-safe kernel
+ * design").
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - All data pointers are DEVICE pointers unless the comment says "host".
+ *   The caller allocates and owns every buffer; the library keeps no
+ *   per-call state and allocates nothing.
+ * - bf16 values travel as their raw 16-bit patterns (uint16_t).
+ * - Activations are row-major [T_max, d]: one row per token slot of the
+ *   continuous batch.  T_max is the static batch capacity; the number of
+ *   live tokens, T_valid, lives in device memory, so one captured graph
+ *   serves every batch.
+ * - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
+ *   stream), never synchronises, never copies between host and device, and
+ *   can be captured into a HIP graph.  Per-step data (T_valid, subscription
+ *   masks, alpha, clamp values, ring heads) is read from device memory at
+ *   run time, so a graph can be replayed with new requests without
+ *   recapture.
+ * - Host-side argument checks return a status immediately and launch
+ *   nothing.  Data errors found on the device never abort: they are ORed
+ *   into a caller-owned error word (xmix_route_build) and the offending
+ *   token is routed to no app.
+ * - Rows of unsubscribed tokens or requests are never written in any
+ *   output ("don't use, don't pay").
+ * - No C++ exception crosses this interface.
+ */
+#ifndef XMIX_H
+#define XMIX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    XMIX_OK = 0,
+    XMIX_E_INVAL = 1,        /* bad pointer, size or combination of sizes */
+    XMIX_E_UNSUPPORTED = 2,  /* valid request outside what this build supports */
+    XMIX_E_WORKSPACE = 3,    /* workspace missing or smaller than required */
+    XMIX_E_LAUNCH = 4        /* the HIP runtime rejected a launch */
+} xmix_status;
+
+typedef enum { XMIX_F32 = 0, XMIX_BF16 = 1 } xmix_dtype;
+
+enum { XMIX_PROBE_TOKEN = 0, XMIX_PROBE_MEAN = 1 };
+
+/* Device error-word bits set by xmix_route_build. */
+enum {
+    XMIX_ERR_REQUEST_RANGE = 1u,  /* a live token named a request id >= R_max */
+    XMIX_ERR_T_VALID = 2u         /* *T_valid was outside [0, T_max]; clamped */
+};
+
+#define XMIX_MAX_APPS 32
+#define XMIX_MAX_TOPK 64
+#define XMIX_MAX_CLAMP 16
+#define XMIX_MAX_SEGMENTS 4
+
+/* Routing table of one hook step (device arrays, caller-owned):
+ *   tok_mask  [T_max]          app bitmask of each token slot (0: none)
+ *   app_count [n_apps]         number of tokens subscribed to app a
+ *   app_tokens[n_apps][T_max]  ascending token slots of app a, then -1
+ * n_apps <= 32: bit a of a mask is app a. */
+typedef struct {
+    uint32_t *tok_mask;
+    int32_t *app_count;
+    int32_t *app_tokens;
+    int32_t T_max;
+    int32_t n_apps;
+} xmix_route;
+
+/* Readback ring (device memory, caller-owned):
+ *   slots [capacity][row_bytes]  row = 16-byte header {int32 token,
+ *                                int32 request, int32 layer_id, int32 app_id}
+ *                                followed by the payload bytes
+ *   head  [2]                    head[0]: monotonic count of rows ever
+ *                                written; slot of row i is i mod capacity.
+ *                                head[1]: internal, must be zero when the
+ *                                ring is created; every call leaves it zero.
+ * A reader that consumed up to row r can read rows [r, head[0]); if
+ * head[0] - r > capacity, the oldest rows were overwritten. */
+typedef struct {
+    uint8_t *slots;
+    uint64_t *head;
+    int32_t capacity;
+    int32_t row_bytes;
+} xmix_ring;
+
+const char *xmix_status_string(xmix_status s);
+const char *xmix_version(void);
+
+/* ---------------------------------------------------------------- routing
+ * Token -> request -> app-bitmask table (Sec. 4.2 "Toggling semantics",
+ * "Composition model"; Sec. 4.3 "Graph-level toggling and continuous
+ * batching": per-request activation inside one batch, without CPU work).
+ *   tok_mask[t] = sub_mask[req_of_token[t]] & (2^n_apps - 1) for
+ *                 t < *T_valid and 0 <= req_of_token[t] < R_max, else 0.
+ *   app_tokens[a][0..app_count[a]) lists, ascending, the tokens with bit a;
+ *   the rest of the row is -1.
+ * req_of_token [T_max] int32: request id per token slot; negative = padding.
+ * T_valid      [1] int32: live tokens; out of [0, T_max] sets
+ *              XMIX_ERR_T_VALID and is clamped.
+ * sub_mask     [R_max] uint32: app subscription bitmask per request.
+ * err_word     [1] uint32: error bits are ORed in (never cleared here).
+ * rt           host struct with device arrays; rt->T_max >= 1,
+ *              1 <= rt->n_apps <= 32.
+ * Errors: XMIX_E_INVAL for a null pointer or a size out of range. */
+xmix_status xmix_route_build(const int32_t *req_of_token, const int32_t *T_valid,
+                             const uint32_t *sub_mask, int32_t R_max,
+                             const xmix_route *rt, uint32_t *err_word, void *stream);
+
+/* --------------------------------------------------------------- steering
+ * Additive steering, the Write primitive (Sec. 3: add or subtract a vector
+ * on the activation; Fig. 2b's steering_vector write).  For each token t with
+ * at least one steering bit:
+ *   h[t,:] <- round( h[t,:] + sum_{s: bit app_bits[s] in tok_mask[t]}
+ *                                alpha[req[t]][s] * vecs[s,:] )
+ * accumulated in fp64 and rounded once to the storage type (RNE).  Other
+ * rows are not touched.
+ * h        [T_max, d] of dtype `dt`, updated in place.
+ * vecs     [n_steer, d] of dtype `dt`.
+ * app_bits host [n_steer]: the route bit that gates vector s (static per
+ *          deployment, baked into the launch).
+ * alpha    [R_max][n_steer] fp32 per (request, vector); a negative value
+ *          subtracts.
+ * Requires 1 <= n_steer <= 32, d % 8 == 0 (bf16) or d % 4 == 0 (fp32). */
+xmix_status xmix_steer_apply(void *h, xmix_dtype dt, int32_t d, const xmix_route *rt,
+                             const int32_t *req_of_token, const void *vecs,
+                             const int32_t *app_bits, const float *alpha,
+                             int32_t n_steer, int32_t R_max, void *stream);
+
+/* ------------------------------------------------------------------ probes
+ * Linear probes with a logistic link, the Read primitive (Sec. 3: a linear
+ * probe scoring activations; Table 1 App-4).
+ * mode XMIX_PROBE_TOKEN: for each token t with bit app_bits[p]:
+ *   logit_out[p][t] = b[p] + w[p,:] . h[t,:],  score_out[p][t] = sigmoid(logit)
+ *   outputs are [n_probe][T_max] fp32.
+ * mode XMIX_PROBE_MEAN: for each request r whose span
+ *   [cu_seqlens[r], cu_seqlens[r+1]) is non-empty and whose first token has
+ *   bit app_bits[p]:
+ *   logit_out[p][r] = b[p] + mean_{t in span} (w[p,:] . h[t,:]) (the probe of
+ *   the span's mean activation), score as above; outputs are [n_probe][R_max].
+ *   The span sums are reduced in a fixed order (bit-reproducible).
+ * h [T_max, d] and w [n_probe, d] of dtype dt; b [n_probe] fp32;
+ * app_bits host [n_probe]; cu_seqlens [R_max + 1] int32 (MEAN only, spans
+ * contiguous and inside [0, T_max]); the probe reads h as given (call it
+ * before any write at the same hook).
+ * ws: device workspace of at least xmix_probe_workspace(...) bytes (may be
+ * NULL when that is 0).  Requires 1 <= n_probe <= 32. */
+size_t xmix_probe_workspace(int32_t T_max, int32_t n_probe, int32_t mode);
+xmix_status xmix_probe_score(const void *h, xmix_dtype dt, int32_t d, const xmix_route *rt,
+                             const void *w, const float *b, const int32_t *app_bits,
+                             int32_t n_probe, int32_t mode, const int32_t *cu_seqlens,
+                             int32_t R_max, float *logit_out, float *score_out,
+                             void *ws, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------- SAE encode + TopK
+ * TopK sparse-autoencoder encode of the tokens subscribed to app `app_bit`
+ * (sparse autoencoders and feature dictionaries as app artefacts, Sec. 3;
+ * feature activations as gate signals, Sec. 4.2):
+ *   pre_j = b_enc[j] + W_enc[j,:] . (h[t,:] - b_dec)    for all j < m
+ *   the k largest pre_j (equal values: lower j first), ordered by pre
+ *   descending;  idx_out[t][q] = j,  val_out[t][q] = bf16(max(pre_j, 0)).
+ * Rows t of idx_out/val_out ([T_max, k]) are written only for subscribed t.
+ * h [T_max, d] bf16; W_enc [m, d] bf16 latent-major; b_enc [m], b_dec [d]
+ * bf16.  c_fold [m] fp32, nullable: b_enc - W_enc . b_dec as produced by
+ * xmix_sae_fold_bias.  With c_fold the call never reads b_enc or b_dec and
+ * streams W_enc once; with NULL it folds into the workspace first (one extra
+ * read of W_enc).  The GEMM takes h exactly (bf16 x bf16 products, fp32
+ * accumulation), so the fold keeps the subtraction of b_dec exact.
+ * Requires d % 64 == 0, m % 256 == 0, 1 <= k <= min(64, m).
+ * ws: at least xmix_sae_encode_workspace(T_max, d, m, k) bytes. */
+size_t xmix_sae_encode_workspace(int32_t T_max, int32_t d, int32_t m, int32_t k);
+xmix_status xmix_sae_encode_topk(const uint16_t *h, int32_t d, const xmix_route *rt,
+                                 int32_t app_bit, const uint16_t *W_enc,
+                                 const uint16_t *b_enc, const uint16_t *b_dec,
+                                 const float *c_fold, int32_t m, int32_t k,
+                                 int32_t *idx_out, uint16_t *val_out,
+                                 void *ws, size_t ws_bytes, void *stream);
+
+/* One-time fold of the encoder biases, run when an SAE app is loaded:
+ *   c_fold[j] = b_enc[j] - W_enc[j,:] . b_dec   (fp32). */
+xmix_status xmix_sae_fold_bias(const uint16_t *W_enc, const uint16_t *b_enc,
+                               const uint16_t *b_dec, int32_t m, int32_t d,
+                               float *c_fold, void *stream);
+
+/* ------------------------------------------------------- SAE clamp-decode
+ * Feature clamp with the decoded delta added back (a Write whose payload
+ * comes from a Read of the same hook, Sec. 3).  For each token t with bit
+ * app_bit:
+ *   z_j     = the encoded value of j if j is in idx[t,:], else 0
+ *   delta   = sum_q (clamp_vals[q] - z_{clamp_ids[q]}) * W_dec[clamp_ids[q],:]
+ *   h[t,:] <- bf16( h[t,:] + delta )        (fp32 accumulation, one RNE)
+ * which equals decode(z') - decode(z) with z' = z clamped: the SAE's
+ * reconstruction error stays in the residual.  Only n_clamp rows of W_dec
+ * are read.
+ * h [T_max, d] bf16 in place; idx/val [T_max, k] from xmix_sae_encode_topk;
+ * W_dec [m, d] bf16; clamp_ids [n_clamp] int32 in [0, m) and clamp_vals
+ * [n_clamp] fp32 (device, may change between replays); delta_out
+ * [T_max, d] fp32, nullable, receives delta of every processed token.
+ * Requires d % 8 == 0, 1 <= k <= 64, 1 <= n_clamp <= 16. */
+xmix_status xmix_sae_clamp_decode(uint16_t *h, int32_t d, const xmix_route *rt,
+                                  int32_t app_bit, const int32_t *idx,
+                                  const uint16_t *val, int32_t k,
+                                  const uint16_t *W_dec, int32_t m,
+                                  const int32_t *clamp_ids, const float *clamp_vals,
+                                  int32_t n_clamp, float *delta_out, void *stream);
+
+/* ----------------------------------------------------- readback compaction
+ * Buffer-mediated readback (Sec. 1; Sec. 4.2 "State and dataflow"): the
+ * tokens with bit app_bit, ascending, are appended to `ring`:
+ *   slot (head + i) mod capacity <- {t, req_of_token[t], layer_id, app_id}
+ *                                   ++ seg[0] row t ++ ... ++ seg[n-1] row t
+ *   head += count
+ * A later row overwrites an older one in the same slot (only the last
+ * `capacity` rows of one call are written).
+ * seg_rows  host [n_seg] device pointers; segment s of row t starts at
+ *           seg_rows[s] + t * seg_bytes[s].
+ * seg_bytes host [n_seg], each a positive multiple of 4;
+ *           16 + sum(seg_bytes) must equal ring->row_bytes.
+ * ring      host struct; slots 16-byte aligned, row_bytes % 16 == 0.
+ * Requires 1 <= n_seg <= 4. */
+xmix_status xmix_readback_compact(const void *const *seg_rows, const int32_t *seg_bytes,
+                                  int32_t n_seg, const xmix_route *rt, int32_t app_bit,
+                                  const int32_t *req_of_token, int32_t layer_id,
+                                  int32_t app_id, const xmix_ring *ring, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* XMIX_H */

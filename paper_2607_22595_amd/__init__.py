@@ -1,0 +1,244 @@
+"""Python binding of libxmix, the MI355X (gfx950) per-layer MI hook step.
+
+Argument marshalling only: every function below checks shapes and dtypes,
+takes device pointers and the current HIP stream from torch tensors, and
+calls the C entry point of the same name (declared in include/xmix.h).
+All arithmetic runs in the library's HIP kernels.  There is no fallback:
+importing this package fails if the built library is missing.
+
+bf16 data is carried in ``torch.bfloat16`` tensors (raw bits on the C
+side).  Route and ring descriptors own the device buffers the C structs
+point to.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libxmix.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is missing: build the HIP library first "
+        "(python -c 'import __graft_entry__ as g; g.build()' or "
+        "python paper_2607_22595_amd/build.py)")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+XMIX_OK, XMIX_E_INVAL, XMIX_E_UNSUPPORTED, XMIX_E_WORKSPACE, XMIX_E_LAUNCH = range(5)
+XMIX_F32, XMIX_BF16 = 0, 1
+XMIX_PROBE_TOKEN, XMIX_PROBE_MEAN = 0, 1
+XMIX_ERR_REQUEST_RANGE, XMIX_ERR_T_VALID = 1, 2
+MAX_APPS, MAX_TOPK, MAX_CLAMP, MAX_SEGMENTS = 32, 64, 16, 4
+
+
+class XmixRoute(ctypes.Structure):
+    _fields_ = [("tok_mask", ctypes.c_void_p), ("app_count", ctypes.c_void_p),
+                ("app_tokens", ctypes.c_void_p), ("T_max", ctypes.c_int32),
+                ("n_apps", ctypes.c_int32)]
+
+
+class XmixRing(ctypes.Structure):
+    _fields_ = [("slots", ctypes.c_void_p), ("head", ctypes.c_void_p),
+                ("capacity", ctypes.c_int32), ("row_bytes", ctypes.c_int32)]
+
+
+_vp, _i32, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+_st = ctypes.c_int
+_sigs = {
+    "xmix_status_string": ([_st], ctypes.c_char_p),
+    "xmix_version": ([], ctypes.c_char_p),
+    "xmix_route_build": ([_vp, _vp, _vp, _i32, ctypes.POINTER(XmixRoute), _vp, _vp], _st),
+    "xmix_steer_apply": ([_vp, _st, _i32, ctypes.POINTER(XmixRoute), _vp, _vp, _vp, _vp, _i32,
+                          _i32, _vp], _st),
+    "xmix_probe_workspace": ([_i32, _i32, _i32], _sz),
+    "xmix_probe_score": ([_vp, _st, _i32, ctypes.POINTER(XmixRoute), _vp, _vp, _vp, _i32, _i32,
+                          _vp, _i32, _vp, _vp, _vp, _sz, _vp], _st),
+    "xmix_sae_encode_workspace": ([_i32, _i32, _i32, _i32], _sz),
+    "xmix_sae_encode_topk": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _vp, _vp,
+                              _i32, _i32, _vp, _vp, _vp, _sz, _vp], _st),
+    "xmix_sae_fold_bias": ([_vp, _vp, _vp, _i32, _i32, _vp, _vp], _st),
+    "xmix_sae_clamp_decode": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32, _vp,
+                               _i32, _vp, _vp, _i32, _vp, _vp], _st),
+    "xmix_readback_compact": ([_vp, _vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _i32, _i32,
+                               ctypes.POINTER(XmixRing), _vp], _st),
+}
+for _name, (_args, _res) in _sigs.items():
+    _fn = getattr(_lib, _name)
+    _fn.argtypes = _args
+    _fn.restype = _res
+
+EXPORTED = tuple(_sigs)
+
+
+class XmixError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        msg = _lib.xmix_status_string(status).decode()
+        super().__init__(f"{fn}: {msg} (status {status})")
+        self.status = status
+
+
+def _check(fn: str, status: int) -> None:
+    if status != XMIX_OK:
+        raise XmixError(fn, status)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensor must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return XMIX_BF16
+    if t.dtype == torch.float32:
+        return XMIX_F32
+    raise TypeError(f"unsupported activation dtype {t.dtype}")
+
+
+def version() -> str:
+    return _lib.xmix_version().decode()
+
+
+# ---------------------------------------------------------------- descriptors
+
+class Route:
+    """Device routing table of one hook step (owns its buffers)."""
+
+    def __init__(self, T_max: int, n_apps: int, device="cuda"):
+        if not (1 <= n_apps <= MAX_APPS):
+            raise ValueError("n_apps must be in [1, 32]")
+        self.T_max, self.n_apps = int(T_max), int(n_apps)
+        self.tok_mask = torch.zeros(T_max, dtype=torch.int32, device=device)
+        self.app_count = torch.zeros(n_apps, dtype=torch.int32, device=device)
+        self.app_tokens = torch.full((n_apps, T_max), -1, dtype=torch.int32, device=device)
+        self.struct = XmixRoute(self.tok_mask.data_ptr(), self.app_count.data_ptr(),
+                                self.app_tokens.data_ptr(), self.T_max, self.n_apps)
+
+
+class Ring:
+    """Device readback ring: slots [capacity, row_bytes] and head [2] (uint64)."""
+
+    def __init__(self, capacity: int, row_bytes: int, device="cuda"):
+        self.capacity, self.row_bytes = int(capacity), int(row_bytes)
+        self.slots = torch.zeros((capacity, row_bytes), dtype=torch.uint8, device=device)
+        self.head = torch.zeros(2, dtype=torch.int64, device=device)
+        self.struct = XmixRing(self.slots.data_ptr(), self.head.data_ptr(), self.capacity,
+                               self.row_bytes)
+
+
+# ------------------------------------------------------------------ entries
+
+def xmix_route_build(req_of_token, T_valid, sub_mask, route: Route, err_word, stream=None):
+    """req_of_token int32 [T_max]; T_valid int32 [1]; sub_mask int32 [R_max]
+    (uint32 bit patterns); err_word int32 [1] (bits ORed in)."""
+    assert req_of_token.dtype == torch.int32 and req_of_token.numel() == route.T_max
+    assert T_valid.dtype == torch.int32 and sub_mask.dtype == torch.int32
+    _check("xmix_route_build", _lib.xmix_route_build(
+        _ptr(req_of_token), _ptr(T_valid), _ptr(sub_mask), sub_mask.numel(),
+        ctypes.byref(route.struct), _ptr(err_word), _stream(stream)))
+
+
+def xmix_steer_apply(h, route: Route, req_of_token, vecs, app_bits: Sequence[int], alpha,
+                     stream=None):
+    """h [T_max, d] bf16/fp32 in place; vecs [n_steer, d] same dtype;
+    alpha fp32 [R_max, n_steer]; app_bits: host list of route bits."""
+    T_max, d = h.shape
+    assert T_max == route.T_max and vecs.dtype == h.dtype and vecs.shape[-1] == d
+    n = len(app_bits)
+    assert alpha.dtype == torch.float32 and alpha.dim() == 2 and alpha.shape[1] == n
+    bits = (ctypes.c_int32 * n)(*app_bits)
+    _check("xmix_steer_apply", _lib.xmix_steer_apply(
+        _ptr(h), _dt(h), d, ctypes.byref(route.struct), _ptr(req_of_token), _ptr(vecs), bits,
+        _ptr(alpha), n, alpha.shape[0], _stream(stream)))
+
+
+def probe_workspace(T_max: int, n_probe: int, mode: int) -> int:
+    return int(_lib.xmix_probe_workspace(T_max, n_probe, mode))
+
+
+def xmix_probe_score(h, route: Route, w, b, app_bits: Sequence[int], mode: int, logit_out,
+                     score_out, cu_seqlens=None, ws=None, stream=None):
+    """Token mode: outputs fp32 [n_probe, T_max].  Mean mode: outputs fp32
+    [n_probe, R_max] with cu_seqlens int32 [R_max + 1]."""
+    T_max, d = h.shape
+    n = len(app_bits)
+    assert w.dtype == h.dtype and w.shape == (n, d) and b.dtype == torch.float32
+    R_max = 0
+    if mode == XMIX_PROBE_MEAN:
+        R_max = cu_seqlens.numel() - 1
+        assert logit_out.shape == (n, R_max)
+    else:
+        assert logit_out.shape == (n, T_max)
+    bits = (ctypes.c_int32 * n)(*app_bits)
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("xmix_probe_score", _lib.xmix_probe_score(
+        _ptr(h), _dt(h), d, ctypes.byref(route.struct), _ptr(w), _ptr(b), bits, n, mode,
+        _ptr(cu_seqlens), R_max, _ptr(logit_out), _ptr(score_out), _ptr(ws), ws_bytes,
+        _stream(stream)))
+
+
+def sae_encode_workspace(T_max: int, d: int, m: int, k: int) -> int:
+    return int(_lib.xmix_sae_encode_workspace(T_max, d, m, k))
+
+
+def xmix_sae_fold_bias(W_enc, b_enc, b_dec, c_fold, stream=None):
+    m, d = W_enc.shape
+    assert W_enc.dtype == torch.bfloat16 and c_fold.dtype == torch.float32 and c_fold.numel() == m
+    _check("xmix_sae_fold_bias", _lib.xmix_sae_fold_bias(
+        _ptr(W_enc), _ptr(b_enc), _ptr(b_dec), m, d, _ptr(c_fold), _stream(stream)))
+
+
+def xmix_sae_encode_topk(h, route: Route, app_bit: int, W_enc, b_enc, b_dec, c_fold, k: int,
+                         idx_out, val_out, ws, stream=None):
+    """h bf16 [T_max, d]; W_enc bf16 [m, d]; c_fold fp32 [m] or None;
+    idx_out int32 [T_max, k]; val_out bf16 [T_max, k]; ws uint8 workspace."""
+    T_max, d = h.shape
+    m = W_enc.shape[0]
+    assert h.dtype == torch.bfloat16 and W_enc.dtype == torch.bfloat16
+    assert idx_out.dtype == torch.int32 and idx_out.shape == (T_max, k)
+    assert val_out.dtype == torch.bfloat16 and val_out.shape == (T_max, k)
+    ws_bytes = ws.numel() * ws.element_size()
+    _check("xmix_sae_encode_topk", _lib.xmix_sae_encode_topk(
+        _ptr(h), d, ctypes.byref(route.struct), app_bit, _ptr(W_enc), _ptr(b_enc), _ptr(b_dec),
+        _ptr(c_fold), m, k, _ptr(idx_out), _ptr(val_out), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def xmix_sae_clamp_decode(h, route: Route, app_bit: int, idx, val, W_dec, clamp_ids,
+                          clamp_vals, delta_out=None, stream=None):
+    T_max, d = h.shape
+    k = idx.shape[1]
+    m = W_dec.shape[0]
+    assert h.dtype == torch.bfloat16 and W_dec.dtype == torch.bfloat16
+    assert clamp_ids.dtype == torch.int32 and clamp_vals.dtype == torch.float32
+    _check("xmix_sae_clamp_decode", _lib.xmix_sae_clamp_decode(
+        _ptr(h), d, ctypes.byref(route.struct), app_bit, _ptr(idx), _ptr(val), k, _ptr(W_dec), m,
+        _ptr(clamp_ids), _ptr(clamp_vals), clamp_ids.numel(), _ptr(delta_out), _stream(stream)))
+
+
+def xmix_readback_compact(segments: Sequence[torch.Tensor], route: Route, app_bit: int,
+                          req_of_token, layer_id: int, app_id: int, ring: Ring, stream=None):
+    """segments: device tensors whose row t (dim 0) is copied verbatim."""
+    n = len(segments)
+    ptrs = (ctypes.c_void_p * n)(*[_ptr(s) for s in segments])
+    sizes = (ctypes.c_int32 * n)(*[s[0].numel() * s.element_size() for s in segments])
+    _check("xmix_readback_compact", _lib.xmix_readback_compact(
+        ptrs, sizes, n, ctypes.byref(route.struct), app_bit, _ptr(req_of_token), layer_id,
+        app_id, ctypes.byref(ring.struct), _stream(stream)))

@@ -1,0 +1,197 @@
+// C ABI of the hook-step library: host-side argument checks, workspace
+// sizing and launch.  Nothing here allocates, synchronises or copies; every
+// call only enqueues kernels on the caller's stream.
+#include <stdint.h>
+#include <string.h>
+
+#include "../../include/xmix.h"
+#include "launch.hpp"
+
+using namespace xmix;
+
+namespace {
+
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+xmix_status launched(hipError_t e) { return e == hipSuccess ? XMIX_OK : XMIX_E_LAUNCH; }
+
+bool route_ok(const xmix_route* rt) {
+    return rt && rt->tok_mask && rt->app_count && rt->app_tokens && rt->T_max >= 1 &&
+           rt->n_apps >= 1 && rt->n_apps <= XMIX_MAX_APPS;
+}
+
+bool bits_ok(const int32_t* bits, int32_t n, int32_t n_apps, BitList* out) {
+    if (!bits || n < 1 || n > 32) return false;
+    memset(out, 0, sizeof(*out));
+    for (int i = 0; i < n; ++i) {
+        if (bits[i] < 0 || bits[i] >= n_apps) return false;
+        out->bit[i] = bits[i];
+    }
+    return true;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+const int32_t* app_list(const xmix_route* rt, int32_t a) {
+    return rt->app_tokens + static_cast<int64_t>(a) * rt->T_max;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* xmix_status_string(xmix_status s) {
+    switch (s) {
+        case XMIX_OK: return "ok";
+        case XMIX_E_INVAL: return "invalid argument";
+        case XMIX_E_UNSUPPORTED: return "unsupported size or combination";
+        case XMIX_E_WORKSPACE: return "workspace missing or too small";
+        case XMIX_E_LAUNCH: return "kernel launch failed";
+    }
+    return "unknown status";
+}
+
+const char* xmix_version(void) { return "xmix-gfx950 0.1"; }
+
+xmix_status xmix_route_build(const int32_t* req_of_token, const int32_t* T_valid,
+                             const uint32_t* sub_mask, int32_t R_max, const xmix_route* rt,
+                             uint32_t* err_word, void* stream) {
+    if (!req_of_token || !T_valid || !sub_mask || !err_word || R_max < 1 || !route_ok(rt))
+        return XMIX_E_INVAL;
+    return launched(launch_route_build(req_of_token, T_valid, sub_mask, R_max, rt->T_max,
+                                       rt->n_apps, rt->tok_mask, rt->app_count, rt->app_tokens,
+                                       err_word, as_stream(stream)));
+}
+
+xmix_status xmix_steer_apply(void* h, xmix_dtype dt, int32_t d, const xmix_route* rt,
+                             const int32_t* req_of_token, const void* vecs,
+                             const int32_t* app_bits, const float* alpha, int32_t n_steer,
+                             int32_t R_max, void* stream) {
+    if (!h || !req_of_token || !vecs || !alpha || !route_ok(rt) || R_max < 1 || d < 1)
+        return XMIX_E_INVAL;
+    if (dt != XMIX_BF16 && dt != XMIX_F32) return XMIX_E_INVAL;
+    if (d % (dt == XMIX_BF16 ? 8 : 4) != 0 || !aligned16(h) || !aligned16(vecs))
+        return XMIX_E_INVAL;
+    BitList bits;
+    if (!bits_ok(app_bits, n_steer, rt->n_apps, &bits)) return XMIX_E_INVAL;
+    return launched(launch_steer(h, dt == XMIX_BF16, d, rt->T_max, rt->tok_mask, req_of_token,
+                                 vecs, bits, alpha, n_steer, as_stream(stream)));
+}
+
+size_t xmix_probe_workspace(int32_t T_max, int32_t n_probe, int32_t mode) {
+    if (mode != XMIX_PROBE_MEAN || T_max < 1 || n_probe < 1) return 0;
+    return static_cast<size_t>(T_max) * static_cast<size_t>(n_probe) * sizeof(float);
+}
+
+xmix_status xmix_probe_score(const void* h, xmix_dtype dt, int32_t d, const xmix_route* rt,
+                             const void* w, const float* b, const int32_t* app_bits,
+                             int32_t n_probe, int32_t mode, const int32_t* cu_seqlens,
+                             int32_t R_max, float* logit_out, float* score_out, void* ws,
+                             size_t ws_bytes, void* stream) {
+    if (!h || !w || !b || !logit_out || !score_out || !route_ok(rt) || d < 1) return XMIX_E_INVAL;
+    if (dt != XMIX_BF16 && dt != XMIX_F32) return XMIX_E_INVAL;
+    if (d % (dt == XMIX_BF16 ? 8 : 4) != 0 || !aligned16(h) || !aligned16(w)) return XMIX_E_INVAL;
+    if (mode != XMIX_PROBE_TOKEN && mode != XMIX_PROBE_MEAN) return XMIX_E_INVAL;
+    if (mode == XMIX_PROBE_MEAN && (!cu_seqlens || R_max < 1)) return XMIX_E_INVAL;
+    BitList bits;
+    if (!bits_ok(app_bits, n_probe, rt->n_apps, &bits)) return XMIX_E_INVAL;
+    const size_t need = xmix_probe_workspace(rt->T_max, n_probe, mode);
+    if (need && (!ws || ws_bytes < need)) return XMIX_E_WORKSPACE;
+    return launched(launch_probe(h, dt == XMIX_BF16, d, rt->T_max, rt->tok_mask, w, b, bits,
+                                 n_probe, mode, cu_seqlens, R_max, logit_out, score_out,
+                                 static_cast<float*>(ws), as_stream(stream)));
+}
+
+size_t xmix_sae_encode_workspace(int32_t T_max, int32_t d, int32_t m, int32_t k) {
+    (void)d;
+    if (T_max < 1 || m < 256 || k < 1) return 0;
+    // folded bias (used when the caller passes none), then the candidates
+    const size_t fold = (static_cast<size_t>(m) * sizeof(float) + 255u) / 256u * 256u;
+    return fold + sae_candidate_bytes(T_max, m, k);
+}
+
+xmix_status xmix_sae_fold_bias(const uint16_t* W_enc, const uint16_t* b_enc,
+                               const uint16_t* b_dec, int32_t m, int32_t d, float* c_fold,
+                               void* stream) {
+    if (!W_enc || !b_enc || !b_dec || !c_fold || m < 1 || d < 8 || d % 8 != 0 ||
+        !aligned16(W_enc) || !aligned16(b_dec))
+        return XMIX_E_INVAL;
+    return launched(launch_sae_fold(W_enc, b_enc, b_dec, m, d, c_fold, as_stream(stream)));
+}
+
+xmix_status xmix_sae_encode_topk(const uint16_t* h, int32_t d, const xmix_route* rt,
+                                 int32_t app_bit, const uint16_t* W_enc, const uint16_t* b_enc,
+                                 const uint16_t* b_dec, const float* c_fold, int32_t m,
+                                 int32_t k, int32_t* idx_out, uint16_t* val_out, void* ws,
+                                 size_t ws_bytes, void* stream) {
+    if (!h || !W_enc || !idx_out || !val_out || !route_ok(rt)) return XMIX_E_INVAL;
+    if (app_bit < 0 || app_bit >= rt->n_apps) return XMIX_E_INVAL;
+    if (!c_fold && (!b_enc || !b_dec)) return XMIX_E_INVAL;
+    if (d < 64 || d % 64 != 0 || !aligned16(h) || !aligned16(W_enc)) return XMIX_E_INVAL;
+    if (m < 256 || m % 256 != 0 || k < 1 || k > XMIX_MAX_TOPK || k > m) return XMIX_E_INVAL;
+    // the merge keeps (m / 256) * k candidates per token in registers
+    if (static_cast<int64_t>(m / 256) * k > 64 * 256) return XMIX_E_UNSUPPORTED;
+    const size_t need = xmix_sae_encode_workspace(rt->T_max, d, m, k);
+    if (!ws || ws_bytes < need || !aligned16(ws)) return XMIX_E_WORKSPACE;
+    const size_t fold_bytes = (static_cast<size_t>(m) * sizeof(float) + 255u) / 256u * 256u;
+    float* fold = static_cast<float*>(ws);
+    void* cand = static_cast<char*>(ws) + fold_bytes;
+    hipStream_t st = as_stream(stream);
+    if (!c_fold) {
+        if (!aligned16(b_dec)) return XMIX_E_INVAL;
+        if (launch_sae_fold(W_enc, b_enc, b_dec, m, d, fold, st) != hipSuccess) return XMIX_E_LAUNCH;
+        c_fold = fold;
+    }
+    return launched(launch_sae_encode(h, d, rt->T_max, rt->app_count + app_bit,
+                                      app_list(rt, app_bit), W_enc, c_fold, m, k, idx_out,
+                                      val_out, cand, st));
+}
+
+xmix_status xmix_sae_clamp_decode(uint16_t* h, int32_t d, const xmix_route* rt,
+                                  int32_t app_bit, const int32_t* idx, const uint16_t* val,
+                                  int32_t k, const uint16_t* W_dec, int32_t m,
+                                  const int32_t* clamp_ids, const float* clamp_vals,
+                                  int32_t n_clamp, float* delta_out, void* stream) {
+    if (!h || !idx || !val || !W_dec || !clamp_ids || !clamp_vals || !route_ok(rt))
+        return XMIX_E_INVAL;
+    if (app_bit < 0 || app_bit >= rt->n_apps) return XMIX_E_INVAL;
+    if (d < 8 || d % 8 != 0 || m < 1 || k < 1 || k > XMIX_MAX_TOPK) return XMIX_E_INVAL;
+    if (n_clamp < 1 || n_clamp > XMIX_MAX_CLAMP) return XMIX_E_INVAL;
+    if (!aligned16(h) || !aligned16(W_dec) || (delta_out && !aligned16(delta_out)))
+        return XMIX_E_INVAL;
+    return launched(launch_clamp_decode(h, d, rt->app_count + app_bit, app_list(rt, app_bit),
+                                        rt->T_max, idx, val, k, W_dec, m, clamp_ids, clamp_vals,
+                                        n_clamp, delta_out, as_stream(stream)));
+}
+
+xmix_status xmix_readback_compact(const void* const* seg_rows, const int32_t* seg_bytes,
+                                  int32_t n_seg, const xmix_route* rt, int32_t app_bit,
+                                  const int32_t* req_of_token, int32_t layer_id, int32_t app_id,
+                                  const xmix_ring* ring, void* stream) {
+    if (!seg_rows || !seg_bytes || !req_of_token || !ring || !route_ok(rt)) return XMIX_E_INVAL;
+    if (n_seg < 1 || n_seg > XMIX_MAX_SEGMENTS) return XMIX_E_INVAL;
+    if (app_bit < 0 || app_bit >= rt->n_apps) return XMIX_E_INVAL;
+    if (!ring->slots || !ring->head || ring->capacity < 1 || ring->row_bytes < 16 ||
+        ring->row_bytes % 16 != 0 || !aligned16(ring->slots) ||
+        (reinterpret_cast<uintptr_t>(ring->head) & 7u) != 0)
+        return XMIX_E_INVAL;
+    Segments segs;
+    memset(&segs, 0, sizeof(segs));
+    int64_t total = 16;
+    for (int s = 0; s < n_seg; ++s) {
+        if (!seg_rows[s] || seg_bytes[s] < 4 || seg_bytes[s] % 4 != 0 ||
+            (reinterpret_cast<uintptr_t>(seg_rows[s]) & 3u) != 0)
+            return XMIX_E_INVAL;
+        segs.ptr[s] = static_cast<const uint8_t*>(seg_rows[s]);
+        segs.words[s] = seg_bytes[s] / 4;
+        total += seg_bytes[s];
+    }
+    segs.n = n_seg;
+    if (total != ring->row_bytes) return XMIX_E_INVAL;
+    return launched(launch_compact(segs, rt->app_count + app_bit, app_list(rt, app_bit),
+                                   rt->T_max, req_of_token, layer_id, app_id, ring->slots,
+                                   ring->head, ring->capacity, ring->row_bytes,
+                                   as_stream(stream)));
+}
+
+}  // extern "C"

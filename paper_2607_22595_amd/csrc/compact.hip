@@ -1,0 +1,71 @@
+// Readback compaction into a fixed-capacity device ring.  One wave per row of
+// the app's token list (the list is already ascending and compact, built by
+// the routing kernel's ballot/prefix pass); slot = (head + i) mod capacity.
+// Every workgroup reads head[0] before it takes a ticket from head[1]; the
+// workgroup drawing the last ticket has therefore seen every other read, and
+// it alone advances head[0] and returns the ticket counter to zero.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace xmix {
+
+constexpr int kCompactThreads = 256;
+constexpr int kRowsPerBlock = kCompactThreads / kWave;
+
+__global__ void __launch_bounds__(kCompactThreads)
+compact_kernel(Segments segs, const int32_t* __restrict__ app_count,
+               const int32_t* __restrict__ tok_list, const int32_t* __restrict__ req,
+               int32_t layer_id, int32_t app_id, uint8_t* __restrict__ slots,
+               uint64_t* __restrict__ head, int32_t capacity, int32_t row_bytes) {
+    __shared__ uint64_t h0_s;
+    __shared__ int32_t cnt_s;
+    if (threadIdx.x == 0) {
+        h0_s = __atomic_load_n(&head[0], __ATOMIC_RELAXED);
+        cnt_s = *app_count;
+    }
+    __syncthreads();
+    const uint64_t h0 = h0_s;
+    const int32_t cnt = cnt_s;
+
+    const int wave = threadIdx.x / kWave, lane = lane_id();
+    const int32_t i = blockIdx.x * kRowsPerBlock + wave;
+    // rows older than the last `capacity` of this call would be overwritten
+    if (i < cnt && static_cast<int64_t>(i) >= static_cast<int64_t>(cnt) - capacity) {
+        const int32_t t = tok_list[i];
+        uint32_t* dst = reinterpret_cast<uint32_t*>(
+            slots + static_cast<int64_t>((h0 + static_cast<uint64_t>(i)) % static_cast<uint64_t>(capacity)) * row_bytes);
+        if (lane < 4) {
+            const int32_t hdr = lane == 0 ? t : lane == 1 ? req[t] : lane == 2 ? layer_id : app_id;
+            dst[lane] = static_cast<uint32_t>(hdr);
+        }
+        int32_t off = 4;
+        for (int s = 0; s < segs.n; ++s) {
+            const int32_t nw = segs.words[s];
+            const uint32_t* src = reinterpret_cast<const uint32_t*>(segs.ptr[s]) + static_cast<int64_t>(t) * nw;
+            for (int32_t w = lane; w < nw; w += kWave) dst[off + w] = src[w];
+            off += nw;
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __threadfence();
+        const uint64_t ticket = atomicAdd(reinterpret_cast<unsigned long long*>(&head[1]), 1ull);
+        if (ticket == gridDim.x - 1) {
+            __atomic_store_n(&head[0], h0 + static_cast<uint64_t>(cnt), __ATOMIC_RELAXED);
+            atomicExch(reinterpret_cast<unsigned long long*>(&head[1]), 0ull);
+        }
+    }
+}
+
+hipError_t launch_compact(const Segments& segs, const int32_t* app_count,
+                          const int32_t* tok_list, int32_t T_max, const int32_t* req,
+                          int32_t layer_id, int32_t app_id, uint8_t* slots, uint64_t* head,
+                          int32_t capacity, int32_t row_bytes, hipStream_t stream) {
+    const int blocks = (T_max + kRowsPerBlock - 1) / kRowsPerBlock;
+    hipLaunchKernelGGL(compact_kernel, dim3(blocks), dim3(kCompactThreads), 0, stream, segs,
+                       app_count, tok_list, req, layer_id, app_id, slots, head, capacity,
+                       row_bytes);
+    return hipGetLastError();
+}
+
+}  // namespace xmix

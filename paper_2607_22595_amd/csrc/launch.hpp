@@ -1,0 +1,54 @@
+// Kernel launchers behind the C ABI (internal; one definition per .hip file).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace xmix {
+
+struct BitList {  // static app bits, passed by value into a launch
+    int32_t bit[32];
+};
+
+hipError_t launch_route_build(const int32_t* req, const int32_t* T_valid, const uint32_t* sub,
+                              int32_t R_max, int32_t T_max, int32_t n_apps, uint32_t* tok_mask,
+                              int32_t* app_count, int32_t* app_tokens, uint32_t* err_word,
+                              hipStream_t stream);
+
+hipError_t launch_steer(void* h, bool bf16, int32_t d, int32_t T_max, const uint32_t* tok_mask,
+                        const int32_t* req, const void* vecs, const BitList& bits,
+                        const float* alpha, int32_t n_steer, hipStream_t stream);
+
+hipError_t launch_probe(const void* h, bool bf16, int32_t d, int32_t T_max,
+                        const uint32_t* tok_mask, const void* w, const float* b,
+                        const BitList& bits, int32_t n_probe, int32_t mode,
+                        const int32_t* cu_seqlens, int32_t R_max, float* logit, float* score,
+                        float* ws, hipStream_t stream);
+
+size_t sae_candidate_bytes(int32_t T_max, int32_t m, int32_t k);
+hipError_t launch_sae_fold(const uint16_t* W_enc, const uint16_t* b_enc, const uint16_t* b_dec,
+                           int32_t m, int32_t d, float* c_fold, hipStream_t stream);
+hipError_t launch_sae_encode(const uint16_t* h, int32_t d, int32_t T_max,
+                             const int32_t* app_count, const int32_t* tok_list,
+                             const uint16_t* W_enc, const float* c_fold, int32_t m, int32_t k,
+                             int32_t* idx_out, uint16_t* val_out, void* cand,
+                             hipStream_t stream);
+
+hipError_t launch_clamp_decode(uint16_t* h, int32_t d, const int32_t* app_count,
+                               const int32_t* tok_list, int32_t T_max, const int32_t* idx,
+                               const uint16_t* val, int32_t k, const uint16_t* W_dec, int32_t m,
+                               const int32_t* clamp_ids, const float* clamp_vals,
+                               int32_t n_clamp, float* delta_out, hipStream_t stream);
+
+struct Segments {
+    const uint8_t* ptr[4];
+    int32_t words[4];  // 4-byte words per row of each segment
+    int32_t n;
+};
+hipError_t launch_compact(const Segments& segs, const int32_t* app_count,
+                          const int32_t* tok_list, int32_t T_max, const int32_t* req,
+                          int32_t layer_id, int32_t app_id, uint8_t* slots, uint64_t* head,
+                          int32_t capacity, int32_t row_bytes, hipStream_t stream);
+
+}  // namespace xmix

@@ -1,0 +1,193 @@
+"""One hook step of a continuously batched forward pass, on the GPU.
+
+``HookStep`` uploads a workload (activations per hooked layer, the apps'
+parameters, the batch's request layout and subscriptions) into device
+buffers of static shape and runs the step through the C ABI, in this
+order for every layer:
+
+  1. route build (once per step: the batch and subscriptions are shared by
+     all hooked layers);
+  2. reads of the activation as the model produced it: per-token probes,
+     mean-pooled probes, SAE encodes;
+  3. writes: steering, then each SAE app's clamp-decode;
+  4. readback of SAE results into each app's ring.
+
+Reads before writes means every app at a hook sees the same activation,
+whatever else is subscribed.  All buffers are allocated here, once; ``run``
+only enqueues kernels, so it can be captured into a HIP graph and replayed
+after the device-side inputs (subscriptions, alpha, clamp values) change.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional
+
+import numpy as np
+import torch
+
+from . import (XMIX_PROBE_MEAN, XMIX_PROBE_TOKEN, Ring, Route, probe_workspace,
+               sae_encode_workspace, xmix_probe_score, xmix_readback_compact,
+               xmix_route_build, xmix_sae_clamp_decode, xmix_sae_encode_topk,
+               xmix_sae_fold_bias, xmix_steer_apply)
+
+
+def to_device_bits(a: np.ndarray, device) -> torch.Tensor:
+    """uint16 bf16 bit patterns (numpy) -> torch.bfloat16 on the device."""
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(device).view(torch.bfloat16)
+
+
+def to_device(a: np.ndarray, dtype, device) -> torch.Tensor:
+    if a.dtype == np.uint16:
+        return to_device_bits(a, device)
+    if a.dtype == np.uint32:
+        a = a.view(np.int32)
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device=device, dtype=dtype)
+
+
+@dataclass
+class _Probes:
+    mode: int
+    w: torch.Tensor
+    b: torch.Tensor
+    bits: List[int]
+    logit: torch.Tensor
+    score: torch.Tensor
+    ws: Optional[torch.Tensor]
+
+
+@dataclass
+class _Sae:
+    bit: int
+    m: int
+    k: int
+    W_enc: torch.Tensor
+    b_enc: torch.Tensor
+    b_dec: torch.Tensor
+    c_fold: Optional[torch.Tensor]
+    idx: torch.Tensor
+    val: torch.Tensor
+    ws: torch.Tensor
+    W_dec: Optional[torch.Tensor] = None
+    clamp_ids: Optional[torch.Tensor] = None
+    clamp_vals: Optional[torch.Tensor] = None
+    ring: Optional[Ring] = None
+
+
+@dataclass
+class _Layer:
+    layer_id: int
+    h_in: torch.Tensor
+    h: torch.Tensor
+    steer_v: Optional[torch.Tensor] = None
+    steer_bits: List[int] = field(default_factory=list)
+    probes: List[_Probes] = field(default_factory=list)
+    saes: List[_Sae] = field(default_factory=list)
+
+
+class HookStep:
+    def __init__(self, wl, device="cuda", fold_bias: bool = True):
+        dev = torch.device(device)
+        self.wl = wl
+        self.device = dev
+        act = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+        self.req = to_device(wl.req, torch.int32, dev)
+        self.T_valid = torch.tensor([wl.T_valid], dtype=torch.int32, device=dev)
+        self.sub = to_device(wl.sub.astype(np.uint32), torch.int32, dev)
+        self.alpha = to_device(wl.alpha.astype(np.float32), torch.float32, dev)
+        self.err = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.cu = None if wl.cu_seqlens is None else to_device(wl.cu_seqlens, torch.int32, dev)
+        self.route = Route(wl.T_max, wl.n_apps, dev)
+        self.layers: List[_Layer] = []
+        for L in wl.layers:
+            h_in = to_device(L.h, act, dev)
+            lay = _Layer(L.layer_id, h_in, h_in.clone())
+            if L.steer:
+                lay.steer_v = to_device(np.stack([s.v for s in L.steer]), act, dev)
+                lay.steer_bits = [s.bit for s in L.steer]
+            for mode, name in ((XMIX_PROBE_TOKEN, "token"), (XMIX_PROBE_MEAN, "mean")):
+                ps = [p for p in L.probes if p.mode == name]
+                if not ps:
+                    continue
+                n_out = wl.T_max if mode == XMIX_PROBE_TOKEN else wl.R_max
+                nb = probe_workspace(wl.T_max, len(ps), mode)
+                lay.probes.append(_Probes(
+                    mode, to_device(np.stack([p.w for p in ps]), act, dev),
+                    torch.tensor([p.b for p in ps], dtype=torch.float32, device=dev),
+                    [p.bit for p in ps],
+                    torch.zeros((len(ps), n_out), dtype=torch.float32, device=dev),
+                    torch.zeros((len(ps), n_out), dtype=torch.float32, device=dev),
+                    torch.empty(nb, dtype=torch.uint8, device=dev) if nb else None))
+            for s in L.saes:
+                d = wl.d
+                sae = _Sae(
+                    s.bit, s.m, s.k, to_device_bits(s.W_enc, dev), to_device_bits(s.b_enc, dev),
+                    to_device_bits(s.b_dec, dev), None,
+                    torch.zeros((wl.T_max, s.k), dtype=torch.int32, device=dev),
+                    torch.zeros((wl.T_max, s.k), dtype=torch.bfloat16, device=dev),
+                    torch.empty(sae_encode_workspace(wl.T_max, d, s.m, s.k), dtype=torch.uint8,
+                                device=dev))
+                if fold_bias:
+                    sae.c_fold = torch.empty(s.m, dtype=torch.float32, device=dev)
+                    xmix_sae_fold_bias(sae.W_enc, sae.b_enc, sae.b_dec, sae.c_fold)
+                if s.W_dec is not None and s.clamp_ids is not None:
+                    sae.W_dec = to_device_bits(s.W_dec, dev)
+                    sae.clamp_ids = to_device(s.clamp_ids, torch.int32, dev)
+                    sae.clamp_vals = to_device(s.clamp_vals, torch.float32, dev)
+                if s.ring_capacity:
+                    sae.ring = Ring(s.ring_capacity, 16 + s.k * 4 + s.k * 2, dev)
+                lay.saes.append(sae)
+            self.layers.append(lay)
+
+    def reset(self):
+        """Restore every layer's activation to its input value."""
+        for lay in self.layers:
+            lay.h.copy_(lay.h_in)
+
+    def run(self, stream=None):
+        """Enqueue one full hook step (all layers) on `stream`."""
+        xmix_route_build(self.req, self.T_valid, self.sub, self.route, self.err, stream)
+        for lay in self.layers:
+            for p in lay.probes:
+                xmix_probe_score(lay.h, self.route, p.w, p.b, p.bits, p.mode, p.logit, p.score,
+                                 cu_seqlens=self.cu, ws=p.ws, stream=stream)
+            for s in lay.saes:
+                xmix_sae_encode_topk(lay.h, self.route, s.bit, s.W_enc, s.b_enc, s.b_dec,
+                                     s.c_fold, s.k, s.idx, s.val, s.ws, stream)
+            if lay.steer_v is not None:
+                xmix_steer_apply(lay.h, self.route, self.req, lay.steer_v, lay.steer_bits,
+                                 self.alpha, stream)
+            for s in lay.saes:
+                if s.W_dec is not None:
+                    xmix_sae_clamp_decode(lay.h, self.route, s.bit, s.idx, s.val, s.W_dec,
+                                          s.clamp_ids, s.clamp_vals, stream=stream)
+            for s in lay.saes:
+                if s.ring is not None:
+                    xmix_readback_compact([s.idx, s.val], self.route, s.bit, self.req,
+                                          lay.layer_id, s.bit, s.ring, stream)
+
+    def hbm_bytes(self) -> int:
+        """Algorithmic bytes of one step: what the method must touch."""
+        wl = self.wl
+        esz = 2 if wl.dtype == "bf16" else 4
+        sub = wl.sub.astype(np.uint64)
+        live = np.zeros(wl.T_max, np.uint64)
+        ok = (wl.req >= 0) & (np.arange(wl.T_max) < wl.T_valid)
+        live[ok] = sub[wl.req[ok]]
+        total = 0
+        for L in wl.layers:
+            steer_bits = sum(1 << s.bit for s in L.steer)
+            read_bits = steer_bits | sum(1 << p.bit for p in L.probes) | sum(1 << s.bit for s in L.saes)
+            rows_read = int(np.count_nonzero(live & np.uint64(read_bits)))
+            rows_written = int(np.count_nonzero(live & np.uint64(steer_bits | sum(
+                1 << s.bit for s in L.saes if s.W_dec is not None))))
+            total += (rows_read + rows_written) * wl.d * esz
+            total += len(L.steer) * wl.d * esz + len(L.probes) * wl.d * esz
+            for s in L.saes:
+                total += s.m * wl.d * 2 + s.m * 4        # W_enc + folded bias
+                n_sub = int(np.count_nonzero(live & np.uint64(1 << s.bit)))
+                total += n_sub * s.k * 6                 # idx + val
+                if s.W_dec is not None:
+                    total += len(s.clamp_ids) * wl.d * 2
+                if s.ring_capacity:
+                    total += min(n_sub, s.ring_capacity) * (16 + s.k * 6)
+        return total

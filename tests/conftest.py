@@ -23,3 +23,19 @@ def oracle():
 def synth():
     import synth as _s
     return _s
+
+
+def pytest_collection_modifyitems(config, items):
+    # GPU tests need an MI355X; on a machine without any GPU they are skipped
+    # (on a GPU machine a missing HIP library is an error, not a skip).
+    try:
+        import torch
+        has_gpu = torch.cuda.is_available()
+    except Exception:
+        has_gpu = False
+    if has_gpu:
+        return
+    skip = pytest.mark.skip(reason="no GPU on this machine")
+    for item in items:
+        if "gpu" in item.keywords:
+            item.add_marker(skip)

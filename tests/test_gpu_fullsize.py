@@ -1,0 +1,162 @@
+"""Full-size hook steps in the launch configuration the benchmark times
+(HookStep.run, static shapes), checked against the oracle on every output
+the oracle can afford: all of routing, steering, probes and readback, and a
+seeded sample of tokens for the SAE encode (each sampled token is checked
+over all m latents).  Clamp-decode and readback are stage-isolated: the
+oracle consumes the GPU's own encode results."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from parity import (bf16_f64, check_delta, check_probe, check_residual, check_steer,
+                    check_topk, torch_bits)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def HookStep():
+    from paper_2607_22595_amd.hookstep import HookStep as HS
+    return HS
+
+
+def _sample(tokens, n, name):
+    if len(tokens) <= n:
+        return np.asarray(tokens)
+    pick = synth.permutation(f"test/sample/{name}", len(tokens))[:n]
+    return np.sort(np.asarray(tokens)[pick])
+
+
+def _probe_outputs(step, wl, L, lay, tm):
+    for p_dev in lay.probes:
+        name = "token" if p_dev.mode == 0 else "mean"
+        ps = [p for p in L.probes if p.mode == name]
+        w = np.stack([p.w for p in ps])
+        b = np.array([p.b for p in ps], np.float32)
+        bits = [p.bit for p in ps]
+        hv = bf16_f64(L.h)
+        absdot = np.abs(bf16_f64(w)) @ np.abs(hv).T
+        if name == "token":
+            lr, sr = oracle.probe_token(L.h, tm, w, b, bits)
+            floor = absdot
+        else:
+            lr, sr = oracle.probe_mean(L.h, tm, w, b, bits, wl.cu_seqlens)
+            cu = wl.cu_seqlens
+            floor = np.stack([[absdot[q, cu[r]:cu[r + 1]].mean() for r in range(wl.R_max)]
+                              for q in range(len(ps))])
+        written = ~np.isnan(lr)
+        check_probe(p_dev.logit.cpu().numpy(), p_dev.score.cpu().numpy(), lr, sr, written, floor)
+
+
+def test_decode_8b_shape_four_layers(HookStep):
+    wl = synth.make("c2")
+    step = HookStep(wl)
+    step.run()
+    torch.cuda.synchronize()
+    tm, cnt, lists, err = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    assert np.array_equal(step.route.tok_mask.cpu().numpy().view(np.uint32), tm)
+    assert np.array_equal(step.route.app_tokens.cpu().numpy(), lists)
+    for L, lay in zip(wl.layers, step.layers):
+        bits = [s.bit for s in L.steer]
+        ref = oracle.steer(L.h, tm, wl.req, np.stack([s.v for s in L.steer]), bits, wl.alpha)
+        rows = (tm & np.uint32(sum(1 << b for b in bits))) != 0
+        check_steer(torch_bits(lay.h), ref, L.h, rows)
+        _probe_outputs(step, wl, L, lay, tm)
+
+
+def test_decode_sae_with_ring(HookStep):
+    wl = synth.make("c3")
+    step = HookStep(wl)
+    L, lay = wl.layers[0], step.layers[0]
+    s, sd = L.saes[0], lay.saes[0]
+    tm, cnt, lists, err = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    toks = lists[0, :cnt[0]]
+    assert len(toks) == 128
+    slots = np.zeros((s.ring_capacity, 16 + s.k * 6), np.uint8)
+    head = 0
+    for rep in range(3):        # 3 x 128 rows into 256 slots: wrap-around
+        step.run()
+        torch.cuda.synchronize()
+        idx = sd.idx.cpu().numpy()
+        val = torch_bits(sd.val)
+        slots, head = oracle.compact([idx.view(np.uint8).reshape(wl.T_max, -1),
+                                      val.view(np.uint8).reshape(wl.T_max, -1)],
+                                     tm, s.bit, wl.req, 0, s.bit, slots, head)
+        assert int(sd.ring.head[0].item()) == head
+        assert np.array_equal(sd.ring.slots.cpu().numpy(), slots)
+    sample = _sample(toks, 32, "c3")
+    idx_ref, _, _, pre = oracle.sae_encode(L.h, sample, s.W_enc, s.b_enc, s.b_dec, s.k,
+                                           want_pre=True)
+    for q, t in enumerate(sample):
+        check_topk(idx[t], val[t], idx_ref[q], pre[q], s.k)
+
+
+def test_prefill_sae_and_probes(HookStep):
+    wl = synth.make("c4")
+    step = HookStep(wl)
+    step.run()
+    torch.cuda.synchronize()
+    L, lay = wl.layers[0], step.layers[0]
+    tm, cnt, lists, err = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    _probe_outputs(step, wl, L, lay, tm)
+    s, sd = L.saes[0], lay.saes[0]
+    idx = sd.idx.cpu().numpy()
+    val = torch_bits(sd.val)
+    # a sample spanning the first, last and a middle token-tile of every request
+    sample = np.unique(np.concatenate([wl.cu_seqlens[:-1][:4], [8191, 4095],
+                                       _sample(np.arange(wl.T_max), 4, "c4")]))
+    idx_ref, _, _, pre = oracle.sae_encode(L.h, sample, s.W_enc, s.b_enc, s.b_dec, s.k,
+                                           want_pre=True)
+    for q, t in enumerate(sample):
+        check_topk(idx[t], val[t], idx_ref[q], pre[q], s.k)
+    # properties that hold on every token: k distinct in-range indices,
+    # values non-increasing and non-negative
+    assert np.all((idx >= 0) & (idx < s.m))
+    srt = np.sort(idx, axis=1)
+    assert np.all(srt[:, 1:] != srt[:, :-1])
+    v = bf16_f64(val)
+    assert np.all(v >= 0) and np.all(np.diff(v, axis=1) <= 0)
+
+
+def test_decode_70b_shape_steer_probe_clamp(HookStep):
+    # the first two of the eight clamp apps (same seeds and bits as the full
+    # 32-app workload), steering and probes at full size
+    from parity import bf16_ulp
+    wl = synth.make("c5", n_clamp_apps=2)
+    step = HookStep(wl)
+    step.run()
+    torch.cuda.synchronize()
+    L, lay = wl.layers[0], step.layers[0]
+    tm, cnt, lists, err = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    _probe_outputs(step, wl, L, lay, tm)
+    # the oracle chain: steer from h_in, then each clamp app in order, each
+    # clamp fed the GPU's own encode results
+    bits = [s.bit for s in L.steer]
+    h_ref = oracle.steer(L.h, tm, wl.req, np.stack([s.v for s in L.steer]), bits, wl.alpha)
+    steer_rows = (tm & np.uint32(sum(1 << b for b in bits))) != 0
+    dmax = np.zeros(wl.T_max)
+    stages = steer_rows.astype(np.int64)
+    for s, sd in zip(L.saes, lay.saes):
+        idx = sd.idx.cpu().numpy()
+        val = torch_bits(sd.val)
+        toks = lists[s.bit, :cnt[s.bit]]
+        sample = _sample(toks, 4, f"c5/{s.bit}")
+        idx_ref, _, _, pre = oracle.sae_encode(L.h, sample, s.W_enc, s.b_enc, s.b_dec, s.k,
+                                               want_pre=True)
+        for q, t in enumerate(sample):
+            check_topk(idx[t], val[t], idx_ref[q], pre[q], s.k)
+        h_ref, dref = oracle.clamp_decode(h_ref, tm, s.bit, idx, val, s.W_dec, s.clamp_ids,
+                                          s.clamp_vals, want_delta=True)
+        rows = ((tm >> np.uint32(s.bit)) & 1) == 1
+        dmax[rows] += np.max(np.abs(dref[rows]), axis=1)
+        stages += rows
+    got = torch_bits(lay.h)
+    untouched = stages == 0
+    assert np.array_equal(got[untouched], L.h[untouched])
+    # one rounding per stage on both sides: one ulp per stage, plus the
+    # decoded-delta tolerance of every clamp stage
+    g, r = bf16_f64(got), bf16_f64(h_ref)
+    tol = stages[:, None] * bf16_ulp(r) + 2e-2 * dmax[:, None]
+    assert np.all(np.abs(g - r) <= tol)

@@ -1,0 +1,371 @@
+"""GPU (HIP, gfx950) vs CPU oracle, stage by stage, at sizes the oracle
+finishes in seconds.  Every call goes through the C ABI via the binding.
+
+Sizes span several tiles and a ragged tail: T not a multiple of 64 or of
+the 128-token encode tile, m several 256-latent tiles, padding tokens."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from parity import (bf16_f64, check_delta, check_probe, check_residual, check_steer,
+                    check_topk, torch_bits)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def px():
+    import paper_2607_22595_amd as px
+    return px
+
+
+def dev_bits(a):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
+
+
+def dev_i32(a):
+    return torch.from_numpy(np.ascontiguousarray(a).astype(np.uint32).view(np.int32)
+                            if np.asarray(a).dtype == np.uint32 else
+                            np.ascontiguousarray(a, np.int32)).cuda()
+
+
+def gpu_route(px, req, T_valid, sub, n_apps):
+    rt = px.Route(len(req), n_apps)
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    px.xmix_route_build(dev_i32(req), torch.tensor([T_valid], dtype=torch.int32, device="cuda"),
+                        dev_i32(np.asarray(sub, np.uint32)), rt, err)
+    torch.cuda.synchronize()
+    return rt, err
+
+
+# -------------------------------------------------------------------- route
+
+@pytest.mark.parametrize("seed", range(10))
+def test_route_bit_exact(px, seed):
+    rng = np.random.default_rng(100 + seed)
+    T_max = int(rng.choice([1, 17, 64, 65, 1000, 1024, 1500, 8192]))
+    R = int(rng.integers(1, 600))
+    n_apps = int(rng.integers(1, 33))
+    req = rng.integers(-2, R + 2, T_max).astype(np.int32)
+    sub = rng.integers(0, 2 ** 32, R, dtype=np.uint64).astype(np.uint32)
+    T_valid = int(rng.choice([T_max, max(T_max - 7, 0), -1, T_max + 3]))
+    rt, err = gpu_route(px, req, T_valid, sub, n_apps)
+    tm, cnt, lists, e = oracle.route(req, T_valid, sub, n_apps)
+    assert np.array_equal(rt.tok_mask.cpu().numpy().view(np.uint32), tm)
+    assert np.array_equal(rt.app_count.cpu().numpy(), cnt)
+    assert np.array_equal(rt.app_tokens.cpu().numpy(), lists)
+    assert int(err.item()) == e
+
+
+@pytest.mark.parametrize("fill", [0, 0xFFFFFFFF])
+def test_route_all_zero_and_all_one_masks(px, fill):
+    T = 300
+    req = np.arange(T, dtype=np.int32) % 77
+    sub = np.full(77, fill, np.uint32)
+    rt, err = gpu_route(px, req, T, sub, 32)
+    tm, cnt, lists, e = oracle.route(req, T, sub, 32)
+    assert np.array_equal(rt.app_tokens.cpu().numpy(), lists) and int(err.item()) == e == 0
+    assert np.array_equal(rt.app_count.cpu().numpy(), cnt)
+
+
+# ----------------------------------------------------------------- steering
+
+def _steer_case(px, wl, layer=0, alpha=None):
+    L = wl.layers[layer]
+    tm, _, _, _ = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    rt, _ = gpu_route(px, wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    a = wl.alpha if alpha is None else alpha
+    bits = [s.bit for s in L.steer]
+    v = np.stack([s.v for s in L.steer])
+    if wl.dtype == "bf16":
+        h = dev_bits(L.h)
+        vd = dev_bits(v)
+    else:
+        h = torch.from_numpy(L.h.copy()).cuda()
+        vd = torch.from_numpy(v).cuda()
+    px.xmix_steer_apply(h, rt, dev_i32(wl.req), vd, bits, torch.from_numpy(a).cuda())
+    torch.cuda.synchronize()
+    ref = oracle.steer(L.h, tm, wl.req, v, bits, a)
+    rows = (tm & np.uint32(sum(1 << b for b in bits))) != 0
+    got = torch_bits(h) if wl.dtype == "bf16" else h.cpu().numpy()
+    return check_steer(got, ref, L.h, rows, wl.dtype == "bf16")
+
+
+def test_steer_toy_fp32(px):
+    _steer_case(px, synth.make("c1"))
+
+
+def test_steer_decode_8b_shape(px):
+    wl = synth.make("c2", n_layers=2)
+    for layer in range(2):
+        _steer_case(px, wl, layer)
+
+
+def test_steer_alpha_zero_is_identity(px):
+    wl = synth.make("c2", d=512, T=100, n_layers=1)
+    L = wl.layers[0]
+    rt, _ = gpu_route(px, wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    h = dev_bits(L.h)
+    px.xmix_steer_apply(h, rt, dev_i32(wl.req), dev_bits(np.stack([s.v for s in L.steer])),
+                        [s.bit for s in L.steer], torch.zeros_like(torch.from_numpy(wl.alpha)).cuda())
+    assert np.array_equal(bf16_f64(torch_bits(h)), bf16_f64(L.h))
+
+
+def test_steer_70b_shape_16_vectors(px):
+    wl = synth.make("c5", m=256, k=8)   # steering and probes at full size
+    _steer_case(px, wl)
+
+
+def test_steer_padding_and_ragged(px):
+    wl = synth.make("c2", d=264 - 8, T=77, n_layers=1)
+    wl.req[70:] = -1
+    wl.T_valid = 70
+    _steer_case(px, wl)
+
+
+# ------------------------------------------------------------------- probes
+
+def _probe_case(px, wl, layer=0):
+    L = wl.layers[layer]
+    tm, _, _, _ = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    rt, _ = gpu_route(px, wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    h = dev_bits(L.h) if wl.dtype == "bf16" else torch.from_numpy(L.h).cuda()
+    hv = bf16_f64(L.h) if wl.dtype == "bf16" else L.h.astype(np.float64)
+    for mode_name, mode in (("token", px.XMIX_PROBE_TOKEN), ("mean", px.XMIX_PROBE_MEAN)):
+        ps = [p for p in L.probes if p.mode == mode_name]
+        if not ps:
+            continue
+        w = np.stack([p.w for p in ps])
+        b = np.array([p.b for p in ps], np.float32)
+        bits = [p.bit for p in ps]
+        n_out = wl.T_max if mode == px.XMIX_PROBE_TOKEN else wl.R_max
+        lo = torch.full((len(ps), n_out), float("nan"), device="cuda")
+        so = torch.full((len(ps), n_out), float("nan"), device="cuda")
+        nb = px.probe_workspace(wl.T_max, len(ps), mode)
+        ws = torch.empty(max(nb, 1), dtype=torch.uint8, device="cuda")
+        wd = dev_bits(w) if wl.dtype == "bf16" else torch.from_numpy(w).cuda()
+        cu = None if wl.cu_seqlens is None else dev_i32(wl.cu_seqlens)
+        px.xmix_probe_score(h, rt, wd, torch.from_numpy(b).cuda(), bits, mode, lo, so,
+                            cu_seqlens=cu, ws=ws)
+        torch.cuda.synchronize()
+        wv = bf16_f64(w) if wl.dtype == "bf16" else w.astype(np.float64)
+        absdot = np.abs(wv) @ np.abs(hv).T        # [n_probe, T]
+        if mode == px.XMIX_PROBE_TOKEN:
+            lr, sr = oracle.probe_token(L.h, tm, w, b, bits)
+            floor = absdot
+        else:
+            lr, sr = oracle.probe_mean(L.h, tm, w, b, bits, wl.cu_seqlens)
+            cu = wl.cu_seqlens
+            floor = np.stack([[absdot[p, cu[r]:cu[r + 1]].mean() if cu[r + 1] > cu[r] else 0.0
+                               for r in range(wl.R_max)] for p in range(len(ps))])
+        written = ~np.isnan(lr)
+        lg, sg = lo.cpu().numpy(), so.cpu().numpy()
+        assert np.all(np.isnan(lg[~written])), "unsubscribed outputs were written"
+        check_probe(lg, sg, lr, sr, written, floor)
+
+
+def test_probe_toy_fp32(px):
+    _probe_case(px, synth.make("c1"))
+
+
+def test_probe_decode_8b_shape(px):
+    _probe_case(px, synth.make("c2", n_layers=1))
+
+
+def test_probe_prefill_token_and_pooled_small(px):
+    _probe_case(px, synth.make("c4", d=512, T=2000, R=5, len_lo=100, len_hi=700, m=256, k=8))
+
+
+def test_probe_70b_shape(px):
+    _probe_case(px, synth.make("c5", m=256, k=8))
+
+
+# --------------------------------------------------------------- SAE encode
+
+def _encode(px, wl, sae, h_bits, fold=True):
+    rt, _ = gpu_route(px, wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    h = dev_bits(h_bits)
+    W = dev_bits(sae.W_enc)
+    be, bd = dev_bits(sae.b_enc), dev_bits(sae.b_dec)
+    c = None
+    if fold:
+        c = torch.empty(sae.m, dtype=torch.float32, device="cuda")
+        px.xmix_sae_fold_bias(W, be, bd, c)
+    idx = torch.full((wl.T_max, sae.k), -7, dtype=torch.int32, device="cuda")
+    val = torch.zeros((wl.T_max, sae.k), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(px.sae_encode_workspace(wl.T_max, wl.d, sae.m, sae.k), dtype=torch.uint8,
+                     device="cuda")
+    px.xmix_sae_encode_topk(h, rt, sae.bit, W, be, bd, c, sae.k, idx, val, ws)
+    torch.cuda.synchronize()
+    return rt, idx.cpu().numpy(), torch_bits(val)
+
+
+def _check_encode(wl, sae, h_bits, idx, val, tokens):
+    idx_ref, _, _, pre = oracle.sae_encode(h_bits, tokens, sae.W_enc, sae.b_enc, sae.b_dec,
+                                           sae.k, want_pre=True)
+    swaps = 0
+    for q, t in enumerate(tokens):
+        swaps += check_topk(idx[t], val[t], idx_ref[q], pre[q], sae.k)
+    return swaps
+
+
+@pytest.mark.parametrize("d,m,k,T", [(256, 1024, 16, 64), (512, 2048, 64, 200), (320, 768, 1, 37),
+                                     (128, 256, 64, 130)])
+def test_encode_topk_small(px, d, m, k, T):
+    wl = synth.make("c3", d=d, m=m, k=k, T=T)
+    sae = wl.layers[0].saes[0]
+    rt, idx, val = _encode(px, wl, sae, wl.layers[0].h)
+    tm, cnt, lists, _ = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    toks = lists[0, :cnt[0]]
+    _check_encode(wl, sae, wl.layers[0].h, idx, val, toks)
+    # unsubscribed rows are not written
+    off = np.setdiff1d(np.arange(T), toks)
+    assert np.all(idx[off] == -7)
+
+
+def test_encode_without_folded_bias(px):
+    wl = synth.make("c3", d=256, m=512, k=32, T=50)
+    sae = wl.layers[0].saes[0]
+    rt, idx, val = _encode(px, wl, sae, wl.layers[0].h, fold=False)
+    tm, cnt, lists, _ = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    _check_encode(wl, sae, wl.layers[0].h, idx, val, lists[0, :cnt[0]])
+
+
+def test_encode_all_tokens_many_token_tiles(px):
+    # every token subscribed, 3 token tiles with a ragged last tile
+    wl = synth.make("c3", d=256, m=1024, k=8, T=300, n_sub=300)
+    sae = wl.layers[0].saes[0]
+    rt, idx, val = _encode(px, wl, sae, wl.layers[0].h)
+    _check_encode(wl, sae, wl.layers[0].h, idx, val, np.arange(300))
+
+
+def test_encode_exact_ties_take_lower_index(px):
+    """Duplicated dictionary rows give bit-identical pre-activations; the
+    lower latent index must win, across tiles and inside one tile."""
+    wl = synth.make("c3", d=256, m=1024, k=16, T=40)
+    sae = wl.layers[0].saes[0]
+    W = sae.W_enc.copy()
+    b = sae.b_enc.copy()
+    for src, dst in ((5, 900), (5, 6), (300, 301), (300, 1000), (77, 513)):
+        W[dst] = W[src]
+        b[dst] = b[src]
+    sae.W_enc, sae.b_enc = W, b
+    rt, idx, val = _encode(px, wl, sae, wl.layers[0].h)
+    tm, cnt, lists, _ = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    toks = lists[0, :cnt[0]]
+    _check_encode(wl, sae, wl.layers[0].h, idx, val, toks)
+    for t in toks:
+        s = set(idx[t].tolist())
+        for lo_, hi_ in ((5, 900), (5, 6), (300, 301), (300, 1000), (77, 513)):
+            if hi_ in s:
+                assert lo_ in s, f"token {t}: {hi_} selected without its lower twin {lo_}"
+
+
+def test_encode_clustered_winners_in_one_tile(px):
+    """All k winners planted in one 256-latent tile."""
+    d, m, k = 256, 1024, 64
+    wl = synth.make("c3", d=d, m=m, k=k, T=20, n_sub=20)
+    sae = wl.layers[0].saes[0]
+    hv = bf16_f64(wl.layers[0].h)
+    W = sae.W_enc.copy()
+    t0 = 3
+    for r in range(k):
+        row = hv[t0] * 3.0 * (1.0 - 0.004 * r) / d
+        W[512 + r] = torch.from_numpy(row.astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    sae.W_enc = W
+    rt, idx, val = _encode(px, wl, sae, wl.layers[0].h)
+    _check_encode(wl, sae, wl.layers[0].h, idx, val, np.arange(20))
+    assert set(idx[t0].tolist()) == set(range(512, 512 + k))
+
+
+def test_encode_no_subscribers_writes_nothing(px):
+    wl = synth.make("c3", d=256, m=512, k=8, T=64, n_sub=0)
+    sae = wl.layers[0].saes[0]
+    rt, idx, val = _encode(px, wl, sae, wl.layers[0].h)
+    assert np.all(idx == -7)
+
+
+# ------------------------------------------------------------- clamp-decode
+
+@pytest.mark.parametrize("d,m,k,T", [(256, 1024, 16, 64), (512, 768, 64, 90)])
+def test_clamp_decode_stage_isolated(px, d, m, k, T):
+    wl = synth.make("c5", d=d, T=T, m=m, k=k, p=0.5)
+    L = wl.layers[0]
+    for sae in L.saes[:3]:
+        rt, idx, val = _encode(px, wl, sae, L.h)
+        tm, cnt, lists, _ = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+        # make one clamp id hit a selected feature of the first subscribed token
+        ids = sae.clamp_ids.copy()
+        if cnt[sae.bit]:
+            ids[0] = idx[lists[sae.bit, 0], 0]
+        h = dev_bits(L.h)
+        delta = torch.zeros((T, d), dtype=torch.float32, device="cuda")
+        px.xmix_sae_clamp_decode(h, rt, sae.bit, torch.from_numpy(idx).cuda(),
+                                 dev_bits(val), dev_bits(sae.W_dec), dev_i32(ids),
+                                 torch.from_numpy(sae.clamp_vals).cuda(), delta)
+        torch.cuda.synchronize()
+        ref, dref = oracle.clamp_decode(L.h, tm, sae.bit, idx, val, sae.W_dec, ids,
+                                        sae.clamp_vals, want_delta=True)
+        rows = (tm >> np.uint32(sae.bit)) & 1 == 1
+        got = torch_bits(h)
+        assert np.array_equal(got[~rows], L.h[~rows])
+        dg = delta.cpu().numpy()
+        for t in np.nonzero(rows)[0]:
+            check_delta(dg[t], dref[t])
+            check_residual(got[t], ref[t], dref[t])
+
+
+def test_clamp_to_current_value_leaves_h(px):
+    wl = synth.make("c5", d=256, T=32, m=512, k=8, p=1.0)
+    L = wl.layers[0]
+    sae = L.saes[0]
+    rt, idx, val = _encode(px, wl, sae, L.h)
+    # clamp token 0's own top-4 features to the values it already has: delta = 0
+    cids = idx[0, :4].copy()
+    cvals = bf16_f64(val[0, :4]).astype(np.float32)
+    h = dev_bits(L.h)
+    only_t0 = np.array([0] + [-1] * (wl.T_max - 1), np.int32)
+    rt1, _ = gpu_route(px, only_t0, wl.T_max, wl.sub, wl.n_apps)
+    px.xmix_sae_clamp_decode(h, rt1, sae.bit, torch.from_numpy(idx).cuda(), dev_bits(val),
+                             dev_bits(sae.W_dec), dev_i32(cids), torch.from_numpy(cvals).cuda())
+    torch.cuda.synchronize()
+    assert np.array_equal(bf16_f64(torch_bits(h)), bf16_f64(L.h))
+
+
+# ---------------------------------------------------------------- readback
+
+def test_readback_ring_bit_exact_with_wraparound(px):
+    wl = synth.make("c3", d=256, m=512, k=16, T=100, ring_capacity=64)
+    sae = wl.layers[0].saes[0]
+    rt, idx, val = _encode(px, wl, sae, wl.layers[0].h)
+    ring = px.Ring(64, 16 + 16 * 6)
+    tm = rt.tok_mask.cpu().numpy().view(np.uint32)
+    slots = np.zeros((64, 16 + 16 * 6), np.uint8)
+    head = 0
+    idx_d, val_d = torch.from_numpy(idx).cuda(), dev_bits(val)
+    for step in range(3):   # 3 x 50 rows into 64 slots: wraps and overwrites
+        px.xmix_readback_compact([idx_d, val_d], rt, sae.bit, dev_i32(wl.req), 7, sae.bit, ring)
+        torch.cuda.synchronize()
+        slots, head = oracle.compact([idx.view(np.uint8).reshape(wl.T_max, -1),
+                                      val.view(np.uint8).reshape(wl.T_max, -1)],
+                                     tm, sae.bit, wl.req, 7, sae.bit, slots, head)
+        assert int(ring.head[0].item()) == head
+        assert int(ring.head[1].item()) == 0
+        assert np.array_equal(ring.slots.cpu().numpy(), slots)
+
+
+def test_readback_more_rows_than_capacity(px):
+    T = 300
+    req = np.arange(T, dtype=np.int32)
+    sub = np.ones(T, np.uint32)
+    rt, _ = gpu_route(px, req, T, sub, 1)
+    rows = np.arange(T * 8, dtype=np.int32).reshape(T, 8)
+    ring = px.Ring(100, 16 + 32)
+    px.xmix_readback_compact([torch.from_numpy(rows).cuda()], rt, 0, dev_i32(req), 1, 0, ring)
+    torch.cuda.synchronize()
+    slots, head = oracle.compact([rows.view(np.uint8).reshape(T, -1)], np.ones(T, np.uint32), 0,
+                                 req, 1, 0, np.zeros((100, 48), np.uint8), 0)
+    assert head == int(ring.head[0].item()) == 300
+    assert np.array_equal(ring.slots.cpu().numpy(), slots)
