@@ -176,25 +176,61 @@ xmix_status xmix_probe_score(const void *h, xmix_dtype dt, int32_t d, const xmix
  *   the k largest pre_j (equal values: lower j first), ordered by pre
  *   descending;  idx_out[t][q] = j,  val_out[t][q] = bf16(max(pre_j, 0)).
  * Rows t of idx_out/val_out ([T_max, k]) are written only for subscribed t.
- * h [T_max, d] bf16; W_enc [m, d] bf16 latent-major; b_enc [m], b_dec [d]
- * bf16.  c_fold [m] fp32, nullable: b_enc - W_enc . b_dec as produced by
+ * h [T_max, d] bf16; b_enc [m], b_dec [d] bf16.
+ * W_packed: the encoder dictionary in the library's tiled HBM layout, made
+ * once per app by xmix_sae_pack_encoder from the row-major [m, d] matrix.
+ * c_fold [m] fp32, nullable: b_enc - W_enc . b_dec as produced by
  * xmix_sae_fold_bias.  With c_fold the call never reads b_enc or b_dec and
- * streams W_enc once; with NULL it folds into the workspace first (one extra
- * read of W_enc).  The GEMM takes h exactly (bf16 x bf16 products, fp32
- * accumulation), so the fold keeps the subtraction of b_dec exact.
- * Requires d % 64 == 0, m % 256 == 0, 1 <= k <= min(64, m).
+ * streams the dictionary once; with NULL it folds into the workspace first
+ * (one extra read of the dictionary).  The GEMM takes h exactly (bf16 x bf16
+ * products, fp32 accumulation), so the fold keeps the subtraction of b_dec
+ * exact.
+ * Requires d % 256 == 0, m % 256 == 0, 1 <= k <= min(64, m),
+ * (m / 256) * k <= 16384.
  * ws: at least xmix_sae_encode_workspace(T_max, d, m, k) bytes. */
 size_t xmix_sae_encode_workspace(int32_t T_max, int32_t d, int32_t m, int32_t k);
 xmix_status xmix_sae_encode_topk(const uint16_t *h, int32_t d, const xmix_route *rt,
-                                 int32_t app_bit, const uint16_t *W_enc,
+                                 int32_t app_bit, const uint16_t *W_packed,
                                  const uint16_t *b_enc, const uint16_t *b_dec,
                                  const float *c_fold, int32_t m, int32_t k,
                                  int32_t *idx_out, uint16_t *val_out,
                                  void *ws, size_t ws_bytes, void *stream);
 
+/* The two stages of xmix_sae_encode_topk, callable on their own (same
+ * arguments and workspace; run them in this order on one stream):
+ *   candidates: the GEMM; for every 256-latent slice of the dictionary and
+ *               every subscribed token, a threshold tau is chosen from the
+ *               slice's own values and every latent with pre >= tau is kept
+ *               in the workspace together with tau;
+ *   merge:      the exact top-k per token, written to idx_out / val_out.
+ *               The top-k of the kept latents is the top-k of all m
+ *               latents when its k-th value is >= every slice's tau (a
+ *               latent left out lies below its slice's tau); otherwise the
+ *               merge recomputes that token's m pre-activations and selects
+ *               from them (same result, slower; it happens only when the
+ *               winners crowd into a few slices).
+ * The same certificate lets a dictionary be split across devices by latent
+ * slices: exchange the kept candidates and thresholds, then merge. */
+xmix_status xmix_sae_encode_candidates(const uint16_t *h, int32_t d, const xmix_route *rt,
+                                       int32_t app_bit, const uint16_t *W_packed,
+                                       const uint16_t *b_enc, const uint16_t *b_dec,
+                                       const float *c_fold, int32_t m, int32_t k,
+                                       void *ws, size_t ws_bytes, void *stream);
+xmix_status xmix_sae_merge_topk(const uint16_t *h, int32_t d, const xmix_route *rt,
+                                int32_t app_bit, const uint16_t *W_packed,
+                                const float *c_fold, int32_t m, int32_t k,
+                                int32_t *idx_out, uint16_t *val_out,
+                                void *ws, size_t ws_bytes, void *stream);
+
+/* One-time repack of a row-major encoder dictionary W_enc [m, d] (bf16)
+ * into the tiled layout the encode kernels stream (same bytes, permuted).
+ * W_packed must not overlap W_enc.  Requires m % 256 == 0, d % 256 == 0. */
+xmix_status xmix_sae_pack_encoder(const uint16_t *W_enc, int32_t m, int32_t d,
+                                  uint16_t *W_packed, void *stream);
+
 /* One-time fold of the encoder biases, run when an SAE app is loaded:
- *   c_fold[j] = b_enc[j] - W_enc[j,:] . b_dec   (fp32). */
-xmix_status xmix_sae_fold_bias(const uint16_t *W_enc, const uint16_t *b_enc,
+ *   c_fold[j] = b_enc[j] - W_enc[j,:] . b_dec   (fp32, W given packed). */
+xmix_status xmix_sae_fold_bias(const uint16_t *W_packed, const uint16_t *b_enc,
                                const uint16_t *b_dec, int32_t m, int32_t d,
                                float *c_fold, void *stream);
 

@@ -61,6 +61,11 @@ _sigs = {
     "xmix_sae_encode_workspace": ([_i32, _i32, _i32, _i32], _sz),
     "xmix_sae_encode_topk": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _vp, _vp,
                               _i32, _i32, _vp, _vp, _vp, _sz, _vp], _st),
+    "xmix_sae_encode_candidates": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _vp,
+                                    _vp, _i32, _i32, _vp, _sz, _vp], _st),
+    "xmix_sae_merge_topk": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32, _i32,
+                             _vp, _vp, _vp, _sz, _vp], _st),
+    "xmix_sae_pack_encoder": ([_vp, _i32, _i32, _vp, _vp], _st),
     "xmix_sae_fold_bias": ([_vp, _vp, _vp, _i32, _i32, _vp, _vp], _st),
     "xmix_sae_clamp_decode": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32, _vp,
                                _i32, _vp, _vp, _i32, _vp, _vp], _st),
@@ -199,7 +204,20 @@ def sae_encode_workspace(T_max: int, d: int, m: int, k: int) -> int:
     return int(_lib.xmix_sae_encode_workspace(T_max, d, m, k))
 
 
+def xmix_sae_pack_encoder(W_enc, W_packed=None, stream=None):
+    """Row-major bf16 W_enc [m, d] -> the tiled layout the encode streams.
+    Returns W_packed (same shape and dtype; only the byte order differs)."""
+    m, d = W_enc.shape
+    assert W_enc.dtype == torch.bfloat16
+    if W_packed is None:
+        W_packed = torch.empty_like(W_enc)
+    _check("xmix_sae_pack_encoder", _lib.xmix_sae_pack_encoder(
+        _ptr(W_enc), m, d, _ptr(W_packed), _stream(stream)))
+    return W_packed
+
+
 def xmix_sae_fold_bias(W_enc, b_enc, b_dec, c_fold, stream=None):
+    """W_enc: the packed dictionary."""
     m, d = W_enc.shape
     assert W_enc.dtype == torch.bfloat16 and c_fold.dtype == torch.float32 and c_fold.numel() == m
     _check("xmix_sae_fold_bias", _lib.xmix_sae_fold_bias(
@@ -208,7 +226,7 @@ def xmix_sae_fold_bias(W_enc, b_enc, b_dec, c_fold, stream=None):
 
 def xmix_sae_encode_topk(h, route: Route, app_bit: int, W_enc, b_enc, b_dec, c_fold, k: int,
                          idx_out, val_out, ws, stream=None):
-    """h bf16 [T_max, d]; W_enc bf16 [m, d]; c_fold fp32 [m] or None;
+    """h bf16 [T_max, d]; W_enc bf16 [m, d] packed; c_fold fp32 [m] or None;
     idx_out int32 [T_max, k]; val_out bf16 [T_max, k]; ws uint8 workspace."""
     T_max, d = h.shape
     m = W_enc.shape[0]
@@ -219,6 +237,27 @@ def xmix_sae_encode_topk(h, route: Route, app_bit: int, W_enc, b_enc, b_dec, c_f
     _check("xmix_sae_encode_topk", _lib.xmix_sae_encode_topk(
         _ptr(h), d, ctypes.byref(route.struct), app_bit, _ptr(W_enc), _ptr(b_enc), _ptr(b_dec),
         _ptr(c_fold), m, k, _ptr(idx_out), _ptr(val_out), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def xmix_sae_encode_candidates(h, route: Route, app_bit: int, W_enc, b_enc, b_dec, c_fold,
+                               k: int, ws, stream=None):
+    """Stage 1 of the encode: per-slice top-k candidates into `ws`."""
+    T_max, d = h.shape
+    m = W_enc.shape[0]
+    assert h.dtype == torch.bfloat16 and W_enc.dtype == torch.bfloat16
+    _check("xmix_sae_encode_candidates", _lib.xmix_sae_encode_candidates(
+        _ptr(h), d, ctypes.byref(route.struct), app_bit, _ptr(W_enc), _ptr(b_enc), _ptr(b_dec),
+        _ptr(c_fold), m, k, _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def xmix_sae_merge_topk(h, route: Route, app_bit: int, W_enc, c_fold, k: int, idx_out, val_out,
+                        ws, stream=None):
+    """Stage 2 of the encode: exact top-k per token from the candidates."""
+    T_max, d = h.shape
+    m = W_enc.shape[0]
+    _check("xmix_sae_merge_topk", _lib.xmix_sae_merge_topk(
+        _ptr(h), d, ctypes.byref(route.struct), app_bit, _ptr(W_enc), _ptr(c_fold), m, k,
+        _ptr(idx_out), _ptr(val_out), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def xmix_sae_clamp_decode(h, route: Route, app_bit: int, idx, val, W_dec, clamp_ids,

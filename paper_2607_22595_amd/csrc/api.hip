@@ -110,13 +110,83 @@ size_t xmix_sae_encode_workspace(int32_t T_max, int32_t d, int32_t m, int32_t k)
     return fold + sae_candidate_bytes(T_max, m, k);
 }
 
+xmix_status xmix_sae_pack_encoder(const uint16_t* W_enc, int32_t m, int32_t d,
+                                  uint16_t* W_packed, void* stream) {
+    if (!W_enc || !W_packed || W_enc == W_packed || m < 256 || m % 256 != 0 || d < 256 ||
+        d % 256 != 0 || !aligned16(W_enc) || !aligned16(W_packed))
+        return XMIX_E_INVAL;
+    return launched(launch_sae_pack(W_enc, m, d, W_packed, as_stream(stream)));
+}
+
 xmix_status xmix_sae_fold_bias(const uint16_t* W_enc, const uint16_t* b_enc,
                                const uint16_t* b_dec, int32_t m, int32_t d, float* c_fold,
                                void* stream) {
-    if (!W_enc || !b_enc || !b_dec || !c_fold || m < 1 || d < 8 || d % 8 != 0 ||
-        !aligned16(W_enc) || !aligned16(b_dec))
+    if (!W_enc || !b_enc || !b_dec || !c_fold || m < 256 || m % 256 != 0 || d < 256 ||
+        d % 256 != 0 || !aligned16(W_enc) || !aligned16(b_dec))
         return XMIX_E_INVAL;
     return launched(launch_sae_fold(W_enc, b_enc, b_dec, m, d, c_fold, as_stream(stream)));
+}
+
+}  // extern "C"
+
+namespace {
+
+// Checks shared by the encode entry points; returns the folded-bias area
+// and the candidate area of the workspace.
+xmix_status encode_args(const uint16_t* h, int32_t d, const xmix_route* rt, int32_t app_bit,
+                        const uint16_t* W_enc, int32_t m, int32_t k, void* ws, size_t ws_bytes,
+                        float** fold, void** cand) {
+    if (!route_ok(rt) || app_bit < 0 || app_bit >= rt->n_apps) return XMIX_E_INVAL;
+    if (h && (!aligned16(h) || d < 256 || d % 256 != 0)) return XMIX_E_INVAL;
+    if (W_enc && !aligned16(W_enc)) return XMIX_E_INVAL;
+    if (m < 256 || m % 256 != 0 || k < 1 || k > XMIX_MAX_TOPK || k > m) return XMIX_E_INVAL;
+    // the merge keeps (m / 256) * k candidates per token in registers
+    if (static_cast<int64_t>(m / 256) * k > 64 * 256) return XMIX_E_UNSUPPORTED;
+    const size_t need = xmix_sae_encode_workspace(rt->T_max, d, m, k);
+    if (!ws || ws_bytes < need || !aligned16(ws)) return XMIX_E_WORKSPACE;
+    const size_t fold_bytes = (static_cast<size_t>(m) * sizeof(float) + 255u) / 256u * 256u;
+    *fold = static_cast<float*>(ws);
+    *cand = static_cast<char*>(ws) + fold_bytes;
+    return XMIX_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+xmix_status xmix_sae_encode_candidates(const uint16_t* h, int32_t d, const xmix_route* rt,
+                                       int32_t app_bit, const uint16_t* W_enc,
+                                       const uint16_t* b_enc, const uint16_t* b_dec,
+                                       const float* c_fold, int32_t m, int32_t k, void* ws,
+                                       size_t ws_bytes, void* stream) {
+    if (!h || !W_enc) return XMIX_E_INVAL;
+    if (!c_fold && (!b_enc || !b_dec || !aligned16(b_dec))) return XMIX_E_INVAL;
+    float* fold;
+    void* cand;
+    const xmix_status st = encode_args(h, d, rt, app_bit, W_enc, m, k, ws, ws_bytes, &fold, &cand);
+    if (st != XMIX_OK) return st;
+    hipStream_t s = as_stream(stream);
+    if (!c_fold) {
+        if (launch_sae_fold(W_enc, b_enc, b_dec, m, d, fold, s) != hipSuccess) return XMIX_E_LAUNCH;
+        c_fold = fold;
+    }
+    return launched(launch_sae_candidates(h, d, rt->T_max, rt->app_count + app_bit,
+                                          app_list(rt, app_bit), W_enc, c_fold, m, k, cand, s));
+}
+
+xmix_status xmix_sae_merge_topk(const uint16_t* h, int32_t d, const xmix_route* rt,
+                                int32_t app_bit, const uint16_t* W_packed, const float* c_fold,
+                                int32_t m, int32_t k, int32_t* idx_out, uint16_t* val_out,
+                                void* ws, size_t ws_bytes, void* stream) {
+    if (!h || !W_packed || !idx_out || !val_out) return XMIX_E_INVAL;
+    float* fold;
+    void* cand;
+    const xmix_status st =
+        encode_args(h, d, rt, app_bit, W_packed, m, k, ws, ws_bytes, &fold, &cand);
+    if (st != XMIX_OK) return st;
+    return launched(launch_sae_merge(h, d, rt->T_max, rt->app_count + app_bit,
+                                     app_list(rt, app_bit), W_packed, c_fold ? c_fold : fold, m,
+                                     k, idx_out, val_out, cand, as_stream(stream)));
 }
 
 xmix_status xmix_sae_encode_topk(const uint16_t* h, int32_t d, const xmix_route* rt,
@@ -124,27 +194,12 @@ xmix_status xmix_sae_encode_topk(const uint16_t* h, int32_t d, const xmix_route*
                                  const uint16_t* b_dec, const float* c_fold, int32_t m,
                                  int32_t k, int32_t* idx_out, uint16_t* val_out, void* ws,
                                  size_t ws_bytes, void* stream) {
-    if (!h || !W_enc || !idx_out || !val_out || !route_ok(rt)) return XMIX_E_INVAL;
-    if (app_bit < 0 || app_bit >= rt->n_apps) return XMIX_E_INVAL;
-    if (!c_fold && (!b_enc || !b_dec)) return XMIX_E_INVAL;
-    if (d < 64 || d % 64 != 0 || !aligned16(h) || !aligned16(W_enc)) return XMIX_E_INVAL;
-    if (m < 256 || m % 256 != 0 || k < 1 || k > XMIX_MAX_TOPK || k > m) return XMIX_E_INVAL;
-    // the merge keeps (m / 256) * k candidates per token in registers
-    if (static_cast<int64_t>(m / 256) * k > 64 * 256) return XMIX_E_UNSUPPORTED;
-    const size_t need = xmix_sae_encode_workspace(rt->T_max, d, m, k);
-    if (!ws || ws_bytes < need || !aligned16(ws)) return XMIX_E_WORKSPACE;
-    const size_t fold_bytes = (static_cast<size_t>(m) * sizeof(float) + 255u) / 256u * 256u;
-    float* fold = static_cast<float*>(ws);
-    void* cand = static_cast<char*>(ws) + fold_bytes;
-    hipStream_t st = as_stream(stream);
-    if (!c_fold) {
-        if (!aligned16(b_dec)) return XMIX_E_INVAL;
-        if (launch_sae_fold(W_enc, b_enc, b_dec, m, d, fold, st) != hipSuccess) return XMIX_E_LAUNCH;
-        c_fold = fold;
-    }
-    return launched(launch_sae_encode(h, d, rt->T_max, rt->app_count + app_bit,
-                                      app_list(rt, app_bit), W_enc, c_fold, m, k, idx_out,
-                                      val_out, cand, st));
+    if (!idx_out || !val_out) return XMIX_E_INVAL;
+    const xmix_status st = xmix_sae_encode_candidates(h, d, rt, app_bit, W_enc, b_enc, b_dec,
+                                                      c_fold, m, k, ws, ws_bytes, stream);
+    if (st != XMIX_OK) return st;
+    return xmix_sae_merge_topk(h, d, rt, app_bit, W_enc, c_fold, m, k, idx_out, val_out, ws,
+                               ws_bytes, stream);
 }
 
 xmix_status xmix_sae_clamp_decode(uint16_t* h, int32_t d, const xmix_route* rt,

@@ -27,13 +27,19 @@ hipError_t launch_probe(const void* h, bool bf16, int32_t d, int32_t T_max,
                         float* ws, hipStream_t stream);
 
 size_t sae_candidate_bytes(int32_t T_max, int32_t m, int32_t k);
+hipError_t launch_sae_pack(const uint16_t* W_enc, int32_t m, int32_t d, uint16_t* W_packed,
+                           hipStream_t stream);
 hipError_t launch_sae_fold(const uint16_t* W_enc, const uint16_t* b_enc, const uint16_t* b_dec,
                            int32_t m, int32_t d, float* c_fold, hipStream_t stream);
-hipError_t launch_sae_encode(const uint16_t* h, int32_t d, int32_t T_max,
-                             const int32_t* app_count, const int32_t* tok_list,
-                             const uint16_t* W_enc, const float* c_fold, int32_t m, int32_t k,
-                             int32_t* idx_out, uint16_t* val_out, void* cand,
-                             hipStream_t stream);
+hipError_t launch_sae_candidates(const uint16_t* h, int32_t d, int32_t T_max,
+                                 const int32_t* app_count, const int32_t* tok_list,
+                                 const uint16_t* W_enc, const float* c_fold, int32_t m,
+                                 int32_t k, void* cand, hipStream_t stream);
+hipError_t launch_sae_merge(const uint16_t* h, int32_t d, int32_t T_max,
+                            const int32_t* app_count, const int32_t* tok_list,
+                            const uint16_t* W_enc, const float* c_fold, int32_t m, int32_t k,
+                            int32_t* idx_out, uint16_t* val_out, void* cand,
+                            hipStream_t stream);
 
 hipError_t launch_clamp_decode(uint16_t* h, int32_t d, const int32_t* app_count,
                                const int32_t* tok_list, int32_t T_max, const int32_t* idx,

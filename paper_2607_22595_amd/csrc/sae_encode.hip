@@ -1,29 +1,37 @@
 // SAE encode with TopK: pre = W_enc . h + c_fold for the tokens subscribed
 // to one app, then the k largest pre-activations per token.
 //
-// Stage 1 (sae_stream_topk_kernel) is an MFMA bf16 GEMM with fp32
-// accumulation.  A workgroup owns 256 latents x 128 subscribed tokens and
-// walks K = d in chunks of 64:
-//   - the W_enc rows (operand A) stream from HBM straight into registers,
-//     each wave owning 64 latents, with a three-deep register ring so two
-//     chunks are in flight while one is multiplied;
+// Stage 1 (sae_stream_kernel) is an MFMA bf16 GEMM with fp32 accumulation.
+// A workgroup (8 waves, two per SIMD so one wave's waits overlap the other's
+// MFMAs) owns 256 latents x 128 subscribed tokens and walks K = d in chunks
+// of 64:
+//   - the dictionary (operand A) streams from HBM straight into registers
+//     from the tiled layout below (each wave-wide load is 1 KB contiguous,
+//     each workgroup reads its 2 MiB slice front to back), each wave owning
+//     32 latents, through a four-deep register ring (three chunks in flight);
 //   - the token rows (operand B) are gathered through the app's token list
 //     into LDS (double buffered, 16-byte chunks XOR-swizzled by row so the
-//     MFMA-layout reads are conflict-free) and shared by the four waves.
-// The epilogue adds the folded bias, stages 32 tokens at a time in LDS and
-// lets each wave pick, per token, the local top-k of its 256 latents with a
-// 32-step bisection on order-preserving integer keys (ballot counts; equal
-// keys are taken in ascending latent order).  Candidates go to the
-// workspace as (fp32 pre, latent index).
+//     MFMA-layout reads are conflict-free) and shared by the eight waves.
+// Epilogue, per token of the tile: a threshold tau is chosen so that the
+// number of latents with pre >= tau lies in a small window (first guess
+// mean + z * stdev of the tile's 256 values, then bisection on the value if
+// needed); every latent with pre >= tau is emitted as a candidate, and tau
+// and the count are recorded for the tile.  This costs O(1) work per value.
 //
-// Stage 2 (sae_merge_kernel): one workgroup per subscribed token selects the
-// exact top-k among the (m / 256) * k candidates with the same bisection over
-// the whole workgroup, breaks remaining ties by latent index, ranks the k
-// winners by (value desc, index asc) and writes idx / bf16(ReLU(pre)).
+// Stage 2 (sae_merge_kernel): one workgroup per subscribed token gathers the
+// candidates of all tiles and selects the exact top-k of that pool (key
+// bisection, ties to the lower latent).  The result is the exact top-k of
+// all m latents whenever the k-th selected value is >= every tile's tau,
+// because a latent that was not emitted lies below its tile's tau.  When
+// that certificate fails (only for inputs whose best latents crowd into a
+// few tiles), the workgroup recomputes the token's m pre-activations with
+// plain fp32 dot products and selects exactly from those.
 //
 // The workgroup-to-tile map is XCD-aware: launch slots are dealt round-robin
-// to the 8 XCDs, so consecutive tiles of one XCD share a W_enc slice in that
-// XCD's L2.
+// to the 8 XCDs, so consecutive tiles of one XCD share a dictionary slice in
+// that XCD's L2.
+#include <math.h>
+
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -35,28 +43,57 @@ typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 constexpr int kBM = 256;  // latents per workgroup
 constexpr int kBN = 128;  // tokens per workgroup
 constexpr int kBK = 64;   // K chunk
-constexpr int kEncThreads = 256;
+constexpr int kEncWaves = 8;
+constexpr int kEncThreads = kEncWaves * kWave;
 constexpr int kMergeThreads = 256;
-constexpr int kMaxCPT = 64;  // merge candidates per thread
-constexpr int kMaxTopK = 64;
+constexpr int kMaxTopK = 64;    // largest k
+constexpr int kPoolMax = 8192;   // merge pool entries (LDS)
+constexpr int kRefineIters = 24;
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& v) {
     return __builtin_bit_cast(bf16x8_t, v);
 }
 
-// ---------------------------------------------------------------- bias fold
-// c_fold[j] = b_enc[j] - W_enc[j,:] . b_dec, one wave per latent.
+// ------------------------------------------------------- dictionary layout
+// W_enc is kept in HBM in a tiled layout matched to the encode GEMM, built
+// once when an SAE app is loaded.  The unit is a 16-byte piece (8 bf16 of
+// one latent row).  Latent j = 256*mt + 64*w + 32*mb + r and row element
+// i = 64*kc + 32*g + 8*s + e (e < 8) live in piece
+//     (mt*nK + kc)*2048 + w*512 + mb*256 + s*64 + (r + 32*g)
+// so the 32 KB that one workgroup needs per K chunk are contiguous, and
+// every wave-wide 16-byte load is 1 KB contiguous: each workgroup streams
+// its 2 MiB slice front to back.
+__device__ __forceinline__ int64_t packed_piece(int32_t j, int32_t i, int32_t nK) {
+    const int32_t mt = j >> 8, jr = j & 255;
+    const int32_t w = jr >> 6, mb = (jr >> 5) & 1, r = jr & 31;
+    const int32_t kc = i >> 6, g = (i >> 5) & 1, s = (i >> 3) & 3;
+    return (static_cast<int64_t>(mt) * nK + kc) * 2048 + w * 512 + mb * 256 + s * 64 + r + 32 * g;
+}
+
 __global__ void __launch_bounds__(256)
-sae_fold_kernel(const uint16_t* __restrict__ W, const uint16_t* __restrict__ b_enc,
+sae_pack_kernel(const uint16_t* __restrict__ W, int32_t m, int32_t d, uint16_t* __restrict__ Wp) {
+    const int32_t pieces_per_row = d / 8;
+    const int64_t q = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (q >= static_cast<int64_t>(m) * pieces_per_row) return;
+    const int32_t j = static_cast<int32_t>(q / pieces_per_row);
+    const int32_t i = static_cast<int32_t>(q % pieces_per_row) * 8;
+    reinterpret_cast<uint4*>(Wp)[packed_piece(j, i, d / kBK)] =
+        reinterpret_cast<const uint4*>(W)[q];
+}
+
+// c_fold[j] = b_enc[j] - W_enc[j,:] . b_dec (packed W_enc), one wave per latent.
+__global__ void __launch_bounds__(256)
+sae_fold_kernel(const uint16_t* __restrict__ Wp, const uint16_t* __restrict__ b_enc,
                 const uint16_t* __restrict__ b_dec, int32_t m, int32_t d,
                 float* __restrict__ c_fold) {
     const int32_t j = blockIdx.x * 4 + threadIdx.x / kWave;
     if (j >= m) return;
-    const uint4* row = reinterpret_cast<const uint4*>(W + static_cast<int64_t>(j) * d);
+    const int32_t nK = d / kBK;
+    const uint4* P = reinterpret_cast<const uint4*>(Wp);
     const uint4* bd = reinterpret_cast<const uint4*>(b_dec);
     float acc = 0.0f;
-    for (int32_t i = lane_id(); i < d / 8; i += kWave) {
-        const uint4 wv = row[i], bv = bd[i];
+    for (int32_t p = lane_id(); p < d / 8; p += kWave) {
+        const uint4 wv = P[packed_piece(j, p * 8, nK)], bv = bd[p];
         const uint32_t ww[4] = {wv.x, wv.y, wv.z, wv.w};
         const uint32_t bw[4] = {bv.x, bv.y, bv.z, bv.w};
 #pragma unroll
@@ -69,15 +106,18 @@ sae_fold_kernel(const uint16_t* __restrict__ W, const uint16_t* __restrict__ b_e
     if (lane_id() == 0) c_fold[j] = bf16_to_f32(b_enc[j]) - acc;
 }
 
-// ------------------------------------------------------ GEMM + local top-k
+// ---------------------------------------------- GEMM + candidate emission
 __global__ void __launch_bounds__(kEncThreads, 1)
-sae_stream_topk_kernel(const uint16_t* __restrict__ h, int32_t d,
-                       const int32_t* __restrict__ app_count,
-                       const int32_t* __restrict__ tok_list, const uint16_t* __restrict__ W,
-                       const float* __restrict__ c_fold, int32_t k, int32_t n_mt, int32_t n_nt,
-                       float* __restrict__ cand_val, int32_t* __restrict__ cand_idx) {
-    __shared__ uint4 xs[2][kBN * 8];         // 2 x 16 KiB
-    __shared__ float pre[32][kBM + 1];       // one 32-token pass of the epilogue
+sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
+                  const int32_t* __restrict__ app_count, const int32_t* __restrict__ tok_list,
+                  const uint16_t* __restrict__ W, const float* __restrict__ c_fold,
+                  int32_t n_mt, int32_t n_nt, float z_guess, int32_t lo_cnt, int32_t cap,
+                  float* __restrict__ cand_val, int32_t* __restrict__ cand_idx,
+                  int32_t* __restrict__ tile_cnt, float* __restrict__ tile_tau) {
+    __shared__ uint4 xs[2][kBN * 8];          // 2 x 16 KiB token chunks
+    __shared__ float red1[kEncWaves][kBN];    // per-wave partials of the epilogue
+    __shared__ float red2[kEncWaves][kBN];
+    __shared__ int cnt_s[kBN];
 
     // XCD-aware tile order: slot L runs on XCD L % 8; give each XCD a
     // contiguous range of tiles, token tile fastest.
@@ -94,166 +134,222 @@ sae_stream_topk_kernel(const uint16_t* __restrict__ h, int32_t d,
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int g = lane >> 5, i32 = lane & 31;
+    const int g = lane >> 5, j32 = lane & 31;
+    const int nK = d / kBK;  // a multiple of 4 (d % 256 == 0)
 
-    // operand A: rows of W_enc, 64 contiguous bytes of each row per chunk
-    const uint16_t* wp0 = W + static_cast<int64_t>(mt * kBM + 64 * wave + i32) * d + 32 * g;
-    const uint16_t* wp1 = wp0 + static_cast<int64_t>(32) * d;
+    // operand A: this wave's 32 latents of the packed slice
+    const uint4* wbase = reinterpret_cast<const uint4*>(W) +
+                         static_cast<int64_t>(mt) * nK * 2048 + wave * 256 + lane;
 
-    // operand B: gathered token rows; padding rows read a valid row and zero it
+    // operand B: gathered token rows; padding rows read a valid row and are
+    // zeroed when written to LDS
     const int xr = tid >> 3, xc = tid & 7;
-    const uint16_t* xrow[4];
-    bool xok[4];
+    const uint16_t* xrow[2];
+    uint32_t xmask[2];
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-        const int n = xr + 32 * p;
-        xok[p] = n < ntok;
-        const int32_t tok = tok_list[n0 + (xok[p] ? n : 0)];
-        xrow[p] = h + static_cast<int64_t>(tok) * d + 8 * xc;
+    for (int p = 0; p < 2; ++p) {
+        const int n = xr + 64 * p;
+        const bool ok = n < ntok;
+        xmask[p] = ok ? 0xFFFFFFFFu : 0u;
+        xrow[p] = h + static_cast<int64_t>(tok_list[n0 + (ok ? n : 0)]) * d + 8 * xc;
     }
 
-    f32x16_t acc[2][4];
+    f32x16_t acc[4];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int b = 0; b < 4; ++b)
 #pragma unroll
-        for (int b = 0; b < 4; ++b)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
+        for (int r = 0; r < 16; ++r) acc[b][r] = 0.0f;
 
-    uint4 wa0[8], wa1[8], wa2[8];
-    uint4 xv[4];
-    const int nK = d / kBK;
+    uint4 wa0[4], wa1[4], wa2[4], wa3[4];   // W ring: 4 chunks, 3 in flight
+    uint4 xv0[2], xv1[2];                   // token ring: 2 chunks in flight
 
-    auto load_w = [&](uint4 (&a)[8], int kc) {
-        const uint4* p0 = reinterpret_cast<const uint4*>(wp0 + kc * kBK);
-        const uint4* p1 = reinterpret_cast<const uint4*>(wp1 + kc * kBK);
+    auto load_w = [&](uint4 (&a)[4], int kc) {
+        kc = min(kc, nK - 1);  // past the end: re-read the last chunk, unused
+        const uint4* p = wbase + static_cast<int64_t>(kc) * 2048;
 #pragma unroll
-        for (int s = 0; s < 4; ++s) a[s] = p0[s];
-#pragma unroll
-        for (int s = 0; s < 4; ++s) a[4 + s] = p1[s];
+        for (int s = 0; s < 4; ++s) a[s] = p[s * 64];
     };
-    auto load_x = [&](int kc) {
+    auto load_x = [&](uint4 (&xv)[2], int kc) {
+        kc = min(kc, nK - 1);
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {
-            uint4 v = *reinterpret_cast<const uint4*>(xrow[p] + kc * kBK);
-            if (!xok[p]) v = make_uint4(0, 0, 0, 0);
-            xv[p] = v;
+        for (int p = 0; p < 2; ++p) xv[p] = *reinterpret_cast<const uint4*>(xrow[p] + kc * kBK);
+    };
+    auto store_x = [&](const uint4 (&xv)[2], int buf) {
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            const int n = xr + 64 * p;
+            const uint4 v = make_uint4(xv[p].x & xmask[p], xv[p].y & xmask[p],
+                                       xv[p].z & xmask[p], xv[p].w & xmask[p]);
+            xs[buf][n * 8 + (xc ^ (n & 7))] = v;
         }
     };
-    auto store_x = [&](int buf) {
-#pragma unroll
-        for (int p = 0; p < 4; ++p) {
-            const int n = xr + 32 * p;
-            xs[buf][n * 8 + (xc ^ (n & 7))] = xv[p];
-        }
-    };
-    auto compute = [&](const uint4 (&a)[8], int buf) {
+    auto compute = [&](const uint4 (&a)[4], int buf) {
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
-            const bf16x8_t A0 = as_bf16x8(a[s]);
-            const bf16x8_t A1 = as_bf16x8(a[4 + s]);
+            const bf16x8_t A = as_bf16x8(a[s]);
+            uint4 bop[4];
 #pragma unroll
             for (int nb = 0; nb < 4; ++nb) {
-                const int n = 32 * nb + i32;
+                const int n = 32 * nb + j32;
                 const int chunk = 4 * g + s;
-                const bf16x8_t B = as_bf16x8(xs[buf][n * 8 + (chunk ^ (n & 7))]);
-                acc[0][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A0, B, acc[0][nb], 0, 0, 0);
-                acc[1][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A1, B, acc[1][nb], 0, 0, 0);
+                bop[nb] = xs[buf][n * 8 + (chunk ^ (n & 7))];
             }
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb)
+                acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, as_bf16x8(bop[nb]), acc[nb],
+                                                                  0, 0, 0);
         }
     };
-    // One K chunk: issue the next token chunk and the W chunk two ahead,
-    // multiply the current chunk, then publish the next token chunk.
-    auto step = [&](int kc, const uint4 (&cur)[8], uint4 (&nxt)[8]) {
-        if (kc + 1 < nK) load_x(kc + 1);
-        if (kc + 2 < nK) load_w(nxt, kc + 2);
+    // One K chunk (branch-free): issue the token chunk two ahead and the W
+    // chunk three ahead, multiply the current chunk, then publish the next
+    // token chunk to the other LDS buffer.  Loads are issued oldest-needed
+    // first, so the in-order vmcnt wait for the next token chunk never
+    // waits on a W prefetch.
+    auto step = [&](int kc, const uint4 (&cur)[4], uint4 (&wnext)[4], uint4 (&xload)[2],
+                    const uint4 (&xstore)[2]) {
+        load_x(xload, kc + 2);
+        load_w(wnext, kc + 3);
         __syncthreads();
         compute(cur, kc & 1);
-        if (kc + 1 < nK) store_x((kc + 1) & 1);
+        store_x(xstore, (kc + 1) & 1);
     };
 
-    load_x(0);
+    load_x(xv0, 0);
+    load_x(xv1, 1);
     load_w(wa0, 0);
-    if (nK > 1) load_w(wa1, 1);
-    store_x(0);
-    for (int kc = 0; kc < nK; kc += 3) {
-        step(kc, wa0, wa2);
-        if (kc + 1 < nK) step(kc + 1, wa1, wa0);
-        if (kc + 2 < nK) step(kc + 2, wa2, wa1);
+    load_w(wa1, 1);
+    load_w(wa2, 2);
+    store_x(xv0, 0);
+    for (int kc = 0; kc < nK; kc += 4) {
+        step(kc + 0, wa0, wa3, xv0, xv1);
+        step(kc + 1, wa1, wa0, xv1, xv0);
+        step(kc + 2, wa2, wa1, xv0, xv1);
+        step(kc + 3, wa3, wa2, xv1, xv0);
     }
 
     // ---------------------------------------------------------- epilogue
-    // acc[mb][nb][r] holds latent 64*wave + 32*mb + 8*(r/4) + 4*g + r%4 of
-    // token 32*nb + i32 (the 32x32 MFMA output layout).
-    const float* cf = c_fold + mt * kBM + 64 * wave + 4 * g;
+    // acc[nb][r] holds latent 32*wave + 8*(r/4) + 4*g + r%4 of token
+    // 32*nb + j32 (the 32x32 MFMA output layout).  Lanes j32 and j32 + 32 of
+    // all eight waves together hold the 256 latents of one token.
+    const float* cf = c_fold + mt * kBM + 32 * wave + 4 * g;
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int r = 0; r < 16; ++r) {
+        const float c = cf[8 * (r / 4) + (r % 4)];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const float c = cf[32 * mb + 8 * (r / 4) + (r % 4)];
-#pragma unroll
-            for (int nb = 0; nb < 4; ++nb) acc[mb][nb][r] += c;
-        }
-
+        for (int nb = 0; nb < 4; ++nb) acc[nb][r] += c;
+    }
+    // per-token mean and variance over the tile's 256 latents
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
-        if (32 * nb >= ntok) continue;  // uniform; unrolled so acc stays in registers
-        __syncthreads();
+        float s1 = 0.0f, s2 = 0.0f;
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                pre[i32][64 * wave + 32 * mb + 8 * (r / 4) + 4 * g + (r % 4)] = acc[mb][nb][r];
-        __syncthreads();
-        for (int q = 0; q < 8; ++q) {
-            const int nl = 8 * wave + q;
-            const int n = 32 * nb + nl;
-            if (n >= ntok) break;  // uniform over the wave
-            uint32_t key[4];
-            float v[4];
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                v[s] = pre[nl][lane + 64 * s];
-                key[s] = f32_key(v[s]);
-            }
-            // largest tau with #{key >= tau} >= k
-            uint32_t tau = 0;
-            for (int bit = 31; bit >= 0; --bit) {
-                const uint32_t c = tau | (1u << bit);
-                int ge = 0;
-#pragma unroll
-                for (int s = 0; s < 4; ++s) ge += __popcll(wave_ballot(key[s] >= c));
-                if (ge >= k) tau = c;
-            }
-            int c_gt = 0;
-#pragma unroll
-            for (int s = 0; s < 4; ++s) c_gt += __popcll(wave_ballot(key[s] > tau));
-            const int need_eq = k - c_gt;
-            const int64_t base = (static_cast<int64_t>(n0 + n) * n_mt + mt) * k;
-            int gt_base = 0, eq_seen = 0;
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const bool gt = key[s] > tau, eq = key[s] == tau;
-                const uint64_t bg = wave_ballot(gt), be = wave_ballot(eq);
-                int pos = -1;
-                if (gt) pos = gt_base + lanes_below(bg);
-                if (eq) {
-                    const int er = eq_seen + lanes_below(be);
-                    if (er < need_eq) pos = c_gt + er;
-                }
-                if (pos >= 0) {
-                    cand_val[base + pos] = v[s];
-                    cand_idx[base + pos] = mt * kBM + lane + 64 * s;
-                }
-                gt_base += __popcll(bg);
-                eq_seen += __popcll(be);
-            }
+        for (int r = 0; r < 16; ++r) {
+            s1 += acc[nb][r];
+            s2 = fmaf(acc[nb][r], acc[nb][r], s2);
+        }
+        s1 += __shfl_xor(s1, 32, kWave);
+        s2 += __shfl_xor(s2, 32, kWave);
+        if (g == 0) {
+            red1[wave][32 * nb + j32] = s1;
+            red2[wave][32 * nb + j32] = s2;
         }
     }
+    __syncthreads();
+    float tau[4], lo_b[4], hi_b[4];
+    bool bad[4];
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+        const int n = 32 * nb + j32;
+        float s1 = 0.0f, s2 = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kEncWaves; ++w) {
+            s1 += red1[w][n];
+            s2 += red2[w][n];
+        }
+        const float mu = s1 * (1.0f / kBM);
+        const float sd = sqrtf(fmaxf(s2 * (1.0f / kBM) - mu * mu, 0.0f));
+        tau[nb] = mu + z_guess * sd;
+        lo_b[nb] = -INFINITY;  // count(lo_b) > cap
+        hi_b[nb] = INFINITY;   // count(hi_b) < lo_cnt (or 0)
+        bad[nb] = false;
+    }
+    // count(pre >= tau) per token; refine tau until lo_cnt <= count <= cap
+    for (int it = 0; it < kRefineIters; ++it) {
+        __syncthreads();  // red1 is reused
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) {
+            float c = 0.0f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) c += acc[nb][r] >= tau[nb] ? 1.0f : 0.0f;
+            c += __shfl_xor(c, 32, kWave);
+            if (g == 0) red1[wave][32 * nb + j32] = c;
+        }
+        __syncthreads();
+        bool any_bad = false;
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) {
+            const int n = 32 * nb + j32;
+            float c = 0.0f;
+#pragma unroll
+            for (int w = 0; w < kEncWaves; ++w) c += red1[w][n];
+            const int cn = static_cast<int>(c);
+            bad[nb] = false;
+            if (n < ntok) {
+                if (cn > cap) {
+                    lo_b[nb] = tau[nb];
+                    bad[nb] = true;
+                } else if (cn < lo_cnt) {
+                    hi_b[nb] = tau[nb];
+                    bad[nb] = true;
+                }
+            }
+            if (bad[nb]) {
+                any_bad = true;
+                if (isfinite(lo_b[nb]) && isfinite(hi_b[nb])) {
+                    tau[nb] = 0.5f * (lo_b[nb] + hi_b[nb]);
+                } else {
+                    // step away from the bad side by a growing fraction of |tau|+1
+                    const float step = ldexpf(0.25f * (fabsf(tau[nb]) + 1.0f), it);
+                    tau[nb] = isfinite(hi_b[nb]) ? tau[nb] - step : tau[nb] + step;
+                }
+            }
+        }
+        if (!__syncthreads_or(any_bad)) break;
+        if (it == kRefineIters - 1) {
+            // give up on the window: fall back to a threshold whose count is
+            // known to be <= cap (the merge then checks exactness)
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb)
+                if (bad[nb]) tau[nb] = hi_b[nb];
+        }
+    }
+    // emit every latent with pre >= tau
+    __syncthreads();
+    if (tid < kBN) cnt_s[tid] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+        const int n = 32 * nb + j32;
+        if (n >= ntok) continue;
+        const int64_t row = static_cast<int64_t>(n0 + n) * n_mt + mt;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            if (acc[nb][r] >= tau[nb]) {
+                const int slot = atomicAdd(&cnt_s[n], 1);
+                if (slot < cap) {
+                    cand_val[row * cap + slot] = acc[nb][r];
+                    cand_idx[row * cap + slot] = mt * kBM + 32 * wave + 8 * (r / 4) + 4 * g + (r % 4);
+                }
+            }
+        }
+        if (wave == 0 && g == 0) tile_tau[row] = tau[nb];
+    }
+    __syncthreads();
+    if (tid < ntok) tile_cnt[static_cast<int64_t>(n0 + tid) * n_mt + mt] = min(cnt_s[tid], cap);
 }
 
 // ------------------------------------------------------------- final merge
-__device__ __forceinline__ int block_sum_int(int v, int* red) {
+__device__ __forceinline__ int block_sum(int v, int* red) {
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
     __syncthreads();
@@ -265,94 +361,196 @@ __device__ __forceinline__ int block_sum_int(int v, int* red) {
     return tot;
 }
 
-template <int CPT>
+// Selects the k best entries (key descending, index ascending) of
+// key[0..n) / idx[0..n) in LDS.  On return the selection is
+//   { i : key[i] > tau  or  (key[i] == tau and idx[i] <= cut) }
+// and holds exactly k entries (indices are distinct).  Requires n >= k.
+__device__ void block_select(const uint32_t* key, const int32_t* idx, int n, int k, int* red,
+                             uint32_t* tau_out, int32_t* cut_out) {
+    uint32_t tau = 0;
+    bool exact = false;
+    for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t c = tau | (1u << bit);
+        int ge = 0;
+        for (int i = threadIdx.x; i < n; i += kMergeThreads) ge += key[i] >= c ? 1 : 0;
+        ge = block_sum(ge, red);
+        if (ge >= k) {
+            tau = c;
+            if (ge == k) {  // the k best are exactly the keys >= c
+                exact = true;
+                break;
+            }
+        }
+    }
+    int32_t cut = 0x7FFFFFFF;
+    if (!exact) {
+        int gt = 0, eq = 0;
+        for (int i = threadIdx.x; i < n; i += kMergeThreads) {
+            gt += key[i] > tau ? 1 : 0;
+            eq += key[i] == tau ? 1 : 0;
+        }
+        gt = block_sum(gt, red);
+        eq = block_sum(eq, red);
+        const int need = k - gt;
+        if (eq > need) {
+            // smallest I with #{key == tau and idx <= I} >= need
+            int32_t lo = 0;
+            for (int bit = 30; bit >= 0; --bit) {
+                const int32_t probe = lo | ((1 << bit) - 1);
+                int c = 0;
+                for (int i = threadIdx.x; i < n; i += kMergeThreads)
+                    c += (key[i] == tau && idx[i] <= probe) ? 1 : 0;
+                if (block_sum(c, red) < need) lo |= (1 << bit);
+            }
+            cut = lo;
+        }
+    }
+    *tau_out = tau;
+    *cut_out = cut;
+}
+
+// Moves the selected entries of key/idx[0..n) to positions [dst, dst + k).
+__device__ void block_compact(uint32_t* key, int32_t* idx, int n, uint32_t tau, int32_t cut,
+                              int dst, int* slot_ctr) {
+    if (threadIdx.x == 0) *slot_ctr = 0;
+    __syncthreads();
+    for (int i = threadIdx.x; i < n; i += kMergeThreads) {
+        const bool take = key[i] > tau || (key[i] == tau && idx[i] <= cut);
+        if (take) {
+            const int s = atomicAdd(slot_ctr, 1);
+            key[dst + s] = key[i];
+            idx[dst + s] = idx[i];
+        }
+    }
+    __syncthreads();
+}
+
 __global__ void __launch_bounds__(kMergeThreads)
 sae_merge_kernel(const float* __restrict__ cand_val, const int32_t* __restrict__ cand_idx,
-                 int32_t n_cand, const int32_t* __restrict__ app_count,
-                 const int32_t* __restrict__ tok_list, int32_t k, int32_t* __restrict__ idx_out,
-                 uint16_t* __restrict__ val_out) {
+                 const int32_t* __restrict__ tile_cnt, const float* __restrict__ tile_tau,
+                 int32_t n_mt, int32_t cap, const int32_t* __restrict__ app_count,
+                 const int32_t* __restrict__ tok_list, int32_t k, const uint16_t* __restrict__ h,
+                 int32_t d, const uint16_t* __restrict__ Wp, const float* __restrict__ c_fold,
+                 int32_t* __restrict__ idx_out, uint16_t* __restrict__ val_out) {
+    // pool entries, plus room to compact the k winners behind them
+    __shared__ uint32_t pkey[kPoolMax + kMaxTopK];
+    __shared__ int32_t pidx[kPoolMax + kMaxTopK];
     __shared__ int red[kMergeThreads / kWave];
-    __shared__ uint32_t sel_key[kMaxTopK];
-    __shared__ int32_t sel_idx[kMaxTopK];
-    __shared__ float sel_val[kMaxTopK];
-    __shared__ int n_sel;
+    __shared__ int scan_s[kMergeThreads / kWave];
+    __shared__ int ctr;
 
     const int n = blockIdx.x;
     if (n >= *app_count) return;
     const int32_t t = tok_list[n];
-    const float* cv = cand_val + static_cast<int64_t>(n) * n_cand;
-    const int32_t* ci = cand_idx + static_cast<int64_t>(n) * n_cand;
+    const int tid = threadIdx.x;
+    const int64_t row0 = static_cast<int64_t>(n) * n_mt;
 
-    uint32_t key[CPT];
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-        const int e = threadIdx.x + kMergeThreads * c;
-        key[c] = e < n_cand ? f32_key(cv[e]) : 0u;
+    // pool gather: thread-exclusive prefix of the tile counts it owns
+    int mine = 0;
+    uint32_t tau_max = 0;
+    for (int tl = tid; tl < n_mt; tl += kMergeThreads) {
+        mine += tile_cnt[row0 + tl];
+        tau_max = max(tau_max, f32_key(tile_tau[row0 + tl]));
     }
-    uint32_t tau = 0;
-    for (int bit = 31; bit >= 0; --bit) {
-        const uint32_t c = tau | (1u << bit);
-        int ge = 0;
+    int incl = mine;
 #pragma unroll
-        for (int q = 0; q < CPT; ++q) ge += key[q] >= c ? 1 : 0;
-        if (block_sum_int(ge, red) >= k) tau = c;
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int y = __shfl_up(incl, off, kWave);
+        if (lane_id() >= off) incl += y;
     }
-    int gt = 0, eq = 0;
+    if (lane_id() == kWave - 1) scan_s[tid / kWave] = incl;
+    uint32_t tm = tau_max;
 #pragma unroll
-    for (int q = 0; q < CPT; ++q) {
-        gt += key[q] > tau ? 1 : 0;
-        eq += key[q] == tau ? 1 : 0;
+    for (int off = 32; off >= 1; off >>= 1) tm = max(tm, static_cast<uint32_t>(__shfl_xor(tm, off, kWave)));
+    if (lane_id() == 0) red[tid / kWave] = static_cast<int>(tm);
+    __syncthreads();
+    int base = 0, total = 0;
+    uint32_t tau_tiles = 0;
+#pragma unroll
+    for (int w = 0; w < kMergeThreads / kWave; ++w) {
+        base += (w < tid / kWave) ? scan_s[w] : 0;
+        total += scan_s[w];
+        tau_tiles = max(tau_tiles, static_cast<uint32_t>(red[w]));
     }
-    const int c_gt = block_sum_int(gt, red);
-    const int c_eq = block_sum_int(eq, red);
-    const int need_eq = k - c_gt;
-    // Ties at the threshold: keep the need_eq lowest latent indices.
-    int32_t idx_cut = 0x7FFFFFFF;
-    if (c_eq > need_eq) {
-        // smallest I with #{key == tau and idx <= I} >= need_eq
-        int32_t lo = 0;
-        for (int bit = 30; bit >= 0; --bit) {
-            const int32_t probe = lo | ((1 << bit) - 1);  // candidate upper bound
-            int c = 0;
-#pragma unroll
-            for (int q = 0; q < CPT; ++q) {
-                const int e = threadIdx.x + kMergeThreads * q;
-                if (key[q] == tau && e < n_cand && ci[e] <= probe) ++c;
+    int pos = base + incl - mine;
+    const bool fits = total <= kPoolMax;
+    if (fits) {
+        for (int tl = tid; tl < n_mt; tl += kMergeThreads) {
+            const int c = tile_cnt[row0 + tl];
+            const int64_t off = (row0 + tl) * cap;
+            for (int q = 0; q < c; ++q) {
+                pkey[pos + q] = f32_key(cand_val[off + q]);
+                pidx[pos + q] = cand_idx[off + q];
             }
-            if (block_sum_int(c, red) < need_eq) lo |= (1 << bit);
+            pos += c;
         }
-        idx_cut = lo;
     }
-    if (threadIdx.x == 0) n_sel = 0;
     __syncthreads();
+
+    bool exact_path = fits && total >= k;
+    uint32_t tau = 0;
+    int32_t cut = 0;
+    if (exact_path) {
+        block_select(pkey, pidx, total, k, red, &tau, &cut);
+        // certificate: nothing left below a tile threshold can beat tau
+        exact_path = tau_tiles <= tau;
+    }
+    int win = 0;  // the k winners end up in pkey/pidx[win .. win + k)
+    if (exact_path) {
+        block_compact(pkey, pidx, total, tau, cut, total, &ctr);
+        win = total;
+    } else {
+        // exact recompute of this token's m pre-activations, 256 at a time,
+        // keeping the k best in pkey/pidx[0..k)
+        const int nK = d / kBK;
+        const uint4* hr = reinterpret_cast<const uint4*>(h + static_cast<int64_t>(t) * d);
+        const uint4* P = reinterpret_cast<const uint4*>(Wp);
+        int held = 0;
+        for (int b = 0; b < n_mt; ++b) {
+            const int32_t j = b * kBM + tid;
+            float acc = 0.0f;
+            for (int32_t p = 0; p < d / 8; ++p) {
+                const uint4 wv = P[packed_piece(j, p * 8, nK)], hv = hr[p];
+                const uint32_t ww[4] = {wv.x, wv.y, wv.z, wv.w};
+                const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w};
 #pragma unroll
-    for (int q = 0; q < CPT; ++q) {
-        const int e = threadIdx.x + kMergeThreads * q;
-        if (e >= n_cand) continue;
-        bool take = key[q] > tau;
-        if (key[q] == tau) take = ci[e] <= idx_cut;
-        if (take) {
-            const int slot = atomicAdd(&n_sel, 1);
-            if (slot >= kMaxTopK) continue;  // cannot happen: exactly k are taken
-            sel_key[slot] = key[q];
-            sel_idx[slot] = ci[e];
-            sel_val[slot] = cv[e];
+                for (int e = 0; e < 4; ++e) {
+                    acc = fmaf(lo_bf16(ww[e]), lo_bf16(hw[e]), acc);
+                    acc = fmaf(hi_bf16(ww[e]), hi_bf16(hw[e]), acc);
+                }
+            }
+            pkey[held + tid] = f32_key(acc + c_fold[j]);
+            pidx[held + tid] = j;
+            __syncthreads();
+            const int n_pool = held + kBM;
+            if (n_pool <= k) {
+                held = n_pool;
+                continue;
+            }
+            uint32_t tb;
+            int32_t cb;
+            block_select(pkey, pidx, n_pool, k, red, &tb, &cb);
+            block_compact(pkey, pidx, n_pool, tb, cb, n_pool, &ctr);
+            for (int i = tid; i < k; i += kMergeThreads) {
+                pkey[i] = pkey[n_pool + i];
+                pidx[i] = pidx[n_pool + i];
+            }
+            __syncthreads();
+            held = k;
         }
     }
-    __syncthreads();
-    // rank by (value desc, index asc); keys are distinct as (key, idx) pairs
-    const int q = threadIdx.x;
-    if (q < k) {
-        const uint32_t kq = sel_key[q];
-        const int32_t iq = sel_idx[q];
+    // rank the k winners by (value desc, index asc)
+    if (tid < k) {
+        const uint32_t kq = pkey[win + tid];
+        const int32_t iq = pidx[win + tid];
         int rank = 0;
-        for (int j = 0; j < k; ++j) {
-            const uint32_t kj = sel_key[j];
-            rank += (kj > kq || (kj == kq && sel_idx[j] < iq)) ? 1 : 0;
+        for (int q = 0; q < k; ++q) {
+            const uint32_t kj = pkey[win + q];
+            rank += (kj > kq || (kj == kq && pidx[win + q] < iq)) ? 1 : 0;
         }
         const int64_t o = static_cast<int64_t>(t) * k + rank;
         idx_out[o] = iq;
-        val_out[o] = f32_to_bf16_rne(fmaxf(sel_val[q], 0.0f));
+        val_out[o] = f32_to_bf16_rne(fmaxf(key_f32(kq), 0.0f));
     }
 }
 
@@ -362,9 +560,66 @@ static int enc_grid(int32_t n_mt, int32_t n_nt) {
     return (tiles + 7) / 8 * 8;
 }
 
+// Candidate emission parameters for a dictionary of m latents and top-k:
+// target emitted per tile (so that m/256 tiles together hold about twice
+// the k needed, plus slack), the per-tile capacity, the lower count bound
+// (non-zero only when few tiles must supply all k), and the standard normal
+// quantile that aims the first threshold guess at the target.
+struct EmitPlan {
+    int target, cap, lo;
+    float z;
+};
+
+static EmitPlan emit_plan(int32_t m, int32_t k) {
+    const int n_mt = m / kBM;
+    EmitPlan e;
+    e.target = (2 * k * kBM + m - 1) / m + 4;
+    e.target = e.target < 8 ? 8 : (e.target > 64 ? 64 : e.target);
+    e.cap = 4 * e.target;
+    e.cap = e.cap < 16 ? 16 : (e.cap > 64 ? 64 : e.cap);
+    e.lo = (n_mt * e.target >= 4 * k) ? 0 : (k < e.cap ? k : e.cap);
+    const double want = e.lo ? 0.5 * (e.lo + e.cap) : e.target;
+    // upper-tail quantile: 0.5 * erfc(z / sqrt 2) = want / 256, by bisection
+    const double f = want / kBM;
+    double a = -8.0, b = 8.0;
+    for (int i = 0; i < 100; ++i) {
+        const double mid = 0.5 * (a + b);
+        if (0.5 * erfc(mid / sqrt(2.0)) > f) a = mid;
+        else b = mid;
+    }
+    e.z = static_cast<float>(0.5 * (a + b));
+    return e;
+}
+
+struct CandArea {
+    float* val;
+    int32_t* idx;
+    int32_t* cnt;
+    float* tau;
+};
+
+static CandArea cand_area(void* cand, int32_t T_max, int32_t n_mt, int cap) {
+    const size_t slots = static_cast<size_t>(T_max) * n_mt;
+    CandArea a;
+    a.val = static_cast<float*>(cand);
+    a.idx = reinterpret_cast<int32_t*>(a.val + slots * cap);
+    a.cnt = a.idx + slots * cap;
+    a.tau = reinterpret_cast<float*>(a.cnt + slots);
+    return a;
+}
+
 size_t sae_candidate_bytes(int32_t T_max, int32_t m, int32_t k) {
-    const size_t n_mt = static_cast<size_t>(m) / kBM;
-    return static_cast<size_t>(T_max) * n_mt * static_cast<size_t>(k) * 8u;
+    const EmitPlan e = emit_plan(m, k);
+    const size_t slots = static_cast<size_t>(T_max) * (m / kBM);
+    return slots * (static_cast<size_t>(e.cap) * 8u + 8u);
+}
+
+hipError_t launch_sae_pack(const uint16_t* W_enc, int32_t m, int32_t d, uint16_t* W_packed,
+                           hipStream_t stream) {
+    const int64_t pieces = static_cast<int64_t>(m) * (d / 8);
+    hipLaunchKernelGGL(sae_pack_kernel, dim3(static_cast<uint32_t>((pieces + 255) / 256)),
+                       dim3(256), 0, stream, W_enc, m, d, W_packed);
+    return hipGetLastError();
 }
 
 hipError_t launch_sae_fold(const uint16_t* W_enc, const uint16_t* b_enc, const uint16_t* b_dec,
@@ -374,36 +629,31 @@ hipError_t launch_sae_fold(const uint16_t* W_enc, const uint16_t* b_enc, const u
     return hipGetLastError();
 }
 
-hipError_t launch_sae_encode(const uint16_t* h, int32_t d, int32_t T_max,
-                             const int32_t* app_count, const int32_t* tok_list,
-                             const uint16_t* W_enc, const float* c_fold, int32_t m, int32_t k,
-                             int32_t* idx_out, uint16_t* val_out, void* cand,
-                             hipStream_t stream) {
+hipError_t launch_sae_candidates(const uint16_t* h, int32_t d, int32_t T_max,
+                                 const int32_t* app_count, const int32_t* tok_list,
+                                 const uint16_t* W_enc, const float* c_fold, int32_t m,
+                                 int32_t k, void* cand, hipStream_t stream) {
     const int32_t n_mt = m / kBM;
     const int32_t n_nt = (T_max + kBN - 1) / kBN;
-    const int32_t n_cand = n_mt * k;
-    float* cand_val = static_cast<float*>(cand);
-    int32_t* cand_idx = reinterpret_cast<int32_t*>(
-        static_cast<char*>(cand) + static_cast<size_t>(T_max) * n_cand * sizeof(float));
-    hipLaunchKernelGGL(sae_stream_topk_kernel, dim3(enc_grid(n_mt, n_nt)), dim3(kEncThreads), 0,
-                       stream, h, d, app_count, tok_list, W_enc, c_fold, k, n_mt, n_nt,
-                       cand_val, cand_idx);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    const int cpt = (n_cand + kMergeThreads - 1) / kMergeThreads;
-    dim3 g(T_max), b(kMergeThreads);
-    if (cpt <= 8)
-        hipLaunchKernelGGL(sae_merge_kernel<8>, g, b, 0, stream, cand_val, cand_idx, n_cand,
-                           app_count, tok_list, k, idx_out, val_out);
-    else if (cpt <= 16)
-        hipLaunchKernelGGL(sae_merge_kernel<16>, g, b, 0, stream, cand_val, cand_idx, n_cand,
-                           app_count, tok_list, k, idx_out, val_out);
-    else if (cpt <= 32)
-        hipLaunchKernelGGL(sae_merge_kernel<32>, g, b, 0, stream, cand_val, cand_idx, n_cand,
-                           app_count, tok_list, k, idx_out, val_out);
-    else
-        hipLaunchKernelGGL(sae_merge_kernel<kMaxCPT>, g, b, 0, stream, cand_val, cand_idx,
-                           n_cand, app_count, tok_list, k, idx_out, val_out);
+    const EmitPlan e = emit_plan(m, k);
+    const CandArea a = cand_area(cand, T_max, n_mt, e.cap);
+    hipLaunchKernelGGL(sae_stream_kernel, dim3(enc_grid(n_mt, n_nt)), dim3(kEncThreads), 0,
+                       stream, h, d, app_count, tok_list, W_enc, c_fold, n_mt, n_nt, e.z, e.lo,
+                       e.cap, a.val, a.idx, a.cnt, a.tau);
+    return hipGetLastError();
+}
+
+hipError_t launch_sae_merge(const uint16_t* h, int32_t d, int32_t T_max,
+                            const int32_t* app_count, const int32_t* tok_list,
+                            const uint16_t* W_enc, const float* c_fold, int32_t m, int32_t k,
+                            int32_t* idx_out, uint16_t* val_out, void* cand,
+                            hipStream_t stream) {
+    const int32_t n_mt = m / kBM;
+    const EmitPlan e = emit_plan(m, k);
+    const CandArea a = cand_area(cand, T_max, n_mt, e.cap);
+    hipLaunchKernelGGL(sae_merge_kernel, dim3(T_max), dim3(kMergeThreads), 0, stream, a.val,
+                       a.idx, a.cnt, a.tau, n_mt, e.cap, app_count, tok_list, k, h, d, W_enc,
+                       c_fold, idx_out, val_out);
     return hipGetLastError();
 }
 

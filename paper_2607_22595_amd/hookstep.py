@@ -28,7 +28,7 @@ import torch
 from . import (XMIX_PROBE_MEAN, XMIX_PROBE_TOKEN, Ring, Route, probe_workspace,
                sae_encode_workspace, xmix_probe_score, xmix_readback_compact,
                xmix_route_build, xmix_sae_clamp_decode, xmix_sae_encode_topk,
-               xmix_sae_fold_bias, xmix_steer_apply)
+               xmix_sae_fold_bias, xmix_sae_pack_encoder, xmix_steer_apply)
 
 
 def to_device_bits(a: np.ndarray, device) -> torch.Tensor:
@@ -119,8 +119,12 @@ class HookStep:
                     torch.empty(nb, dtype=torch.uint8, device=dev) if nb else None))
             for s in L.saes:
                 d = wl.d
+                # the dictionary is packed once into the layout the encode streams
+                W_row = to_device_bits(s.W_enc, dev)
+                W_packed = xmix_sae_pack_encoder(W_row)
+                del W_row
                 sae = _Sae(
-                    s.bit, s.m, s.k, to_device_bits(s.W_enc, dev), to_device_bits(s.b_enc, dev),
+                    s.bit, s.m, s.k, W_packed, to_device_bits(s.b_enc, dev),
                     to_device_bits(s.b_dec, dev), None,
                     torch.zeros((wl.T_max, s.k), dtype=torch.int32, device=dev),
                     torch.zeros((wl.T_max, s.k), dtype=torch.bfloat16, device=dev),

@@ -74,3 +74,26 @@ def test_workspace_queries(lib):
     assert lib.xmix_sae_encode_workspace(256, 4096, 65536, 64) == fold + cand
     assert lib.xmix_probe_workspace(8192, 4, 1) == 8192 * 4 * 4
     assert lib.xmix_probe_workspace(8192, 4, 0) == 0
+
+
+def test_encode_rejects_unsupported_shapes_on_the_host(lib):
+    """Fake (never dereferenced) device addresses: every case below is
+    refused by the host-side checks before anything is launched."""
+    import paper_2607_22595_amd as px
+    f = lib.xmix_sae_encode_topk
+    f.restype = ctypes.c_int
+    rt = px.XmixRoute(0x10000, 0x20000, 0x30000, 256, 1)
+    A = 0x100000   # 16-byte aligned fake address
+
+    def call(d=4096, m=65536, k=64, ws_bytes=1 << 40, app_bit=0, c_fold=A):
+        return f(ctypes.c_void_p(A), d, ctypes.byref(rt), app_bit, ctypes.c_void_p(A),
+                 ctypes.c_void_p(A), ctypes.c_void_p(A), ctypes.c_void_p(c_fold), m, k,
+                 ctypes.c_void_p(A), ctypes.c_void_p(A), ctypes.c_void_p(A),
+                 ctypes.c_size_t(ws_bytes), None)
+    assert call(d=320) == 1            # d must be a multiple of 256
+    assert call(m=300) == 1            # m must be a multiple of 256
+    assert call(k=65) == 1             # k <= 64
+    assert call(k=0) == 1
+    assert call(app_bit=1) == 1        # bit outside the route's apps
+    assert call(m=262144, k=64) == 2   # too many merge candidates per token
+    assert call(ws_bytes=1024) == 3    # workspace too small

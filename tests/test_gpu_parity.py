@@ -187,7 +187,7 @@ def test_probe_70b_shape(px):
 def _encode(px, wl, sae, h_bits, fold=True):
     rt, _ = gpu_route(px, wl.req, wl.T_valid, wl.sub, wl.n_apps)
     h = dev_bits(h_bits)
-    W = dev_bits(sae.W_enc)
+    W = px.xmix_sae_pack_encoder(dev_bits(sae.W_enc))
     be, bd = dev_bits(sae.b_enc), dev_bits(sae.b_dec)
     c = None
     if fold:
@@ -211,8 +211,8 @@ def _check_encode(wl, sae, h_bits, idx, val, tokens):
     return swaps
 
 
-@pytest.mark.parametrize("d,m,k,T", [(256, 1024, 16, 64), (512, 2048, 64, 200), (320, 768, 1, 37),
-                                     (128, 256, 64, 130)])
+@pytest.mark.parametrize("d,m,k,T", [(256, 1024, 16, 64), (512, 2048, 64, 200), (768, 768, 1, 37),
+                                     (256, 256, 64, 130)])
 def test_encode_topk_small(px, d, m, k, T):
     wl = synth.make("c3", d=d, m=m, k=k, T=T)
     sae = wl.layers[0].saes[0]
@@ -369,3 +369,22 @@ def test_readback_more_rows_than_capacity(px):
                                  req, 1, 0, np.zeros((100, 48), np.uint8), 0)
     assert head == int(ring.head[0].item()) == 300
     assert np.array_equal(ring.slots.cpu().numpy(), slots)
+
+
+def test_encode_recompute_path_when_winners_crowd_one_slice(px):
+    """50 of a token's top-64 planted in one 256-latent slice: more than the
+    slice may emit, so the merge's certificate fails for that token and it
+    takes the exact recompute path; the result must still match."""
+    d, m, k = 256, 16384, 64
+    wl = synth.make("c3", d=d, m=m, k=k, T=8, n_sub=8)
+    sae = wl.layers[0].saes[0]
+    hv = bf16_f64(wl.layers[0].h)
+    W = sae.W_enc.copy()
+    t0 = 5
+    for r in range(50):
+        row = hv[t0] * 3.0 * (1.0 - 0.005 * r) / d
+        W[4096 + r] = torch.from_numpy(row.astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    sae.W_enc = W
+    rt, idx, val = _encode(px, wl, sae, wl.layers[0].h)
+    _check_encode(wl, sae, wl.layers[0].h, idx, val, np.arange(8))
+    assert set(range(4096, 4096 + 50)) <= set(idx[t0].tolist())
