@@ -10,8 +10,9 @@
 //     each workgroup reads its 2 MiB slice front to back), each wave owning
 //     32 latents, through a four-deep register ring (three chunks in flight);
 //   - the token rows (operand B) are gathered through the app's token list
-//     into LDS (double buffered, 16-byte chunks XOR-swizzled by row so the
-//     MFMA-layout reads are conflict-free) and shared by the eight waves.
+//     into LDS (double buffered; the 16-byte chunk c of row n is stored at
+//     c ^ ((n >> 1) & 7), so the 16 rows one MFMA-layout read touches per
+//     LDS cycle land in 16 distinct bank groups) and shared by the 8 waves.
 // Epilogue, per token of the tile: a threshold tau is chosen so that the
 // number of latents with pre >= tau lies in a small window (first guess
 // mean + z * stdev of the tile's 256 values, then bisection on the value if
@@ -49,6 +50,7 @@ constexpr int kMergeThreads = 256;
 constexpr int kMaxTopK = 64;    // largest k
 constexpr int kPoolMax = 8192;   // merge pool entries (LDS)
 constexpr int kRefineIters = 24;
+constexpr int kLatentFastTiles = 4;  // token tiles up to which the latent tile runs fastest
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& v) {
     return __builtin_bit_cast(bf16x8_t, v);
@@ -57,17 +59,18 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& v) {
 // ------------------------------------------------------- dictionary layout
 // W_enc is kept in HBM in a tiled layout matched to the encode GEMM, built
 // once when an SAE app is loaded.  The unit is a 16-byte piece (8 bf16 of
-// one latent row).  Latent j = 256*mt + 64*w + 32*mb + r and row element
+// one latent row).  Latent j = 256*mt + 32*w + r and row element
 // i = 64*kc + 32*g + 8*s + e (e < 8) live in piece
-//     (mt*nK + kc)*2048 + w*512 + mb*256 + s*64 + (r + 32*g)
-// so the 32 KB that one workgroup needs per K chunk are contiguous, and
-// every wave-wide 16-byte load is 1 KB contiguous: each workgroup streams
-// its 2 MiB slice front to back.
-__device__ __forceinline__ int64_t packed_piece(int32_t j, int32_t i, int32_t nK) {
+//     (kc*n_mt + mt)*2048 + w*256 + s*64 + (r + 32*g)
+// so the 32 KB one workgroup needs per K chunk are contiguous, every
+// wave-wide 16-byte load is 1 KB contiguous, and at each K step the whole
+// grid streams one contiguous region (chunk-major order spreads concurrent
+// workgroups over all HBM channels instead of one stride class).
+__device__ __forceinline__ int64_t packed_piece(int32_t j, int32_t i, int32_t n_mt) {
     const int32_t mt = j >> 8, jr = j & 255;
-    const int32_t w = jr >> 6, mb = (jr >> 5) & 1, r = jr & 31;
+    const int32_t w = jr >> 5, r = jr & 31;
     const int32_t kc = i >> 6, g = (i >> 5) & 1, s = (i >> 3) & 3;
-    return (static_cast<int64_t>(mt) * nK + kc) * 2048 + w * 512 + mb * 256 + s * 64 + r + 32 * g;
+    return (static_cast<int64_t>(kc) * n_mt + mt) * 2048 + w * 256 + s * 64 + r + 32 * g;
 }
 
 __global__ void __launch_bounds__(256)
@@ -77,7 +80,7 @@ sae_pack_kernel(const uint16_t* __restrict__ W, int32_t m, int32_t d, uint16_t* 
     if (q >= static_cast<int64_t>(m) * pieces_per_row) return;
     const int32_t j = static_cast<int32_t>(q / pieces_per_row);
     const int32_t i = static_cast<int32_t>(q % pieces_per_row) * 8;
-    reinterpret_cast<uint4*>(Wp)[packed_piece(j, i, d / kBK)] =
+    reinterpret_cast<uint4*>(Wp)[packed_piece(j, i, m / kBM)] =
         reinterpret_cast<const uint4*>(W)[q];
 }
 
@@ -88,12 +91,12 @@ sae_fold_kernel(const uint16_t* __restrict__ Wp, const uint16_t* __restrict__ b_
                 float* __restrict__ c_fold) {
     const int32_t j = blockIdx.x * 4 + threadIdx.x / kWave;
     if (j >= m) return;
-    const int32_t nK = d / kBK;
+    const int32_t n_mt = m / kBM;
     const uint4* P = reinterpret_cast<const uint4*>(Wp);
     const uint4* bd = reinterpret_cast<const uint4*>(b_dec);
     float acc = 0.0f;
     for (int32_t p = lane_id(); p < d / 8; p += kWave) {
-        const uint4 wv = P[packed_piece(j, p * 8, nK)], bv = bd[p];
+        const uint4 wv = P[packed_piece(j, p * 8, n_mt)], bv = bd[p];
         const uint32_t ww[4] = {wv.x, wv.y, wv.z, wv.w};
         const uint32_t bw[4] = {bv.x, bv.y, bv.z, bv.w};
 #pragma unroll
@@ -112,20 +115,32 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
                   const int32_t* __restrict__ app_count, const int32_t* __restrict__ tok_list,
                   const uint16_t* __restrict__ W, const float* __restrict__ c_fold,
                   int32_t n_mt, int32_t n_nt, float z_guess, int32_t lo_cnt, int32_t cap,
-                  float* __restrict__ cand_val, int32_t* __restrict__ cand_idx,
-                  int32_t* __restrict__ tile_cnt, float* __restrict__ tile_tau) {
+                  uint2* __restrict__ cand, int32_t* __restrict__ tile_cnt,
+                  float* __restrict__ tile_tau) {
     __shared__ uint4 xs[2][kBN * 8];          // 2 x 16 KiB token chunks
     __shared__ float red1[kEncWaves][kBN];    // per-wave partials of the epilogue
     __shared__ float red2[kEncWaves][kBN];
     __shared__ int cnt_s[kBN];
 
-    // XCD-aware tile order: slot L runs on XCD L % 8; give each XCD a
-    // contiguous range of tiles, token tile fastest.
+    // Tile order.  Few token tiles (decode): latent tile fastest, so the
+    // workgroups of the first token tile, the ones with live tokens, are
+    // dispatched first and spread over every CU (interleaving them with
+    // tiles past the live count would leave every other CU idle).  Many
+    // token tiles (prefill): XCD-aware, slot L runs on XCD L % 8 and each
+    // XCD takes a contiguous range of tiles with the token tile fastest, so
+    // the workgroups sharing a dictionary slice share that XCD's L2.
     const int L = blockIdx.x;
-    const int per_xcd = gridDim.x / 8;
-    const int u = (L % 8) * per_xcd + (L / 8);
-    const int nt = u % n_nt;
-    const int mt = u / n_nt;
+    int nt, mt;
+    if (n_nt <= kLatentFastTiles) {
+        nt = L / n_mt;
+        mt = L % n_mt;
+        if (nt >= n_nt) return;
+    } else {
+        const int per_xcd = gridDim.x / 8;
+        const int u = (L % 8) * per_xcd + (L / 8);
+        nt = u % n_nt;
+        mt = u / n_nt;
+    }
     if (mt >= n_mt) return;
     const int cnt = *app_count;
     const int n0 = nt * kBN;
@@ -138,8 +153,9 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     const int nK = d / kBK;  // a multiple of 4 (d % 256 == 0)
 
     // operand A: this wave's 32 latents of the packed slice
-    const uint4* wbase = reinterpret_cast<const uint4*>(W) +
-                         static_cast<int64_t>(mt) * nK * 2048 + wave * 256 + lane;
+    const uint4* wbase = reinterpret_cast<const uint4*>(W) + static_cast<int64_t>(mt) * 2048 +
+                         wave * 256 + lane;
+    const int64_t wstride = static_cast<int64_t>(n_mt) * 2048;  // pieces per K chunk
 
     // operand B: gathered token rows; padding rows read a valid row and are
     // zeroed when written to LDS
@@ -154,6 +170,14 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
         xrow[p] = h + static_cast<int64_t>(tok_list[n0 + (ok ? n : 0)]) * d + 8 * xc;
     }
 
+    // folded bias of this lane's 16 latents, fetched before the K loop
+    float cfv[16];
+    {
+        const float* cf = c_fold + mt * kBM + 32 * wave + 4 * g;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) cfv[r] = cf[8 * (r / 4) + (r % 4)];
+    }
+
     f32x16_t acc[4];
 #pragma unroll
     for (int b = 0; b < 4; ++b)
@@ -165,7 +189,7 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
 
     auto load_w = [&](uint4 (&a)[4], int kc) {
         kc = min(kc, nK - 1);  // past the end: re-read the last chunk, unused
-        const uint4* p = wbase + static_cast<int64_t>(kc) * 2048;
+        const uint4* p = wbase + kc * wstride;
 #pragma unroll
         for (int s = 0; s < 4; ++s) a[s] = p[s * 64];
     };
@@ -180,7 +204,7 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
             const int n = xr + 64 * p;
             const uint4 v = make_uint4(xv[p].x & xmask[p], xv[p].y & xmask[p],
                                        xv[p].z & xmask[p], xv[p].w & xmask[p]);
-            xs[buf][n * 8 + (xc ^ (n & 7))] = v;
+            xs[buf][n * 8 + (xc ^ ((n >> 1) & 7))] = v;
         }
     };
     auto compute = [&](const uint4 (&a)[4], int buf) {
@@ -192,7 +216,7 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
             for (int nb = 0; nb < 4; ++nb) {
                 const int n = 32 * nb + j32;
                 const int chunk = 4 * g + s;
-                bop[nb] = xs[buf][n * 8 + (chunk ^ (n & 7))];
+                bop[nb] = xs[buf][n * 8 + (chunk ^ ((n >> 1) & 7))];
             }
 #pragma unroll
             for (int nb = 0; nb < 4; ++nb)
@@ -231,12 +255,10 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     // acc[nb][r] holds latent 32*wave + 8*(r/4) + 4*g + r%4 of token
     // 32*nb + j32 (the 32x32 MFMA output layout).  Lanes j32 and j32 + 32 of
     // all eight waves together hold the 256 latents of one token.
-    const float* cf = c_fold + mt * kBM + 32 * wave + 4 * g;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-        const float c = cf[8 * (r / 4) + (r % 4)];
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb) acc[nb][r] += c;
+        for (int nb = 0; nb < 4; ++nb) acc[nb][r] += cfv[r];
     }
     // per-token mean and variance over the tile's 256 latents
 #pragma unroll
@@ -323,7 +345,8 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
                 if (bad[nb]) tau[nb] = hi_b[nb];
         }
     }
-    // emit every latent with pre >= tau
+    // emit every latent with pre >= tau: one LDS atomic per lane and token
+    // reserves the lane's slots, then (value, latent) pairs are stored
     __syncthreads();
     if (tid < kBN) cnt_s[tid] = 0;
     __syncthreads();
@@ -332,13 +355,20 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
         const int n = 32 * nb + j32;
         if (n >= ntok) continue;
         const int64_t row = static_cast<int64_t>(n0 + n) * n_mt + mt;
+        int c = 0;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            if (acc[nb][r] >= tau[nb]) {
-                const int slot = atomicAdd(&cnt_s[n], 1);
-                if (slot < cap) {
-                    cand_val[row * cap + slot] = acc[nb][r];
-                    cand_idx[row * cap + slot] = mt * kBM + 32 * wave + 8 * (r / 4) + 4 * g + (r % 4);
+        for (int r = 0; r < 16; ++r) c += acc[nb][r] >= tau[nb] ? 1 : 0;
+        if (c > 0) {
+            int slot = atomicAdd(&cnt_s[n], c);
+            uint2* dst = cand + row * cap;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                if (acc[nb][r] >= tau[nb]) {
+                    if (slot < cap)
+                        dst[slot] = make_uint2(__float_as_uint(acc[nb][r]),
+                                               static_cast<uint32_t>(mt * kBM + 32 * wave +
+                                                                     8 * (r / 4) + 4 * g + (r % 4)));
+                    ++slot;
                 }
             }
         }
@@ -426,8 +456,7 @@ __device__ void block_compact(uint32_t* key, int32_t* idx, int n, uint32_t tau, 
 }
 
 __global__ void __launch_bounds__(kMergeThreads)
-sae_merge_kernel(const float* __restrict__ cand_val, const int32_t* __restrict__ cand_idx,
-                 const int32_t* __restrict__ tile_cnt, const float* __restrict__ tile_tau,
+sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ tile_cnt, const float* __restrict__ tile_tau,
                  int32_t n_mt, int32_t cap, const int32_t* __restrict__ app_count,
                  const int32_t* __restrict__ tok_list, int32_t k, const uint16_t* __restrict__ h,
                  int32_t d, const uint16_t* __restrict__ Wp, const float* __restrict__ c_fold,
@@ -479,8 +508,9 @@ sae_merge_kernel(const float* __restrict__ cand_val, const int32_t* __restrict__
             const int c = tile_cnt[row0 + tl];
             const int64_t off = (row0 + tl) * cap;
             for (int q = 0; q < c; ++q) {
-                pkey[pos + q] = f32_key(cand_val[off + q]);
-                pidx[pos + q] = cand_idx[off + q];
+                const uint2 e = cand[off + q];
+                pkey[pos + q] = f32_key(__uint_as_float(e.x));
+                pidx[pos + q] = static_cast<int32_t>(e.y);
             }
             pos += c;
         }
@@ -502,7 +532,6 @@ sae_merge_kernel(const float* __restrict__ cand_val, const int32_t* __restrict__
     } else {
         // exact recompute of this token's m pre-activations, 256 at a time,
         // keeping the k best in pkey/pidx[0..k)
-        const int nK = d / kBK;
         const uint4* hr = reinterpret_cast<const uint4*>(h + static_cast<int64_t>(t) * d);
         const uint4* P = reinterpret_cast<const uint4*>(Wp);
         int held = 0;
@@ -510,7 +539,7 @@ sae_merge_kernel(const float* __restrict__ cand_val, const int32_t* __restrict__
             const int32_t j = b * kBM + tid;
             float acc = 0.0f;
             for (int32_t p = 0; p < d / 8; ++p) {
-                const uint4 wv = P[packed_piece(j, p * 8, nK)], hv = hr[p];
+                const uint4 wv = P[packed_piece(j, p * 8, n_mt)], hv = hr[p];
                 const uint32_t ww[4] = {wv.x, wv.y, wv.z, wv.w};
                 const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w};
 #pragma unroll
@@ -592,18 +621,16 @@ static EmitPlan emit_plan(int32_t m, int32_t k) {
 }
 
 struct CandArea {
-    float* val;
-    int32_t* idx;
-    int32_t* cnt;
-    float* tau;
+    uint2* cand;   // (fp32 bits, latent) pairs, [T_max][n_mt][cap]
+    int32_t* cnt;  // [T_max][n_mt]
+    float* tau;    // [T_max][n_mt]
 };
 
-static CandArea cand_area(void* cand, int32_t T_max, int32_t n_mt, int cap) {
+static CandArea cand_area(void* base, int32_t T_max, int32_t n_mt, int cap) {
     const size_t slots = static_cast<size_t>(T_max) * n_mt;
     CandArea a;
-    a.val = static_cast<float*>(cand);
-    a.idx = reinterpret_cast<int32_t*>(a.val + slots * cap);
-    a.cnt = a.idx + slots * cap;
+    a.cand = static_cast<uint2*>(base);
+    a.cnt = reinterpret_cast<int32_t*>(a.cand + slots * cap);
     a.tau = reinterpret_cast<float*>(a.cnt + slots);
     return a;
 }
@@ -639,7 +666,7 @@ hipError_t launch_sae_candidates(const uint16_t* h, int32_t d, int32_t T_max,
     const CandArea a = cand_area(cand, T_max, n_mt, e.cap);
     hipLaunchKernelGGL(sae_stream_kernel, dim3(enc_grid(n_mt, n_nt)), dim3(kEncThreads), 0,
                        stream, h, d, app_count, tok_list, W_enc, c_fold, n_mt, n_nt, e.z, e.lo,
-                       e.cap, a.val, a.idx, a.cnt, a.tau);
+                       e.cap, a.cand, a.cnt, a.tau);
     return hipGetLastError();
 }
 
@@ -651,8 +678,8 @@ hipError_t launch_sae_merge(const uint16_t* h, int32_t d, int32_t T_max,
     const int32_t n_mt = m / kBM;
     const EmitPlan e = emit_plan(m, k);
     const CandArea a = cand_area(cand, T_max, n_mt, e.cap);
-    hipLaunchKernelGGL(sae_merge_kernel, dim3(T_max), dim3(kMergeThreads), 0, stream, a.val,
-                       a.idx, a.cnt, a.tau, n_mt, e.cap, app_count, tok_list, k, h, d, W_enc,
+    hipLaunchKernelGGL(sae_merge_kernel, dim3(T_max), dim3(kMergeThreads), 0, stream, a.cand,
+                       a.cnt, a.tau, n_mt, e.cap, app_count, tok_list, k, h, d, W_enc,
                        c_fold, idx_out, val_out);
     return hipGetLastError();
 }
