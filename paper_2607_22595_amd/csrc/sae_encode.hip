@@ -46,9 +46,6 @@ constexpr int kBN = 128;  // tokens per workgroup
 constexpr int kBK = 64;   // K chunk
 constexpr int kEncWaves = 8;
 constexpr int kEncThreads = kEncWaves * kWave;
-constexpr int kMergeThreads = 256;
-constexpr int kMaxTopK = 64;    // largest k
-constexpr int kPoolMax = 8192;   // merge pool entries (LDS)
 constexpr int kRefineIters = 24;
 constexpr int kLatentFastTiles = 4;  // token tiles up to which the latent tile runs fastest
 
@@ -379,31 +376,40 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
 }
 
 // ------------------------------------------------------------- final merge
-__device__ __forceinline__ int block_sum(int v, int* red) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
-    __syncthreads();
-    if (lane_id() == 0) red[threadIdx.x / kWave] = v;
-    __syncthreads();
-    int tot = 0;
-#pragma unroll
-    for (int w = 0; w < kMergeThreads / kWave; ++w) tot += red[w];
-    return tot;
+// Keys are order-preserving integer images of the fp32 values and the
+// selection order is (key descending, latent ascending).
+
+// Makes this wave's LDS writes visible to its other lanes.
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Selects the k best entries (key descending, index ascending) of
-// key[0..n) / idx[0..n) in LDS.  On return the selection is
+__device__ __forceinline__ int wave_count(bool p) { return __popcll(wave_ballot(p)); }
+
+// Selects the k best of the pool key[0..n) / idx[0..n) (this wave's LDS
+// region, n <= 64 * R).  On return the selection is
 //   { i : key[i] > tau  or  (key[i] == tau and idx[i] <= cut) }
-// and holds exactly k entries (indices are distinct).  Requires n >= k.
-__device__ void block_select(const uint32_t* key, const int32_t* idx, int n, int k, int* red,
-                             uint32_t* tau_out, int32_t* cut_out) {
+// with exactly k entries.  Requires n >= k.  Counts are ballot popcounts
+// (no cross-lane shuffles), R per bisection step.
+template <int R>
+__device__ void wave_select(const uint32_t* key, const int32_t* idx, int n, int k,
+                            uint32_t* tau_out, int32_t* cut_out) {
+    const int lane = lane_id();
+    uint32_t kr[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int i = lane + kWave * r;
+        kr[r] = i < n ? key[i] : 0u;  // real keys are >= 1; 0 never counts
+    }
     uint32_t tau = 0;
     bool exact = false;
     for (int bit = 31; bit >= 0; --bit) {
         const uint32_t c = tau | (1u << bit);
         int ge = 0;
-        for (int i = threadIdx.x; i < n; i += kMergeThreads) ge += key[i] >= c ? 1 : 0;
-        ge = block_sum(ge, red);
+#pragma unroll
+        for (int r = 0; r < R; ++r) ge += wave_count(kr[r] >= c);
         if (ge >= k) {
             tau = c;
             if (ge == k) {  // the k best are exactly the keys >= c
@@ -415,22 +421,27 @@ __device__ void block_select(const uint32_t* key, const int32_t* idx, int n, int
     int32_t cut = 0x7FFFFFFF;
     if (!exact) {
         int gt = 0, eq = 0;
-        for (int i = threadIdx.x; i < n; i += kMergeThreads) {
-            gt += key[i] > tau ? 1 : 0;
-            eq += key[i] == tau ? 1 : 0;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            gt += wave_count(kr[r] > tau);
+            eq += wave_count(kr[r] == tau);
         }
-        gt = block_sum(gt, red);
-        eq = block_sum(eq, red);
         const int need = k - gt;
         if (eq > need) {
             // smallest I with #{key == tau and idx <= I} >= need
+            int32_t ir[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const int i = lane + kWave * r;
+                ir[r] = i < n ? idx[i] : 0;
+            }
             int32_t lo = 0;
             for (int bit = 30; bit >= 0; --bit) {
                 const int32_t probe = lo | ((1 << bit) - 1);
                 int c = 0;
-                for (int i = threadIdx.x; i < n; i += kMergeThreads)
-                    c += (key[i] == tau && idx[i] <= probe) ? 1 : 0;
-                if (block_sum(c, red) < need) lo |= (1 << bit);
+#pragma unroll
+                for (int r = 0; r < R; ++r) c += wave_count(kr[r] == tau && ir[r] <= probe);
+                if (c < need) lo |= (1 << bit);
             }
             cut = lo;
         }
@@ -439,104 +450,176 @@ __device__ void block_select(const uint32_t* key, const int32_t* idx, int n, int
     *cut_out = cut;
 }
 
-// Moves the selected entries of key/idx[0..n) to positions [dst, dst + k).
-__device__ void block_compact(uint32_t* key, int32_t* idx, int n, uint32_t tau, int32_t cut,
-                              int dst, int* slot_ctr) {
-    if (threadIdx.x == 0) *slot_ctr = 0;
-    __syncthreads();
-    for (int i = threadIdx.x; i < n; i += kMergeThreads) {
-        const bool take = key[i] > tau || (key[i] == tau && idx[i] <= cut);
+// Moves the selected entries of the pool to lanes 0..k-1 (returned in
+// wk/wi; other lanes get key 0), in a fixed order (pool position).
+template <int R>
+__device__ void wave_take(const uint32_t* key, const int32_t* idx, int n, uint32_t tau,
+                          int32_t cut, uint32_t* stage_k, int32_t* stage_i, uint32_t* wk,
+                          int32_t* wi) {
+    const int lane = lane_id();
+    int base = 0;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int i = lane + kWave * r;
+        const uint32_t kv = i < n ? key[i] : 0u;
+        const int32_t iv = i < n ? idx[i] : 0;
+        const bool take = i < n && (kv > tau || (kv == tau && iv <= cut));
+        const uint64_t b = wave_ballot(take);
         if (take) {
-            const int s = atomicAdd(slot_ctr, 1);
-            key[dst + s] = key[i];
-            idx[dst + s] = idx[i];
+            stage_k[base + lanes_below(b)] = kv;
+            stage_i[base + lanes_below(b)] = iv;
         }
+        base += __popcll(b);
     }
-    __syncthreads();
+    wave_sync();
+    *wk = lane < base ? stage_k[lane] : 0u;
+    *wi = lane < base ? stage_i[lane] : 0x7FFFFFFF;
 }
 
-__global__ void __launch_bounds__(kMergeThreads)
-sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ tile_cnt, const float* __restrict__ tile_tau,
-                 int32_t n_mt, int32_t cap, const int32_t* __restrict__ app_count,
-                 const int32_t* __restrict__ tok_list, int32_t k, const uint16_t* __restrict__ h,
-                 int32_t d, const uint16_t* __restrict__ Wp, const float* __restrict__ c_fold,
-                 int32_t* __restrict__ idx_out, uint16_t* __restrict__ val_out) {
-    // pool entries, plus room to compact the k winners behind them
-    __shared__ uint32_t pkey[kPoolMax + kMaxTopK];
-    __shared__ int32_t pidx[kPoolMax + kMaxTopK];
-    __shared__ int red[kMergeThreads / kWave];
-    __shared__ int scan_s[kMergeThreads / kWave];
-    __shared__ int ctr;
+// Sorts one (key, latent) pair per lane across the wave: key descending,
+// latent ascending (bitonic network over shuffles).
+__device__ __forceinline__ void wave_sort_desc(uint32_t& key, int32_t& idx) {
+    const int lane = lane_id();
+#pragma unroll
+    for (int size = 2; size <= kWave; size <<= 1) {
+#pragma unroll
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            const uint32_t ok = static_cast<uint32_t>(__shfl_xor(static_cast<int>(key), stride, kWave));
+            const int32_t oi = __shfl_xor(idx, stride, kWave);
+            const bool mine_better = key > ok || (key == ok && idx < oi);
+            const bool first_half = (lane & stride) == 0;
+            const bool descending = (lane & size) == 0;
+            const bool keep_better = first_half == descending;
+            if (keep_better != mine_better) {
+                key = ok;
+                idx = oi;
+            }
+        }
+    }
+}
 
+constexpr int kMergeThreads = 256;
+constexpr int kMergeR = 32;                        // pool entries per lane
+constexpr int kPoolMax = kMergeR * kWave;          // 2048
+
+// One workgroup per subscribed token.  Every thread gathers the candidates
+// of the slices it owns (count, threshold and the slice's pair block are
+// loaded together, so the gather costs one memory round trip), a prefix
+// over the workgroup places them in an LDS pool, and wave 0 selects, checks
+// the certificate, sorts and writes; the other waves then leave.
+__global__ void __launch_bounds__(kMergeThreads)
+sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ tile_cnt,
+                 const float* __restrict__ tile_tau, int32_t n_mt, int32_t cap,
+                 const int32_t* __restrict__ app_count, const int32_t* __restrict__ tok_list,
+                 int32_t k, const uint16_t* __restrict__ h, int32_t d,
+                 const uint16_t* __restrict__ Wp, const float* __restrict__ c_fold,
+                 int32_t* __restrict__ idx_out, uint16_t* __restrict__ val_out) {
+    __shared__ uint32_t K[kPoolMax + kWave];
+    __shared__ int32_t I[kPoolMax + kWave];
+    __shared__ int scan_s[kMergeThreads / kWave];
+    __shared__ uint32_t tmax_s[kMergeThreads / kWave];
+    const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
     const int n = blockIdx.x;
-    if (n >= *app_count) return;
+    if (n >= *app_count) return;  // uniform over the workgroup
     const int32_t t = tok_list[n];
-    const int tid = threadIdx.x;
     const int64_t row0 = static_cast<int64_t>(n) * n_mt;
 
-    // pool gather: thread-exclusive prefix of the tile counts it owns
-    int mine = 0;
-    uint32_t tau_max = 0;
-    for (int tl = tid; tl < n_mt; tl += kMergeThreads) {
-        mine += tile_cnt[row0 + tl];
-        tau_max = max(tau_max, f32_key(tile_tau[row0 + tl]));
-    }
-    int incl = mine;
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        const int y = __shfl_up(incl, off, kWave);
-        if (lane_id() >= off) incl += y;
-    }
-    if (lane_id() == kWave - 1) scan_s[tid / kWave] = incl;
-    uint32_t tm = tau_max;
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) tm = max(tm, static_cast<uint32_t>(__shfl_xor(tm, off, kWave)));
-    if (lane_id() == 0) red[tid / kWave] = static_cast<int>(tm);
-    __syncthreads();
-    int base = 0, total = 0;
+    int total = 0;
     uint32_t tau_tiles = 0;
+    for (int t0 = 0; t0 < n_mt; t0 += kMergeThreads) {
+        const int tl = t0 + tid;
+        const bool own = tl < n_mt;
+        const int64_t row = row0 + (own ? tl : 0);
+        // count, threshold and the first 16 pairs of the slice, in one round
+        const uint4* src = reinterpret_cast<const uint4*>(cand + row * cap);
+        const int last = cap / 2 - 1;
+        uint4 v[8];
 #pragma unroll
-    for (int w = 0; w < kMergeThreads / kWave; ++w) {
-        base += (w < tid / kWave) ? scan_s[w] : 0;
-        total += scan_s[w];
-        tau_tiles = max(tau_tiles, static_cast<uint32_t>(red[w]));
-    }
-    int pos = base + incl - mine;
-    const bool fits = total <= kPoolMax;
-    if (fits) {
-        for (int tl = tid; tl < n_mt; tl += kMergeThreads) {
-            const int c = tile_cnt[row0 + tl];
-            const int64_t off = (row0 + tl) * cap;
-            for (int q = 0; q < c; ++q) {
-                const uint2 e = cand[off + q];
-                pkey[pos + q] = f32_key(__uint_as_float(e.x));
-                pidx[pos + q] = static_cast<int32_t>(e.y);
+        for (int u = 0; u < 8; ++u) v[u] = src[min(u, last)];
+        const int c = own ? tile_cnt[row] : 0;
+        const uint32_t tk = own ? f32_key(tile_tau[row]) : 0u;
+        // workgroup prefix of the counts
+        int incl = c;
+#pragma unroll
+        for (int off = 1; off < kWave; off <<= 1) {
+            const int y = __shfl_up(incl, off, kWave);
+            if (lane >= off) incl += y;
+        }
+        uint32_t tm = tk;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1)
+            tm = max(tm, static_cast<uint32_t>(__shfl_xor(static_cast<int>(tm), off, kWave)));
+        __syncthreads();  // scan_s / tmax_s reuse
+        if (lane == kWave - 1) scan_s[wave] = incl;
+        if (lane == 0) tmax_s[wave] = tm;
+        __syncthreads();
+        int base = total, round = 0;
+#pragma unroll
+        for (int w = 0; w < kMergeThreads / kWave; ++w) {
+            base += (w < wave) ? scan_s[w] : 0;
+            round += scan_s[w];
+            tau_tiles = max(tau_tiles, tmax_s[w]);
+        }
+        const int pos = base + incl - c;
+        const int end = total + round;
+        total = end;
+        if (end > kPoolMax) continue;  // uniform: the pool overflows, recompute below
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int q = 2 * u;
+            if (q < c) {
+                K[pos + q] = f32_key(__uint_as_float(v[u].x));
+                I[pos + q] = static_cast<int32_t>(v[u].y);
             }
-            pos += c;
+            if (q + 1 < c) {
+                K[pos + q + 1] = f32_key(__uint_as_float(v[u].z));
+                I[pos + q + 1] = static_cast<int32_t>(v[u].w);
+            }
+        }
+        // slices with more than 16 candidates (rare): the rest of the block
+        for (int q0 = 16; q0 < c; q0 += 16) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = src[min(q0 / 2 + u, last)];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int q = q0 + 2 * u;
+                if (q < c) {
+                    K[pos + q] = f32_key(__uint_as_float(v[u].x));
+                    I[pos + q] = static_cast<int32_t>(v[u].y);
+                }
+                if (q + 1 < c) {
+                    K[pos + q + 1] = f32_key(__uint_as_float(v[u].z));
+                    I[pos + q + 1] = static_cast<int32_t>(v[u].w);
+                }
+            }
         }
     }
     __syncthreads();
+    if (wave != 0) return;
 
-    bool exact_path = fits && total >= k;
-    uint32_t tau = 0;
-    int32_t cut = 0;
+    uint32_t wk = 0;
+    int32_t wi = 0x7FFFFFFF;
+    bool exact_path = total <= kPoolMax && total >= k;
     if (exact_path) {
-        block_select(pkey, pidx, total, k, red, &tau, &cut);
-        // certificate: nothing left below a tile threshold can beat tau
+        uint32_t tau;
+        int32_t cut;
+        // register footprint matched to the pool size
+        if (total <= 4 * kWave) wave_select<4>(K, I, total, k, &tau, &cut);
+        else if (total <= 8 * kWave) wave_select<8>(K, I, total, k, &tau, &cut);
+        else if (total <= 16 * kWave) wave_select<16>(K, I, total, k, &tau, &cut);
+        else wave_select<kMergeR>(K, I, total, k, &tau, &cut);
+        // certificate: nothing left below a slice threshold can beat tau
         exact_path = tau_tiles <= tau;
+        if (exact_path) wave_take<kMergeR>(K, I, total, tau, cut, K + kPoolMax, I + kPoolMax, &wk, &wi);
     }
-    int win = 0;  // the k winners end up in pkey/pidx[win .. win + k)
-    if (exact_path) {
-        block_compact(pkey, pidx, total, tau, cut, total, &ctr);
-        win = total;
-    } else {
-        // exact recompute of this token's m pre-activations, 256 at a time,
-        // keeping the k best in pkey/pidx[0..k)
+    if (!exact_path) {
+        // exact recompute of this token's m pre-activations, one latent per
+        // lane per round, keeping the k best in LDS [0, k)
         const uint4* hr = reinterpret_cast<const uint4*>(h + static_cast<int64_t>(t) * d);
         const uint4* P = reinterpret_cast<const uint4*>(Wp);
         int held = 0;
-        for (int b = 0; b < n_mt; ++b) {
-            const int32_t j = b * kBM + tid;
+        for (int j0 = 0; j0 < n_mt * kBM; j0 += kWave) {
+            const int32_t j = j0 + lane;
             float acc = 0.0f;
             for (int32_t p = 0; p < d / 8; ++p) {
                 const uint4 wv = P[packed_piece(j, p * 8, n_mt)], hv = hr[p];
@@ -548,38 +631,36 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
                     acc = fmaf(hi_bf16(ww[e]), hi_bf16(hw[e]), acc);
                 }
             }
-            pkey[held + tid] = f32_key(acc + c_fold[j]);
-            pidx[held + tid] = j;
-            __syncthreads();
-            const int n_pool = held + kBM;
-            if (n_pool <= k) {
+            K[held + lane] = f32_key(acc + c_fold[j]);
+            I[held + lane] = j;
+            wave_sync();
+            const int n_pool = held + kWave;
+            if (n_pool > k) {
+                uint32_t tb;
+                int32_t cb;
+                wave_select<2>(K, I, n_pool, k, &tb, &cb);
+                uint32_t a;
+                int32_t b;
+                wave_take<2>(K, I, n_pool, tb, cb, K + 2 * kWave, I + 2 * kWave, &a, &b);
+                if (lane < k) {
+                    K[lane] = a;
+                    I[lane] = b;
+                }
+                wave_sync();
+                held = k;
+            } else {
                 held = n_pool;
-                continue;
             }
-            uint32_t tb;
-            int32_t cb;
-            block_select(pkey, pidx, n_pool, k, red, &tb, &cb);
-            block_compact(pkey, pidx, n_pool, tb, cb, n_pool, &ctr);
-            for (int i = tid; i < k; i += kMergeThreads) {
-                pkey[i] = pkey[n_pool + i];
-                pidx[i] = pidx[n_pool + i];
-            }
-            __syncthreads();
-            held = k;
         }
+        wk = lane < k ? K[lane] : 0u;
+        wi = lane < k ? I[lane] : 0x7FFFFFFF;
     }
-    // rank the k winners by (value desc, index asc)
-    if (tid < k) {
-        const uint32_t kq = pkey[win + tid];
-        const int32_t iq = pidx[win + tid];
-        int rank = 0;
-        for (int q = 0; q < k; ++q) {
-            const uint32_t kj = pkey[win + q];
-            rank += (kj > kq || (kj == kq && pidx[win + q] < iq)) ? 1 : 0;
-        }
-        const int64_t o = static_cast<int64_t>(t) * k + rank;
-        idx_out[o] = iq;
-        val_out[o] = f32_to_bf16_rne(fmaxf(key_f32(kq), 0.0f));
+    // order the k winners by (value desc, index asc) and write them
+    wave_sort_desc(wk, wi);
+    if (lane < k) {
+        const int64_t o = static_cast<int64_t>(t) * k + lane;
+        idx_out[o] = wi;
+        val_out[o] = f32_to_bf16_rne(fmaxf(key_f32(wk), 0.0f));
     }
 }
 
@@ -602,8 +683,8 @@ struct EmitPlan {
 static EmitPlan emit_plan(int32_t m, int32_t k) {
     const int n_mt = m / kBM;
     EmitPlan e;
-    e.target = (2 * k * kBM + m - 1) / m + 4;
-    e.target = e.target < 8 ? 8 : (e.target > 64 ? 64 : e.target);
+    e.target = (2 * k * kBM + m - 1) / m + 1;
+    e.target = e.target < 2 ? 2 : (e.target > 64 ? 64 : e.target);
     e.cap = 4 * e.target;
     e.cap = e.cap < 16 ? 16 : (e.cap > 64 ? 64 : e.cap);
     e.lo = (n_mt * e.target >= 4 * k) ? 0 : (k < e.cap ? k : e.cap);
