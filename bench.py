@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run three device copies of 512 MiB, the known-size reference "
+                         "for scaling HBM counter readings")
     return ap.parse_args()
 
 
@@ -164,6 +167,13 @@ def main():
     from paper_2607_22595_amd.hookstep import HookStep
 
     torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        src = torch.empty(512 * 2 ** 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     out = {}
     if not args.no_decode:
         out, wl = run_decode(torch, px, synth, HookStep, args)

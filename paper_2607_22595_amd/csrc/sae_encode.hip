@@ -48,6 +48,8 @@ constexpr int kEncWaves = 8;
 constexpr int kEncThreads = kEncWaves * kWave;
 constexpr int kRefineIters = 24;
 constexpr int kLatentFastTiles = 4;  // token tiles up to which the latent tile runs fastest
+constexpr int kBlkTok = 8;           // prefill block: token tiles
+constexpr int kBlkLat = 4;           // prefill block: latent tiles
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& v) {
     return __builtin_bit_cast(bf16x8_t, v);
@@ -122,10 +124,14 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     // Tile order.  Few token tiles (decode): latent tile fastest, so the
     // workgroups of the first token tile, the ones with live tokens, are
     // dispatched first and spread over every CU (interleaving them with
-    // tiles past the live count would leave every other CU idle).  Many
-    // token tiles (prefill): XCD-aware, slot L runs on XCD L % 8 and each
-    // XCD takes a contiguous range of tiles with the token tile fastest, so
-    // the workgroups sharing a dictionary slice share that XCD's L2.
+    // tiles past the live count would leave every other CU idle).
+    // Many token tiles (prefill): launch slot L runs on XCD L % 8; XCD x
+    // owns the latent tiles [x*M8, (x+1)*M8) and walks them in blocks of 8
+    // token tiles x 4 latent tiles, 32 consecutive slots per block, token
+    // blocks fastest.  The 32 workgroups of a block run together on the
+    // XCD's 32 CUs, so each K chunk of 8 token tiles and 4 dictionary
+    // slices is fetched into the XCD's L2 once and read by 4 and 8
+    // workgroups; consecutive blocks reuse the same 4 slices.
     const int L = blockIdx.x;
     int nt, mt;
     if (n_nt <= kLatentFastTiles) {
@@ -133,10 +139,15 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
         mt = L % n_mt;
         if (nt >= n_nt) return;
     } else {
-        const int per_xcd = gridDim.x / 8;
-        const int u = (L % 8) * per_xcd + (L / 8);
-        nt = u % n_nt;
-        mt = u / n_nt;
+        const int xcd = L % 8, slot = L / 8;
+        const int m8 = (n_mt + 7) / 8;              // latent tiles per XCD
+        const int nbt = (n_nt + kBlkTok - 1) / kBlkTok;
+        const int b = slot / (kBlkTok * kBlkLat), p = slot % (kBlkTok * kBlkLat);
+        const int bt = b % nbt, bl = b / nbt;
+        const int lt = kBlkLat * bl + p / kBlkTok;
+        nt = kBlkTok * bt + p % kBlkTok;
+        if (nt >= n_nt || lt >= m8) return;
+        mt = xcd * m8 + lt;
     }
     if (mt >= n_mt) return;
     const int cnt = *app_count;
@@ -666,8 +677,11 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
 
 // ------------------------------------------------------------------ launch
 static int enc_grid(int32_t n_mt, int32_t n_nt) {
-    const int tiles = n_mt * n_nt;
-    return (tiles + 7) / 8 * 8;
+    if (n_nt <= kLatentFastTiles) return n_mt * n_nt;
+    const int m8 = (n_mt + 7) / 8;
+    const int nbt = (n_nt + kBlkTok - 1) / kBlkTok;
+    const int nbl = (m8 + kBlkLat - 1) / kBlkLat;
+    return 8 * nbt * nbl * kBlkTok * kBlkLat;
 }
 
 // Candidate emission parameters for a dictionary of m latents and top-k:
