@@ -103,11 +103,11 @@ xmix_status xmix_probe_score(const void* h, xmix_dtype dt, int32_t d, const xmix
 }
 
 size_t xmix_sae_encode_workspace(int32_t T_max, int32_t d, int32_t m, int32_t k) {
-    (void)d;
-    if (T_max < 1 || m < 256 || k < 1) return 0;
+    if (T_max < 1 || d < 1 || m < 256 || k < 1) return 0;
     // folded bias (used when the caller passes none), then the candidates
+    // (and, for many token slots, the staged token rows)
     const size_t fold = (static_cast<size_t>(m) * sizeof(float) + 255u) / 256u * 256u;
-    return fold + sae_candidate_bytes(T_max, m, k);
+    return fold + sae_candidate_bytes(T_max, d, m, k);
 }
 
 xmix_status xmix_sae_pack_encoder(const uint16_t* W_enc, int32_t m, int32_t d,

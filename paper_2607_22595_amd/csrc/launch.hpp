@@ -26,7 +26,7 @@ hipError_t launch_probe(const void* h, bool bf16, int32_t d, int32_t T_max,
                         const int32_t* cu_seqlens, int32_t R_max, float* logit, float* score,
                         float* ws, hipStream_t stream);
 
-size_t sae_candidate_bytes(int32_t T_max, int32_t m, int32_t k);
+size_t sae_candidate_bytes(int32_t T_max, int32_t d, int32_t m, int32_t k);
 hipError_t launch_sae_pack(const uint16_t* W_enc, int32_t m, int32_t d, uint16_t* W_packed,
                            hipStream_t stream);
 hipError_t launch_sae_fold(const uint16_t* W_enc, const uint16_t* b_enc, const uint16_t* b_dec,

@@ -56,19 +56,21 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& v) {
 }
 
 // ------------------------------------------------------- dictionary layout
-// W_enc is kept in HBM in a tiled layout matched to the encode GEMM, built
+// W_enc is kept in HBM in a tiled layout matched to the encode GEMMs, built
 // once when an SAE app is loaded.  The unit is a 16-byte piece (8 bf16 of
 // one latent row).  Latent j = 256*mt + 32*w + r and row element
-// i = 64*kc + 32*g + 8*s + e (e < 8) live in piece
+// i = 64*kc + 16*s + 8*g + e (e < 8) live in piece
 //     (kc*n_mt + mt)*2048 + w*256 + s*64 + (r + 32*g)
-// so the 32 KB one workgroup needs per K chunk are contiguous, every
-// wave-wide 16-byte load is 1 KB contiguous, and at each K step the whole
-// grid streams one contiguous region (chunk-major order spreads concurrent
-// workgroups over all HBM channels instead of one stride class).
+// so the 32 KB of a 256-latent slice per K chunk of 64 are contiguous,
+// every wave-wide 16-byte load is 1 KB contiguous (the A operand of one
+// 32x32x16 MFMA step s: lane r + 32*g holds elements 16*s + 8*g .. + 7),
+// each half chunk (steps 0-1, steps 2-3) is 2 KB contiguous per 32
+// latents, and at each K step the whole grid streams one contiguous region
+// (chunk-major order spreads concurrent workgroups over all HBM channels).
 __device__ __forceinline__ int64_t packed_piece(int32_t j, int32_t i, int32_t n_mt) {
     const int32_t mt = j >> 8, jr = j & 255;
     const int32_t w = jr >> 5, r = jr & 31;
-    const int32_t kc = i >> 6, g = (i >> 5) & 1, s = (i >> 3) & 3;
+    const int32_t kc = i >> 6, s = (i >> 4) & 3, g = (i >> 3) & 1;
     return (static_cast<int64_t>(kc) * n_mt + mt) * 2048 + w * 256 + s * 64 + r + 32 * g;
 }
 
@@ -223,7 +225,7 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
 #pragma unroll
             for (int nb = 0; nb < 4; ++nb) {
                 const int n = 32 * nb + j32;
-                const int chunk = 4 * g + s;
+                const int chunk = 2 * s + g;
                 bop[nb] = xs[buf][n * 8 + (chunk ^ ((n >> 1) & 7))];
             }
 #pragma unroll
@@ -381,6 +383,305 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
             }
         }
         if (wave == 0 && g == 0) tile_tau[row] = tau[nb];
+    }
+    __syncthreads();
+    if (tid < ntok) tile_cnt[static_cast<int64_t>(n0 + tid) * n_mt + mt] = min(cnt_s[tid], cap);
+}
+
+// ------------------------------------------ prefill GEMM + candidate emission
+// Many subscribed tokens make the encode MFMA-bound.  The token rows are
+// first gathered into a staged layout (sae_xstage_kernel): plane j holds
+// elements [32j, 32j+32) of every listed token, 64 contiguous bytes per
+// token, zero past the subscribed count.  sae_gemm_kernel then runs 4 waves
+// (one per SIMD) on a 256-latent x 256-token tile, each wave a 128 x 128
+// quarter held in 256 accumulator registers.  Both operands of each K
+// stage of 32 (a 16 KB dictionary half chunk, 2 KB contiguous per 32
+// latents, and a 16 KB token plane slice) are copied by the load unit
+// straight into LDS (global_load_lds, no register staging) into a ring of
+// 4 stages, three in flight.  Per stage a wave waits for its own copies of
+// the oldest stage, meets the others at a barrier, refills the stage freed
+// by the previous step, and runs 32 MFMAs whose operands come from LDS;
+// the operands of the stage's second step are read before the next barrier
+// and multiplied after it, so the matrix unit has work while the waves
+// meet.  The epilogue is the same threshold emission as the decode kernel,
+// per token over the tile's 256 latents.
+constexpr int kGemmThreads = 256;
+constexpr int kGemmTok = 256;       // tokens per tile
+constexpr int kStagePieces = 1024;  // 16-byte pieces per operand per stage
+constexpr int kPrefillMinT = 1025;  // token slots from which the prefill GEMM runs
+constexpr int kGBlkTok = 8;         // XCD block: token tiles
+constexpr int kGBlkLat = 4;         // XCD block: latent tiles
+
+// Stage-plane LDS swizzle: the 16-byte piece c of token n sits at
+// n*4 + (c ^ gsw(n)); with it the MFMA-layout reads of 16 tokens x 4
+// pieces hit distinct banks.
+__device__ __forceinline__ int gsw(int n) { return ((n >> 3) ^ (n >> 4)) & 3; }
+
+// s_waitcnt: at most n vector-memory operations of this wave outstanding
+// and no LDS operation.
+#define XMIX_WAIT_VM_LGKM0(n) \
+    __builtin_amdgcn_s_waitcnt(((n) & 15) | (7 << 4) | (((n) >> 4) << 14))
+
+__global__ void __launch_bounds__(256)
+sae_xstage_kernel(const uint16_t* __restrict__ h, int32_t d, const int32_t* __restrict__ app_count,
+                  const int32_t* __restrict__ tok_list, int32_t n_pad, uint16_t* __restrict__ xs) {
+    // one 16-byte piece per thread, output order (plane, token, piece)
+    const int64_t q = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    const int64_t total = static_cast<int64_t>(n_pad) * (d / 8);
+    if (q >= total) return;
+    const int32_t c = static_cast<int32_t>(q & 3);
+    const int64_t jn = q >> 2;
+    const int32_t n = static_cast<int32_t>(jn % n_pad);
+    const int32_t j = static_cast<int32_t>(jn / n_pad);
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (n < *app_count)
+        v = *reinterpret_cast<const uint4*>(h + static_cast<int64_t>(tok_list[n]) * d + 32 * j + 8 * c);
+    reinterpret_cast<uint4*>(xs)[q] = v;
+}
+
+__global__ void __launch_bounds__(kGemmThreads, 1)
+sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
+                const int32_t* __restrict__ app_count, const uint16_t* __restrict__ W,
+                const float* __restrict__ c_fold, int32_t n_mt, int32_t n_nt, float z_guess,
+                int32_t lo_cnt, int32_t cap, uint2* __restrict__ cand,
+                int32_t* __restrict__ tile_cnt, float* __restrict__ tile_tau) {
+    __shared__ uint4 wsA[kStagePieces], wsB[kStagePieces], wsC[kStagePieces], wsD[kStagePieces];
+    __shared__ uint4 xsA[kStagePieces], xsB[kStagePieces], xsC[kStagePieces], xsD[kStagePieces];
+    __shared__ float red1[2][kGemmTok];
+    __shared__ float red2[2][kGemmTok];
+    __shared__ int cnt_s[kGemmTok];
+
+    // Tile order: launch slot L runs on XCD L % 8, which owns the latent
+    // tiles [x*M8, (x+1)*M8) and walks them in blocks of 8 token tiles x 4
+    // latent tiles (32 consecutive slots, one per CU of the XCD), token
+    // blocks fastest, so each stage of a block's operands is fetched into
+    // the XCD's L2 once and read by 4 and 8 workgroups.
+    const int L = blockIdx.x;
+    const int xcd = L % 8, slot = L / 8;
+    const int m8 = (n_mt + 7) / 8;
+    const int nbt = (n_nt + kGBlkTok - 1) / kGBlkTok;
+    const int b = slot / (kGBlkTok * kGBlkLat), p = slot % (kGBlkTok * kGBlkLat);
+    const int bt = b % nbt, bl = b / nbt;
+    const int lt = kGBlkLat * bl + p / kGBlkTok;
+    const int nt = kGBlkTok * bt + p % kGBlkTok;
+    if (nt >= n_nt || lt >= m8) return;
+    const int mt = xcd * m8 + lt;
+    if (mt >= n_mt) return;
+    const int cnt = *app_count;
+    const int n0 = nt * kGemmTok;
+    if (n0 >= cnt) return;
+    const int ntok = min(kGemmTok, cnt - n0);
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave & 1, wn = wave >> 1;  // latent half, token half
+    const int g = lane >> 5, j32 = lane & 31;
+    const int nS = d / 32;                    // stages, a multiple of 8
+
+    const uint4* W4 = reinterpret_cast<const uint4*>(W);
+    const uint4* X4 = reinterpret_cast<const uint4*>(xs_g);
+    const int64_t wstride = static_cast<int64_t>(n_mt) * 2048;  // pieces per K chunk of 64
+    const int64_t xplane = static_cast<int64_t>(n_pad) * 4;     // pieces per stage plane
+    // copy sources: lane-contiguous LDS destinations q*256 + wave*64 + lane
+    int wsrc[4], xsrc[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int P = q * 256 + wave * 64 + lane;
+        wsrc[q] = mt * 2048 + (P >> 7) * 256 + (P & 127);
+        const int n = P >> 2;
+        xsrc[q] = (n0 + n) * 4 + ((P & 3) ^ gsw(n));
+    }
+    // issue the 8 copies of stage j (past the end: the last stage again, so
+    // every stage issues the same number of operations for the waits below)
+    auto copy_stage = [&](int j, uint4* wdst, uint4* xdst) __attribute__((always_inline)) {
+        j = min(j, nS - 1);
+        const int kc = j >> 1, hh = j & 1;
+        const uint4* wsrc_j = W4 + kc * wstride + hh * 128;
+        const uint4* xsrc_j = X4 + j * xplane;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            __builtin_amdgcn_global_load_lds(wsrc_j + wsrc[q], wdst + q * 256 + wave * 64, 16, 0, 0);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            __builtin_amdgcn_global_load_lds(xsrc_j + xsrc[q], xdst + q * 256 + wave * 64, 16, 0, 0);
+    };
+
+    f32x16_t acc[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[a][nb][r] = 0.0f;
+
+    uint4 FA[4], FB[4], PA[4], PB[4];
+    auto read_step = [&](const uint4* wb, const uint4* xb, int s, uint4 (&A)[4], uint4 (&B)[4])
+        __attribute__((always_inline)) {
+#pragma unroll
+        for (int a = 0; a < 4; ++a) A[a] = wb[(4 * wm + a) * 128 + s * 64 + lane];
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) {
+            const int n = 128 * wn + 32 * nb + j32;
+            B[nb] = xb[n * 4 + ((2 * s + g) ^ gsw(n))];
+        }
+    };
+    auto mfma_step = [&](const uint4 (&A)[4], const uint4 (&B)[4]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb)
+                acc[a][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(A[a]),
+                                                                     as_bf16x8(B[nb]), acc[a][nb],
+                                                                     0, 0, 0);
+    };
+    // One stage: wait for this wave's copies of stage j (two younger stages,
+    // 16 copies, may stay in flight) and its LDS reads, meet at the barrier
+    // (now every copy of stage j has landed and every wave is done with the
+    // buffer of stage j - 1), refill that buffer with stage j + 3, then read
+    // step 0, multiply the carried step of stage j - 1, read step 1 (carried
+    // across the next barrier), multiply step 0.
+    auto stage = [&](int j, const uint4* wb, const uint4* xb, uint4* wfree, uint4* xfree,
+                     bool first) __attribute__((always_inline)) {
+        XMIX_WAIT_VM_LGKM0(16);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        copy_stage(j + 3, wfree, xfree);
+        read_step(wb, xb, 0, FA, FB);
+        if (!first) mfma_step(PA, PB);
+        read_step(wb, xb, 1, PA, PB);
+        mfma_step(FA, FB);
+        // instruction order: step-0 reads, then the carried MFMAs with the
+        // copies between them, then step-0 MFMAs with the step-1 reads
+        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+        if (!first) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            }
+        } else {
+            __builtin_amdgcn_sched_group_barrier(0x020, 8, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+    };
+
+    copy_stage(0, wsA, xsA);
+    copy_stage(1, wsB, xsB);
+    copy_stage(2, wsC, xsC);
+    stage(0, wsA, xsA, wsD, xsD, true);
+    stage(1, wsB, xsB, wsA, xsA, false);
+    stage(2, wsC, xsC, wsB, xsB, false);
+    stage(3, wsD, xsD, wsC, xsC, false);
+    for (int j = 4; j < nS; j += 4) {
+        stage(j + 0, wsA, xsA, wsD, xsD, false);
+        stage(j + 1, wsB, xsB, wsA, xsA, false);
+        stage(j + 2, wsC, xsC, wsB, xsB, false);
+        stage(j + 3, wsD, xsD, wsC, xsC, false);
+    }
+    mfma_step(PA, PB);
+    XMIX_WAIT_VM_LGKM0(0);  // the trailing refills land before the workgroup ends
+
+    // ---------------------------------------------------------- epilogue
+    // acc[a][nb][r] holds latent 128*wm + 32*a + 8*(r/4) + 4*g + r%4 of
+    // token 128*wn + 32*nb + j32; lanes j32 and j32 + 32 of waves (0, wn)
+    // and (1, wn) together hold the 256 latents of one token.  The tokens of
+    // one nb are finished at a time, so only their 64 values per lane need
+    // vector registers.
+    cnt_s[tid] = 0;
+    const float* cf = c_fold + mt * 256 + 128 * wm + 4 * g;
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+        const int n = 128 * wn + 32 * nb + j32;
+        float v[64];
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float4 c4 = *reinterpret_cast<const float4*>(cf + 32 * a + 8 * q);
+                v[16 * a + 4 * q + 0] = acc[a][nb][4 * q + 0] + c4.x;
+                v[16 * a + 4 * q + 1] = acc[a][nb][4 * q + 1] + c4.y;
+                v[16 * a + 4 * q + 2] = acc[a][nb][4 * q + 2] + c4.z;
+                v[16 * a + 4 * q + 3] = acc[a][nb][4 * q + 3] + c4.w;
+            }
+        // mean and variance over the tile's 256 latents
+        float s1 = 0.0f, s2 = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 64; ++i) {
+            s1 += v[i];
+            s2 = fmaf(v[i], v[i], s2);
+        }
+        s1 += __shfl_xor(s1, 32, kWave);
+        s2 += __shfl_xor(s2, 32, kWave);
+        __syncthreads();  // red1/red2 are reused
+        if (g == 0) {
+            red1[wm][n] = s1;
+            red2[wm][n] = s2;
+        }
+        __syncthreads();
+        const float mu = (red1[0][n] + red1[1][n]) * (1.0f / 256.0f);
+        const float sd = sqrtf(fmaxf((red2[0][n] + red2[1][n]) * (1.0f / 256.0f) - mu * mu, 0.0f));
+        float tau = mu + z_guess * sd;
+        float lo_b = -INFINITY, hi_b = INFINITY;
+        // count(pre >= tau) per token; refine tau until lo_cnt <= count <= cap
+        for (int it = 0; it < kRefineIters; ++it) {
+            float c = 0.0f;
+#pragma unroll
+            for (int i = 0; i < 64; ++i) c += v[i] >= tau ? 1.0f : 0.0f;
+            c += __shfl_xor(c, 32, kWave);
+            __syncthreads();  // red1 is reused
+            if (g == 0) red1[wm][n] = c;
+            __syncthreads();
+            const int cn = static_cast<int>(red1[0][n] + red1[1][n]);
+            bool bad = false;
+            if (n < ntok) {
+                if (cn > cap) {
+                    lo_b = tau;
+                    bad = true;
+                } else if (cn < lo_cnt) {
+                    hi_b = tau;
+                    bad = true;
+                }
+            }
+            if (bad) {
+                if (isfinite(lo_b) && isfinite(hi_b)) {
+                    tau = 0.5f * (lo_b + hi_b);
+                } else {
+                    const float step = ldexpf(0.25f * (fabsf(tau) + 1.0f), it);
+                    tau = isfinite(hi_b) ? tau - step : tau + step;
+                }
+            }
+            if (!__syncthreads_or(bad)) break;
+            // out of iterations: a threshold whose count is known to be <= cap
+            if (it == kRefineIters - 1 && bad) tau = hi_b;
+        }
+        // emit every latent with pre >= tau
+        if (n < ntok) {
+            const int64_t row = static_cast<int64_t>(n0 + n) * n_mt + mt;
+            int c = 0;
+#pragma unroll
+            for (int i = 0; i < 64; ++i) c += v[i] >= tau ? 1 : 0;
+            if (c > 0) {
+                int slot = atomicAdd(&cnt_s[n], c);
+                uint2* dst = cand + row * cap;
+#pragma unroll
+                for (int i = 0; i < 64; ++i) {
+                    if (v[i] >= tau) {
+                        if (slot < cap)
+                            dst[slot] = make_uint2(
+                                __float_as_uint(v[i]),
+                                static_cast<uint32_t>(mt * 256 + 128 * wm + 32 * (i >> 4) +
+                                                      8 * ((i >> 2) & 3) + 4 * g + (i & 3)));
+                        ++slot;
+                    }
+                }
+            }
+            if (wm == 0 && g == 0) tile_tau[row] = tau;
+        }
     }
     __syncthreads();
     if (tid < ntok) tile_cnt[static_cast<int64_t>(n0 + tid) * n_mt + mt] = min(cnt_s[tid], cap);
@@ -730,10 +1031,21 @@ static CandArea cand_area(void* base, int32_t T_max, int32_t n_mt, int cap) {
     return a;
 }
 
-size_t sae_candidate_bytes(int32_t T_max, int32_t m, int32_t k) {
+static int32_t stage_tokens(int32_t T_max) {
+    return (T_max + kGemmTok - 1) / kGemmTok * kGemmTok;
+}
+
+static size_t candidate_bytes(int32_t T_max, int32_t m, int32_t k) {
     const EmitPlan e = emit_plan(m, k);
     const size_t slots = static_cast<size_t>(T_max) * (m / kBM);
     return slots * (static_cast<size_t>(e.cap) * 8u + 8u);
+}
+
+size_t sae_candidate_bytes(int32_t T_max, int32_t d, int32_t m, int32_t k) {
+    size_t bytes = (candidate_bytes(T_max, m, k) + 255u) / 256u * 256u;
+    if (T_max >= kPrefillMinT)  // staged token rows of the prefill GEMM
+        bytes += static_cast<size_t>(stage_tokens(T_max)) * d * sizeof(uint16_t);
+    return bytes;
 }
 
 hipError_t launch_sae_pack(const uint16_t* W_enc, int32_t m, int32_t d, uint16_t* W_packed,
@@ -756,9 +1068,25 @@ hipError_t launch_sae_candidates(const uint16_t* h, int32_t d, int32_t T_max,
                                  const uint16_t* W_enc, const float* c_fold, int32_t m,
                                  int32_t k, void* cand, hipStream_t stream) {
     const int32_t n_mt = m / kBM;
-    const int32_t n_nt = (T_max + kBN - 1) / kBN;
     const EmitPlan e = emit_plan(m, k);
     const CandArea a = cand_area(cand, T_max, n_mt, e.cap);
+    if (T_max >= kPrefillMinT) {
+        const int32_t n_pad = stage_tokens(T_max);
+        uint16_t* xs = reinterpret_cast<uint16_t*>(
+            static_cast<char*>(cand) + (candidate_bytes(T_max, m, k) + 255u) / 256u * 256u);
+        const int64_t pieces = static_cast<int64_t>(n_pad) * (d / 8);
+        hipLaunchKernelGGL(sae_xstage_kernel, dim3(static_cast<uint32_t>((pieces + 255) / 256)),
+                           dim3(256), 0, stream, h, d, app_count, tok_list, n_pad, xs);
+        const int32_t n_nt = n_pad / kGemmTok;
+        const int m8 = (n_mt + 7) / 8;
+        const int nbt = (n_nt + kGBlkTok - 1) / kGBlkTok;
+        const int nbl = (m8 + kGBlkLat - 1) / kGBlkLat;
+        hipLaunchKernelGGL(sae_gemm_kernel, dim3(8 * nbt * nbl * kGBlkTok * kGBlkLat),
+                           dim3(kGemmThreads), 0, stream, xs, d, n_pad, app_count, W_enc, c_fold,
+                           n_mt, n_nt, e.z, e.lo, e.cap, a.cand, a.cnt, a.tau);
+        return hipGetLastError();
+    }
+    const int32_t n_nt = (T_max + kBN - 1) / kBN;
     hipLaunchKernelGGL(sae_stream_kernel, dim3(enc_grid(n_mt, n_nt)), dim3(kEncThreads), 0,
                        stream, h, d, app_count, tok_list, W_enc, c_fold, n_mt, n_nt, e.z, e.lo,
                        e.cap, a.cand, a.cnt, a.tau);

@@ -241,6 +241,30 @@ def test_encode_all_tokens_many_token_tiles(px):
     _check_encode(wl, sae, wl.layers[0].h, idx, val, np.arange(300))
 
 
+@pytest.mark.parametrize("d,m,k,T,n_sub", [(256, 1024, 16, 1500, 1100), (512, 2048, 32, 2100, 2100),
+                                           (256, 2560, 64, 1025, 700)])
+def test_encode_prefill_gemm_path(px, d, m, k, T, n_sub):
+    """From 1025 token slots the encode stages the token rows and runs the
+    256 x 256-tile GEMM; ragged subscribed counts leave a partial last tile
+    and padded token planes."""
+    wl = synth.make("c3", d=d, m=m, k=k, T=T, n_sub=n_sub)
+    sae = wl.layers[0].saes[0]
+    rt, idx, val = _encode(px, wl, sae, wl.layers[0].h)
+    tm, cnt, lists, _ = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    toks = lists[0, :cnt[0]]
+    assert len(toks) == n_sub
+    _check_encode(wl, sae, wl.layers[0].h, idx, val, toks)
+    off = np.setdiff1d(np.arange(T), toks)
+    assert np.all(idx[off] == -7)
+
+
+def test_encode_prefill_gemm_no_subscribers(px):
+    wl = synth.make("c3", d=256, m=512, k=8, T=1100, n_sub=0)
+    sae = wl.layers[0].saes[0]
+    rt, idx, val = _encode(px, wl, sae, wl.layers[0].h)
+    assert np.all(idx == -7)
+
+
 def test_encode_exact_ties_take_lower_index(px):
     """Duplicated dictionary rows give bit-identical pre-activations; the
     lower latent index must win, across tiles and inside one tile."""
