@@ -54,6 +54,32 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sae_encode_hbm_traffic.md")
+ENCODE_SOURCE = os.path.join(ROOT, "paper_2607_22595_amd", "csrc", "sae_encode.hip")
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch of the encode GEMM from the committed rocprofv3
+    counter summary (FETCH_SIZE and WRITE_SIZE, each scaled by what the same
+    counter reads for a plain copy of known size), or None when the summary
+    is missing or the kernel source changed since the counters were taken."""
+    import hashlib
+    try:
+        text = open(TRAFFIC_FILE).read()
+        src = hashlib.sha256(open(ENCODE_SOURCE, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    fields = {}
+    for line in text.splitlines():
+        if line.startswith("- ") and ": " in line:
+            k, v = line[2:].split(": ", 1)
+            fields[k.strip("`")] = v.strip().strip("`")
+    if fields.get("source_sha256") != src:
+        return None
+    v = fields.get(f"{workload}_hbm_bytes_per_launch")
+    return float(v) if v else None
+
+
 class Rotation:
     """Graphs of one callable, one per dictionary copy, replayed in turn."""
 
@@ -157,9 +183,8 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build runs the hook step on one GPU; multi-GPU "
-                                   "sharding is a design only (see DESIGN.md)",
-                          "n_gpus": args.gpus}))
+        print(json.dumps({"error": "the hook step runs on one GPU; sharding across GPUs is "
+                                   "described, not implemented", "n_gpus": args.gpus}))
         sys.exit(2)
     import torch
     import synth
@@ -211,9 +236,9 @@ def run_decode(torch, px, synth, HookStep, args):
         "config": {"workload": "decode SAE hook step: route + encode/top-k + ring readback, "
                                "d=4096 m=65536 k=64 T=256 T_sub=128 ring=256",
                    "global_batch": wl.T_valid, "seq_len": 1, "parallelism": "none (1 GPU)"},
-        "roofline": {"bound": "hbm", "kernel": "sae_stream_topk_kernel (encode GEMM)",
+        "roofline": {"bound": "hbm", "kernel": "sae_stream_kernel (encode GEMM)",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic("decode"),
                      "ms_per_launch": ms_enc, "algorithmic_bytes": enc_bytes},
     }
     del step
@@ -222,27 +247,28 @@ def run_decode(torch, px, synth, HookStep, args):
 
 
 def run_prefill(torch, px, synth, HookStep, args):
-    if True:
-        log("generating the prefill workload")
-        wl4 = synth.make("c4")
-        step4 = HookStep(wl4)
-        log("timing the prefill step")
-        ms4, ms4_enc = bench_workload(torch, px, step4, 0, 0, args.prefill_steps,
-                                      max(2, args.warmup // 10))
-        s4 = wl4.layers[0].saes[0]
-        flops = 2.0 * wl4.T_valid * s4.m * wl4.d
-        tf = flops / (ms4_enc * 1e-3) / 1e12
-        res = {
-            "workload": "prefill hook step: route + 4 token probes + 4 pooled probes + SAE "
-                        "encode/top-k, T=8192 R=16 d=4096 m=131072 k=32",
-            "value": wl4.T_valid / (ms4 * 1e-3), "unit": "tokens/s", "ms_per_step": ms4,
-            "steps": args.prefill_steps,
-            "roofline": {"bound": "mfma", "kernel": "sae_stream_topk_kernel (encode GEMM)",
-                         "achieved": tf, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                         "frac": tf / MFMA_BF16_PEAK_TFLOPS, "ms_per_launch": ms4_enc,
-                         "algorithmic_flops": flops}}
-        del step4
-        torch.cuda.empty_cache()
+    log("generating the prefill workload")
+    wl4 = synth.make("c4")
+    step4 = HookStep(wl4)
+    log("timing the prefill step")
+    ms4, ms4_enc = bench_workload(torch, px, step4, 0, 0, args.prefill_steps,
+                                  max(2, args.warmup // 10))
+    s4 = wl4.layers[0].saes[0]
+    flops = 2.0 * wl4.T_valid * s4.m * wl4.d
+    tf = flops / (ms4_enc * 1e-3) / 1e12
+    res = {
+        "workload": "prefill hook step: route + 4 token probes + 4 pooled probes + SAE "
+                    "encode/top-k, T=8192 R=16 d=4096 m=131072 k=32",
+        "value": wl4.T_valid / (ms4 * 1e-3), "unit": "tokens/s", "ms_per_step": ms4,
+        "steps": args.prefill_steps,
+        "roofline": {"bound": "mfma",
+                     "kernel": "sae_xstage_kernel + sae_gemm_kernel (encode GEMM)",
+                     "achieved": tf, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": tf / MFMA_BF16_PEAK_TFLOPS, "ms_per_launch": ms4_enc,
+                     "algorithmic_flops": flops,
+                     "traffic": measured_traffic("prefill")}}
+    del step4
+    torch.cuda.empty_cache()
     return res
 
 
