@@ -398,12 +398,11 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
 // stage of 32 (a 16 KB dictionary half chunk, 2 KB contiguous per 32
 // latents, and a 16 KB token plane slice) are copied by the load unit
 // straight into LDS (global_load_lds, no register staging) into a ring of
-// 4 stages, three in flight.  Per stage a wave waits for its own copies of
-// the oldest stage, meets the others at a barrier, refills the stage freed
-// by the previous step, and runs 32 MFMAs whose operands come from LDS;
-// the operands of the stage's second step are read before the next barrier
-// and multiplied after it, so the matrix unit has work while the waves
-// meet.  The epilogue is the same threshold emission as the decode kernel,
+// 4 stages.  Per pair of stages a wave waits for its own copies of the
+// pair, meets the others at a barrier, refills the pair of buffers freed by
+// the previous step, and runs 64 MFMAs whose operands come from LDS; the
+// operands of the last step are read before the next barrier and
+// multiplied after it, so the matrix unit has work while the waves meet.  The epilogue is the same threshold emission as the decode kernel,
 // per token over the tile's 256 latents.
 constexpr int kGemmThreads = 256;
 constexpr int kGemmTok = 256;       // tokens per tile
@@ -491,8 +490,8 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
         const int n = P >> 2;
         xsrc[q] = (n0 + n) * 4 + ((P & 3) ^ gsw(n));
     }
-    // issue the 8 copies of stage j (past the end: the last stage again, so
-    // every stage issues the same number of operations for the waits below)
+    // issue the 8 copies of stage j (past the end: the last stage again,
+    // which keeps the loop free of branches that would split the schedule)
     auto copy_stage = [&](int j, uint4* wdst, uint4* xdst) __attribute__((always_inline)) {
         j = min(j, nS - 1);
         const int kc = j >> 1, hh = j & 1;
@@ -506,13 +505,25 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
             __builtin_amdgcn_global_load_lds(xsrc_j + xsrc[q], xdst + q * 256 + wave * 64, 16, 0, 0);
     };
 
+    // accumulators start at the folded bias of their latent:
+    // acc[a][nb][r] holds latent 128*wm + 32*a + 8*(r/4) + 4*g + r%4
     f32x16_t acc[4][4];
+    {
+        const float* cf = c_fold + mt * 256 + 128 * wm + 4 * g;
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+        for (int a = 0; a < 4; ++a)
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb)
+            for (int q = 0; q < 4; ++q) {
+                const float4 c4 = *reinterpret_cast<const float4*>(cf + 32 * a + 8 * q);
 #pragma unroll
-            for (int r = 0; r < 16; ++r) acc[a][nb][r] = 0.0f;
+                for (int nb = 0; nb < 4; ++nb) {
+                    acc[a][nb][4 * q + 0] = c4.x;
+                    acc[a][nb][4 * q + 1] = c4.y;
+                    acc[a][nb][4 * q + 2] = c4.z;
+                    acc[a][nb][4 * q + 3] = c4.w;
+                }
+            }
+    }
 
     uint4 FA[4], FB[4], PA[4], PB[4];
     auto read_step = [&](const uint4* wb, const uint4* xb, int s, uint4 (&A)[4], uint4 (&B)[4])
@@ -534,25 +545,33 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
                                                                      as_bf16x8(B[nb]), acc[a][nb],
                                                                      0, 0, 0);
     };
-    // One stage: wait for this wave's copies of stage j (two younger stages,
-    // 16 copies, may stay in flight) and its LDS reads, meet at the barrier
-    // (now every copy of stage j has landed and every wave is done with the
-    // buffer of stage j - 1), refill that buffer with stage j + 3, then read
-    // step 0, multiply the carried step of stage j - 1, read step 1 (carried
-    // across the next barrier), multiply step 0.
-    auto stage = [&](int j, const uint4* wb, const uint4* xb, uint4* wfree, uint4* xfree,
-                     bool first) __attribute__((always_inline)) {
-        XMIX_WAIT_VM_LGKM0(16);
+    // Two stages per barrier.  Wait for this wave's copies of stages j and
+    // j + 1 and its LDS reads, then meet at the barrier: every copy of the
+    // pair has landed and every wave is done with the pair before it, whose
+    // buffers are refilled with stages j + 2 and j + 3 while this pair is
+    // multiplied.  In each stage: read step 0, multiply the carried step,
+    // read step 1 (carried on), multiply step 0.
+    auto stage_pair = [&](int j, const uint4* w0, const uint4* x0, const uint4* w1,
+                          const uint4* x1, uint4* wf0, uint4* xf0, uint4* wf1, uint4* xf1,
+                          bool first) __attribute__((always_inline)) {
+        XMIX_WAIT_VM_LGKM0(0);
         asm volatile("" ::: "memory");
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        copy_stage(j + 3, wfree, xfree);
-        read_step(wb, xb, 0, FA, FB);
+        copy_stage(j + 2, wf0, xf0);
+        read_step(w0, x0, 0, FA, FB);
         if (!first) mfma_step(PA, PB);
-        read_step(wb, xb, 1, PA, PB);
+        read_step(w0, x0, 1, PA, PB);
         mfma_step(FA, FB);
-        // instruction order: step-0 reads, then the carried MFMAs with the
-        // copies between them, then step-0 MFMAs with the step-1 reads
+        copy_stage(j + 3, wf1, xf1);
+        read_step(w1, x1, 0, FA, FB);
+        mfma_step(PA, PB);
+        read_step(w1, x1, 1, PA, PB);
+        mfma_step(FA, FB);
+        // instruction order: first stage's step-0 reads; carried MFMAs with
+        // the first refill between them; step-0 MFMAs with step-1 reads;
+        // second stage's step-0 reads and the second refill between the
+        // carried MFMAs; step-0 MFMAs with step-1 reads
         __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
         if (!first) {
 #pragma unroll
@@ -568,32 +587,44 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
             __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
     };
 
     copy_stage(0, wsA, xsA);
     copy_stage(1, wsB, xsB);
-    copy_stage(2, wsC, xsC);
-    stage(0, wsA, xsA, wsD, xsD, true);
-    stage(1, wsB, xsB, wsA, xsA, false);
-    stage(2, wsC, xsC, wsB, xsB, false);
-    stage(3, wsD, xsD, wsC, xsC, false);
+    stage_pair(0, wsA, xsA, wsB, xsB, wsC, xsC, wsD, xsD, true);
+    stage_pair(2, wsC, xsC, wsD, xsD, wsA, xsA, wsB, xsB, false);
     for (int j = 4; j < nS; j += 4) {
-        stage(j + 0, wsA, xsA, wsD, xsD, false);
-        stage(j + 1, wsB, xsB, wsA, xsA, false);
-        stage(j + 2, wsC, xsC, wsB, xsB, false);
-        stage(j + 3, wsD, xsD, wsC, xsC, false);
+        stage_pair(j + 0, wsA, xsA, wsB, xsB, wsC, xsC, wsD, xsD, false);
+        stage_pair(j + 2, wsC, xsC, wsD, xsD, wsA, xsA, wsB, xsB, false);
     }
     mfma_step(PA, PB);
-    XMIX_WAIT_VM_LGKM0(0);  // the trailing refills land before the workgroup ends
+    // every wave's trailing copies have landed and its reads are done before
+    // the stage buffers are reused below
+    XMIX_WAIT_VM_LGKM0(0);
+    __syncthreads();
 
     // ---------------------------------------------------------- epilogue
     // acc[a][nb][r] holds latent 128*wm + 32*a + 8*(r/4) + 4*g + r%4 of
     // token 128*wn + 32*nb + j32; lanes j32 and j32 + 32 of waves (0, wn)
     // and (1, wn) together hold the 256 latents of one token.  The tokens of
     // one nb are finished at a time, so only their 64 values per lane need
-    // vector registers.
+    // vector registers.  The count pass keeps a bit mask of the lane's
+    // values >= tau; the values are parked in the (now idle) stage buffers
+    // so that the few selected ones are fetched by index, one per round.
     cnt_s[tid] = 0;
-    const float* cf = c_fold + mt * 256 + 128 * wm + 4 * g;
+    float* park = reinterpret_cast<float*>(wsA) + wave * 4096;  // 16 KB per wave
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
         const int n = 128 * wn + 32 * nb + j32;
@@ -601,13 +632,13 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
 #pragma unroll
         for (int a = 0; a < 4; ++a)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const float4 c4 = *reinterpret_cast<const float4*>(cf + 32 * a + 8 * q);
-                v[16 * a + 4 * q + 0] = acc[a][nb][4 * q + 0] + c4.x;
-                v[16 * a + 4 * q + 1] = acc[a][nb][4 * q + 1] + c4.y;
-                v[16 * a + 4 * q + 2] = acc[a][nb][4 * q + 2] + c4.z;
-                v[16 * a + 4 * q + 3] = acc[a][nb][4 * q + 3] + c4.w;
-            }
+            for (int r = 0; r < 16; ++r) v[16 * a + r] = acc[a][nb][r];
+        // park the values in LDS (16-byte groups, lane-contiguous, so the
+        // stores are conflict-free) for the emission below
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+            reinterpret_cast<float4*>(park)[q * 64 + lane] =
+                make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
         // mean and variance over the tile's 256 latents
         float s1 = 0.0f, s2 = 0.0f;
 #pragma unroll
@@ -617,7 +648,7 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
         }
         s1 += __shfl_xor(s1, 32, kWave);
         s2 += __shfl_xor(s2, 32, kWave);
-        __syncthreads();  // red1/red2 are reused
+        __syncthreads();  // red1/red2 and the parked values are reused
         if (g == 0) {
             red1[wm][n] = s1;
             red2[wm][n] = s2;
@@ -627,12 +658,22 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
         const float sd = sqrtf(fmaxf((red2[0][n] + red2[1][n]) * (1.0f / 256.0f) - mu * mu, 0.0f));
         float tau = mu + z_guess * sd;
         float lo_b = -INFINITY, hi_b = INFINITY;
+        uint32_t m0 = 0, m1 = 0;  // bit i: v[i] >= tau (m1: v[32 + i])
+        bool gave_up = false;
+        auto count_at = [&](float t) __attribute__((always_inline)) {
+            m0 = 0;
+            m1 = 0;
+#pragma unroll
+            for (int i = 0; i < 32; ++i) {
+                m0 |= (v[i] >= t ? 1u : 0u) << i;
+                m1 |= (v[32 + i] >= t ? 1u : 0u) << i;
+            }
+            return __popc(m0) + __popc(m1);
+        };
         // count(pre >= tau) per token; refine tau until lo_cnt <= count <= cap
         for (int it = 0; it < kRefineIters; ++it) {
-            float c = 0.0f;
-#pragma unroll
-            for (int i = 0; i < 64; ++i) c += v[i] >= tau ? 1.0f : 0.0f;
-            c += __shfl_xor(c, 32, kWave);
+            const int c_lane = count_at(tau);
+            const float c = static_cast<float>(c_lane + __shfl_xor(c_lane, 32, kWave));
             __syncthreads();  // red1 is reused
             if (g == 0) red1[wm][n] = c;
             __syncthreads();
@@ -657,31 +698,36 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
             }
             if (!__syncthreads_or(bad)) break;
             // out of iterations: a threshold whose count is known to be <= cap
-            if (it == kRefineIters - 1 && bad) tau = hi_b;
-        }
-        // emit every latent with pre >= tau
-        if (n < ntok) {
-            const int64_t row = static_cast<int64_t>(n0 + n) * n_mt + mt;
-            int c = 0;
-#pragma unroll
-            for (int i = 0; i < 64; ++i) c += v[i] >= tau ? 1 : 0;
-            if (c > 0) {
-                int slot = atomicAdd(&cnt_s[n], c);
-                uint2* dst = cand + row * cap;
-#pragma unroll
-                for (int i = 0; i < 64; ++i) {
-                    if (v[i] >= tau) {
-                        if (slot < cap)
-                            dst[slot] = make_uint2(
-                                __float_as_uint(v[i]),
-                                static_cast<uint32_t>(mt * 256 + 128 * wm + 32 * (i >> 4) +
-                                                      8 * ((i >> 2) & 3) + 4 * g + (i & 3)));
-                        ++slot;
-                    }
-                }
+            if (it == kRefineIters - 1) {
+                if (bad) tau = hi_b;
+                gave_up = true;
             }
-            if (wm == 0 && g == 0) tile_tau[row] = tau;
         }
+        if (gave_up) count_at(tau);
+        // emit every latent with pre >= tau: reserve the lane's slots with
+        // one LDS atomic, then write one selected (value, latent) pair per
+        // round, the value read back from where it was parked
+        if (n >= ntok) m0 = m1 = 0;
+        const int c = __popc(m0) + __popc(m1);
+        int slot = 0;
+        if (c > 0) slot = atomicAdd(&cnt_s[n], c);
+        const int64_t row = static_cast<int64_t>(n0 + n) * n_mt + mt;
+        uint2* dst = cand + row * cap;
+        const int lat0 = mt * 256 + 128 * wm + 4 * g;
+        while (__builtin_amdgcn_read_exec() & wave_ballot((m0 | m1) != 0)) {
+            if ((m0 | m1) != 0) {
+                const int i = m0 ? __builtin_ctz(m0) : 32 + __builtin_ctz(m1);
+                if (m0) m0 &= m0 - 1;
+                else m1 &= m1 - 1;
+                const float val = park[((i >> 2) * 64 + lane) * 4 + (i & 3)];
+                if (slot < cap)
+                    dst[slot] = make_uint2(__float_as_uint(val),
+                                           static_cast<uint32_t>(lat0 + 32 * (i >> 4) +
+                                                                 8 * ((i >> 2) & 3) + (i & 3)));
+                ++slot;
+            }
+        }
+        if (n < ntok && wm == 0 && g == 0) tile_tau[row] = tau;
     }
     __syncthreads();
     if (tid < ntok) tile_cnt[static_cast<int64_t>(n0 + tid) * n_mt + mt] = min(cnt_s[tid], cap);
