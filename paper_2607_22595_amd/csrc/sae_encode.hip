@@ -624,7 +624,7 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
     // values >= tau; the values are parked in the (now idle) stage buffers
     // so that the few selected ones are fetched by index, one per round.
     cnt_s[tid] = 0;
-    float* park = reinterpret_cast<float*>(wsA) + wave * 4096;  // 16 KB per wave
+    float* park = reinterpret_cast<float*>(wave == 0 ? wsA : wave == 1 ? wsB : wave == 2 ? wsC : wsD);
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
         const int n = 128 * wn + 32 * nb + j32;
@@ -888,12 +888,13 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
         const int tl = t0 + tid;
         const bool own = tl < n_mt;
         const int64_t row = row0 + (own ? tl : 0);
-        // count, threshold and the first 16 pairs of the slice, in one round
+        // count, threshold and the first 8 pairs of the slice, in one round
+        // (a slice holds about 2-3 candidates; more are fetched below)
         const uint4* src = reinterpret_cast<const uint4*>(cand + row * cap);
         const int last = cap / 2 - 1;
-        uint4 v[8];
+        uint4 v[4];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = src[min(u, last)];
+        for (int u = 0; u < 4; ++u) v[u] = src[min(u, last)];
         const int c = own ? tile_cnt[row] : 0;
         const uint32_t tk = own ? f32_key(tile_tau[row]) : 0u;
         // workgroup prefix of the counts
@@ -923,7 +924,7 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
         total = end;
         if (end > kPoolMax) continue;  // uniform: the pool overflows, recompute below
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < 4; ++u) {
             const int q = 2 * u;
             if (q < c) {
                 K[pos + q] = f32_key(__uint_as_float(v[u].x));
@@ -934,12 +935,12 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
                 I[pos + q + 1] = static_cast<int32_t>(v[u].w);
             }
         }
-        // slices with more than 16 candidates (rare): the rest of the block
-        for (int q0 = 16; q0 < c; q0 += 16) {
+        // slices with more than 8 candidates (rare): the rest of the block
+        for (int q0 = 8; q0 < c; q0 += 8) {
 #pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = src[min(q0 / 2 + u, last)];
+            for (int u = 0; u < 4; ++u) v[u] = src[min(q0 / 2 + u, last)];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
+            for (int u = 0; u < 4; ++u) {
                 const int q = q0 + 2 * u;
                 if (q < c) {
                     K[pos + q] = f32_key(__uint_as_float(v[u].x));
