@@ -119,7 +119,7 @@ def dictionary_copies(torch, W, min_bytes=1.5 * 2 ** 30):
     return [W] + [W.clone() for _ in range(n - 1)]
 
 
-def bench_workload(torch, px, step, sae_layer, sae_idx, steps, warmup):
+def bench_workload(torch, px, step, sae_layer, sae_idx, steps, warmup, encode=True):
     """Times the full step and the encode GEMM (candidates stage)."""
     lay = step.layers[sae_layer]
     sae = lay.saes[sae_idx]
@@ -134,14 +134,16 @@ def bench_workload(torch, px, step, sae_layer, sae_idx, steps, warmup):
     full = Rotation(torch, step.run, copies, set_copy)
     enc = Rotation(torch, lambda: px.xmix_sae_encode_candidates(
         lay.h, step.route, sae.bit, sae.W_enc, sae.b_enc, sae.b_dec, sae.c_fold, sae.k, sae.ws),
-        copies, set_copy)
+        copies, set_copy) if encode else None
     for _ in range(warmup):
         full.replay()
     torch.cuda.synchronize()
     ms_step = time_replays(torch, full, steps)
-    for _ in range(max(warmup // 2, 3)):
-        enc.replay()
-    ms_enc = time_replays(torch, enc, steps)
+    ms_enc = None
+    if encode:
+        for _ in range(max(warmup // 2, 3)):
+            enc.replay()
+        ms_enc = time_replays(torch, enc, steps)
     set_copy(copies[0])
     return ms_step, ms_enc
 
@@ -202,6 +204,8 @@ def main():
     out = {}
     if not args.no_decode:
         out, wl = run_decode(torch, px, synth, HookStep, args)
+    if not args.no_decode:
+        out["steer_probe"] = run_steer_probe(torch, synth, HookStep, args)
     if not args.no_prefill:
         out["prefill"] = run_prefill(torch, px, synth, HookStep, args)
     if not args.no_cpu_baseline and not args.no_decode:
@@ -241,9 +245,44 @@ def run_decode(torch, px, synth, HookStep, args):
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic("decode"),
                      "ms_per_launch": ms_enc, "algorithmic_bytes": enc_bytes},
     }
+    # "don't use, don't pay": the same captured step with no subscriber
+    sub_saved = step.sub.clone()
+    step.sub.zero_()
+    ms_zero, _ = bench_workload(torch, px, step, 0, 0, args.steps, args.warmup, encode=False)
+    step.sub.copy_(sub_saved)
+    out["zero_mask_step_us"] = ms_zero * 1e3
     del step
     torch.cuda.empty_cache()
     return out, wl
+
+
+def run_steer_probe(torch, synth, HookStep, args):
+    """The 4-layer decode step of steering and probe apps (d=4096, T=R=256,
+    bits 0-3 steer, bits 4-7 probe), captured as one graph."""
+    log("timing the 4-layer steering + probe decode step")
+    wl = synth.make("c2")
+    step = HookStep(wl)
+    step.run()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step.run()
+
+    class One:
+        def replay(self):
+            g.replay()
+    one = One()
+    for _ in range(args.warmup):
+        one.replay()
+    ms = time_replays(torch, one, args.steps)
+    res = {"workload": "decode steering + probe step, 4 hooked layers, d=4096 T=R=256, "
+                       "4 steering + 4 probe apps, subscriptions Bernoulli(0.3)",
+           "us_per_step": ms * 1e3, "us_per_layer": ms * 1e3 / len(wl.layers),
+           "value": wl.T_valid * len(wl.layers) / (ms * 1e-3), "unit": "hooked tokens/s per layer",
+           "hbm_bytes": step.hbm_bytes()}
+    del step
+    torch.cuda.empty_cache()
+    return res
 
 
 def run_prefill(torch, px, synth, HookStep, args):
