@@ -57,7 +57,7 @@ typedef enum {
 
 typedef enum { XMIX_F32 = 0, XMIX_BF16 = 1 } xmix_dtype;
 
-enum { XMIX_PROBE_TOKEN = 0, XMIX_PROBE_MEAN = 1 };
+enum { XMIX_PROBE_TOKEN = 0, XMIX_PROBE_MEAN = 1, XMIX_PROBE_LAST = 2 };
 
 /* Device error-word bits set by xmix_route_build. */
 enum {
@@ -155,10 +155,14 @@ xmix_status xmix_steer_apply(void *h, xmix_dtype dt, int32_t d, const xmix_route
  *   logit_out[p][r] = b[p] + mean_{t in span} (w[p,:] . h[t,:]) (the probe of
  *   the span's mean activation), score as above; outputs are [n_probe][R_max].
  *   The span sums are reduced in a fixed order (bit-reproducible).
+ * mode XMIX_PROBE_LAST: the "last token" condition of a read (Sec. 4.1):
+ *   for each request r with a non-empty span whose first token has bit
+ *   app_bits[p], logit_out[p][r] = b[p] + w[p,:] . h[cu_seqlens[r+1]-1,:],
+ *   score as above; outputs are [n_probe][R_max].
  * h [T_max, d] and w [n_probe, d] of dtype dt; b [n_probe] fp32;
- * app_bits host [n_probe]; cu_seqlens [R_max + 1] int32 (MEAN only, spans
- * contiguous and inside [0, T_max]); the probe reads h as given (call it
- * before any write at the same hook).
+ * app_bits host [n_probe]; cu_seqlens [R_max + 1] int32 (MEAN and LAST,
+ * spans contiguous and inside [0, T_max]); the probe reads h as given (call
+ * it before any write at the same hook).
  * ws: device workspace of at least xmix_probe_workspace(...) bytes (may be
  * NULL when that is 0).  Requires 1 <= n_probe <= 32. */
 size_t xmix_probe_workspace(int32_t T_max, int32_t n_probe, int32_t mode);

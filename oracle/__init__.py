@@ -37,12 +37,13 @@ def _load():
     lib.oracle_steer.argtypes = [vp, ctypes.c_int, i32, i32, vp, vp, vp, vp, vp, i32]
     lib.oracle_probe_token.argtypes = [vp, ctypes.c_int, i32, i32, vp, vp, vp, vp, i32, vp, vp]
     lib.oracle_probe_mean.argtypes = [vp, ctypes.c_int, i32, i32, vp, vp, vp, vp, i32, vp, i32, vp, vp]
+    lib.oracle_probe_last.argtypes = [vp, ctypes.c_int, i32, i32, vp, vp, vp, vp, i32, vp, i32, vp, vp]
     lib.oracle_sae_pre.argtypes = [vp, i32, vp, vp, vp, i32, vp]
     lib.oracle_topk.argtypes = [vp, i32, i32, vp, vp, vp]
     lib.oracle_sae_encode.argtypes = [vp, i32, vp, i32, vp, vp, vp, i32, i32, vp, vp, vp, vp]
     lib.oracle_clamp_decode.argtypes = [vp, i32, i32, vp, i32, vp, vp, i32, vp, i32, vp, vp, i32, vp]
     lib.oracle_compact.argtypes = [vp, vp, i32, vp, i32, i32, vp, i32, i32, vp, i32, i32, vp]
-    for n in ("oracle_route", "oracle_steer", "oracle_probe_token", "oracle_probe_mean",
+    for n in ("oracle_route", "oracle_steer", "oracle_probe_token", "oracle_probe_mean", "oracle_probe_last",
               "oracle_sae_pre", "oracle_topk", "oracle_sae_encode", "oracle_clamp_decode",
               "oracle_compact"):
         getattr(lib, n).restype = None
@@ -127,6 +128,23 @@ def probe_mean(h, tok_mask, w, b, app_bits, cu_seqlens):
     logit = np.full((n, R), np.nan)
     score = np.full((n, R), np.nan)
     _load().oracle_probe_mean(_p(h), int(is_bf16), T_max, d, _p(_c(tok_mask, np.uint32)), _p(w),
+                              _p(_c(b, np.float32)), _p(_c(app_bits, np.int32)), n, _p(cu), R,
+                              _p(logit), _p(score))
+    return logit, score
+
+
+def probe_last(h, tok_mask, w, b, app_bits, cu_seqlens):
+    """Returns (logit, score) as float64 [n_probe, R]; NaN where not written."""
+    is_bf16 = h.dtype == np.uint16
+    h = _c(h, h.dtype)
+    T_max, d = h.shape
+    w = _c(w, h.dtype).reshape(-1, d)
+    n = w.shape[0]
+    cu = _c(cu_seqlens, np.int32)
+    R = cu.size - 1
+    logit = np.full((n, R), np.nan)
+    score = np.full((n, R), np.nan)
+    _load().oracle_probe_last(_p(h), int(is_bf16), T_max, d, _p(_c(tok_mask, np.uint32)), _p(w),
                               _p(_c(b, np.float32)), _p(_c(app_bits, np.int32)), n, _p(cu), R,
                               _p(logit), _p(score))
     return logit, score

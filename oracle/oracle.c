@@ -216,6 +216,29 @@ void oracle_probe_mean(const void *h, int is_bf16, int32_t T_max, int32_t d,
     }
 }
 
+/* Last-token probe of each request (the "last token" activation condition
+ * of a read, Sec. 4.1): for each request r with a non-empty span
+ * [cu[r], cu[r+1]) whose first token has bit app_bits[p],
+ *   logit[p][r] = b[p] + sum_i w[p,i] * h[cu[r+1]-1, i]
+ * i.e. the per-token probe of the span's last token. */
+void oracle_probe_last(const void *h, int is_bf16, int32_t T_max, int32_t d,
+                       const uint32_t *tok_mask, const void *w, const float *b,
+                       const int32_t *app_bits, int32_t n_probe,
+                       const int32_t *cu_seqlens, int32_t R,
+                       double *logit, double *score) {
+    (void)T_max;
+    for (int32_t r = 0; r < R; ++r) {
+        for (int32_t p = 0; p < n_probe; ++p) {
+            int32_t lo = cu_seqlens[r], hi = cu_seqlens[r + 1];
+            if (hi <= lo) continue;
+            if (!((tok_mask[lo] >> app_bits[p]) & 1u)) continue;
+            double l = (double)b[p] + dot_row(h, is_bf16, hi - 1, d, w, p);
+            logit[(int64_t)p * R + r] = l;
+            score[(int64_t)p * R + r] = logistic(l);
+        }
+    }
+}
+
 /* --------------------------------------------------------- SAE encode+TopK
  * TopK sparse-autoencoder encoder on one token (the paper names sparse
  * autoencoders and feature dictionaries as app artefacts, Sec. 3, and

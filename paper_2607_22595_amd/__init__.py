@@ -31,7 +31,7 @@ _lib = ctypes.CDLL(LIB_PATH)
 
 XMIX_OK, XMIX_E_INVAL, XMIX_E_UNSUPPORTED, XMIX_E_WORKSPACE, XMIX_E_LAUNCH = range(5)
 XMIX_F32, XMIX_BF16 = 0, 1
-XMIX_PROBE_TOKEN, XMIX_PROBE_MEAN = 0, 1
+XMIX_PROBE_TOKEN, XMIX_PROBE_MEAN, XMIX_PROBE_LAST = 0, 1, 2
 XMIX_ERR_REQUEST_RANGE, XMIX_ERR_T_VALID = 1, 2
 MAX_APPS, MAX_TOPK, MAX_CLAMP, MAX_SEGMENTS = 32, 64, 16, 4
 
@@ -181,13 +181,13 @@ def probe_workspace(T_max: int, n_probe: int, mode: int) -> int:
 
 def xmix_probe_score(h, route: Route, w, b, app_bits: Sequence[int], mode: int, logit_out,
                      score_out, cu_seqlens=None, ws=None, stream=None):
-    """Token mode: outputs fp32 [n_probe, T_max].  Mean mode: outputs fp32
-    [n_probe, R_max] with cu_seqlens int32 [R_max + 1]."""
+    """Token mode: outputs fp32 [n_probe, T_max].  Mean and last-token modes:
+    outputs fp32 [n_probe, R_max] with cu_seqlens int32 [R_max + 1]."""
     T_max, d = h.shape
     n = len(app_bits)
     assert w.dtype == h.dtype and w.shape == (n, d) and b.dtype == torch.float32
     R_max = 0
-    if mode == XMIX_PROBE_MEAN:
+    if mode in (XMIX_PROBE_MEAN, XMIX_PROBE_LAST):
         R_max = cu_seqlens.numel() - 1
         assert logit_out.shape == (n, R_max)
     else:

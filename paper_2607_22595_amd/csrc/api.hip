@@ -91,8 +91,9 @@ xmix_status xmix_probe_score(const void* h, xmix_dtype dt, int32_t d, const xmix
     if (!h || !w || !b || !logit_out || !score_out || !route_ok(rt) || d < 1) return XMIX_E_INVAL;
     if (dt != XMIX_BF16 && dt != XMIX_F32) return XMIX_E_INVAL;
     if (d % (dt == XMIX_BF16 ? 8 : 4) != 0 || !aligned16(h) || !aligned16(w)) return XMIX_E_INVAL;
-    if (mode != XMIX_PROBE_TOKEN && mode != XMIX_PROBE_MEAN) return XMIX_E_INVAL;
-    if (mode == XMIX_PROBE_MEAN && (!cu_seqlens || R_max < 1)) return XMIX_E_INVAL;
+    if (mode != XMIX_PROBE_TOKEN && mode != XMIX_PROBE_MEAN && mode != XMIX_PROBE_LAST)
+        return XMIX_E_INVAL;
+    if (mode != XMIX_PROBE_TOKEN && (!cu_seqlens || R_max < 1)) return XMIX_E_INVAL;
     BitList bits;
     if (!bits_ok(app_bits, n_probe, rt->n_apps, &bits)) return XMIX_E_INVAL;
     const size_t need = xmix_probe_workspace(rt->T_max, n_probe, mode);

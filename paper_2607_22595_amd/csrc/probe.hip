@@ -8,6 +8,9 @@
 // Mean pooling is a segmented reduction in two launches: the token pass
 // writes each token's dot products (without bias) to the workspace, then one
 // workgroup per request sums its contiguous span in a fixed order.
+//
+// Last-token mode runs the token pass with one workgroup per request on the
+// last token of its span, writing [n_probe][R_max].
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -21,11 +24,23 @@ __global__ void __launch_bounds__(kProbeThreads)
 probe_token_kernel(const void* __restrict__ h, int32_t d, int32_t T_max,
                    const uint32_t* __restrict__ tok_mask, const void* __restrict__ w,
                    const float* __restrict__ b, BitList bits, int32_t n_probe,
-                   float* __restrict__ logit, float* __restrict__ score,
-                   float* __restrict__ dots) {
+                   const int32_t* __restrict__ cu, float* __restrict__ logit,
+                   float* __restrict__ score, float* __restrict__ dots) {
     __shared__ float red[kProbeWaves][MAXP];
-    const int32_t t = blockIdx.x;
-    const uint32_t mask = tok_mask[t];
+    // token mode: slot = token; last-token mode (cu given): slot = request,
+    // reading the last token of its span (subscription of its first token)
+    int32_t t = blockIdx.x;
+    int32_t out_len = T_max;
+    uint32_t mask;
+    if (cu) {
+        const int32_t lo = cu[blockIdx.x], hi = cu[blockIdx.x + 1];
+        if (hi <= lo || lo < 0 || hi > T_max) return;
+        t = hi - 1;
+        mask = tok_mask[lo];
+        out_len = static_cast<int32_t>(gridDim.x);
+    } else {
+        mask = tok_mask[t];
+    }
     uint32_t sel = 0;
     for (int p = 0; p < n_probe; ++p) sel |= ((mask >> bits.bit[p]) & 1u) << p;
     if (sel == 0) return;
@@ -83,7 +98,7 @@ probe_token_kernel(const void* __restrict__ h, int32_t d, int32_t T_max,
         float dot = 0.0f;
 #pragma unroll
         for (int wv = 0; wv < kProbeWaves; ++wv) dot += red[wv][p];
-        const int64_t o = static_cast<int64_t>(p) * T_max + t;
+        const int64_t o = static_cast<int64_t>(p) * out_len + blockIdx.x;
         if (dots) {
             dots[o] = dot;
         } else {
@@ -132,21 +147,22 @@ probe_pool_kernel(const float* __restrict__ dots, int32_t T_max,
 template <bool BF16>
 static hipError_t launch_probe_t(const void* h, int32_t d, int32_t T_max,
                                  const uint32_t* tok_mask, const void* w, const float* b,
-                                 const BitList& bits, int32_t n_probe, float* logit,
-                                 float* score, float* dots, hipStream_t stream) {
-    dim3 g(T_max), blk(kProbeThreads);
+                                 const BitList& bits, int32_t n_probe, const int32_t* cu,
+                                 int32_t slots, float* logit, float* score, float* dots,
+                                 hipStream_t stream) {
+    dim3 g(slots), blk(kProbeThreads);
     if (n_probe <= 4)
         hipLaunchKernelGGL((probe_token_kernel<BF16, 4>), g, blk, 0, stream, h, d, T_max,
-                           tok_mask, w, b, bits, n_probe, logit, score, dots);
+                           tok_mask, w, b, bits, n_probe, cu, logit, score, dots);
     else if (n_probe <= 8)
         hipLaunchKernelGGL((probe_token_kernel<BF16, 8>), g, blk, 0, stream, h, d, T_max,
-                           tok_mask, w, b, bits, n_probe, logit, score, dots);
+                           tok_mask, w, b, bits, n_probe, cu, logit, score, dots);
     else if (n_probe <= 16)
         hipLaunchKernelGGL((probe_token_kernel<BF16, 16>), g, blk, 0, stream, h, d, T_max,
-                           tok_mask, w, b, bits, n_probe, logit, score, dots);
+                           tok_mask, w, b, bits, n_probe, cu, logit, score, dots);
     else
         hipLaunchKernelGGL((probe_token_kernel<BF16, 32>), g, blk, 0, stream, h, d, T_max,
-                           tok_mask, w, b, bits, n_probe, logit, score, dots);
+                           tok_mask, w, b, bits, n_probe, cu, logit, score, dots);
     return hipGetLastError();
 }
 
@@ -156,10 +172,12 @@ hipError_t launch_probe(const void* h, bool bf16, int32_t d, int32_t T_max,
                         const int32_t* cu_seqlens, int32_t R_max, float* logit, float* score,
                         float* ws, hipStream_t stream) {
     float* dots = mode == 1 ? ws : nullptr;
-    hipError_t e = bf16 ? launch_probe_t<true>(h, d, T_max, tok_mask, w, b, bits, n_probe, logit,
-                                               score, dots, stream)
-                        : launch_probe_t<false>(h, d, T_max, tok_mask, w, b, bits, n_probe,
-                                                logit, score, dots, stream);
+    const int32_t* cu = mode == 2 ? cu_seqlens : nullptr;  // last-token mode
+    const int32_t slots = mode == 2 ? R_max : T_max;
+    hipError_t e = bf16 ? launch_probe_t<true>(h, d, T_max, tok_mask, w, b, bits, n_probe, cu,
+                                               slots, logit, score, dots, stream)
+                        : launch_probe_t<false>(h, d, T_max, tok_mask, w, b, bits, n_probe, cu,
+                                                slots, logit, score, dots, stream);
     if (e != hipSuccess || mode != 1) return e;
     hipLaunchKernelGGL(probe_pool_kernel, dim3(R_max), dim3(kProbeThreads), 0, stream, ws, T_max,
                        tok_mask, cu_seqlens, b, bits, n_probe, R_max, logit, score);

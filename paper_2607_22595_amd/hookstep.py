@@ -25,7 +25,7 @@ from typing import List, Optional
 import numpy as np
 import torch
 
-from . import (XMIX_PROBE_MEAN, XMIX_PROBE_TOKEN, Ring, Route, probe_workspace,
+from . import (XMIX_PROBE_LAST, XMIX_PROBE_MEAN, XMIX_PROBE_TOKEN, Ring, Route, probe_workspace,
                sae_encode_workspace, xmix_probe_score, xmix_readback_compact,
                xmix_route_build, xmix_sae_clamp_decode, xmix_sae_encode_topk,
                xmix_sae_fold_bias, xmix_sae_pack_encoder, xmix_steer_apply)
@@ -104,7 +104,8 @@ class HookStep:
             if L.steer:
                 lay.steer_v = to_device(np.stack([s.v for s in L.steer]), act, dev)
                 lay.steer_bits = [s.bit for s in L.steer]
-            for mode, name in ((XMIX_PROBE_TOKEN, "token"), (XMIX_PROBE_MEAN, "mean")):
+            for mode, name in ((XMIX_PROBE_TOKEN, "token"), (XMIX_PROBE_MEAN, "mean"),
+                               (XMIX_PROBE_LAST, "last")):
                 ps = [p for p in L.probes if p.mode == name]
                 if not ps:
                     continue

@@ -158,7 +158,7 @@ class ProbeApp:
     bit: int
     w: np.ndarray            # [d], bf16 bits or float32
     b: float                 # fp32 bias
-    mode: str                # "token" or "mean"
+    mode: str                # "token", "mean" or "last"
 
 
 @dataclass
@@ -312,16 +312,18 @@ def make_c3(seed=0, d=4096, m=65536, k=64, T=256, n_sub=None, ring_capacity=256,
 
 
 def make_c4(seed=0, d=4096, T=8192, R=16, len_lo=128, len_hi=1024, m=131072, k=32,
-            n_outliers=8):
+            n_outliers=8, n_last=0):
     """Prefill chunk: ragged requests in contiguous spans; bit 0 SAE encode on
-    every token, bits 1-4 per-token probes, bits 5-8 mean-pooled probes;
-    every request subscribes to every app."""
+    every token, bits 1-4 per-token probes, bits 5-8 mean-pooled probes, and
+    (n_last > 0) bits 9.. last-token probes; every request subscribes to
+    every app."""
     cfg = "c4"
     lens = ragged_lengths(cfg, R, T, len_lo, len_hi, seed)
     cu = np.zeros(R + 1, dtype=np.int32)
     cu[1:] = np.cumsum(lens)
     req = np.repeat(np.arange(R, dtype=np.int32), lens).astype(np.int32)
-    sub = np.full(R, (1 << 9) - 1, dtype=np.uint32)
+    n_apps = 9 + n_last
+    sub = np.full(R, (1 << n_apps) - 1, dtype=np.uint32)
     scale = _outlier_scale(cfg, d, n_outliers, seed)
     h = normal_bf16(f"{cfg}/L0/h", (T, d), 1.0, chan_scale=scale, seed=seed)
     probes = []
@@ -329,9 +331,14 @@ def make_c4(seed=0, d=4096, T=8192, R=16, len_lo=128, len_hi=1024, m=131072, k=3
         w = normal_bf16(f"{cfg}/L0/probe{q}/w", (d,), 1 / np.sqrt(d), seed=seed)
         b = float(normal_f32(f"{cfg}/L0/probe{q}/b", (1,), np.sqrt(0.1), seed=seed)[0])
         probes.append(ProbeApp(1 + q, w, b, "token" if q < 4 else "mean"))
+    for q in range(n_last):
+        w = normal_bf16(f"{cfg}/L0/last{q}/w", (d,), 1 / np.sqrt(d), seed=seed)
+        b = float(normal_f32(f"{cfg}/L0/last{q}/b", (1,), np.sqrt(0.1), seed=seed)[0])
+        probes.append(ProbeApp(9 + q, w, b, "last"))
     sae = _sae(cfg, "sae0", 0, d, m, k, seed)
     alpha = np.zeros((R, 0), dtype=np.float32)
-    return Workload(cfg, "bf16", d, T, T, R, 9, req, sub, alpha, [Layer(0, h, [], probes, [sae])],
+    return Workload(cfg, "bf16", d, T, T, R, n_apps, req, sub, alpha,
+                    [Layer(0, h, [], probes, [sae])],
                     cu_seqlens=cu,
                     description=f"prefill d={d} T={T} R={R} m={m} k={k}")
 

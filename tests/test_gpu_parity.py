@@ -133,7 +133,8 @@ def _probe_case(px, wl, layer=0):
     rt, _ = gpu_route(px, wl.req, wl.T_valid, wl.sub, wl.n_apps)
     h = dev_bits(L.h) if wl.dtype == "bf16" else torch.from_numpy(L.h).cuda()
     hv = bf16_f64(L.h) if wl.dtype == "bf16" else L.h.astype(np.float64)
-    for mode_name, mode in (("token", px.XMIX_PROBE_TOKEN), ("mean", px.XMIX_PROBE_MEAN)):
+    for mode_name, mode in (("token", px.XMIX_PROBE_TOKEN), ("mean", px.XMIX_PROBE_MEAN),
+                            ("last", px.XMIX_PROBE_LAST)):
         ps = [p for p in L.probes if p.mode == mode_name]
         if not ps:
             continue
@@ -155,6 +156,11 @@ def _probe_case(px, wl, layer=0):
         if mode == px.XMIX_PROBE_TOKEN:
             lr, sr = oracle.probe_token(L.h, tm, w, b, bits)
             floor = absdot
+        elif mode == px.XMIX_PROBE_LAST:
+            lr, sr = oracle.probe_last(L.h, tm, w, b, bits, wl.cu_seqlens)
+            cu = wl.cu_seqlens
+            floor = np.stack([[absdot[p, cu[r + 1] - 1] if cu[r + 1] > cu[r] else 0.0
+                               for r in range(wl.R_max)] for p in range(len(ps))])
         else:
             lr, sr = oracle.probe_mean(L.h, tm, w, b, bits, wl.cu_seqlens)
             cu = wl.cu_seqlens
@@ -176,6 +182,18 @@ def test_probe_decode_8b_shape(px):
 
 def test_probe_prefill_token_and_pooled_small(px):
     _probe_case(px, synth.make("c4", d=512, T=2000, R=5, len_lo=100, len_hi=700, m=256, k=8))
+
+
+def test_probe_last_token_with_empty_and_unsubscribed_spans(px):
+    """Last-token reads: one output per request from the last token of its
+    span; an empty span and an unsubscribed request are not written."""
+    wl = synth.make("c4", d=512, T=1200, R=6, len_lo=100, len_hi=400, m=256, k=8, n_last=3)
+    cu = wl.cu_seqlens.copy()
+    cu[3] = cu[2]                       # request 2 gets an empty span ...
+    wl.cu_seqlens = cu
+    wl.req[cu[3]:cu[4]] = 3             # ... and request 3 takes its tokens
+    wl.sub[4] &= ~np.uint32(1 << 10)    # request 4 drops one last-token probe
+    _probe_case(px, wl)
 
 
 def test_probe_70b_shape(px):

@@ -254,6 +254,29 @@ def test_probe_mean_pins():
     assert sm[0, 1] == pytest.approx(1 / (1 + math.exp(-lm[0, 1])), rel=1e-14)
 
 
+def test_probe_last_pins():
+    d = 24
+    lens = [2, 1, 0, 4]
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    T = int(cu[-1])
+    h = synth.normal_bf16("pin/last/h", (T, d), 1.0)
+    w = synth.normal_bf16("pin/last/w", (2, d), 0.3)
+    b = np.array([0.25, -0.5], np.float32)
+    tok_mask = np.full(T, 0b11, np.uint32)
+    tok_mask[cu[3]:cu[4]] = 0b10  # request 3 has only the second probe's bit
+    ll, sl = oracle.probe_last(h, tok_mask, w, b, [0, 1], cu)
+    lt, st = oracle.probe_token(h, np.full(T, 0b11, np.uint32), w, b, [0, 1])
+    # equals the per-token probe of each span's last token
+    assert ll[0, 0] == lt[0, 1] and ll[1, 0] == lt[1, 1]
+    assert ll[0, 1] == lt[0, 2]                         # single-token span
+    assert np.isnan(ll[0, 2]) and np.isnan(ll[1, 2])    # empty span
+    assert np.isnan(ll[0, 3]) and ll[1, 3] == lt[1, 6]  # per-probe subscription
+    hv, wv = bf16_vals(h), bf16_vals(w)
+    ref = float(np.float32(-0.5)) + math.fsum(wv[1, i] * hv[6, i] for i in range(d))
+    assert ll[1, 3] == pytest.approx(ref, rel=1e-13)
+    assert sl[1, 3] == pytest.approx(1 / (1 + math.exp(-ll[1, 3])), rel=1e-14)
+
+
 # ------------------------------------------------------------- SAE encode
 
 def sort_topk(pre, k):
