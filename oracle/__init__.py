@@ -37,13 +37,15 @@ def _load():
     lib.oracle_steer.argtypes = [vp, ctypes.c_int, i32, i32, vp, vp, vp, vp, vp, i32]
     lib.oracle_probe_token.argtypes = [vp, ctypes.c_int, i32, i32, vp, vp, vp, vp, i32, vp, vp]
     lib.oracle_probe_mean.argtypes = [vp, ctypes.c_int, i32, i32, vp, vp, vp, vp, i32, vp, i32, vp, vp]
+    lib.oracle_route_gate.argtypes = [i32, vp, vp, vp, i32, vp, i32, vp, i32, i32, ctypes.c_float]
+    lib.oracle_route_trigger.argtypes = [i32, vp, vp, vp, i32, vp, vp, i32]
     lib.oracle_probe_last.argtypes = [vp, ctypes.c_int, i32, i32, vp, vp, vp, vp, i32, vp, i32, vp, vp]
     lib.oracle_sae_pre.argtypes = [vp, i32, vp, vp, vp, i32, vp]
     lib.oracle_topk.argtypes = [vp, i32, i32, vp, vp, vp]
     lib.oracle_sae_encode.argtypes = [vp, i32, vp, i32, vp, vp, vp, i32, i32, vp, vp, vp, vp]
     lib.oracle_clamp_decode.argtypes = [vp, i32, i32, vp, i32, vp, vp, i32, vp, i32, vp, vp, i32, vp]
     lib.oracle_compact.argtypes = [vp, vp, i32, vp, i32, i32, vp, i32, i32, vp, i32, i32, vp]
-    for n in ("oracle_route", "oracle_steer", "oracle_probe_token", "oracle_probe_mean", "oracle_probe_last",
+    for n in ("oracle_route", "oracle_route_gate", "oracle_route_trigger", "oracle_steer", "oracle_probe_token", "oracle_probe_mean", "oracle_probe_last",
               "oracle_sae_pre", "oracle_topk", "oracle_sae_encode", "oracle_clamp_decode",
               "oracle_compact"):
         getattr(lib, n).restype = None
@@ -86,6 +88,40 @@ def route(req, T_valid, sub, n_apps, R_max=None):
     _load().oracle_route(_p(req), int(T_valid), T_max, _p(sub), int(R_max), int(n_apps),
                          _p(tok_mask), _p(count), _p(app_tokens), _p(err))
     return tok_mask, count[:n_apps], app_tokens[:n_apps], int(err[0])
+
+
+def route_gate(tok_mask, count, app_tokens, app_bit, signal, threshold, signal_bit=-1,
+               req=None):
+    """Activation-driven conditional write: narrows app `app_bit` of a route
+    (tok_mask, count, app_tokens as returned by route()) to the tokens whose
+    signal passes `threshold`; per-request signal when `req` is given.
+    Returns new (tok_mask, count, app_tokens)."""
+    tm = np.array(tok_mask, np.uint32, copy=True)
+    T_max = tm.size
+    n_apps = app_tokens.shape[0]
+    cnt = np.array(count, np.int32, copy=True)
+    lists = np.ascontiguousarray(np.array(app_tokens, np.int32, copy=True))
+    sig = _c(signal, np.float32)
+    per_req = req is not None
+    reqv = _c(req, np.int32) if per_req else np.zeros(1, np.int32)
+    _load().oracle_route_gate(T_max, _p(tm), _p(cnt), _p(lists), int(app_bit), _p(sig),
+                              int(per_req), _p(reqv), int(sig.size), int(signal_bit),
+                              ctypes.c_float(threshold))
+    return tm, cnt[:n_apps], lists
+
+
+def route_trigger(tok_mask, count, app_tokens, app_bit, token_ids, vocab_bits, vocab_size):
+    """Token-driven conditional write: narrows app `app_bit` to the tokens whose
+    id is in the trigger bitmap.  Returns new (tok_mask, count, app_tokens)."""
+    tm = np.array(tok_mask, np.uint32, copy=True)
+    T_max = tm.size
+    n_apps = app_tokens.shape[0]
+    cnt = np.array(count, np.int32, copy=True)
+    lists = np.ascontiguousarray(np.array(app_tokens, np.int32, copy=True))
+    _load().oracle_route_trigger(T_max, _p(tm), _p(cnt), _p(lists), int(app_bit),
+                                 _p(_c(token_ids, np.int32)), _p(_c(vocab_bits, np.uint32)),
+                                 int(vocab_size))
+    return tm, cnt[:n_apps], lists
 
 
 def steer(h, tok_mask, req, v, app_bits, alpha):

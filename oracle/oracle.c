@@ -114,6 +114,62 @@ void oracle_route(const int32_t *req, int32_t T_valid, int32_t T_max,
     *err = e;
 }
 
+/* ------------------------------------------------------ conditional writes
+ * A conditional write is a write that applies only where a device-side
+ * condition holds (Sec. 4.1, `.cond(...)`; Sec. 4.2, condition classes):
+ * activation-driven (a probe's signal from an earlier layer against a
+ * threshold) or token-driven (the token id is in a trigger list).  Both
+ * narrow one app's routing entry: a token keeps bit `app_bit` only if the
+ * condition holds for it, and the app's token list is rebuilt from the
+ * narrowed masks (ascending, -1 after the count).  Other apps are untouched.
+ *
+ * Activation-driven: the condition is  s >= threshold  with
+ *   s = signal[t]                  (signal_per_request == 0), or
+ *   s = signal[req_of_token[t]]    (signal_per_request != 0, ids in [0, n_signal)),
+ * and, when signal_bit >= 0, the token must also carry bit signal_bit (the
+ * signal exists only where the probe app ran).  NaN never passes. */
+void oracle_route_gate(int32_t T_max, uint32_t *tok_mask, int32_t *app_count,
+                       int32_t *app_tokens, int32_t app_bit, const float *signal,
+                       int32_t signal_per_request, const int32_t *req_of_token,
+                       int32_t n_signal, int32_t signal_bit, float threshold) {
+    int32_t *list = app_tokens + (int64_t)app_bit * T_max;
+    int32_t n = 0;
+    for (int32_t t = 0; t < T_max; ++t) {
+        if (!((tok_mask[t] >> app_bit) & 1u)) continue;
+        int pass = 1;
+        if (signal_bit >= 0 && !((tok_mask[t] >> signal_bit) & 1u)) pass = 0;
+        double sv = 0.0;
+        if (pass) {
+            int32_t i = signal_per_request ? req_of_token[t] : t;
+            if (i < 0 || i >= n_signal) pass = 0;
+            else sv = (double)signal[i];
+        }
+        if (pass && !(sv >= (double)threshold)) pass = 0;
+        if (pass) list[n++] = t;
+        else tok_mask[t] &= ~(1u << app_bit);
+    }
+    for (int32_t i = n; i < T_max; ++i) list[i] = -1;
+    app_count[app_bit] = n;
+}
+
+/* Token-driven: the condition is that token_ids[t] lies in [0, vocab_size)
+ * and its bit is set in the trigger bitmap vocab_bits (bit v of word v/32). */
+void oracle_route_trigger(int32_t T_max, uint32_t *tok_mask, int32_t *app_count,
+                          int32_t *app_tokens, int32_t app_bit, const int32_t *token_ids,
+                          const uint32_t *vocab_bits, int32_t vocab_size) {
+    int32_t *list = app_tokens + (int64_t)app_bit * T_max;
+    int32_t n = 0;
+    for (int32_t t = 0; t < T_max; ++t) {
+        if (!((tok_mask[t] >> app_bit) & 1u)) continue;
+        int32_t v = token_ids[t];
+        int pass = v >= 0 && v < vocab_size && ((vocab_bits[v >> 5] >> (v & 31)) & 1u);
+        if (pass) list[n++] = t;
+        else tok_mask[t] &= ~(1u << app_bit);
+    }
+    for (int32_t i = n; i < T_max; ++i) list[i] = -1;
+    app_count[app_bit] = n;
+}
+
 /* ---------------------------------------------------------------- steering
  * Additive steering, the Write primitive (Sec. 3: add or subtract a vector on
  * the activation).  For every token t that has at least one steering bit:

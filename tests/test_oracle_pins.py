@@ -440,3 +440,62 @@ def test_compact_brute_force(cap, head):
             assert np.all(out[s] == 0xEE)
         else:
             assert np.array_equal(out[s], exp[s])
+
+
+# ---------------------------------------------------- conditional writes
+
+def _gate_case(seed):
+    rng = np.random.default_rng(seed)
+    T, R, n_apps = 97, 9, 5
+    req = rng.integers(-1, R, T).astype(np.int32)
+    sub = rng.integers(0, 1 << n_apps, R).astype(np.uint32)
+    return T, R, n_apps, req, sub, rng
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_route_gate_brute_force(seed):
+    T, R, n_apps, req, sub, rng = _gate_case(seed)
+    tm, cnt, lists, _ = oracle.route(req, T, sub, n_apps)
+    sig = rng.normal(size=T).astype(np.float32)
+    sig[rng.integers(0, T, 5)] = np.nan
+    app, sbit, thr = 2, 4, 0.1
+    tm2, cnt2, lists2 = oracle.route_gate(tm, cnt, lists, app, sig, thr, signal_bit=sbit)
+    keep = [t for t in range(T) if (tm[t] >> app) & 1 and (tm[t] >> sbit) & 1 and sig[t] >= thr]
+    assert cnt2[app] == len(keep) and list(lists2[app, :len(keep)]) == keep
+    assert np.all(lists2[app, len(keep):] == -1)
+    for t in range(T):
+        assert ((tm2[t] >> app) & 1) == (t in keep)
+        assert (tm2[t] & ~np.uint32(1 << app)) == (tm[t] & ~np.uint32(1 << app))
+    others = [a for a in range(n_apps) if a != app]
+    assert np.array_equal(lists2[others], lists[others]) and np.array_equal(cnt2[others], cnt[others])
+
+
+def test_route_gate_per_request_and_limits():
+    T, R, n_apps, req, sub, rng = _gate_case(11)
+    tm, cnt, lists, _ = oracle.route(req, T, sub, n_apps)
+    app = 1
+    sig_r = rng.normal(size=R).astype(np.float32)
+    tm2, cnt2, lists2 = oracle.route_gate(tm, cnt, lists, app, sig_r, 0.0, req=req)
+    keep = [t for t in range(T) if (tm[t] >> app) & 1 and sig_r[req[t]] >= 0.0]
+    assert list(lists2[app, :cnt2[app]]) == keep
+    # -inf passes every finite signal, +inf none
+    _, c_all, _ = oracle.route_gate(tm, cnt, lists, app, np.zeros(T, np.float32), -np.inf)
+    _, c_none, _ = oracle.route_gate(tm, cnt, lists, app, np.zeros(T, np.float32), np.inf)
+    assert c_all[app] == cnt[app] and c_none[app] == 0
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_route_trigger_brute_force(seed):
+    T, R, n_apps, req, sub, rng = _gate_case(20 + seed)
+    tm, cnt, lists, _ = oracle.route(req, T, sub, n_apps)
+    V = 1000
+    ids = rng.integers(-5, V + 5, T).astype(np.int32)
+    trig = set(rng.choice(V, 60, replace=False).tolist())
+    bits = np.zeros((V + 31) // 32, np.uint32)
+    for v in trig:
+        bits[v >> 5] |= np.uint32(1 << (v & 31))
+    app = 3
+    tm2, cnt2, lists2 = oracle.route_trigger(tm, cnt, lists, app, ids, bits, V)
+    keep = [t for t in range(T) if (tm[t] >> app) & 1 and int(ids[t]) in trig]
+    assert cnt2[app] == len(keep) and list(lists2[app, :len(keep)]) == keep
+    assert all(((tm2[t] >> app) & 1) == (t in keep) for t in range(T))
