@@ -256,6 +256,47 @@ def run_decode(torch, px, synth, HookStep, args):
     return out, wl
 
 
+def time_conditional(torch, step, wl, args):
+    """Cost of the two conditional-write filters on the c2 batch: route build
+    plus the filter, minus route build alone (each repeated 20 times inside
+    one graph, so graph launch overhead drops out)."""
+    import paper_2607_22595_amd as px
+    import synth
+    logit = step.layers[0].probes[0].logit[0]            # layer-0 probe, bit 4
+    thr = torch.zeros(1, dtype=torch.float32, device="cuda")
+    V = 128256
+    ids = torch.from_numpy(synth.randint("bench/token_ids", wl.T_max, 0, V - 1)
+                           .astype(np.int32)).cuda()
+    vocab_bits = torch.zeros((V + 31) // 32, dtype=torch.int32, device="cuda")
+    vocab_bits[::7] = -1                                  # a trigger set of ~1/7 of the ids
+
+    def build():
+        px.xmix_route_build(step.req, step.T_valid, step.sub, step.route, step.err)
+
+    reps = 20
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                fn()
+
+        class One:
+            def replay(self):
+                g.replay()
+        one = One()
+        for _ in range(args.warmup):
+            one.replay()
+        return time_replays(torch, one, args.steps) * 1e3 / reps
+
+    base = timed(build)
+    gate = timed(lambda: (build(), px.xmix_route_gate(step.route, 1, logit, thr, signal_bit=4)))
+    trig = timed(lambda: (build(), px.xmix_route_trigger(step.route, 2, ids, vocab_bits, V)))
+    return {"route_build": base, "gate": gate - base, "trigger": trig - base}
+
+
 def run_steer_probe(torch, synth, HookStep, args):
     """The 4-layer decode step of steering and probe apps (d=4096, T=R=256,
     bits 0-3 steer, bits 4-7 probe), captured as one graph."""
@@ -280,6 +321,7 @@ def run_steer_probe(torch, synth, HookStep, args):
            "us_per_step": ms * 1e3, "us_per_layer": ms * 1e3 / len(wl.layers),
            "value": wl.T_valid * len(wl.layers) / (ms * 1e-3), "unit": "hooked tokens/s per layer",
            "hbm_bytes": step.hbm_bytes()}
+    res["conditional_us"] = time_conditional(torch, step, wl, args)
     del step
     torch.cuda.empty_cache()
     return res

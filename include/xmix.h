@@ -123,6 +123,37 @@ xmix_status xmix_route_build(const int32_t *req_of_token, const int32_t *T_valid
                              const uint32_t *sub_mask, int32_t R_max,
                              const xmix_route *rt, uint32_t *err_word, void *stream);
 
+/* ------------------------------------------------------ conditional writes
+ * A conditional write applies only where a condition evaluated on the
+ * device holds (Sec. 4.1, `.cond(...)`; Sec. 4.2, "Condition classes": an
+ * activation-driven condition such as a probe from an earlier layer against
+ * a threshold, or a token-driven one such as the token being in a trigger
+ * list; Sec. 4.3, device-side control flow).  Both calls narrow the routing
+ * entry of one app, in place, after xmix_route_build and before the
+ * write calls that use that app:
+ *   a token keeps bit app_bit only if the condition holds for it; the app's
+ *   count and ascending token list are rebuilt (then -1 up to the old count).
+ * Other apps are untouched; the next xmix_route_build starts afresh.
+ *
+ * xmix_route_gate (activation-driven): the condition is  s >= *threshold
+ * with s = signal[t] (req_of_token NULL; signal [T_max], e.g. a token-mode
+ * probe's logit row) or s = signal[req_of_token[t]] (signal [n_signal] per
+ * request, e.g. a pooled or last-token probe's row); when signal_bit >= 0
+ * the token must also carry that bit (the probe ran on it).  NaN and an
+ * index outside [0, n_signal) fail.  threshold is a device scalar (fp32).
+ *
+ * xmix_route_trigger (token-driven): the condition is that token_ids[t]
+ * (device [T_max] int32) lies in [0, vocab_size) and bit token_ids[t] of the
+ * trigger bitmap vocab_bits (device, (vocab_size + 31) / 32 words) is set.
+ *
+ * Errors: XMIX_E_INVAL for a null pointer or app_bit / signal_bit outside
+ * the route's apps. */
+xmix_status xmix_route_gate(const xmix_route *rt, int32_t app_bit, const float *signal,
+                            const int32_t *req_of_token, int32_t n_signal, int32_t signal_bit,
+                            const float *threshold, void *stream);
+xmix_status xmix_route_trigger(const xmix_route *rt, int32_t app_bit, const int32_t *token_ids,
+                               const uint32_t *vocab_bits, int32_t vocab_size, void *stream);
+
 /* --------------------------------------------------------------- steering
  * Additive steering, the Write primitive (Sec. 3: add or subtract a vector
  * on the activation; Fig. 2b's steering_vector write).  For each token t with

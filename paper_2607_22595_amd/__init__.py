@@ -53,6 +53,8 @@ _sigs = {
     "xmix_status_string": ([_st], ctypes.c_char_p),
     "xmix_version": ([], ctypes.c_char_p),
     "xmix_route_build": ([_vp, _vp, _vp, _i32, ctypes.POINTER(XmixRoute), _vp, _vp], _st),
+    "xmix_route_gate": ([ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32, _i32, _vp, _vp], _st),
+    "xmix_route_trigger": ([ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32, _vp], _st),
     "xmix_steer_apply": ([_vp, _st, _i32, ctypes.POINTER(XmixRoute), _vp, _vp, _vp, _vp, _i32,
                           _i32, _vp], _st),
     "xmix_probe_workspace": ([_i32, _i32, _i32], _sz),
@@ -159,6 +161,27 @@ def xmix_route_build(req_of_token, T_valid, sub_mask, route: Route, err_word, st
     _check("xmix_route_build", _lib.xmix_route_build(
         _ptr(req_of_token), _ptr(T_valid), _ptr(sub_mask), sub_mask.numel(),
         ctypes.byref(route.struct), _ptr(err_word), _stream(stream)))
+
+
+def xmix_route_gate(route: Route, app_bit: int, signal, threshold, signal_bit: int = -1,
+                    req_of_token=None, stream=None):
+    """Activation-driven conditional write: keep app `app_bit` only on tokens
+    whose signal (fp32 [T_max] per token, or [R] per request with
+    req_of_token) is >= the device scalar `threshold`."""
+    assert signal.dtype == torch.float32 and threshold.dtype == torch.float32
+    _check("xmix_route_gate", _lib.xmix_route_gate(
+        ctypes.byref(route.struct), app_bit, _ptr(signal), _ptr(req_of_token), signal.numel(),
+        signal_bit, _ptr(threshold), _stream(stream)))
+
+
+def xmix_route_trigger(route: Route, app_bit: int, token_ids, vocab_bits, vocab_size: int,
+                       stream=None):
+    """Token-driven conditional write: keep app `app_bit` only on tokens whose
+    id (int32 [T_max]) is set in the trigger bitmap (int32 words)."""
+    assert token_ids.dtype == torch.int32 and vocab_bits.numel() * 32 >= vocab_size
+    _check("xmix_route_trigger", _lib.xmix_route_trigger(
+        ctypes.byref(route.struct), app_bit, _ptr(token_ids), _ptr(vocab_bits), vocab_size,
+        _stream(stream)))
 
 
 def xmix_steer_apply(h, route: Route, req_of_token, vecs, app_bits: Sequence[int], alpha,

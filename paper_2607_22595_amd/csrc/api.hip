@@ -63,6 +63,29 @@ xmix_status xmix_route_build(const int32_t* req_of_token, const int32_t* T_valid
                                        err_word, as_stream(stream)));
 }
 
+xmix_status xmix_route_gate(const xmix_route* rt, int32_t app_bit, const float* signal,
+                            const int32_t* req_of_token, int32_t n_signal, int32_t signal_bit,
+                            const float* threshold, void* stream) {
+    if (!route_ok(rt) || !signal || !threshold || app_bit < 0 || app_bit >= rt->n_apps ||
+        signal_bit >= rt->n_apps || n_signal < 1)
+        return XMIX_E_INVAL;
+    if (!req_of_token && n_signal < rt->T_max) return XMIX_E_INVAL;  // per-token signal row
+    return launched(launch_route_gate(rt->T_max, app_bit, rt->tok_mask, rt->app_count,
+                                      rt->app_tokens, signal, req_of_token, n_signal,
+                                      signal_bit < 0 ? -1 : signal_bit, threshold,
+                                      as_stream(stream)));
+}
+
+xmix_status xmix_route_trigger(const xmix_route* rt, int32_t app_bit, const int32_t* token_ids,
+                               const uint32_t* vocab_bits, int32_t vocab_size, void* stream) {
+    if (!route_ok(rt) || !token_ids || !vocab_bits || vocab_size < 1 || app_bit < 0 ||
+        app_bit >= rt->n_apps)
+        return XMIX_E_INVAL;
+    return launched(launch_route_trigger(rt->T_max, app_bit, rt->tok_mask, rt->app_count,
+                                         rt->app_tokens, token_ids, vocab_bits, vocab_size,
+                                         as_stream(stream)));
+}
+
 xmix_status xmix_steer_apply(void* h, xmix_dtype dt, int32_t d, const xmix_route* rt,
                              const int32_t* req_of_token, const void* vecs,
                              const int32_t* app_bits, const float* alpha, int32_t n_steer,

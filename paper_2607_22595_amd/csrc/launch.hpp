@@ -16,6 +16,15 @@ hipError_t launch_route_build(const int32_t* req, const int32_t* T_valid, const 
                               int32_t* app_count, int32_t* app_tokens, uint32_t* err_word,
                               hipStream_t stream);
 
+hipError_t launch_route_gate(int32_t T_max, int32_t app_bit, uint32_t* tok_mask,
+                             int32_t* app_count, int32_t* app_tokens, const float* signal,
+                             const int32_t* req, int32_t n_signal, int32_t signal_bit,
+                             const float* threshold, hipStream_t stream);
+hipError_t launch_route_trigger(int32_t T_max, int32_t app_bit, uint32_t* tok_mask,
+                                int32_t* app_count, int32_t* app_tokens,
+                                const int32_t* token_ids, const uint32_t* vocab_bits,
+                                int32_t vocab_size, hipStream_t stream);
+
 hipError_t launch_steer(void* h, bool bf16, int32_t d, int32_t T_max, const uint32_t* tok_mask,
                         const int32_t* req, const void* vecs, const BitList& bits,
                         const float* alpha, int32_t n_steer, hipStream_t stream);
