@@ -747,23 +747,44 @@ __device__ __forceinline__ void wave_sync() {
 __device__ __forceinline__ int wave_count(bool p) { return __popcll(wave_ballot(p)); }
 
 // Selects the k best of the pool key[0..n) / idx[0..n) (this wave's LDS
-// region, n <= 64 * R).  On return the selection is
+// region, n <= 64 * R) and moves them to lanes 0..k-1 (returned in wk/wi,
+// in pool order; other lanes get key 0).  The selection is
 //   { i : key[i] > tau  or  (key[i] == tau and idx[i] <= cut) }
-// with exactly k entries.  Requires n >= k.  Counts are ballot popcounts
-// (no cross-lane shuffles), R per bisection step.
+// with exactly k entries (requires n >= k); tau is returned.  The keys stay
+// in registers for the whole selection.  tau is found by bisection on the
+// key bits below the highest bit in which the pool's keys differ (counts
+// are ballot popcounts), stopping as soon as the count hits k.
 template <int R>
-__device__ void wave_select(const uint32_t* key, const int32_t* idx, int n, int k,
-                            uint32_t* tau_out, int32_t* cut_out) {
+__device__ void wave_select_take(const uint32_t* key, const int32_t* idx, int n, int k,
+                                 uint32_t* stage_k, int32_t* stage_i, uint32_t* tau_out,
+                                 uint32_t* wk, int32_t* wi) {
     const int lane = lane_id();
     uint32_t kr[R];
+    int32_t ir[R];
+    uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         const int i = lane + kWave * r;
         kr[r] = i < n ? key[i] : 0u;  // real keys are >= 1; 0 never counts
+        ir[r] = i < n ? idx[i] : 0;
+        if (i < n) {
+            kmin = min(kmin, kr[r]);
+            kmax = max(kmax, kr[r]);
+        }
     }
-    uint32_t tau = 0;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        kmin = min(kmin, static_cast<uint32_t>(__shfl_xor(static_cast<int>(kmin), off, kWave)));
+        kmax = max(kmax, static_cast<uint32_t>(__shfl_xor(static_cast<int>(kmax), off, kWave)));
+    }
+    // every key shares the bits of kmin above the highest differing bit, so
+    // the k-th largest does too: start the bisection below it
+    const uint32_t diff = kmin ^ kmax;
+    const int top = diff ? 31 - __builtin_clz(diff) : -1;
+    uint32_t tau = top < 31 ? (kmin & ~((2u << top) - 1u)) : 0u;
+    if (top < 0) tau = kmin;
     bool exact = false;
-    for (int bit = 31; bit >= 0; --bit) {
+    for (int bit = top; bit >= 0; --bit) {
         const uint32_t c = tau | (1u << bit);
         int ge = 0;
 #pragma unroll
@@ -787,12 +808,6 @@ __device__ void wave_select(const uint32_t* key, const int32_t* idx, int n, int 
         const int need = k - gt;
         if (eq > need) {
             // smallest I with #{key == tau and idx <= I} >= need
-            int32_t ir[R];
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const int i = lane + kWave * r;
-                ir[r] = i < n ? idx[i] : 0;
-            }
             int32_t lo = 0;
             for (int bit = 30; bit >= 0; --bit) {
                 const int32_t probe = lo | ((1 << bit) - 1);
@@ -804,32 +819,21 @@ __device__ void wave_select(const uint32_t* key, const int32_t* idx, int n, int 
             cut = lo;
         }
     }
-    *tau_out = tau;
-    *cut_out = cut;
-}
-
-// Moves the selected entries of the pool to lanes 0..k-1 (returned in
-// wk/wi; other lanes get key 0), in a fixed order (pool position).
-template <int R>
-__device__ void wave_take(const uint32_t* key, const int32_t* idx, int n, uint32_t tau,
-                          int32_t cut, uint32_t* stage_k, int32_t* stage_i, uint32_t* wk,
-                          int32_t* wi) {
-    const int lane = lane_id();
+    // compact the selection to the front of the stage area
     int base = 0;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         const int i = lane + kWave * r;
-        const uint32_t kv = i < n ? key[i] : 0u;
-        const int32_t iv = i < n ? idx[i] : 0;
-        const bool take = i < n && (kv > tau || (kv == tau && iv <= cut));
+        const bool take = i < n && (kr[r] > tau || (kr[r] == tau && ir[r] <= cut));
         const uint64_t b = wave_ballot(take);
         if (take) {
-            stage_k[base + lanes_below(b)] = kv;
-            stage_i[base + lanes_below(b)] = iv;
+            stage_k[base + lanes_below(b)] = kr[r];
+            stage_i[base + lanes_below(b)] = ir[r];
         }
         base += __popcll(b);
     }
     wave_sync();
+    *tau_out = tau;
     *wk = lane < base ? stage_k[lane] : 0u;
     *wi = lane < base ? stage_i[lane] : 0x7FFFFFFF;
 }
@@ -961,15 +965,15 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
     bool exact_path = total <= kPoolMax && total >= k;
     if (exact_path) {
         uint32_t tau;
-        int32_t cut;
+        uint32_t* sk = K + kPoolMax;
+        int32_t* si = I + kPoolMax;
         // register footprint matched to the pool size
-        if (total <= 4 * kWave) wave_select<4>(K, I, total, k, &tau, &cut);
-        else if (total <= 8 * kWave) wave_select<8>(K, I, total, k, &tau, &cut);
-        else if (total <= 16 * kWave) wave_select<16>(K, I, total, k, &tau, &cut);
-        else wave_select<kMergeR>(K, I, total, k, &tau, &cut);
+        if (total <= 4 * kWave) wave_select_take<4>(K, I, total, k, sk, si, &tau, &wk, &wi);
+        else if (total <= 8 * kWave) wave_select_take<8>(K, I, total, k, sk, si, &tau, &wk, &wi);
+        else if (total <= 16 * kWave) wave_select_take<16>(K, I, total, k, sk, si, &tau, &wk, &wi);
+        else wave_select_take<kMergeR>(K, I, total, k, sk, si, &tau, &wk, &wi);
         // certificate: nothing left below a slice threshold can beat tau
         exact_path = tau_tiles <= tau;
-        if (exact_path) wave_take<kMergeR>(K, I, total, tau, cut, K + kPoolMax, I + kPoolMax, &wk, &wi);
     }
     if (!exact_path) {
         // exact recompute of this token's m pre-activations, one latent per
@@ -995,12 +999,9 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
             wave_sync();
             const int n_pool = held + kWave;
             if (n_pool > k) {
-                uint32_t tb;
-                int32_t cb;
-                wave_select<2>(K, I, n_pool, k, &tb, &cb);
-                uint32_t a;
+                uint32_t tb, a;
                 int32_t b;
-                wave_take<2>(K, I, n_pool, tb, cb, K + 2 * kWave, I + 2 * kWave, &a, &b);
+                wave_select_take<2>(K, I, n_pool, k, K + 2 * kWave, I + 2 * kWave, &tb, &a, &b);
                 if (lane < k) {
                     K[lane] = a;
                     I[lane] = b;
