@@ -257,6 +257,31 @@ xmix_status xmix_sae_merge_topk(const uint16_t *h, int32_t d, const xmix_route *
                                 int32_t *idx_out, uint16_t *val_out,
                                 void *ws, size_t ws_bytes, void *stream);
 
+/* Encode + TopK with the readback of each encoded row fused in (the merge
+ * writes the ring rows itself, saving the separate compaction pass).  Same
+ * arguments and results as xmix_sae_encode_topk / xmix_sae_merge_topk, plus
+ * the readback of xmix_readback_compact for segments (idx_out, val_out):
+ * rows {t, req_of_token[t], layer_id, app_id} + idx[k] (int32) + val[k]
+ * (bf16) in ascending token order at (head + i) mod capacity, only the last
+ * `capacity` rows of the call written, head advanced by the count.
+ * ring->row_bytes must equal 16 + 6 * k.  Calls that overlap on one ring
+ * race, as for xmix_readback_compact. */
+xmix_status xmix_sae_encode_topk_ring(const uint16_t *h, int32_t d, const xmix_route *rt,
+                                      int32_t app_bit, const uint16_t *W_packed,
+                                      const uint16_t *b_enc, const uint16_t *b_dec,
+                                      const float *c_fold, int32_t m, int32_t k,
+                                      int32_t *idx_out, uint16_t *val_out, void *ws,
+                                      size_t ws_bytes, const int32_t *req_of_token,
+                                      int32_t layer_id, int32_t app_id, const xmix_ring *ring,
+                                      void *stream);
+xmix_status xmix_sae_merge_topk_ring(const uint16_t *h, int32_t d, const xmix_route *rt,
+                                     int32_t app_bit, const uint16_t *W_packed,
+                                     const float *c_fold, int32_t m, int32_t k,
+                                     int32_t *idx_out, uint16_t *val_out, void *ws,
+                                     size_t ws_bytes, const int32_t *req_of_token,
+                                     int32_t layer_id, int32_t app_id, const xmix_ring *ring,
+                                     void *stream);
+
 /* One-time repack of a row-major encoder dictionary W_enc [m, d] (bf16)
  * into the tiled layout the encode kernels stream (same bytes, permuted).
  * W_packed must not overlap W_enc.  Requires m % 256 == 0, d % 256 == 0. */

@@ -67,6 +67,12 @@ _sigs = {
                                     _vp, _i32, _i32, _vp, _sz, _vp], _st),
     "xmix_sae_merge_topk": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32, _i32,
                              _vp, _vp, _vp, _sz, _vp], _st),
+    "xmix_sae_encode_topk_ring": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _vp,
+                                   _vp, _i32, _i32, _vp, _vp, _vp, _sz, _vp, _i32, _i32,
+                                   ctypes.POINTER(XmixRing), _vp], _st),
+    "xmix_sae_merge_topk_ring": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32,
+                                  _i32, _vp, _vp, _vp, _sz, _vp, _i32, _i32,
+                                  ctypes.POINTER(XmixRing), _vp], _st),
     "xmix_sae_pack_encoder": ([_vp, _i32, _i32, _vp, _vp], _st),
     "xmix_sae_fold_bias": ([_vp, _vp, _vp, _i32, _i32, _vp, _vp], _st),
     "xmix_sae_clamp_decode": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32, _vp,
@@ -260,6 +266,35 @@ def xmix_sae_encode_topk(h, route: Route, app_bit: int, W_enc, b_enc, b_dec, c_f
     _check("xmix_sae_encode_topk", _lib.xmix_sae_encode_topk(
         _ptr(h), d, ctypes.byref(route.struct), app_bit, _ptr(W_enc), _ptr(b_enc), _ptr(b_dec),
         _ptr(c_fold), m, k, _ptr(idx_out), _ptr(val_out), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def xmix_sae_encode_topk_ring(h, route: Route, app_bit: int, W_enc, b_enc, b_dec, c_fold,
+                              k: int, idx_out, val_out, ws, req_of_token, layer_id: int,
+                              app_id: int, ring: Ring, stream=None):
+    """xmix_sae_encode_topk with the ring readback of (idx, val) rows fused
+    into the merge; ring.row_bytes must be 16 + 6 k."""
+    T_max, d = h.shape
+    m = W_enc.shape[0]
+    assert h.dtype == torch.bfloat16 and W_enc.dtype == torch.bfloat16
+    assert idx_out.dtype == torch.int32 and idx_out.shape == (T_max, k)
+    assert val_out.dtype == torch.bfloat16 and val_out.shape == (T_max, k)
+    assert req_of_token.dtype == torch.int32 and req_of_token.numel() == T_max
+    _check("xmix_sae_encode_topk_ring", _lib.xmix_sae_encode_topk_ring(
+        _ptr(h), d, ctypes.byref(route.struct), app_bit, _ptr(W_enc), _ptr(b_enc), _ptr(b_dec),
+        _ptr(c_fold), m, k, _ptr(idx_out), _ptr(val_out), _ptr(ws), ws.numel() * ws.element_size(),
+        _ptr(req_of_token), layer_id, app_id, ctypes.byref(ring.struct), _stream(stream)))
+
+
+def xmix_sae_merge_topk_ring(h, route: Route, app_bit: int, W_enc, c_fold, k: int, idx_out,
+                             val_out, ws, req_of_token, layer_id: int, app_id: int, ring: Ring,
+                             stream=None):
+    """Stage 2 of the encode with the fused ring readback."""
+    T_max, d = h.shape
+    m = W_enc.shape[0]
+    _check("xmix_sae_merge_topk_ring", _lib.xmix_sae_merge_topk_ring(
+        _ptr(h), d, ctypes.byref(route.struct), app_bit, _ptr(W_enc), _ptr(c_fold), m, k,
+        _ptr(idx_out), _ptr(val_out), _ptr(ws), ws.numel() * ws.element_size(),
+        _ptr(req_of_token), layer_id, app_id, ctypes.byref(ring.struct), _stream(stream)))
 
 
 def xmix_sae_encode_candidates(h, route: Route, app_bit: int, W_enc, b_enc, b_dec, c_fold,

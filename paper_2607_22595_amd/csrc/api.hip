@@ -210,7 +210,54 @@ xmix_status xmix_sae_merge_topk(const uint16_t* h, int32_t d, const xmix_route* 
     if (st != XMIX_OK) return st;
     return launched(launch_sae_merge(h, d, rt->T_max, rt->app_count + app_bit,
                                      app_list(rt, app_bit), W_packed, c_fold ? c_fold : fold, m,
-                                     k, idx_out, val_out, cand, as_stream(stream)));
+                                     k, idx_out, val_out, cand, nullptr, as_stream(stream)));
+}
+
+xmix_status xmix_sae_merge_topk_ring(const uint16_t* h, int32_t d, const xmix_route* rt,
+                                     int32_t app_bit, const uint16_t* W_packed,
+                                     const float* c_fold, int32_t m, int32_t k,
+                                     int32_t* idx_out, uint16_t* val_out, void* ws,
+                                     size_t ws_bytes, const int32_t* req_of_token,
+                                     int32_t layer_id, int32_t app_id, const xmix_ring* ring,
+                                     void* stream) {
+    if (!h || !W_packed || !idx_out || !val_out || !req_of_token || !ring) return XMIX_E_INVAL;
+    if (!ring->slots || !ring->head || ring->capacity < 1 ||
+        ring->row_bytes != 16 + 6 * k || (reinterpret_cast<uintptr_t>(ring->slots) & 3u) != 0 ||
+        (reinterpret_cast<uintptr_t>(ring->head) & 7u) != 0)
+        return XMIX_E_INVAL;
+    float* fold;
+    void* cand;
+    const xmix_status st =
+        encode_args(h, d, rt, app_bit, W_packed, m, k, ws, ws_bytes, &fold, &cand);
+    if (st != XMIX_OK) return st;
+    MergeRing r;
+    r.slots = ring->slots;
+    r.head = ring->head;
+    r.capacity = ring->capacity;
+    r.row_bytes = ring->row_bytes;
+    r.req = req_of_token;
+    r.layer_id = layer_id;
+    r.app_id = app_id;
+    return launched(launch_sae_merge(h, d, rt->T_max, rt->app_count + app_bit,
+                                     app_list(rt, app_bit), W_packed, c_fold ? c_fold : fold, m,
+                                     k, idx_out, val_out, cand, &r, as_stream(stream)));
+}
+
+xmix_status xmix_sae_encode_topk_ring(const uint16_t* h, int32_t d, const xmix_route* rt,
+                                      int32_t app_bit, const uint16_t* W_enc,
+                                      const uint16_t* b_enc, const uint16_t* b_dec,
+                                      const float* c_fold, int32_t m, int32_t k,
+                                      int32_t* idx_out, uint16_t* val_out, void* ws,
+                                      size_t ws_bytes, const int32_t* req_of_token,
+                                      int32_t layer_id, int32_t app_id, const xmix_ring* ring,
+                                      void* stream) {
+    if (!idx_out || !val_out || !req_of_token || !ring || ring->row_bytes != 16 + 6 * k)
+        return XMIX_E_INVAL;
+    const xmix_status st = xmix_sae_encode_candidates(h, d, rt, app_bit, W_enc, b_enc, b_dec,
+                                                      c_fold, m, k, ws, ws_bytes, stream);
+    if (st != XMIX_OK) return st;
+    return xmix_sae_merge_topk_ring(h, d, rt, app_bit, W_enc, c_fold, m, k, idx_out, val_out,
+                                    ws, ws_bytes, req_of_token, layer_id, app_id, ring, stream);
 }
 
 xmix_status xmix_sae_encode_topk(const uint16_t* h, int32_t d, const xmix_route* rt,

@@ -44,11 +44,18 @@ hipError_t launch_sae_candidates(const uint16_t* h, int32_t d, int32_t T_max,
                                  const int32_t* app_count, const int32_t* tok_list,
                                  const uint16_t* W_enc, const float* c_fold, int32_t m,
                                  int32_t k, void* cand, hipStream_t stream);
+struct MergeRing {  // readback of the merged rows into a ring
+    uint8_t* slots;
+    uint64_t* head;
+    int32_t capacity, row_bytes;
+    const int32_t* req;
+    int32_t layer_id, app_id;
+};
 hipError_t launch_sae_merge(const uint16_t* h, int32_t d, int32_t T_max,
                             const int32_t* app_count, const int32_t* tok_list,
                             const uint16_t* W_enc, const float* c_fold, int32_t m, int32_t k,
                             int32_t* idx_out, uint16_t* val_out, void* cand,
-                            hipStream_t stream);
+                            const MergeRing* ring, hipStream_t stream);
 
 hipError_t launch_clamp_decode(uint16_t* h, int32_t d, const int32_t* app_count,
                                const int32_t* tok_list, int32_t T_max, const int32_t* idx,

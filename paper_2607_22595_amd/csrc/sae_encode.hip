@@ -860,6 +860,27 @@ __device__ __forceinline__ void wave_sort_desc(uint32_t& key, int32_t& idx) {
     }
 }
 
+// Optional readback of the merged rows into a ring (same row format and
+// head protocol as the readback compaction).
+struct RingOut {
+    uint8_t* slots;     // null: no readback
+    uint64_t* head;     // [2]: head, ticket counter (zero between calls)
+    int32_t capacity, row_bytes;
+    const int32_t* req;
+    int32_t layer_id, app_id;
+};
+
+// The workgroup's ticket; the last of gridDim.x advances the head by `cnt`
+// (every workgroup read the head before its ticket) and resets the counter.
+__device__ __forceinline__ void ring_ticket(const RingOut& ring, uint64_t h0, int cnt) {
+    __threadfence();
+    const uint64_t ticket = atomicAdd(reinterpret_cast<unsigned long long*>(&ring.head[1]), 1ull);
+    if (ticket == gridDim.x - 1) {
+        __atomic_store_n(&ring.head[0], h0 + static_cast<uint64_t>(cnt), __ATOMIC_RELAXED);
+        atomicExch(reinterpret_cast<unsigned long long*>(&ring.head[1]), 0ull);
+    }
+}
+
 constexpr int kMergeThreads = 256;
 constexpr int kMergeR = 32;                        // pool entries per lane
 constexpr int kPoolMax = kMergeR * kWave;          // 2048
@@ -875,14 +896,23 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
                  const int32_t* __restrict__ app_count, const int32_t* __restrict__ tok_list,
                  int32_t k, const uint16_t* __restrict__ h, int32_t d,
                  const uint16_t* __restrict__ Wp, const float* __restrict__ c_fold,
-                 int32_t* __restrict__ idx_out, uint16_t* __restrict__ val_out) {
+                 int32_t* __restrict__ idx_out, uint16_t* __restrict__ val_out,
+                 RingOut ring) {
     __shared__ uint32_t K[kPoolMax + kWave];
     __shared__ int32_t I[kPoolMax + kWave];
     __shared__ int scan_s[kMergeThreads / kWave];
     __shared__ uint32_t tmax_s[kMergeThreads / kWave];
     const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
     const int n = blockIdx.x;
-    if (n >= *app_count) return;  // uniform over the workgroup
+    const int cnt = *app_count;
+    // readback ring (optional): every workgroup reads the head before it
+    // takes a ticket; the one drawing the last ticket advances the head
+    uint64_t h0 = 0;
+    if (ring.slots && tid == 0) h0 = __atomic_load_n(&ring.head[0], __ATOMIC_RELAXED);
+    if (n >= cnt) {  // uniform over the workgroup
+        if (ring.slots && tid == 0) ring_ticket(ring, h0, cnt);
+        return;
+    }
     const int32_t t = tok_list[n];
     const int64_t row0 = static_cast<int64_t>(n) * n_mt;
 
@@ -1017,10 +1047,31 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
     }
     // order the k winners by (value desc, index asc) and write them
     wave_sort_desc(wk, wi);
+    const uint16_t vb = f32_to_bf16_rne(fmaxf(key_f32(wk), 0.0f));
     if (lane < k) {
         const int64_t o = static_cast<int64_t>(t) * k + lane;
         idx_out[o] = wi;
-        val_out[o] = f32_to_bf16_rne(fmaxf(key_f32(wk), 0.0f));
+        val_out[o] = vb;
+    }
+    if (ring.slots) {
+        // ring row {token, request, layer, app} + idx[k] + val[k]; only the
+        // last `capacity` rows of this call are written
+        h0 = static_cast<uint64_t>(__shfl(static_cast<long long>(h0), 0, kWave));
+        if (static_cast<int64_t>(n) >= static_cast<int64_t>(cnt) - ring.capacity) {
+            uint8_t* row = ring.slots + static_cast<int64_t>((h0 + static_cast<uint64_t>(n)) %
+                                                             static_cast<uint64_t>(ring.capacity)) *
+                                            ring.row_bytes;
+            if (lane < 4) {
+                const int32_t hdr = lane == 0 ? t : lane == 1 ? ring.req[t]
+                                  : lane == 2 ? ring.layer_id : ring.app_id;
+                reinterpret_cast<int32_t*>(row)[lane] = hdr;
+            }
+            if (lane < k) {
+                reinterpret_cast<int32_t*>(row + 16)[lane] = wi;
+                reinterpret_cast<uint16_t*>(row + 16 + 4 * k)[lane] = vb;
+            }
+        }
+        if (lane == 0) ring_ticket(ring, h0, cnt);
     }
 }
 
@@ -1145,13 +1196,23 @@ hipError_t launch_sae_merge(const uint16_t* h, int32_t d, int32_t T_max,
                             const int32_t* app_count, const int32_t* tok_list,
                             const uint16_t* W_enc, const float* c_fold, int32_t m, int32_t k,
                             int32_t* idx_out, uint16_t* val_out, void* cand,
-                            hipStream_t stream) {
+                            const MergeRing* ring, hipStream_t stream) {
     const int32_t n_mt = m / kBM;
     const EmitPlan e = emit_plan(m, k);
     const CandArea a = cand_area(cand, T_max, n_mt, e.cap);
+    RingOut r{};
+    if (ring) {
+        r.slots = ring->slots;
+        r.head = ring->head;
+        r.capacity = ring->capacity;
+        r.row_bytes = ring->row_bytes;
+        r.req = ring->req;
+        r.layer_id = ring->layer_id;
+        r.app_id = ring->app_id;
+    }
     hipLaunchKernelGGL(sae_merge_kernel, dim3(T_max), dim3(kMergeThreads), 0, stream, a.cand,
                        a.cnt, a.tau, n_mt, e.cap, app_count, tok_list, k, h, d, W_enc,
-                       c_fold, idx_out, val_out);
+                       c_fold, idx_out, val_out, r);
     return hipGetLastError();
 }
 

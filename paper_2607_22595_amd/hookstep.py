@@ -10,7 +10,8 @@ order for every layer:
   2. reads of the activation as the model produced it: per-token probes,
      mean-pooled probes, SAE encodes;
   3. writes: steering, then each SAE app's clamp-decode;
-  4. readback of SAE results into each app's ring.
+  4. readback of SAE results into each app's ring (by default fused into
+     the encode's merge, which writes the ring rows itself).
 
 Reads before writes means every app at a hook sees the same activation,
 whatever else is subscribed.  All buffers are allocated here, once; ``run``
@@ -28,6 +29,7 @@ import torch
 from . import (XMIX_PROBE_LAST, XMIX_PROBE_MEAN, XMIX_PROBE_TOKEN, Ring, Route, probe_workspace,
                sae_encode_workspace, xmix_probe_score, xmix_readback_compact,
                xmix_route_build, xmix_sae_clamp_decode, xmix_sae_encode_topk,
+               xmix_sae_encode_topk_ring,
                xmix_sae_fold_bias, xmix_sae_pack_encoder, xmix_steer_apply)
 
 
@@ -85,9 +87,10 @@ class _Layer:
 
 
 class HookStep:
-    def __init__(self, wl, device="cuda", fold_bias: bool = True):
+    def __init__(self, wl, device="cuda", fold_bias: bool = True, fuse_readback: bool = True):
         dev = torch.device(device)
         self.wl = wl
+        self.fuse_readback = fuse_readback
         self.device = dev
         act = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
         self.req = to_device(wl.req, torch.int32, dev)
@@ -156,8 +159,14 @@ class HookStep:
                 xmix_probe_score(lay.h, self.route, p.w, p.b, p.bits, p.mode, p.logit, p.score,
                                  cu_seqlens=self.cu, ws=p.ws, stream=stream)
             for s in lay.saes:
-                xmix_sae_encode_topk(lay.h, self.route, s.bit, s.W_enc, s.b_enc, s.b_dec,
-                                     s.c_fold, s.k, s.idx, s.val, s.ws, stream)
+                if s.ring is not None and self.fuse_readback:
+                    # the merge writes the ring rows itself
+                    xmix_sae_encode_topk_ring(lay.h, self.route, s.bit, s.W_enc, s.b_enc, s.b_dec,
+                                              s.c_fold, s.k, s.idx, s.val, s.ws, self.req,
+                                              lay.layer_id, s.bit, s.ring, stream)
+                else:
+                    xmix_sae_encode_topk(lay.h, self.route, s.bit, s.W_enc, s.b_enc, s.b_dec,
+                                         s.c_fold, s.k, s.idx, s.val, s.ws, stream)
             if lay.steer_v is not None:
                 xmix_steer_apply(lay.h, self.route, self.req, lay.steer_v, lay.steer_bits,
                                  self.alpha, stream)
@@ -166,7 +175,7 @@ class HookStep:
                     xmix_sae_clamp_decode(lay.h, self.route, s.bit, s.idx, s.val, s.W_dec,
                                           s.clamp_ids, s.clamp_vals, stream=stream)
             for s in lay.saes:
-                if s.ring is not None:
+                if s.ring is not None and not self.fuse_readback:
                     xmix_readback_compact([s.idx, s.val], self.route, s.bit, self.req,
                                           lay.layer_id, s.bit, s.ring, stream)
 

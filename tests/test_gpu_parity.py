@@ -413,6 +413,42 @@ def test_readback_more_rows_than_capacity(px):
     assert np.array_equal(ring.slots.cpu().numpy(), slots)
 
 
+@pytest.mark.parametrize("T,n_sub,cap,k", [(100, 50, 64, 16), (1500, 1100, 500, 8)])
+def test_encode_with_fused_readback_bit_exact(px, T, n_sub, cap, k):
+    """The merge writes the ring rows itself: same rows and head as the
+    compaction of the encode's own outputs (3 calls: wrap-around and, in the
+    second case, more rows per call than slots, on the prefill GEMM path)."""
+    wl = synth.make("c3", d=256, m=1024, k=k, T=T, n_sub=n_sub, ring_capacity=cap)
+    sae = wl.layers[0].saes[0]
+    rt, _ = gpu_route(px, wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    h = dev_bits(wl.layers[0].h)
+    W = px.xmix_sae_pack_encoder(dev_bits(sae.W_enc))
+    be, bd = dev_bits(sae.b_enc), dev_bits(sae.b_dec)
+    c = torch.empty(sae.m, dtype=torch.float32, device="cuda")
+    px.xmix_sae_fold_bias(W, be, bd, c)
+    idx_d = torch.full((T, k), -7, dtype=torch.int32, device="cuda")
+    val_d = torch.zeros((T, k), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(px.sae_encode_workspace(T, wl.d, sae.m, k), dtype=torch.uint8, device="cuda")
+    row = 16 + 6 * k
+    ring = px.Ring(cap, row)
+    tm = rt.tok_mask.cpu().numpy().view(np.uint32)
+    slots = np.zeros((cap, row), np.uint8)
+    head = 0
+    for step in range(3):
+        px.xmix_sae_encode_topk_ring(h, rt, sae.bit, W, be, bd, c, k, idx_d, val_d, ws,
+                                     dev_i32(wl.req), 5, sae.bit, ring)
+        torch.cuda.synchronize()
+        idx, val = idx_d.cpu().numpy(), torch_bits(val_d)
+        slots, head = oracle.compact([idx.view(np.uint8).reshape(T, -1),
+                                      val.view(np.uint8).reshape(T, -1)],
+                                     tm, sae.bit, wl.req, 5, sae.bit, slots, head)
+        assert int(ring.head[0].item()) == head == (step + 1) * n_sub
+        assert int(ring.head[1].item()) == 0
+        assert np.array_equal(ring.slots.cpu().numpy(), slots)
+    toks = np.flatnonzero(tm & 1)
+    _check_encode(wl, sae, wl.layers[0].h, idx, val, toks[:40])
+
+
 def test_encode_recompute_path_when_winners_crowd_one_slice(px):
     """50 of a token's top-64 planted in one 256-latent slice: more than the
     slice may emit, so the merge's certificate fails for that token and it
