@@ -416,6 +416,9 @@ constexpr int kGBlkLat = 4;         // XCD block: latent tiles
 // pieces hit distinct banks.
 __device__ __forceinline__ int gsw(int n) { return ((n >> 3) ^ (n >> 4)) & 3; }
 
+// Word 3 of a raw buffer resource (32-bit element format, no swizzle).
+constexpr int kBufferDword3 = 0x00020000;
+
 // s_waitcnt: at most n vector-memory operations of this wave outstanding
 // and no LDS operation.
 #define XMIX_WAIT_VM_LGKM0(n) \
@@ -481,28 +484,40 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
     const uint4* X4 = reinterpret_cast<const uint4*>(xs_g);
     const int64_t wstride = static_cast<int64_t>(n_mt) * 2048;  // pieces per K chunk of 64
     const int64_t xplane = static_cast<int64_t>(n_pad) * 4;     // pieces per stage plane
-    // copy sources: lane-contiguous LDS destinations q*256 + wave*64 + lane
+    // copy sources, in pieces from the start of the stage's operand block
+    // (lane-contiguous LDS destinations q*256 + wave*64 + lane)
     int wsrc[4], xsrc[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
         const int P = q * 256 + wave * 64 + lane;
-        wsrc[q] = mt * 2048 + (P >> 7) * 256 + (P & 127);
+        wsrc[q] = (P >> 7) * 256 + (P & 127);
         const int n = P >> 2;
-        xsrc[q] = (n0 + n) * 4 + ((P & 3) ^ gsw(n));
+        xsrc[q] = n * 4 + ((P & 3) ^ gsw(n));
     }
+    W4 += static_cast<int64_t>(mt) * 2048;  // this tile's latent slice
+    X4 += static_cast<int64_t>(n0) * 4;     // this tile's tokens
     // issue the 8 copies of stage j (past the end: the last stage again,
-    // which keeps the loop free of branches that would split the schedule)
+    // which keeps the loop free of branches that would split the schedule).
+    // Each copy is a buffer load whose resource covers exactly the stage's
+    // operand block (its base and size are scalar), so the per-lane offset is
+    // a fixed 32-bit value and an offset outside the block would read zeros.
     auto copy_stage = [&](int j, uint4* wdst, uint4* xdst) __attribute__((always_inline)) {
         j = min(j, nS - 1);
         const int kc = j >> 1, hh = j & 1;
-        const uint4* wsrc_j = W4 + kc * wstride + hh * 128;
-        const uint4* xsrc_j = X4 + j * xplane;
+        const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint4*>(W4 + kc * wstride + hh * 128), 0, 2048 * 16, kBufferDword3);
+        const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint4*>(X4 + j * xplane), 0, kStagePieces * 16, kBufferDword3);
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-            __builtin_amdgcn_global_load_lds(wsrc_j + wsrc[q], wdst + q * 256 + wave * 64, 16, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                wr, (__attribute__((address_space(3))) void*)(wdst + q * 256 + wave * 64),
+                16, static_cast<unsigned>(wsrc[q]) * 16u, 0, 0, 0);
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-            __builtin_amdgcn_global_load_lds(xsrc_j + xsrc[q], xdst + q * 256 + wave * 64, 16, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                xr, (__attribute__((address_space(3))) void*)(xdst + q * 256 + wave * 64),
+                16, static_cast<unsigned>(xsrc[q]) * 16u, 0, 0, 0);
     };
 
     // accumulators start at the folded bias of their latent:
