@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample")
+    ap.add_argument("--c5", action="store_true",
+                    help="also time the 70B-shaped decode step (d=8192, T=R=512, 16 steering, "
+                         "8 probe and 8 SAE clamp apps with 1 GiB dictionaries each)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run three device copies of 512 MiB, the known-size reference "
                          "for scaling HBM counter readings")
@@ -208,6 +211,8 @@ def main():
         out["steer_probe"] = run_steer_probe(torch, synth, HookStep, args)
     if not args.no_prefill:
         out["prefill"] = run_prefill(torch, px, synth, HookStep, args)
+    if args.c5:
+        out["decode_70b"] = run_c5(torch, synth, HookStep, args)
     if not args.no_cpu_baseline and not args.no_decode:
         log("timing the CPU oracle")
         out["cpu_baseline"] = cpu_baseline_decode(wl, args.cpu_seconds)
@@ -323,6 +328,51 @@ def run_steer_probe(torch, synth, HookStep, args):
            "hbm_bytes": step.hbm_bytes()}
     res["conditional_us"] = time_conditional(torch, step, wl, args)
     del step
+    torch.cuda.empty_cache()
+    return res
+
+
+def run_c5(torch, synth, HookStep, args):
+    """The 70B-shaped decode step: steering, probes and eight SAE clamp apps,
+    each encoding its subscribers over its own 1 GiB dictionary, captured as
+    one graph.  The eight dictionaries (8 GiB) exceed every cache, so each
+    replay streams them from HBM."""
+    log("generating the 70B-shaped decode workload (8 dictionaries)")
+    wl = synth.make("c5")
+    step = HookStep(wl)
+    step.run()
+    torch.cuda.synchronize()
+    # every replay starts from the same residual rows (steering and clamping
+    # write them), restored by a device copy that is timed on its own too
+    graphs = {}
+    for name, body in (("step", lambda: (step.reset(), step.run())), ("restore", step.reset)):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            body()
+        graphs[name] = g
+
+    class One:
+        def __init__(self, g):
+            self.g = g
+
+        def replay(self):
+            self.g.replay()
+    log("timing the 70B-shaped decode step")
+    times = {}
+    for name, g in graphs.items():
+        one = One(g)
+        for _ in range(3):
+            one.replay()
+        times[name] = time_replays(torch, one, max(10, args.steps // 10))
+    ms = times["step"] - times["restore"]
+    nbytes = step.hbm_bytes()
+    res = {"workload": "decode step d=8192 T=R=512: 16 steering, 8 probe and 8 SAE clamp apps "
+                       "(m=65536, k=64, 4 clamped features each), subscriptions Bernoulli(0.2)",
+           "ms_per_step": ms, "restore_ms": times["restore"],
+           "value": wl.T_valid / (ms * 1e-3), "unit": "tokens/s",
+           "algorithmic_bytes": nbytes, "achieved_GBps": nbytes / (ms * 1e-3) / 1e9,
+           "frac_of_hbm_peak": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+    del step, graphs
     torch.cuda.empty_cache()
     return res
 

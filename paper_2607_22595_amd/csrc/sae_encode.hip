@@ -25,8 +25,11 @@
 // all m latents whenever the k-th selected value is >= every tile's tau,
 // because a latent that was not emitted lies below its tile's tau.  When
 // that certificate fails (only for inputs whose best latents crowd into a
-// few tiles), the workgroup recomputes the token's m pre-activations with
-// plain fp32 dot products and selects exactly from those.
+// few tiles), the workgroup recomputes the failing tiles' 256
+// pre-activations with plain fp32 dot products and selects again.  The
+// first threshold guess of a tile leaves its strongest values out of the
+// statistics (above mean + 4 stdev), so that a few strong latents, such as
+// features clamped high by a steering app, do not lift it.
 //
 // The workgroup-to-tile map is XCD-aware: launch slots are dealt round-robin
 // to the 8 XCDs, so consecutive tiles of one XCD share a dictionary slice in
@@ -47,9 +50,22 @@ constexpr int kBK = 64;   // K chunk
 constexpr int kEncWaves = 8;
 constexpr int kEncThreads = kEncWaves * kWave;
 constexpr int kRefineIters = 24;
+// Values above mean + kTrimZ * stdev of a tile's 256 pre-activations are left
+// out of the statistics behind the first threshold guess (one strong latent
+// would otherwise raise the guess for its whole tile); kTrimCount packs
+// their number into the count reduction.
+constexpr float kTrimZ = 4.0f;
+constexpr float kTrimCount = 512.0f;
 constexpr int kLatentFastTiles = 4;  // token tiles up to which the latent tile runs fastest
 constexpr int kBlkTok = 8;           // prefill block: token tiles
 constexpr int kBlkLat = 4;           // prefill block: latent tiles
+
+// mean + z * stdev of n values with sum s1 and sum of squares s2
+__device__ __forceinline__ float trimmed_guess(float s1, float s2, int n, float z) {
+    const float inv = 1.0f / static_cast<float>(n > 0 ? n : 1);
+    const float mu = s1 * inv;
+    return mu + z * sqrtf(fmaxf(s2 * inv - mu * mu, 0.0f));
+}
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& v) {
     return __builtin_bit_cast(bf16x8_t, v);
@@ -121,6 +137,7 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     __shared__ uint4 xs[2][kBN * 8];          // 2 x 16 KiB token chunks
     __shared__ float red1[kEncWaves][kBN];    // per-wave partials of the epilogue
     __shared__ float red2[kEncWaves][kBN];
+    __shared__ float red3[kEncWaves][kBN];
     __shared__ int cnt_s[kBN];
 
     // Tile order.  Few token tiles (decode): latent tile fastest, so the
@@ -287,7 +304,7 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
         }
     }
     __syncthreads();
-    float tau[4], lo_b[4], hi_b[4];
+    float tau[4], lo_b[4], hi_b[4], sum1[4], sum2[4], cut[4];
     bool bad[4];
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
@@ -301,11 +318,16 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
         const float mu = s1 * (1.0f / kBM);
         const float sd = sqrtf(fmaxf(s2 * (1.0f / kBM) - mu * mu, 0.0f));
         tau[nb] = mu + z_guess * sd;
+        sum1[nb] = s1;
+        sum2[nb] = s2;
+        cut[nb] = mu + kTrimZ * sd;
         lo_b[nb] = -INFINITY;  // count(lo_b) > cap
         hi_b[nb] = INFINITY;   // count(hi_b) < lo_cnt (or 0)
         bad[nb] = false;
     }
-    // count(pre >= tau) per token; refine tau until lo_cnt <= count <= cap
+    // count(pre >= tau) per token; refine tau until lo_cnt <= count <= cap.
+    // The first count also sums the values above the trim cut, and a token
+    // that has any takes its guess again from the statistics without them.
     for (int it = 0; it < kRefineIters; ++it) {
         __syncthreads();  // red1 is reused
 #pragma unroll
@@ -313,6 +335,22 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
             float c = 0.0f;
 #pragma unroll
             for (int r = 0; r < 16; ++r) c += acc[nb][r] >= tau[nb] ? 1.0f : 0.0f;
+            if (it == 0) {
+                float e1 = 0.0f, e2 = 0.0f;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const bool o = acc[nb][r] > cut[nb];
+                    c += o ? kTrimCount : 0.0f;
+                    e1 += o ? acc[nb][r] : 0.0f;
+                    e2 = fmaf(o ? acc[nb][r] : 0.0f, acc[nb][r], e2);
+                }
+                e1 += __shfl_xor(e1, 32, kWave);
+                e2 += __shfl_xor(e2, 32, kWave);
+                if (g == 0) {
+                    red2[wave][32 * nb + j32] = e1;
+                    red3[wave][32 * nb + j32] = e2;
+                }
+            }
             c += __shfl_xor(c, 32, kWave);
             if (g == 0) red1[wave][32 * nb + j32] = c;
         }
@@ -324,7 +362,12 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
             float c = 0.0f;
 #pragma unroll
             for (int w = 0; w < kEncWaves; ++w) c += red1[w][n];
-            const int cn = static_cast<int>(c);
+            int cn = static_cast<int>(c);
+            int ne = 0;
+            if (it == 0) {
+                ne = cn / static_cast<int>(kTrimCount);
+                cn -= ne * static_cast<int>(kTrimCount);
+            }
             bad[nb] = false;
             if (n < ntok) {
                 if (cn > cap) {
@@ -333,6 +376,20 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
                 } else if (cn < lo_cnt) {
                     hi_b[nb] = tau[nb];
                     bad[nb] = true;
+                }
+            }
+            if (ne > 0 && n < ntok) {
+                float e1 = 0.0f, e2 = 0.0f;
+#pragma unroll
+                for (int w = 0; w < kEncWaves; ++w) {
+                    e1 += red2[w][n];
+                    e2 += red3[w][n];
+                }
+                const float t = trimmed_guess(sum1[nb] - e1, sum2[nb] - e2, kBM - ne, z_guess);
+                if (t > lo_b[nb] && t < hi_b[nb]) {
+                    tau[nb] = t;
+                    any_bad = true;
+                    continue;
                 }
             }
             if (bad[nb]) {
@@ -451,6 +508,7 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
     __shared__ uint4 xsA[kStagePieces], xsB[kStagePieces], xsC[kStagePieces], xsD[kStagePieces];
     __shared__ float red1[2][kGemmTok];
     __shared__ float red2[2][kGemmTok];
+    __shared__ float red3[2][kGemmTok];
     __shared__ int cnt_s[kGemmTok];
 
     // Tile order: launch slot L runs on XCD L % 8, which owns the latent
@@ -669,9 +727,11 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
             red2[wm][n] = s2;
         }
         __syncthreads();
-        const float mu = (red1[0][n] + red1[1][n]) * (1.0f / 256.0f);
-        const float sd = sqrtf(fmaxf((red2[0][n] + red2[1][n]) * (1.0f / 256.0f) - mu * mu, 0.0f));
+        const float sum1 = red1[0][n] + red1[1][n], sum2 = red2[0][n] + red2[1][n];
+        const float mu = sum1 * (1.0f / 256.0f);
+        const float sd = sqrtf(fmaxf(sum2 * (1.0f / 256.0f) - mu * mu, 0.0f));
         float tau = mu + z_guess * sd;
+        const float cut = mu + kTrimZ * sd;
         float lo_b = -INFINITY, hi_b = INFINITY;
         uint32_t m0 = 0, m1 = 0;  // bit i: v[i] >= tau (m1: v[32 + i])
         bool gave_up = false;
@@ -685,14 +745,47 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
             }
             return __popc(m0) + __popc(m1);
         };
-        // count(pre >= tau) per token; refine tau until lo_cnt <= count <= cap
+        // count(pre >= tau) per token; refine tau until lo_cnt <= count <= cap.
+        // The first count also sums the values above the trim cut (all of
+        // them are among the counted ones: the cut lies above tau), and a
+        // token that has any takes its guess again without them.
         for (int it = 0; it < kRefineIters; ++it) {
             const int c_lane = count_at(tau);
-            const float c = static_cast<float>(c_lane + __shfl_xor(c_lane, 32, kWave));
-            __syncthreads();  // red1 is reused
-            if (g == 0) red1[wm][n] = c;
+            int ne = 0;
+            float e1 = 0.0f, e2 = 0.0f;
+            if (it == 0) {
+                uint32_t b0 = m0, b1 = m1;
+                while (b0 | b1) {
+                    const int i = b0 ? __builtin_ctz(b0) : 32 + __builtin_ctz(b1);
+                    if (b0) b0 &= b0 - 1;
+                    else b1 &= b1 - 1;
+                    const float val = park[((i >> 2) * 64 + lane) * 4 + (i & 3)];
+                    if (val > cut) {
+                        ++ne;
+                        e1 += val;
+                        e2 = fmaf(val, val, e2);
+                    }
+                }
+                e1 += __shfl_xor(e1, 32, kWave);
+                e2 += __shfl_xor(e2, 32, kWave);
+            }
+            const int cp = c_lane + static_cast<int>(kTrimCount) * ne;
+            const float c = static_cast<float>(cp + __shfl_xor(cp, 32, kWave));
+            __syncthreads();  // red1..red3 are reused
+            if (g == 0) {
+                red1[wm][n] = c;
+                if (it == 0) {
+                    red2[wm][n] = e1;
+                    red3[wm][n] = e2;
+                }
+            }
             __syncthreads();
-            const int cn = static_cast<int>(red1[0][n] + red1[1][n]);
+            int cn = static_cast<int>(red1[0][n] + red1[1][n]);
+            int nt = 0;
+            if (it == 0) {
+                nt = cn / static_cast<int>(kTrimCount);
+                cn -= nt * static_cast<int>(kTrimCount);
+            }
             bool bad = false;
             if (n < ntok) {
                 if (cn > cap) {
@@ -703,7 +796,14 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
                     bad = true;
                 }
             }
-            if (bad) {
+            float t_trim = NAN;
+            if (nt > 0 && n < ntok)
+                t_trim = trimmed_guess(sum1 - (red2[0][n] + red2[1][n]),
+                                       sum2 - (red3[0][n] + red3[1][n]), 256 - nt, z_guess);
+            if (t_trim > lo_b && t_trim < hi_b) {
+                tau = t_trim;
+                bad = true;
+            } else if (bad) {
                 if (isfinite(lo_b) && isfinite(hi_b)) {
                     tau = 0.5f * (lo_b + hi_b);
                 } else {
@@ -770,7 +870,7 @@ __device__ __forceinline__ int wave_count(bool p) { return __popcll(wave_ballot(
 // key bits below the highest bit in which the pool's keys differ (counts
 // are ballot popcounts), stopping as soon as the count hits k.
 template <int R>
-__device__ void wave_select_take(const uint32_t* key, const int32_t* idx, int n, int k,
+__device__ __forceinline__ void wave_select_take(const uint32_t* key, const int32_t* idx, int n, int k,
                                  uint32_t* stage_k, int32_t* stage_i, uint32_t* tau_out,
                                  uint32_t* wk, int32_t* wi) {
     const int lane = lane_id();
@@ -899,12 +999,50 @@ __device__ __forceinline__ void ring_ticket(const RingOut& ring, uint64_t h0, in
 constexpr int kMergeThreads = 256;
 constexpr int kMergeR = 32;                        // pool entries per lane
 constexpr int kPoolMax = kMergeR * kWave;          // 2048
+constexpr int kMaxRepair = 16;                     // slices one repair redoes
+enum { kRepairNone = 0, kRepairSlices = 1, kRepairAll = 2 };
+
+// The k best of the pool key[0..n) (k <= n <= kPoolMax), by wave 0, with a
+// register footprint matched to the pool size; the 64 entries past
+// kPoolMax are the staging area.
+__device__ __forceinline__ void pool_select(uint32_t* K, int32_t* I, int n, int k,
+                                            uint32_t* tau, uint32_t* wk, int32_t* wi) {
+    uint32_t* sk = K + kPoolMax;
+    int32_t* si = I + kPoolMax;
+    if (n <= 4 * kWave) wave_select_take<4>(K, I, n, k, sk, si, tau, wk, wi);
+    else if (n <= 8 * kWave) wave_select_take<8>(K, I, n, k, sk, si, tau, wk, wi);
+    else if (n <= 16 * kWave) wave_select_take<16>(K, I, n, k, sk, si, tau, wk, wi);
+    else wave_select_take<kMergeR>(K, I, n, k, sk, si, tau, wk, wi);
+}
+
+// pre-activation of latent j without the bias: plain fp32 dot product of
+// the packed dictionary row with the token row
+__device__ __forceinline__ float latent_dot(const uint16_t* __restrict__ Wp,
+                                            const uint16_t* __restrict__ hrow, int32_t j,
+                                            int32_t d, int32_t n_mt) {
+    const uint4* P = reinterpret_cast<const uint4*>(Wp);
+    const uint4* hr = reinterpret_cast<const uint4*>(hrow);
+    float acc = 0.0f;
+#pragma unroll 4
+    for (int32_t p = 0; p < d / 8; ++p) {
+        const uint4 wv = P[packed_piece(j, p * 8, n_mt)], hv = hr[p];
+        const uint32_t ww[4] = {wv.x, wv.y, wv.z, wv.w};
+        const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            acc = fmaf(lo_bf16(ww[e]), lo_bf16(hw[e]), acc);
+            acc = fmaf(hi_bf16(ww[e]), hi_bf16(hw[e]), acc);
+        }
+    }
+    return acc;
+}
 
 // One workgroup per subscribed token.  Every thread gathers the candidates
 // of the slices it owns (count, threshold and the slice's pair block are
 // loaded together, so the gather costs one memory round trip), a prefix
-// over the workgroup places them in an LDS pool, and wave 0 selects, checks
-// the certificate, sorts and writes; the other waves then leave.
+// over the workgroup places them in an LDS pool, and wave 0 selects and
+// checks the certificate; a failed check is repaired by the whole
+// workgroup; wave 0 then sorts and writes.
 __global__ void __launch_bounds__(kMergeThreads)
 sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ tile_cnt,
                  const float* __restrict__ tile_tau, int32_t n_mt, int32_t cap,
@@ -917,6 +1055,9 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
     __shared__ int32_t I[kPoolMax + kWave];
     __shared__ int scan_s[kMergeThreads / kWave];
     __shared__ uint32_t tmax_s[kMergeThreads / kWave];
+    __shared__ int mode_s, pool_n_s, nfail_s;
+    __shared__ uint32_t floor_s;
+    __shared__ int fail_s[kMaxRepair];
     const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
     const int n = blockIdx.x;
     const int cnt = *app_count;
@@ -1003,63 +1144,116 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
         }
     }
     __syncthreads();
-    if (wave != 0) return;
-
+    // wave 0 selects the k best of the pool and checks the certificate
     uint32_t wk = 0;
     int32_t wi = 0x7FFFFFFF;
-    bool exact_path = total <= kPoolMax && total >= k;
-    if (exact_path) {
-        uint32_t tau;
-        uint32_t* sk = K + kPoolMax;
-        int32_t* si = I + kPoolMax;
-        // register footprint matched to the pool size
-        if (total <= 4 * kWave) wave_select_take<4>(K, I, total, k, sk, si, &tau, &wk, &wi);
-        else if (total <= 8 * kWave) wave_select_take<8>(K, I, total, k, sk, si, &tau, &wk, &wi);
-        else if (total <= 16 * kWave) wave_select_take<16>(K, I, total, k, sk, si, &tau, &wk, &wi);
-        else wave_select_take<kMergeR>(K, I, total, k, sk, si, &tau, &wk, &wi);
-        // certificate: nothing left below a slice threshold can beat tau
-        exact_path = tau_tiles <= tau;
+    if (wave == 0) {
+        const bool fits = total <= kPoolMax && total >= k;
+        uint32_t tau = 0;
+        if (fits) pool_select(K, I, total, k, &tau, &wk, &wi);
+        if (lane == 0) {
+            mode_s = !fits ? kRepairAll : (tau_tiles <= tau ? kRepairNone : kRepairSlices);
+            floor_s = tau;
+            pool_n_s = total;
+            nfail_s = 0;
+        }
     }
-    if (!exact_path) {
-        // exact recompute of this token's m pre-activations, one latent per
-        // lane per round, keeping the k best in LDS [0, k)
-        const uint4* hr = reinterpret_cast<const uint4*>(h + static_cast<int64_t>(t) * d);
-        const uint4* P = reinterpret_cast<const uint4*>(Wp);
-        int held = 0;
-        for (int j0 = 0; j0 < n_mt * kBM; j0 += kWave) {
-            const int32_t j = j0 + lane;
-            float acc = 0.0f;
-            for (int32_t p = 0; p < d / 8; ++p) {
-                const uint4 wv = P[packed_piece(j, p * 8, n_mt)], hv = hr[p];
-                const uint32_t ww[4] = {wv.x, wv.y, wv.z, wv.w};
-                const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w};
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    acc = fmaf(lo_bf16(ww[e]), lo_bf16(hw[e]), acc);
-                    acc = fmaf(hi_bf16(ww[e]), hi_bf16(hw[e]), acc);
+    __syncthreads();
+    if (mode_s != kRepairNone) {  // uniform
+        // Repair: whole slices are recomputed exactly (an fp32 dot product
+        // per latent, one latent per thread) and every value that can still
+        // reach the top k enters the pool.  After a failed certificate only
+        // the slices whose threshold lies above the k-th selected value are
+        // redone, their emitted candidates first taken out of the pool; when
+        // the pool itself was unusable (or too many slices failed), all are.
+        const uint16_t* hrow = h + static_cast<int64_t>(t) * d;
+        bool all = mode_s == kRepairAll;
+        if (!all) {
+            const uint32_t tau = floor_s;
+            for (int tl = tid; tl < n_mt; tl += kMergeThreads) {
+                if (f32_key(tile_tau[row0 + tl]) > tau) {
+                    const int q = atomicAdd(&nfail_s, 1);
+                    if (q < kMaxRepair) fail_s[q] = tl;
                 }
             }
-            K[held + lane] = f32_key(acc + c_fold[j]);
-            I[held + lane] = j;
-            wave_sync();
-            const int n_pool = held + kWave;
-            if (n_pool > k) {
-                uint32_t tb, a;
-                int32_t b;
-                wave_select_take<2>(K, I, n_pool, k, K + 2 * kWave, I + 2 * kWave, &tb, &a, &b);
-                if (lane < k) {
-                    K[lane] = a;
-                    I[lane] = b;
+            __syncthreads();
+            all = nfail_s > kMaxRepair;
+            if (!all && wave == 0) {
+                const int nf = nfail_s, n0 = pool_n_s;
+                int out = 0;
+                for (int b0 = 0; b0 < n0; b0 += kWave) {
+                    const int i = b0 + lane;
+                    const uint32_t kk = i < n0 ? K[i] : 0u;
+                    const int32_t ii = i < n0 ? I[i] : 0;
+                    bool keep = i < n0;
+                    for (int f = 0; f < nf; ++f) keep = keep && ii / kBM != fail_s[f];
+                    const uint64_t bal = wave_ballot(keep);
+                    wave_sync();  // this round's reads come before its writes
+                    if (keep) {
+                        K[out + lanes_below(bal)] = kk;
+                        I[out + lanes_below(bal)] = ii;
+                    }
+                    out += __popcll(bal);
                 }
                 wave_sync();
-                held = k;
-            } else {
-                held = n_pool;
+                if (lane == 0) {
+                    pool_n_s = out;
+                    // a little below tau, so that a value whose recomputed
+                    // rounding differs from the GEMM's still enters
+                    const float tv = key_f32(tau);
+                    floor_s = f32_key(tv - fabsf(tv) * 0x1p-12f);
+                }
             }
+            __syncthreads();
         }
-        wk = lane < k ? K[lane] : 0u;
-        wi = lane < k ? I[lane] : 0x7FFFFFFF;
+        for (int pass = all ? 1 : 0; pass < 2; ++pass) {
+            if (pass == 1) {
+                if (tid == 0) {
+                    pool_n_s = 0;
+                    floor_s = 0u;
+                }
+                __syncthreads();
+            }
+            const int n_slices = pass == 1 ? n_mt : nfail_s;
+            for (int q = 0; q < n_slices; ++q) {
+                const int sl = pass == 1 ? q : fail_s[q];
+                const int pn = pool_n_s;
+                __syncthreads();  // every thread has read the pool size
+                if (pn > kPoolMax - kBM) {
+                    // room for a whole slice: keep the k best, raise the floor
+                    if (wave == 0) {
+                        uint32_t tk, a;
+                        int32_t b;
+                        wave_select_take<kMergeR>(K, I, pn, k, K + kPoolMax, I + kPoolMax, &tk,
+                                                  &a, &b);
+                        if (lane < k) {
+                            K[lane] = a;
+                            I[lane] = b;
+                        }
+                        if (lane == 0) {
+                            pool_n_s = k;
+                            floor_s = max(floor_s, tk);
+                        }
+                    }
+                    __syncthreads();
+                }
+                const int32_t j = sl * kBM + tid;
+                const uint32_t key = f32_key(latent_dot(Wp, hrow, j, d, n_mt) + c_fold[j]);
+                if (key >= floor_s) {
+                    const int pos = atomicAdd(&pool_n_s, 1);
+                    K[pos] = key;
+                    I[pos] = j;
+                }
+                __syncthreads();
+            }
+            if (pool_n_s >= k) break;  // uniform; else (rounding) redo every slice
+        }
+        if (wave == 0) {
+            uint32_t tau;
+            pool_select(K, I, pool_n_s, k, &tau, &wk, &wi);
+        }
     }
+    if (wave != 0) return;
     // order the k winners by (value desc, index asc) and write them
     wave_sort_desc(wk, wi);
     const uint16_t vb = f32_to_bf16_rne(fmaxf(key_f32(wk), 0.0f));

@@ -451,8 +451,8 @@ def test_encode_with_fused_readback_bit_exact(px, T, n_sub, cap, k):
 
 def test_encode_recompute_path_when_winners_crowd_one_slice(px):
     """50 of a token's top-64 planted in one 256-latent slice: more than the
-    slice may emit, so the merge's certificate fails for that token and it
-    takes the exact recompute path; the result must still match."""
+    slice may emit, so the merge's certificate fails for that token and the
+    repair recomputes that slice; the result must still match."""
     d, m, k = 256, 16384, 64
     wl = synth.make("c3", d=d, m=m, k=k, T=8, n_sub=8)
     sae = wl.layers[0].saes[0]
@@ -466,3 +466,57 @@ def test_encode_recompute_path_when_winners_crowd_one_slice(px):
     rt, idx, val = _encode(px, wl, sae, wl.layers[0].h)
     _check_encode(wl, sae, wl.layers[0].h, idx, val, np.arange(8))
     assert set(range(4096, 4096 + 50)) <= set(idx[t0].tolist())
+
+
+def to_bf16_bits(a):
+    return torch.from_numpy(np.asarray(a, np.float32)).to(torch.bfloat16).view(torch.int16) \
+        .numpy().view(np.uint16)
+
+
+@pytest.mark.parametrize("n_tied", [10, 20, 64])
+def test_encode_repair_of_tied_slices(px, n_tied):
+    """n_tied slices whose 256 pre-activations are all exactly 40 (zero
+    dictionary rows, bias 40), far above every other latent.  No threshold
+    splits a tie, so these slices emit nothing and fail the certificate.
+    10: the merge recomputes them one by one and its pool overflows on the
+    way (compaction to the k best); 20: more than it repairs slice by
+    slice, so every slice is recomputed; 64: nothing is emitted at all.
+    The k lowest latents of the tie win."""
+    d, m, k, T = 256, 16384, 64, 6
+    wl = synth.make("c3", d=d, m=m, k=k, T=T, n_sub=T)
+    sae = wl.layers[0].saes[0]
+    W, b = sae.W_enc.copy(), sae.b_enc.copy()
+    slices = np.arange(64) if n_tied == 64 else 1 + 3 * np.arange(n_tied)
+    for s in slices:
+        W[256 * s:256 * (s + 1)] = 0
+        b[256 * s:256 * (s + 1)] = 0x4220  # 40.0
+    sae.W_enc, sae.b_enc = W, b
+    rt, idx, val = _encode(px, wl, sae, wl.layers[0].h)
+    _check_encode(wl, sae, wl.layers[0].h, idx, val, np.arange(T))
+    first = 256 * int(slices[0])
+    for t in range(T):
+        assert sorted(idx[t].tolist()) == list(range(first, first + k))
+        assert np.all(bf16_f64(val[t]) == 40.0)
+
+
+@pytest.mark.parametrize("T", [64, 1100])
+def test_encode_with_strong_latents_per_token(px, T):
+    """Every token's row is moved along three dictionary rows so that those
+    latents stand far above its others (as clamping features high does).
+    The first threshold guess of their slices leaves such values out of the
+    tile statistics; the top-k must match the oracle either way.  64 token
+    slots run the decode kernel, 1100 the prefill GEMM."""
+    d, m, k = 256, 4096, 32
+    wl = synth.make("c3", d=d, m=m, k=k, T=T, n_sub=T)
+    sae = wl.layers[0].saes[0]
+    Wf = bf16_f64(sae.W_enc)
+    h = bf16_f64(wl.layers[0].h)
+    picks = synth.randint("test/strong_latents", 3 * T, 0, m - 1).reshape(T, 3)
+    for t in range(T):
+        for j in picks[t]:
+            h[t] += 60.0 * Wf[j] / np.dot(Wf[j], Wf[j])
+    hb = to_bf16_bits(h)
+    rt, idx, val = _encode(px, wl, sae, hb)
+    _check_encode(wl, sae, hb, idx, val, np.arange(T))
+    for t in range(T):
+        assert set(picks[t].tolist()) <= set(idx[t].tolist())
