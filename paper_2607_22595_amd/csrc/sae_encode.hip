@@ -27,9 +27,12 @@
 // that certificate fails (only for inputs whose best latents crowd into a
 // few tiles), the workgroup recomputes the failing tiles' 256
 // pre-activations with plain fp32 dot products and selects again.  The
-// first threshold guess of a tile leaves its strongest values out of the
-// statistics (above mean + 4 stdev), so that a few strong latents, such as
-// features clamped high by a steering app, do not lift it.
+// decode kernel's first threshold guess leaves a tile's strongest values
+// out of the statistics (above mean + 5 stdev), so that a few strong
+// latents, such as features clamped high by a steering app, do not lift it:
+// with a decode dictionary's ratio of k to m the certificate has little
+// slack.  The prefill kernel keeps the plain statistics (a GEMM epilogue
+// pays for every extra pass, and the repair covers the rare failure).
 //
 // The workgroup-to-tile map is XCD-aware: launch slots are dealt round-robin
 // to the 8 XCDs, so consecutive tiles of one XCD share a dictionary slice in
@@ -54,7 +57,7 @@ constexpr int kRefineIters = 24;
 // out of the statistics behind the first threshold guess (one strong latent
 // would otherwise raise the guess for its whole tile); kTrimCount packs
 // their number into the count reduction.
-constexpr float kTrimZ = 4.0f;
+constexpr float kTrimZ = 5.0f;
 constexpr float kTrimCount = 512.0f;
 constexpr int kLatentFastTiles = 4;  // token tiles up to which the latent tile runs fastest
 constexpr int kBlkTok = 8;           // prefill block: token tiles
@@ -287,14 +290,18 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
 #pragma unroll
         for (int nb = 0; nb < 4; ++nb) acc[nb][r] += cfv[r];
     }
-    // per-token mean and variance over the tile's 256 latents
+    // per-token mean and variance over the tile's 256 latents (and this
+    // lane's largest value, which tells whether it holds any to trim)
+    float mx[4];
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
         float s1 = 0.0f, s2 = 0.0f;
+        mx[nb] = -INFINITY;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             s1 += acc[nb][r];
             s2 = fmaf(acc[nb][r], acc[nb][r], s2);
+            mx[nb] = fmaxf(mx[nb], acc[nb][r]);
         }
         s1 += __shfl_xor(s1, 32, kWave);
         s2 += __shfl_xor(s2, 32, kWave);
@@ -337,12 +344,14 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
             for (int r = 0; r < 16; ++r) c += acc[nb][r] >= tau[nb] ? 1.0f : 0.0f;
             if (it == 0) {
                 float e1 = 0.0f, e2 = 0.0f;
+                if (mx[nb] > cut[nb]) {
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const bool o = acc[nb][r] > cut[nb];
-                    c += o ? kTrimCount : 0.0f;
-                    e1 += o ? acc[nb][r] : 0.0f;
-                    e2 = fmaf(o ? acc[nb][r] : 0.0f, acc[nb][r], e2);
+                    for (int r = 0; r < 16; ++r) {
+                        const bool o = acc[nb][r] > cut[nb];
+                        c += o ? kTrimCount : 0.0f;
+                        e1 += o ? acc[nb][r] : 0.0f;
+                        e2 = fmaf(o ? acc[nb][r] : 0.0f, acc[nb][r], e2);
+                    }
                 }
                 e1 += __shfl_xor(e1, 32, kWave);
                 e2 += __shfl_xor(e2, 32, kWave);
@@ -508,7 +517,6 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
     __shared__ uint4 xsA[kStagePieces], xsB[kStagePieces], xsC[kStagePieces], xsD[kStagePieces];
     __shared__ float red1[2][kGemmTok];
     __shared__ float red2[2][kGemmTok];
-    __shared__ float red3[2][kGemmTok];
     __shared__ int cnt_s[kGemmTok];
 
     // Tile order: launch slot L runs on XCD L % 8, which owns the latent
@@ -727,11 +735,9 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
             red2[wm][n] = s2;
         }
         __syncthreads();
-        const float sum1 = red1[0][n] + red1[1][n], sum2 = red2[0][n] + red2[1][n];
-        const float mu = sum1 * (1.0f / 256.0f);
-        const float sd = sqrtf(fmaxf(sum2 * (1.0f / 256.0f) - mu * mu, 0.0f));
+        const float mu = (red1[0][n] + red1[1][n]) * (1.0f / 256.0f);
+        const float sd = sqrtf(fmaxf((red2[0][n] + red2[1][n]) * (1.0f / 256.0f) - mu * mu, 0.0f));
         float tau = mu + z_guess * sd;
-        const float cut = mu + kTrimZ * sd;
         float lo_b = -INFINITY, hi_b = INFINITY;
         uint32_t m0 = 0, m1 = 0;  // bit i: v[i] >= tau (m1: v[32 + i])
         bool gave_up = false;
@@ -745,47 +751,14 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
             }
             return __popc(m0) + __popc(m1);
         };
-        // count(pre >= tau) per token; refine tau until lo_cnt <= count <= cap.
-        // The first count also sums the values above the trim cut (all of
-        // them are among the counted ones: the cut lies above tau), and a
-        // token that has any takes its guess again without them.
+        // count(pre >= tau) per token; refine tau until lo_cnt <= count <= cap
         for (int it = 0; it < kRefineIters; ++it) {
             const int c_lane = count_at(tau);
-            int ne = 0;
-            float e1 = 0.0f, e2 = 0.0f;
-            if (it == 0) {
-                uint32_t b0 = m0, b1 = m1;
-                while (b0 | b1) {
-                    const int i = b0 ? __builtin_ctz(b0) : 32 + __builtin_ctz(b1);
-                    if (b0) b0 &= b0 - 1;
-                    else b1 &= b1 - 1;
-                    const float val = park[((i >> 2) * 64 + lane) * 4 + (i & 3)];
-                    if (val > cut) {
-                        ++ne;
-                        e1 += val;
-                        e2 = fmaf(val, val, e2);
-                    }
-                }
-                e1 += __shfl_xor(e1, 32, kWave);
-                e2 += __shfl_xor(e2, 32, kWave);
-            }
-            const int cp = c_lane + static_cast<int>(kTrimCount) * ne;
-            const float c = static_cast<float>(cp + __shfl_xor(cp, 32, kWave));
-            __syncthreads();  // red1..red3 are reused
-            if (g == 0) {
-                red1[wm][n] = c;
-                if (it == 0) {
-                    red2[wm][n] = e1;
-                    red3[wm][n] = e2;
-                }
-            }
+            const float c = static_cast<float>(c_lane + __shfl_xor(c_lane, 32, kWave));
+            __syncthreads();  // red1 is reused
+            if (g == 0) red1[wm][n] = c;
             __syncthreads();
-            int cn = static_cast<int>(red1[0][n] + red1[1][n]);
-            int nt = 0;
-            if (it == 0) {
-                nt = cn / static_cast<int>(kTrimCount);
-                cn -= nt * static_cast<int>(kTrimCount);
-            }
+            const int cn = static_cast<int>(red1[0][n] + red1[1][n]);
             bool bad = false;
             if (n < ntok) {
                 if (cn > cap) {
@@ -796,14 +769,7 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
                     bad = true;
                 }
             }
-            float t_trim = NAN;
-            if (nt > 0 && n < ntok)
-                t_trim = trimmed_guess(sum1 - (red2[0][n] + red2[1][n]),
-                                       sum2 - (red3[0][n] + red3[1][n]), 256 - nt, z_guess);
-            if (t_trim > lo_b && t_trim < hi_b) {
-                tau = t_trim;
-                bad = true;
-            } else if (bad) {
+            if (bad) {
                 if (isfinite(lo_b) && isfinite(hi_b)) {
                     tau = 0.5f * (lo_b + hi_b);
                 } else {
@@ -866,22 +832,21 @@ __device__ __forceinline__ int wave_count(bool p) { return __popcll(wave_ballot(
 // in pool order; other lanes get key 0).  The selection is
 //   { i : key[i] > tau  or  (key[i] == tau and idx[i] <= cut) }
 // with exactly k entries (requires n >= k); tau is returned.  The keys stay
-// in registers for the whole selection.  tau is found by bisection on the
-// key bits below the highest bit in which the pool's keys differ (counts
-// are ballot popcounts), stopping as soon as the count hits k.
+// in registers for the whole selection; the latents are read from LDS only
+// where needed (entries tied at tau, and the k taken).  tau is found by
+// bisection on the key bits below the highest bit in which the pool's keys
+// differ (counts are ballot popcounts), stopping as soon as the count hits k.
 template <int R>
-__device__ __forceinline__ void wave_select_take(const uint32_t* key, const int32_t* idx, int n, int k,
-                                 uint32_t* stage_k, int32_t* stage_i, uint32_t* tau_out,
-                                 uint32_t* wk, int32_t* wi) {
+__device__ __forceinline__ void wave_select_take(const uint32_t* key, const int32_t* idx, int n,
+                                                 int k, uint32_t* stage_k, int32_t* stage_i,
+                                                 uint32_t* tau_out, uint32_t* wk, int32_t* wi) {
     const int lane = lane_id();
     uint32_t kr[R];
-    int32_t ir[R];
     uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         const int i = lane + kWave * r;
         kr[r] = i < n ? key[i] : 0u;  // real keys are >= 1; 0 never counts
-        ir[r] = i < n ? idx[i] : 0;
         if (i < n) {
             kmin = min(kmin, kr[r]);
             kmax = max(kmax, kr[r]);
@@ -922,13 +887,17 @@ __device__ __forceinline__ void wave_select_take(const uint32_t* key, const int3
         }
         const int need = k - gt;
         if (eq > need) {
-            // smallest I with #{key == tau and idx <= I} >= need
+            // smallest I with #{key == tau and idx <= I} >= need; the tied
+            // latents are read from LDS, only in rounds that hold a tie
             int32_t lo = 0;
             for (int bit = 30; bit >= 0; --bit) {
                 const int32_t probe = lo | ((1 << bit) - 1);
                 int c = 0;
 #pragma unroll
-                for (int r = 0; r < R; ++r) c += wave_count(kr[r] == tau && ir[r] <= probe);
+                for (int r = 0; r < R; ++r) {
+                    const bool tie = kr[r] == tau;
+                    if (wave_ballot(tie)) c += wave_count(tie && idx[lane + kWave * r] <= probe);
+                }
                 if (c < need) lo |= (1 << bit);
             }
             cut = lo;
@@ -939,13 +908,19 @@ __device__ __forceinline__ void wave_select_take(const uint32_t* key, const int3
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         const int i = lane + kWave * r;
-        const bool take = i < n && (kr[r] > tau || (kr[r] == tau && ir[r] <= cut));
-        const uint64_t b = wave_ballot(take);
-        if (take) {
-            stage_k[base + lanes_below(b)] = kr[r];
-            stage_i[base + lanes_below(b)] = ir[r];
+        bool take = i < n && kr[r] >= tau;
+        const uint64_t cand = wave_ballot(take);
+        if (cand) {
+            int32_t ir = 0;
+            if (take) ir = idx[i];
+            take = take && (kr[r] > tau || ir <= cut);
+            const uint64_t b = wave_ballot(take);
+            if (take) {
+                stage_k[base + lanes_below(b)] = kr[r];
+                stage_i[base + lanes_below(b)] = ir;
+            }
+            base += __popcll(b);
         }
-        base += __popcll(b);
     }
     wave_sync();
     *tau_out = tau;
@@ -1000,7 +975,8 @@ constexpr int kMergeThreads = 256;
 constexpr int kMergeR = 32;                        // pool entries per lane
 constexpr int kPoolMax = kMergeR * kWave;          // 2048
 constexpr int kMaxRepair = 16;                     // slices one repair redoes
-enum { kRepairNone = 0, kRepairSlices = 1, kRepairAll = 2 };
+constexpr int kRepairR = 6;                        // repair pool entries per lane
+constexpr int kRepairPool = kRepairR * kWave;      // 384 >= k + one slice
 
 // The k best of the pool key[0..n) (k <= n <= kPoolMax), by wave 0, with a
 // register footprint matched to the pool size; the 64 entries past
@@ -1055,8 +1031,8 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
     __shared__ int32_t I[kPoolMax + kWave];
     __shared__ int scan_s[kMergeThreads / kWave];
     __shared__ uint32_t tmax_s[kMergeThreads / kWave];
-    __shared__ int mode_s, pool_n_s, nfail_s;
-    __shared__ uint32_t floor_s;
+    __shared__ int pool_n_s, nfail_s, fix_s;
+    __shared__ uint32_t floor_s, sel_tau_s;
     __shared__ int fail_s[kMaxRepair];
     const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
     const int n = blockIdx.x;
@@ -1152,61 +1128,67 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
         uint32_t tau = 0;
         if (fits) pool_select(K, I, total, k, &tau, &wk, &wi);
         if (lane == 0) {
-            mode_s = !fits ? kRepairAll : (tau_tiles <= tau ? kRepairNone : kRepairSlices);
-            floor_s = tau;
-            pool_n_s = total;
+            sel_tau_s = tau;
+            fix_s = !fits ? 2 : (tau_tiles <= tau ? 0 : 1);
             nfail_s = 0;
         }
     }
     __syncthreads();
-    if (mode_s != kRepairNone) {  // uniform
+    if (fix_s != 0) {  // uniform
         // Repair: whole slices are recomputed exactly (an fp32 dot product
-        // per latent, one latent per thread) and every value that can still
-        // reach the top k enters the pool.  After a failed certificate only
-        // the slices whose threshold lies above the k-th selected value are
-        // redone, their emitted candidates first taken out of the pool; when
-        // the pool itself was unusable (or too many slices failed), all are.
+        // per latent, one latent per thread).  The pool is cut down to what
+        // can still reach the top k, then after every slice wave 0 keeps the
+        // k best of the pool and that slice's values above the floor (at most
+        // kRepairPool entries), raising the floor to the k-th.  After a
+        // failed certificate only the slices whose threshold lies above the
+        // k-th selected value are redone and the pool keeps its other entries
+        // at or above that value; when the pool was unusable, more than
+        // kMaxRepair slices failed or too many entries are kept, every slice
+        // is redone from an empty pool.
         const uint16_t* hrow = h + static_cast<int64_t>(t) * d;
-        bool all = mode_s == kRepairAll;
+        const uint32_t st = sel_tau_s;
+        bool all = fix_s == 2;
         if (!all) {
-            const uint32_t tau = floor_s;
             for (int tl = tid; tl < n_mt; tl += kMergeThreads) {
-                if (f32_key(tile_tau[row0 + tl]) > tau) {
+                if (f32_key(tile_tau[row0 + tl]) > st) {
                     const int q = atomicAdd(&nfail_s, 1);
                     if (q < kMaxRepair) fail_s[q] = tl;
                 }
             }
             __syncthreads();
             all = nfail_s > kMaxRepair;
-            if (!all && wave == 0) {
-                const int nf = nfail_s, n0 = pool_n_s;
-                int out = 0;
-                for (int b0 = 0; b0 < n0; b0 += kWave) {
-                    const int i = b0 + lane;
-                    const uint32_t kk = i < n0 ? K[i] : 0u;
-                    const int32_t ii = i < n0 ? I[i] : 0;
-                    bool keep = i < n0;
-                    for (int f = 0; f < nf; ++f) keep = keep && ii / kBM != fail_s[f];
-                    const uint64_t bal = wave_ballot(keep);
-                    wave_sync();  // this round's reads come before its writes
-                    if (keep) {
-                        K[out + lanes_below(bal)] = kk;
-                        I[out + lanes_below(bal)] = ii;
-                    }
-                    out += __popcll(bal);
-                }
-                wave_sync();
-                if (lane == 0) {
-                    pool_n_s = out;
-                    // a little below tau, so that a value whose recomputed
-                    // rounding differs from the GEMM's still enters
-                    const float tv = key_f32(tau);
-                    floor_s = f32_key(tv - fabsf(tv) * 0x1p-12f);
-                }
-            }
-            __syncthreads();
         }
+        if (!all && wave == 0) {
+            // a little below the k-th value, so that a value whose recomputed
+            // rounding differs from the GEMM's still enters
+            const float tv = key_f32(st);
+            const uint32_t fl = f32_key(tv - fabsf(tv) * 0x1p-12f);
+            const int nf = nfail_s;
+            int out = 0;
+            for (int b0 = 0; b0 < total; b0 += kWave) {
+                const int i = b0 + lane;
+                const uint32_t kk = i < total ? K[i] : 0u;
+                const int32_t ii = i < total ? I[i] : 0;
+                bool keep = i < total && kk >= fl;
+                for (int f = 0; f < nf; ++f) keep = keep && ii / kBM != fail_s[f];
+                const uint64_t bal = wave_ballot(keep);
+                wave_sync();  // this round's reads come before its writes
+                if (keep) {
+                    K[out + lanes_below(bal)] = kk;
+                    I[out + lanes_below(bal)] = ii;
+                }
+                out += __popcll(bal);
+            }
+            wave_sync();
+            if (lane == 0) {
+                pool_n_s = out;
+                floor_s = fl;
+            }
+        }
+        __syncthreads();
+        if (!all && pool_n_s > kRepairPool - kBM) all = true;
         for (int pass = all ? 1 : 0; pass < 2; ++pass) {
+            __syncthreads();  // every thread has read the pool size
             if (pass == 1) {
                 if (tid == 0) {
                     pool_n_s = 0;
@@ -1214,18 +1196,24 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
                 }
                 __syncthreads();
             }
-            const int n_slices = pass == 1 ? n_mt : nfail_s;
-            for (int q = 0; q < n_slices; ++q) {
-                const int sl = pass == 1 ? q : fail_s[q];
+            const int n_rep = pass == 1 ? n_mt : nfail_s;
+            for (int q = 0; q < n_rep; ++q) {
+                const int32_t j = (pass == 1 ? q : fail_s[q]) * kBM + tid;
+                const uint32_t key = f32_key(latent_dot(Wp, hrow, j, d, n_mt) + c_fold[j]);
+                if (key >= floor_s) {
+                    const int pos = atomicAdd(&pool_n_s, 1);
+                    K[pos] = key;
+                    I[pos] = j;
+                }
+                __syncthreads();
                 const int pn = pool_n_s;
                 __syncthreads();  // every thread has read the pool size
-                if (pn > kPoolMax - kBM) {
-                    // room for a whole slice: keep the k best, raise the floor
+                if (pn > k) {
                     if (wave == 0) {
                         uint32_t tk, a;
                         int32_t b;
-                        wave_select_take<kMergeR>(K, I, pn, k, K + kPoolMax, I + kPoolMax, &tk,
-                                                  &a, &b);
+                        wave_select_take<kRepairR>(K, I, pn, k, K + kPoolMax, I + kPoolMax, &tk,
+                                                   &a, &b);
                         if (lane < k) {
                             K[lane] = a;
                             I[lane] = b;
@@ -1237,20 +1225,12 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
                     }
                     __syncthreads();
                 }
-                const int32_t j = sl * kBM + tid;
-                const uint32_t key = f32_key(latent_dot(Wp, hrow, j, d, n_mt) + c_fold[j]);
-                if (key >= floor_s) {
-                    const int pos = atomicAdd(&pool_n_s, 1);
-                    K[pos] = key;
-                    I[pos] = j;
-                }
-                __syncthreads();
             }
-            if (pool_n_s >= k) break;  // uniform; else (rounding) redo every slice
+            if (pool_n_s >= k) break;  // else (rounding) redo every slice
         }
         if (wave == 0) {
-            uint32_t tau;
-            pool_select(K, I, pool_n_s, k, &tau, &wk, &wi);
+            wk = lane < k ? K[lane] : 0u;
+            wi = lane < k ? I[lane] : 0x7FFFFFFF;
         }
     }
     if (wave != 0) return;

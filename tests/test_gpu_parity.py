@@ -503,9 +503,10 @@ def test_encode_repair_of_tied_slices(px, n_tied):
 def test_encode_with_strong_latents_per_token(px, T):
     """Every token's row is moved along three dictionary rows so that those
     latents stand far above its others (as clamping features high does).
-    The first threshold guess of their slices leaves such values out of the
-    tile statistics; the top-k must match the oracle either way.  64 token
-    slots run the decode kernel, 1100 the prefill GEMM."""
+    64 token slots run the decode kernel, whose first threshold guess leaves
+    such values out of the tile statistics; 1100 run the prefill GEMM, which
+    keeps the plain statistics and leaves failures to the merge's repair.
+    The top-k must match the oracle either way."""
     d, m, k = 256, 4096, 32
     wl = synth.make("c3", d=d, m=m, k=k, T=T, n_sub=T)
     sae = wl.layers[0].saes[0]
