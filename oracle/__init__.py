@@ -35,6 +35,7 @@ def _load():
     lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_route.argtypes = [vp, i32, i32, vp, i32, i32, vp, vp, vp, vp]
     lib.oracle_steer.argtypes = [vp, ctypes.c_int, i32, i32, vp, vp, vp, vp, vp, i32]
+    lib.oracle_router_write.argtypes = [vp, ctypes.c_int, i32, i32, vp, vp, vp, i32]
     lib.oracle_probe_token.argtypes = [vp, ctypes.c_int, i32, i32, vp, vp, vp, vp, i32, vp, vp]
     lib.oracle_probe_mean.argtypes = [vp, ctypes.c_int, i32, i32, vp, vp, vp, vp, i32, vp, i32, vp, vp]
     lib.oracle_route_gate.argtypes = [i32, vp, vp, vp, i32, vp, i32, vp, i32, i32, ctypes.c_float]
@@ -134,6 +135,18 @@ def steer(h, tok_mask, req, v, app_bits, alpha):
     alpha = _c(alpha, np.float32).reshape(-1, n_steer) if n_steer else np.zeros((1, 1), np.float32)
     _load().oracle_steer(_p(out), int(is_bf16), T_max, d, _p(_c(tok_mask, np.uint32)),
                          _p(_c(req, np.int32)), _p(v), _p(_c(app_bits, np.int32)), _p(alpha), n_steer)
+    return out
+
+
+def router_write(logits, tok_mask, app_bits, offsets):
+    """Returns the written copy of the router logits [T_max, n_experts]
+    (uint16 bf16 bits or float32); offsets float32 [n_router, n_experts]."""
+    is_bf16 = logits.dtype == np.uint16
+    out = np.array(logits, copy=True, order="C")
+    T_max, E = out.shape
+    off = _c(offsets, np.float32).reshape(-1, E)
+    _load().oracle_router_write(_p(out), int(is_bf16), T_max, E, _p(_c(tok_mask, np.uint32)),
+                                _p(_c(app_bits, np.int32)), _p(off), off.shape[0])
     return out
 
 

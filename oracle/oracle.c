@@ -208,6 +208,37 @@ void oracle_steer(void *h, int is_bf16, int32_t T_max, int32_t d,
     }
 }
 
+/* ------------------------------------------------------ router-logit write
+ * Expert (de)activation on a mixture-of-experts router (Table 1, App-7: a
+ * conditional write whose locus is the router logits).  For every token with
+ * at least one of the router apps' bits:
+ *   logits[t,e] = round( logits[t,e] + offsets[s1,e] + offsets[s2,e] + ... )
+ * over the token's subscribed router apps s1 < s2 < ... (their index in the
+ * app list), added in that order in fp64 and rounded once to the storage
+ * type.  An offset of -inf removes expert e for that app's tokens; a large
+ * finite offset forces it into the router's selection.  Non-finite values
+ * follow IEEE arithmetic.  Other rows are untouched. */
+void oracle_router_write(void *logits, int is_bf16, int32_t T_max, int32_t n_experts,
+                         const uint32_t *tok_mask, const int32_t *app_bits,
+                         const float *offsets, int32_t n_router) {
+    for (int32_t t = 0; t < T_max; ++t) {
+        uint32_t mask = tok_mask[t];
+        int any = 0;
+        for (int32_t s = 0; s < n_router; ++s)
+            if ((mask >> app_bits[s]) & 1u) any = 1;
+        if (!any) continue;
+        for (int32_t e = 0; e < n_experts; ++e) {
+            int64_t at = (int64_t)t * n_experts + e;
+            double acc = is_bf16 ? bf16_to_double(((const uint16_t *)logits)[at])
+                                 : (double)((const float *)logits)[at];
+            for (int32_t s = 0; s < n_router; ++s)
+                if ((mask >> app_bits[s]) & 1u) acc += (double)offsets[(int64_t)s * n_experts + e];
+            if (is_bf16) ((uint16_t *)logits)[at] = oracle_round_bf16(acc);
+            else ((float *)logits)[at] = (float)acc;
+        }
+    }
+}
+
 /* ------------------------------------------------------------------ probes
  * Linear read-out with a logistic link, the Read primitive (Sec. 3: a
  * linear probe that turns activations into a score; Table 1 App-4,

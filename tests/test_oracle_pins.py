@@ -499,3 +499,76 @@ def test_route_trigger_brute_force(seed):
     keep = [t for t in range(T) if (tm[t] >> app) & 1 and int(ids[t]) in trig]
     assert cnt2[app] == len(keep) and list(lists2[app, :len(keep)]) == keep
     assert all(((tm2[t] >> app) & 1) == (t in keep) for t in range(T))
+
+
+# -------------------------------------------------------- router-logit write
+
+def test_router_zero_offsets_is_identity():
+    rng = np.random.default_rng(40)
+    lg = f32_to_bf16_torch(rng.normal(0.0, 1.0, (9, 8)))
+    out = oracle.router_write(lg, np.full(9, 0b11, np.uint32), [0, 1], np.zeros((2, 8), np.float32))
+    assert np.array_equal(out, lg)
+
+
+def test_router_minus_inf_removes_one_expert():
+    """One app deactivates expert 5: only that entry of its tokens becomes
+    -inf; the router's top-2 never picks it; unsubscribed rows keep their
+    bits."""
+    rng = np.random.default_rng(41)
+    T, E = 16, 8
+    lg = rng.normal(0.0, 1.0, (T, E)).astype(np.float32)
+    lg[:, 5] += 10.0                                   # expert 5 would win everywhere
+    off = np.zeros((1, E), np.float32)
+    off[0, 5] = -np.inf
+    tm = (np.arange(T) % 2).astype(np.uint32) << np.uint32(4)  # odd tokens carry bit 4
+    out = oracle.router_write(lg, tm, [4], off)
+    for t in range(T):
+        if tm[t]:
+            assert out[t, 5] == -np.inf
+            keep = np.delete(np.arange(E), 5)
+            assert np.array_equal(out[t, keep], lg[t, keep])
+            assert 5 not in np.argsort(-out[t])[:2]
+        else:
+            assert np.array_equal(out[t], lg[t])
+            assert np.argmax(out[t]) == 5
+
+
+def test_router_sums_apps_in_order_and_rounds_once():
+    """fp32 logits: the sum of the subscribed apps' offsets equals an exact
+    math.fsum rounded once (the terms are chosen so that rounding after each
+    addition would differ); app s is gated by bit app_bits[s]."""
+    T, E = 4, 4
+    lg = np.full((T, E), 1.0, np.float32)
+    off = np.array([[2.0 ** -24, 0.0, 3.0, 0.0],
+                    [2.0 ** -24, 0.0, -1.0, 0.0],
+                    [0.0, 0.0, 0.5, 1e4]], np.float32)
+    bits = [6, 2, 9]
+    tm = np.array([(1 << 6) | (1 << 2), 1 << 9, (1 << 6) | (1 << 2) | (1 << 9), 1 << 3], np.uint32)
+    out = oracle.router_write(lg, tm, bits, off)
+    for t in range(T):
+        sel = [s for s in range(3) if (tm[t] >> bits[s]) & 1]
+        for e in range(E):
+            exact = math.fsum([1.0] + [float(off[s, e]) for s in sel])
+            assert out[t, e] == np.float32(exact)
+    # 1 + 2^-24 + 2^-24 rounds once to 1 + 2^-23, not twice to 1
+    assert out[0, 0] == np.float32(1.0 + 2.0 ** -23)
+    assert np.array_equal(out[3], lg[3])               # bit 3 is no router app
+
+
+def test_router_bf16_rounds_once_from_the_exact_sum():
+    """bf16 logits: the result is the RNE of the exact fp64 sum (checked with
+    the library fp32->bf16 cast on sums that are exact in fp32)."""
+    rng = np.random.default_rng(42)
+    T, E, n = 10, 8, 3
+    lg = f32_to_bf16_torch(rng.integers(-64, 64, (T, E)) / 8.0)
+    off = (rng.integers(-512, 512, (n, E)) / 256.0).astype(np.float32)
+    tm = rng.integers(0, 8, T).astype(np.uint32)
+    out = oracle.router_write(lg, tm, [0, 1, 2], off)
+    lv = bf16_vals(lg)
+    for t in range(T):
+        if tm[t] == 0:
+            assert np.array_equal(out[t], lg[t])
+            continue
+        acc = lv[t] + sum(off[s].astype(np.float64) for s in range(n) if (tm[t] >> s) & 1)
+        assert np.array_equal(acc.astype(np.float32).astype(np.float64), acc)
+        assert np.array_equal(out[t], f32_to_bf16_torch(acc))
