@@ -296,10 +296,21 @@ def time_conditional(torch, step, wl, args):
             one.replay()
         return time_replays(torch, one, args.steps) * 1e3 / reps
 
+    # router-logit write on a Mixtral-shaped router (8 experts, bf16 logits),
+    # bits 0-3 as four router apps; -inf offsets remove experts
+    E = 8
+    router_logits = torch.from_numpy(synth.normal_f32("bench/router_logits", (wl.T_max, E), 1.0)
+                                     ).to(torch.bfloat16).cuda()
+    off = synth.normal_f32("bench/router_offsets", (4, E), 1.0)
+    off[synth.uniform01("bench/router_mask", 4 * E).reshape(4, E) < 0.2] = -np.inf
+    off = torch.from_numpy(off).cuda()
     base = timed(build)
     gate = timed(lambda: (build(), px.xmix_route_gate(step.route, 1, logit, thr, signal_bit=4)))
     trig = timed(lambda: (build(), px.xmix_route_trigger(step.route, 2, ids, vocab_bits, V)))
-    return {"route_build": base, "gate": gate - base, "trigger": trig - base}
+    router = timed(lambda: (build(), px.xmix_router_write(router_logits, step.route, [0, 1, 2, 3],
+                                                          off)))
+    return {"route_build": base, "gate": gate - base, "trigger": trig - base,
+            "router_write_8_experts": router - base}
 
 
 def run_steer_probe(torch, synth, HookStep, args):

@@ -174,6 +174,29 @@ xmix_status xmix_steer_apply(void *h, xmix_dtype dt, int32_t d, const xmix_route
                              const int32_t *app_bits, const float *alpha,
                              int32_t n_steer, int32_t R_max, void *stream);
 
+/* ------------------------------------------------------ router-logit write
+ * Expert (de)activation on a mixture-of-experts router, a write whose locus
+ * is the router logits (Table 1, App-7).  For each token t with at least one
+ * router bit:
+ *   logits[t,e] <- round( logits[t,e] + offsets[s1,e] + offsets[s2,e] + ... )
+ * over the token's subscribed router apps s1 < s2 < ... (their index in
+ * app_bits), added in that order in fp64 and rounded once (RNE) to the
+ * storage type.  An offset of -inf removes expert e for that app's tokens; a
+ * large finite offset forces it into the router's selection; other
+ * non-finite values follow IEEE arithmetic.  Other rows are not touched.
+ * The condition of a conditional app is applied beforehand by narrowing its
+ * routing entry (xmix_route_gate / xmix_route_trigger).
+ * logits   [T_max, n_experts] of dtype `dt`, updated in place (2-byte
+ *          aligned for bf16, 4-byte for fp32).
+ * app_bits host [n_router]: the route bit of each router app.
+ * offsets  [n_router, n_experts] fp32, device.
+ * Requires 1 <= n_router <= 32 and T_max * n_experts < 2^31.
+ * Errors: XMIX_E_INVAL (null pointer, bad dtype, alignment, app bit outside
+ * the route), XMIX_E_UNSUPPORTED (too many elements). */
+xmix_status xmix_router_write(void *logits, xmix_dtype dt, int32_t n_experts,
+                              const xmix_route *rt, const int32_t *app_bits,
+                              const float *offsets, int32_t n_router, void *stream);
+
 /* ------------------------------------------------------------------ probes
  * Linear probes with a logistic link, the Read primitive (Sec. 3: a linear
  * probe scoring activations; Table 1 App-4).

@@ -55,6 +55,8 @@ _sigs = {
     "xmix_route_build": ([_vp, _vp, _vp, _i32, ctypes.POINTER(XmixRoute), _vp, _vp], _st),
     "xmix_route_gate": ([ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32, _i32, _vp, _vp], _st),
     "xmix_route_trigger": ([ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32, _vp], _st),
+    "xmix_router_write": ([_vp, _st, _i32, ctypes.POINTER(XmixRoute), _vp, _vp, _i32, _vp],
+                          _st),
     "xmix_steer_apply": ([_vp, _st, _i32, ctypes.POINTER(XmixRoute), _vp, _vp, _vp, _vp, _i32,
                           _i32, _vp], _st),
     "xmix_probe_workspace": ([_i32, _i32, _i32], _sz),
@@ -202,6 +204,20 @@ def xmix_steer_apply(h, route: Route, req_of_token, vecs, app_bits: Sequence[int
     _check("xmix_steer_apply", _lib.xmix_steer_apply(
         _ptr(h), _dt(h), d, ctypes.byref(route.struct), _ptr(req_of_token), _ptr(vecs), bits,
         _ptr(alpha), n, alpha.shape[0], _stream(stream)))
+
+
+def xmix_router_write(logits, route: Route, app_bits: Sequence[int], offsets, stream=None):
+    """logits [T_max, n_experts] bf16/fp32 in place; offsets fp32
+    [n_router, n_experts] (-inf removes an expert); app_bits: host list of
+    route bits, one per router app."""
+    T_max, E = logits.shape
+    assert T_max == route.T_max and logits.is_contiguous()
+    n = len(app_bits)
+    assert offsets.dtype == torch.float32 and tuple(offsets.shape) == (n, E)
+    bits = (ctypes.c_int32 * n)(*app_bits)
+    _check("xmix_router_write", _lib.xmix_router_write(
+        _ptr(logits), _dt(logits), E, ctypes.byref(route.struct), bits, _ptr(offsets), n,
+        _stream(stream)))
 
 
 def probe_workspace(T_max: int, n_probe: int, mode: int) -> int:

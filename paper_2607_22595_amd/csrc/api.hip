@@ -101,6 +101,22 @@ xmix_status xmix_steer_apply(void* h, xmix_dtype dt, int32_t d, const xmix_route
                                  vecs, bits, alpha, n_steer, as_stream(stream)));
 }
 
+xmix_status xmix_router_write(void* logits, xmix_dtype dt, int32_t n_experts,
+                              const xmix_route* rt, const int32_t* app_bits,
+                              const float* offsets, int32_t n_router, void* stream) {
+    if (!logits || !offsets || !route_ok(rt) || n_experts < 1) return XMIX_E_INVAL;
+    if (dt != XMIX_BF16 && dt != XMIX_F32) return XMIX_E_INVAL;
+    if (reinterpret_cast<uintptr_t>(logits) % (dt == XMIX_BF16 ? 2u : 4u) != 0 ||
+        reinterpret_cast<uintptr_t>(offsets) % 4u != 0)
+        return XMIX_E_INVAL;
+    if (static_cast<int64_t>(rt->T_max) * n_experts > INT32_MAX) return XMIX_E_UNSUPPORTED;
+    BitList bits;
+    if (!bits_ok(app_bits, n_router, rt->n_apps, &bits)) return XMIX_E_INVAL;
+    return launched(launch_router_write(logits, dt == XMIX_BF16, n_experts, rt->T_max,
+                                        rt->tok_mask, bits, offsets, n_router,
+                                        as_stream(stream)));
+}
+
 size_t xmix_probe_workspace(int32_t T_max, int32_t n_probe, int32_t mode) {
     if (mode != XMIX_PROBE_MEAN || T_max < 1 || n_probe < 1) return 0;
     return static_cast<size_t>(T_max) * static_cast<size_t>(n_probe) * sizeof(float);
