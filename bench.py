@@ -313,6 +313,92 @@ def time_conditional(torch, step, wl, args):
             "router_write_8_experts": router - base}
 
 
+def time_step_graph(torch, step, args):
+    """Parameter updates on the library's own step graph of `step` (Sec. 4.3):
+    per step, GPU time (events on the graph's stream) and host time to
+    enqueue, for a plain launch; a launch after an in-memory update of alpha
+    (one hipMemcpyAsync from pinned host memory into the buffer the graph
+    reads); a launch after a kernel-node update that points every steering
+    node at another alpha buffer; the zero-mask step (subscriptions buffer
+    redirected to zeros); and an empty graph of one trivial kernel, the floor
+    of any graph launch."""
+    import ctypes
+    import time
+    import paper_2607_22595_amd as px
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipMemcpyAsync.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                   ctypes.c_int, ctypes.c_void_p]
+    stream = torch.cuda.Stream()
+    step.reset()
+    torch.cuda.synchronize()
+
+    def record():
+        # each replay first restores the residual rows (device copies), so
+        # that steering and clamping do not drift over the replays
+        with torch.cuda.stream(stream):
+            step.reset()
+        step.run(stream)
+    g = px.Graph(record, stream)
+    n = max(50, args.steps)
+
+    def loop(fn):
+        for _ in range(5):
+            fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        t0 = time.perf_counter()
+        for _ in range(n):
+            fn()
+        host = (time.perf_counter() - t0) / n * 1e6
+        e1.record(stream)
+        e1.synchronize()
+        return {"gpu_us": e0.elapsed_time(e1) * 1e3 / n, "host_us": host}
+
+    alpha0 = step.alpha
+    alpha1 = alpha0.clone()
+    pinned = alpha0.cpu().pin_memory()
+    nbytes = alpha0.numel() * 4
+    sptr = stream.cuda_stream
+    res = {"kernel_nodes": g.kernel_nodes, "alpha_bytes": nbytes,
+           "note": "every step graph replay includes the restore copies of the residual rows"}
+    res["launch"] = loop(g.launch)
+
+    def in_memory():
+        hip.hipMemcpyAsync(alpha0.data_ptr(), pinned.data_ptr(), nbytes, 1, sptr)
+        g.launch()
+    res["alpha_in_memory"] = loop(in_memory)
+    cur = [alpha0, alpha1]
+    updated = [0]
+
+    def node_update():
+        updated[0] = g.redirect(cur[0], cur[1])
+        cur.reverse()
+        g.launch()
+    res["alpha_node_update"] = loop(node_update)
+    res["alpha_node_update"]["args_per_update"] = updated[0]
+    if cur[0] is not alpha0:
+        g.redirect(cur[0], alpha0)
+    zeros = torch.zeros_like(step.sub)
+    g.redirect(step.sub, zeros)
+    res["zero_mask"] = loop(g.launch)
+    g.redirect(zeros, step.sub)
+    # the floor: a graph of one library kernel that finds nothing to do (a
+    # router write over a route no token subscribes to)
+    rt = px.Route(1, 1)
+    lg = torch.zeros((1, 1), dtype=torch.float32, device="cuda")
+    off = torch.zeros((1, 1), dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    eg = px.Graph(lambda: px.xmix_router_write(lg, rt, [0], off, stream), stream)
+    res["empty_graph"] = loop(eg.launch)
+    torch.cuda.synchronize()
+    eg.close()
+    g.close()
+    step.reset()
+    return res
+
+
 def run_steer_probe(torch, synth, HookStep, args):
     """The 4-layer decode step of steering and probe apps (d=4096, T=R=256,
     bits 0-3 steer, bits 4-7 probe), captured as one graph."""
@@ -338,6 +424,8 @@ def run_steer_probe(torch, synth, HookStep, args):
            "value": wl.T_valid * len(wl.layers) / (ms * 1e-3), "unit": "hooked tokens/s per layer",
            "hbm_bytes": step.hbm_bytes()}
     res["conditional_us"] = time_conditional(torch, step, wl, args)
+    log("timing parameter updates on the step graph")
+    res["step_graph"] = time_step_graph(torch, step, args)
     del step
     torch.cuda.empty_cache()
     return res
@@ -383,7 +471,10 @@ def run_c5(torch, synth, HookStep, args):
            "value": wl.T_valid / (ms * 1e-3), "unit": "tokens/s",
            "algorithmic_bytes": nbytes, "achieved_GBps": nbytes / (ms * 1e-3) / 1e9,
            "frac_of_hbm_peak": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
-    del step, graphs
+    del graphs
+    log("timing parameter updates on the 70B-shaped step graph")
+    res["step_graph"] = time_step_graph(torch, step, args)
+    del step
     torch.cuda.empty_cache()
     return res
 

@@ -358,6 +358,47 @@ xmix_status xmix_readback_compact(const void *const *seg_rows, const int32_t *se
                                   const int32_t *req_of_token, int32_t layer_id,
                                   int32_t app_id, const xmix_ring *ring, void *stream);
 
+/* ------------------------------------------------------------ step graphs
+ * A hook step captured once and replayed, with the kernel-node parameter
+ * update of Sec. 4.3 (CUDA-graph-safe kernel design: explicit node handles
+ * kept for the dynamic kernels, their arguments updated before launch
+ * instead of recapturing; graph-level toggling).
+ *
+ * xmix_graph_begin starts capturing `stream` (thread-local capture mode);
+ * the caller then enqueues library calls on it; xmix_graph_end stops the
+ * capture, instantiates the graph and returns it in *out, keeping the handle
+ * and the argument values of every kernel node launched by this library.
+ * The calls in between are recorded, not run; no call that synchronises may
+ * be made on the stream meanwhile.  stream must not be the null stream.
+ *
+ * xmix_graph_redirect: every pointer argument of those nodes that holds
+ * `from` is set to `to` for all later launches (one
+ * hipGraphExecKernelNodeSetParams per affected node; the graph is neither
+ * recaptured nor re-instantiated).  `to` must be a device buffer of the same
+ * size and layout as `from`.  *n_args (optional) receives the number of
+ * arguments changed.  The library's own design keeps every per-step value
+ * (subscriptions, alpha, thresholds, clamp values, offsets) in device
+ * memory, where a captured graph reads the current contents without any
+ * update; redirection serves switching between whole parameter buffers.
+ *
+ * xmix_graph_launch enqueues one replay on `stream`.  xmix_graph_kernel_nodes
+ * returns the number of the library's kernel nodes in the graph.
+ * xmix_graph_destroy releases the graph (the caller must not destroy it
+ * while a launch may still be running).
+ *
+ * Ownership: the graph (host memory and HIP graph objects) belongs to the
+ * caller after xmix_graph_end and is freed by xmix_graph_destroy.
+ * Errors: XMIX_E_INVAL for a null argument; XMIX_E_LAUNCH when the runtime
+ * rejects the capture, the instantiation, an update or a launch. */
+typedef struct xmix_graph xmix_graph;
+xmix_status xmix_graph_begin(void *stream);
+xmix_status xmix_graph_end(void *stream, xmix_graph **out);
+int32_t xmix_graph_kernel_nodes(const xmix_graph *g);
+xmix_status xmix_graph_redirect(xmix_graph *g, const void *from, const void *to,
+                                int32_t *n_args);
+xmix_status xmix_graph_launch(const xmix_graph *g, void *stream);
+void xmix_graph_destroy(xmix_graph *g);
+
 #ifdef __cplusplus
 }
 #endif

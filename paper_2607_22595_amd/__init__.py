@@ -55,6 +55,12 @@ _sigs = {
     "xmix_route_build": ([_vp, _vp, _vp, _i32, ctypes.POINTER(XmixRoute), _vp, _vp], _st),
     "xmix_route_gate": ([ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32, _i32, _vp, _vp], _st),
     "xmix_route_trigger": ([ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32, _vp], _st),
+    "xmix_graph_begin": ([_vp], _st),
+    "xmix_graph_end": ([_vp, ctypes.POINTER(ctypes.c_void_p)], _st),
+    "xmix_graph_kernel_nodes": ([_vp], _i32),
+    "xmix_graph_redirect": ([_vp, _vp, _vp, ctypes.POINTER(ctypes.c_int32)], _st),
+    "xmix_graph_launch": ([_vp, _vp], _st),
+    "xmix_graph_destroy": ([_vp], None),
     "xmix_router_write": ([_vp, _st, _i32, ctypes.POINTER(XmixRoute), _vp, _vp, _i32, _vp],
                           _st),
     "xmix_steer_apply": ([_vp, _st, _i32, ctypes.POINTER(XmixRoute), _vp, _vp, _vp, _vp, _i32,
@@ -218,6 +224,54 @@ def xmix_router_write(logits, route: Route, app_bits: Sequence[int], offsets, st
     _check("xmix_router_write", _lib.xmix_router_write(
         _ptr(logits), _dt(logits), E, ctypes.byref(route.struct), bits, _ptr(offsets), n,
         _stream(stream)))
+
+
+class Graph:
+    """A sequence of library calls captured once on `stream` (xmix_graph_begin
+    / xmix_graph_end) and replayed with launch().  redirect(old, new) points
+    every kernel argument that holds tensor `old` at tensor `new` (same size
+    and layout) through a kernel-node parameter update; it returns the
+    number of arguments changed.  Nothing else may run on `stream` during
+    the capture, and `record` must not synchronise or allocate."""
+
+    def __init__(self, record, stream):
+        if not isinstance(stream, torch.cuda.Stream):
+            raise ValueError("capture needs a torch.cuda.Stream (not the null stream)")
+        self.stream = stream
+        self._h = ctypes.c_void_p()
+        _check("xmix_graph_begin", _lib.xmix_graph_begin(_stream(stream)))
+        try:
+            record()
+        finally:
+            st = _lib.xmix_graph_end(_stream(stream), ctypes.byref(self._h))
+        _check("xmix_graph_end", st)
+
+    @property
+    def kernel_nodes(self) -> int:
+        return int(_lib.xmix_graph_kernel_nodes(self._h))
+
+    def redirect(self, old, new) -> int:
+        if old.numel() * old.element_size() != new.numel() * new.element_size():
+            raise ValueError("redirect needs buffers of the same size")
+        n = ctypes.c_int32(0)
+        _check("xmix_graph_redirect", _lib.xmix_graph_redirect(self._h, _ptr(old), _ptr(new),
+                                                               ctypes.byref(n)))
+        return int(n.value)
+
+    def launch(self, stream=None):
+        _check("xmix_graph_launch", _lib.xmix_graph_launch(
+            self._h, _stream(self.stream if stream is None else stream)))
+
+    def close(self):
+        if self._h:
+            _lib.xmix_graph_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def probe_workspace(T_max: int, n_probe: int, mode: int) -> int:

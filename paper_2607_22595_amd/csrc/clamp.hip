@@ -3,6 +3,7 @@
 // rows are read; the dense m x d decode is never formed.  One workgroup per
 // slot of the app's token list (slots past the live count return at once).
 #include "common.hpp"
+#include "kernels.hpp"
 #include "launch.hpp"
 
 namespace xmix {
@@ -78,6 +79,10 @@ hipError_t launch_clamp_decode(uint16_t* h, int32_t d, const int32_t* app_count,
                        app_count, tok_list, idx, val, k, W_dec, m, clamp_ids, clamp_vals,
                        n_clamp, delta_out);
     return hipGetLastError();
+}
+
+void add_clamp_kernels(std::vector<KernelInfo>& t) {
+    t.push_back(kernel_info(clamp_decode_kernel));
 }
 
 }  // namespace xmix

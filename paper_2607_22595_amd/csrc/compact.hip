@@ -5,6 +5,7 @@
 // workgroup drawing the last ticket has therefore seen every other read, and
 // it alone advances head[0] and returns the ticket counter to zero.
 #include "common.hpp"
+#include "kernels.hpp"
 #include "launch.hpp"
 
 namespace xmix {
@@ -66,6 +67,10 @@ hipError_t launch_compact(const Segments& segs, const int32_t* app_count,
                        app_count, tok_list, req, layer_id, app_id, slots, head, capacity,
                        row_bytes);
     return hipGetLastError();
+}
+
+void add_compact_kernels(std::vector<KernelInfo>& t) {
+    t.push_back(kernel_info(compact_kernel));
 }
 
 }  // namespace xmix

@@ -12,6 +12,7 @@
 // Last-token mode runs the token pass with one workgroup per request on the
 // last token of its span, writing [n_probe][R_max].
 #include "common.hpp"
+#include "kernels.hpp"
 #include "launch.hpp"
 
 namespace xmix {
@@ -182,6 +183,18 @@ hipError_t launch_probe(const void* h, bool bf16, int32_t d, int32_t T_max,
     hipLaunchKernelGGL(probe_pool_kernel, dim3(R_max), dim3(kProbeThreads), 0, stream, ws, T_max,
                        tok_mask, cu_seqlens, b, bits, n_probe, R_max, logit, score);
     return hipGetLastError();
+}
+
+void add_probe_kernels(std::vector<KernelInfo>& t) {
+    t.push_back(kernel_info(probe_token_kernel<true, 4>));
+    t.push_back(kernel_info(probe_token_kernel<true, 8>));
+    t.push_back(kernel_info(probe_token_kernel<true, 16>));
+    t.push_back(kernel_info(probe_token_kernel<true, 32>));
+    t.push_back(kernel_info(probe_token_kernel<false, 4>));
+    t.push_back(kernel_info(probe_token_kernel<false, 8>));
+    t.push_back(kernel_info(probe_token_kernel<false, 16>));
+    t.push_back(kernel_info(probe_token_kernel<false, 32>));
+    t.push_back(kernel_info(probe_pool_kernel));
 }
 
 }  // namespace xmix

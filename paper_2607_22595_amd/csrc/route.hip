@@ -8,6 +8,7 @@
 // LDS) plus the running total of earlier chunks.  Workgroup 0 also writes
 // the token masks and the error word.
 #include "common.hpp"
+#include "kernels.hpp"
 #include "launch.hpp"
 
 namespace xmix {
@@ -175,6 +176,12 @@ hipError_t launch_route_trigger(int32_t T_max, int32_t app_bit, uint32_t* tok_ma
     hipLaunchKernelGGL(route_filter_kernel<true>, dim3(1), dim3(kRouteThreads), 0, stream, T_max,
                        app_bit, tok_mask, app_count, app_tokens, g);
     return hipGetLastError();
+}
+
+void add_route_kernels(std::vector<KernelInfo>& t) {
+    t.push_back(kernel_info(route_build_kernel));
+    t.push_back(kernel_info(route_filter_kernel<false>));
+    t.push_back(kernel_info(route_filter_kernel<true>));
 }
 
 }  // namespace xmix

@@ -7,6 +7,7 @@
 // launch-latency bound: one thread per (token slot, expert), tokens without a
 // router bit leave after reading their mask word.
 #include "common.hpp"
+#include "kernels.hpp"
 #include "launch.hpp"
 
 namespace xmix {
@@ -45,6 +46,11 @@ hipError_t launch_router_write(void* logits, bool bf16, int32_t n_experts, int32
         hipLaunchKernelGGL(router_kernel<false>, grid, dim3(kRouterThreads), 0, stream, logits,
                            n_experts, n_elem, tok_mask, bits, offsets, n_router);
     return hipGetLastError();
+}
+
+void add_router_kernels(std::vector<KernelInfo>& t) {
+    t.push_back(kernel_info(router_kernel<true>));
+    t.push_back(kernel_info(router_kernel<false>));
 }
 
 }  // namespace xmix

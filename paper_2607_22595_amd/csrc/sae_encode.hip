@@ -40,6 +40,7 @@
 #include <math.h>
 
 #include "common.hpp"
+#include "kernels.hpp"
 #include "launch.hpp"
 
 namespace xmix {
@@ -1403,6 +1404,15 @@ hipError_t launch_sae_merge(const uint16_t* h, int32_t d, int32_t T_max,
                        a.cnt, a.tau, n_mt, e.cap, app_count, tok_list, k, h, d, W_enc,
                        c_fold, idx_out, val_out, r);
     return hipGetLastError();
+}
+
+void add_sae_kernels(std::vector<KernelInfo>& t) {
+    t.push_back(kernel_info(sae_pack_kernel));
+    t.push_back(kernel_info(sae_fold_kernel));
+    t.push_back(kernel_info(sae_stream_kernel));
+    t.push_back(kernel_info(sae_xstage_kernel));
+    t.push_back(kernel_info(sae_gemm_kernel));
+    t.push_back(kernel_info(sae_merge_kernel));
 }
 
 }  // namespace xmix

@@ -9,6 +9,7 @@
 // coalesced 16-byte load or store.  Rows without a steering bit return
 // before touching memory beyond their mask word.
 #include "common.hpp"
+#include "kernels.hpp"
 #include "launch.hpp"
 
 namespace xmix {
@@ -85,6 +86,11 @@ hipError_t launch_steer(void* h, bool bf16, int32_t d, int32_t T_max, const uint
         hipLaunchKernelGGL(steer_kernel<false>, dim3(T_max), dim3(kSteerThreads), 0, stream, h,
                            d, tok_mask, req, vecs, bits, alpha, n_steer);
     return hipGetLastError();
+}
+
+void add_steer_kernels(std::vector<KernelInfo>& t) {
+    t.push_back(kernel_info(steer_kernel<true>));
+    t.push_back(kernel_info(steer_kernel<false>));
 }
 
 }  // namespace xmix

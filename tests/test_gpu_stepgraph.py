@@ -1,0 +1,140 @@
+"""The library's own step graph (xmix_graph_*): a multi-layer hook step
+captured once on a stream, replayed with per-step values changed in device
+memory, and with whole parameter buffers swapped through kernel-node
+parameter updates (redirect).  Every replay is compared with an eager run
+of the same inputs (bit-identical: the same kernels on the same data), and
+the redirected steering against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from parity import check_steer, torch_bits
+
+pytestmark = pytest.mark.gpu
+
+
+def _workload():
+    # 4 hooked layers: bits 0-3 steer, 4-7 probe, plus a clamp SAE on layer 2
+    wl = synth.make("c2", d=512, T=160, n_layers=4)
+    c5 = synth.make("c5", d=512, T=160, m=1024, k=16, n_steer=0, n_probe=0, n_clamp_apps=1)
+    s = c5.layers[0].saes[0]
+    s.bit = 8
+    wl.n_apps = 9
+    wl.sub = wl.sub | (c5.sub << np.uint32(8))
+    wl.layers[2].saes.append(s)
+    return wl
+
+
+def _h(step):
+    return [torch_bits(lay.h).copy() for lay in step.layers]
+
+
+def _eager(step):
+    step.reset()
+    step.run()
+    torch.cuda.synchronize()
+    return _h(step)
+
+
+def _replay(step, g):
+    step.reset()
+    torch.cuda.synchronize()
+    g.launch()
+    g.stream.synchronize()
+    return _h(step)
+
+
+@pytest.fixture(scope="module")
+def captured():
+    import paper_2607_22595_amd as px
+    from paper_2607_22595_amd.hookstep import HookStep
+    wl = _workload()
+    step = HookStep(wl)
+    step.run()
+    torch.cuda.synchronize()
+    stream = torch.cuda.Stream()
+    g = px.Graph(lambda: step.run(stream), stream)
+    yield wl, step, g
+    torch.cuda.synchronize()
+    g.close()
+
+
+def test_step_graph_replays_match_eager(captured):
+    wl, step, g = captured
+    # route build, 4 x (probe + steer), encode (candidates + merge) and clamp
+    assert g.kernel_nodes >= 11
+    ref = _eager(step)
+    for _ in range(3):
+        got = _replay(step, g)
+        for a, b in zip(got, ref):
+            assert np.array_equal(a, b)
+
+
+def test_in_memory_values_change_without_update(captured):
+    """New alpha, subscriptions and clamp values written into the device
+    buffers the graph reads: the next replay uses them, no update needed."""
+    wl, step, g = captured
+    rng = np.random.default_rng(3)
+    s = step.layers[2].saes[0]
+    for rep in range(2):
+        step.alpha.copy_(torch.from_numpy(rng.uniform(-8, 8, tuple(step.alpha.shape))
+                                          .astype(np.float32)))
+        step.sub.copy_(torch.from_numpy(rng.integers(0, 1 << 9, step.sub.numel())
+                                        .astype(np.uint32).view(np.int32)))
+        s.clamp_vals.copy_(torch.from_numpy(rng.uniform(-5, 15, s.clamp_vals.numel())
+                                            .astype(np.float32)))
+        torch.cuda.synchronize()
+        got = _replay(step, g)
+        ref = _eager(step)
+        for a, b in zip(got, ref):
+            assert np.array_equal(a, b), f"replay {rep}"
+
+
+def test_redirect_steering_alpha_by_node_update(captured):
+    """Swap the whole alpha buffer by a kernel-node update: one argument per
+    steering node (4 layers) changes; the replay equals an eager run with the
+    new buffer and, on layer 0, the oracle's steering."""
+    wl, step, g = captured
+    alpha0 = step.alpha
+    rng = np.random.default_rng(4)
+    alpha1 = torch.from_numpy(rng.uniform(-8, 8, tuple(alpha0.shape)).astype(np.float32)).cuda()
+    n = g.redirect(alpha0, alpha1)
+    assert n == 4
+    got = _replay(step, g)
+    step.alpha = alpha1                      # the eager run reads the new buffer too
+    try:
+        ref = _eager(step)
+    finally:
+        step.alpha = alpha0
+    for a, b in zip(got, ref):
+        assert np.array_equal(a, b)
+    # layer 0 against the oracle: its probes only read, so h0 is the steered input
+    lay0, L0 = step.layers[0], wl.layers[0]
+    tm, _, _, _ = oracle.route(wl.req, wl.T_valid, torch_sub(step), wl.n_apps)
+    v = np.stack([a.v for a in L0.steer])
+    h_ref = oracle.steer(L0.h, tm, wl.req, v, [a.bit for a in L0.steer], alpha1.cpu().numpy())
+    check_steer(got[0], h_ref, L0.h, (tm & 0xF) != 0)
+    assert g.redirect(alpha1, alpha0) == 4   # and back
+    got = _replay(step, g)
+    ref = _eager(step)
+    for a, b in zip(got, ref):
+        assert np.array_equal(a, b)
+
+
+def torch_sub(step):
+    return step.sub.cpu().numpy().view(np.uint32)
+
+
+def test_redirect_subscriptions_and_unknown_buffer(captured):
+    wl, step, g = captured
+    sub0 = step.sub
+    sub1 = torch.zeros_like(sub0)            # nobody subscribed
+    assert g.redirect(sub0, sub1) == 1       # the route build reads it once
+    got = _replay(step, g)
+    for lay, a in zip(step.layers, got):
+        assert np.array_equal(a, torch_bits(lay.h_in))
+    assert g.redirect(sub1, sub0) == 1
+    other = torch.zeros(16, dtype=torch.float32, device="cuda")
+    assert g.redirect(other, torch.zeros_like(other)) == 0
