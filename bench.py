@@ -117,6 +117,46 @@ def time_replays(torch, rot, n):
     return e0.elapsed_time(e1) / n
 
 
+def time_replay_runs(torch, rot, n, runs=7):
+    """n replays of `rot` in `runs` consecutive runs, one HIP event between
+    runs on the current stream (the stream the kernels run on).  Returns the
+    average ms per replay over all n and the per-run averages."""
+    runs = max(1, min(runs, n))
+    sizes = [n // runs + (1 if i < n % runs else 0) for i in range(runs)]
+    s = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(runs + 1)]
+    torch.cuda.synchronize()
+    ev[0].record(s)
+    for i, k in enumerate(sizes):
+        for _ in range(k):
+            rot.replay()
+        ev[i + 1].record(s)
+    ev[-1].synchronize()
+    per_run = [ev[i].elapsed_time(ev[i + 1]) / sizes[i] for i in range(runs)]
+    total = ev[0].elapsed_time(ev[-1])
+    return total / n, per_run, sizes
+
+
+def run_stats(per_run, sizes, tokens_per_step, seed=0):
+    """Median and p10/p90 of the per-run latency; the throughput over all
+    runs (total tokens / total time, the harmonic mean of the per-run
+    throughputs weighted by their replays) and a bootstrap 95 % interval of
+    it over runs."""
+    ms = np.asarray(per_run, np.float64)
+    w = np.asarray(sizes, np.float64)
+    thr = tokens_per_step * w.sum() / (ms * w).sum() * 1e3
+    rng = np.random.default_rng(seed)
+    boot = []
+    for _ in range(2000):
+        i = rng.integers(0, len(ms), len(ms))
+        boot.append(tokens_per_step * w[i].sum() / (ms[i] * w[i]).sum() * 1e3)
+    lo, hi = np.percentile(boot, [2.5, 97.5])
+    return {"runs": len(ms), "replays_per_run": [int(x) for x in sizes],
+            "ms_median": float(np.median(ms)), "ms_p10": float(np.percentile(ms, 10)),
+            "ms_p90": float(np.percentile(ms, 90)), "tokens_per_s": float(thr),
+            "tokens_per_s_ci95": [float(lo), float(hi)]}
+
+
 def dictionary_copies(torch, W, min_bytes=1.5 * 2 ** 30):
     n = max(2, int(np.ceil(min_bytes / (W.numel() * W.element_size()))))
     return [W] + [W.clone() for _ in range(n - 1)]
@@ -141,14 +181,15 @@ def bench_workload(torch, px, step, sae_layer, sae_idx, steps, warmup, encode=Tr
     for _ in range(warmup):
         full.replay()
     torch.cuda.synchronize()
-    ms_step = time_replays(torch, full, steps)
+    ms_step, per_run, sizes = time_replay_runs(torch, full, steps)
+    stats = run_stats(per_run, sizes, step.wl.T_valid)
     ms_enc = None
     if encode:
         for _ in range(max(warmup // 2, 3)):
             enc.replay()
         ms_enc = time_replays(torch, enc, steps)
     set_copy(copies[0])
-    return ms_step, ms_enc
+    return ms_step, ms_enc, stats
 
 
 def cpu_baseline_decode(wl, budget_s):
@@ -224,7 +265,7 @@ def run_decode(torch, px, synth, HookStep, args):
     wl = synth.make("c3")
     step = HookStep(wl)
     log("timing the decode step")
-    ms_step, ms_enc = bench_workload(torch, px, step, 0, 0, args.steps, args.warmup)
+    ms_step, ms_enc, stats = bench_workload(torch, px, step, 0, 0, args.steps, args.warmup)
     s = wl.layers[0].saes[0]
     n_sub = int(np.count_nonzero(wl.sub & 1))
     enc_bytes = s.m * wl.d * 2 + s.m * 4 + n_sub * wl.d * 2   # W_enc + folded bias + tokens
@@ -250,10 +291,11 @@ def run_decode(torch, px, synth, HookStep, args):
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic("decode"),
                      "ms_per_launch": ms_enc, "algorithmic_bytes": enc_bytes},
     }
+    out["step_stats"] = stats
     # "don't use, don't pay": the same captured step with no subscriber
     sub_saved = step.sub.clone()
     step.sub.zero_()
-    ms_zero, _ = bench_workload(torch, px, step, 0, 0, args.steps, args.warmup, encode=False)
+    ms_zero, _, _ = bench_workload(torch, px, step, 0, 0, args.steps, args.warmup, encode=False)
     step.sub.copy_(sub_saved)
     out["zero_mask_step_us"] = ms_zero * 1e3
     del step
@@ -317,17 +359,18 @@ def time_step_graph(torch, step, args):
     """Parameter updates on the library's own step graph of `step` (Sec. 4.3):
     per step, GPU time (events on the graph's stream) and host time to
     enqueue, for a plain launch; a launch after an in-memory update of alpha
-    (one hipMemcpyAsync from pinned host memory into the buffer the graph
-    reads); a launch after a kernel-node update that points every steering
-    node at another alpha buffer; the zero-mask step (subscriptions buffer
-    redirected to zeros); and an empty graph of one trivial kernel, the floor
-    of any graph launch."""
+    (one hipMemcpyAsync into the buffer the graph reads, from pinned host
+    memory or from a preset device buffer); a launch after a kernel-node
+    update that points every steering node at another alpha buffer; the
+    zero-mask step (subscriptions buffer redirected to zeros); and a graph of
+    one kernel that finds nothing to do, the floor of any graph launch."""
     import ctypes
     import time
     import paper_2607_22595_amd as px
     hip = ctypes.CDLL("libamdhip64.so")
     hip.hipMemcpyAsync.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                    ctypes.c_int, ctypes.c_void_p]
+    hip.hipMemcpyAsync.restype = ctypes.c_int
     stream = torch.cuda.Stream()
     step.reset()
     torch.cuda.synchronize()
@@ -365,10 +408,20 @@ def time_step_graph(torch, step, args):
            "note": "every step graph replay includes the restore copies of the residual rows"}
     res["launch"] = loop(g.launch)
 
-    def in_memory():
-        hip.hipMemcpyAsync(alpha0.data_ptr(), pinned.data_ptr(), nbytes, 1, sptr)
+    rc = [0]
+
+    def in_memory_h2d():
+        rc[0] |= hip.hipMemcpyAsync(alpha0.data_ptr(), pinned.data_ptr(), nbytes, 1, sptr)
         g.launch()
-    res["alpha_in_memory"] = loop(in_memory)
+    res["alpha_in_memory_h2d"] = loop(in_memory_h2d)
+    preset = alpha0.clone()
+
+    def in_memory_d2d():
+        rc[0] |= hip.hipMemcpyAsync(alpha0.data_ptr(), preset.data_ptr(), nbytes, 3, sptr)
+        g.launch()
+    res["alpha_in_memory_d2d"] = loop(in_memory_d2d)
+    if rc[0]:
+        raise RuntimeError("hipMemcpyAsync failed in the parameter-update timing")
     cur = [alpha0, alpha1]
     updated = [0]
 
@@ -484,8 +537,8 @@ def run_prefill(torch, px, synth, HookStep, args):
     wl4 = synth.make("c4")
     step4 = HookStep(wl4)
     log("timing the prefill step")
-    ms4, ms4_enc = bench_workload(torch, px, step4, 0, 0, args.prefill_steps,
-                                  max(2, args.warmup // 10))
+    ms4, ms4_enc, stats4 = bench_workload(torch, px, step4, 0, 0, args.prefill_steps,
+                                          max(2, args.warmup // 10))
     s4 = wl4.layers[0].saes[0]
     flops = 2.0 * wl4.T_valid * s4.m * wl4.d
     tf = flops / (ms4_enc * 1e-3) / 1e12
@@ -499,7 +552,8 @@ def run_prefill(torch, px, synth, HookStep, args):
                      "achieved": tf, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": tf / MFMA_BF16_PEAK_TFLOPS, "ms_per_launch": ms4_enc,
                      "algorithmic_flops": flops,
-                     "traffic": measured_traffic("prefill")}}
+                     "traffic": measured_traffic("prefill")},
+        "step_stats": stats4}
     del step4
     torch.cuda.empty_cache()
     return res
