@@ -28,9 +28,10 @@ import torch
 
 from . import (XMIX_PROBE_LAST, XMIX_PROBE_MEAN, XMIX_PROBE_TOKEN, Ring, Route, probe_workspace,
                sae_encode_workspace, xmix_probe_score, xmix_readback_compact,
-               xmix_route_build, xmix_sae_clamp_decode, xmix_sae_encode_topk,
-               xmix_sae_encode_topk_ring,
-               xmix_sae_fold_bias, xmix_sae_pack_encoder, xmix_steer_apply)
+               xmix_route_build, xmix_sae_clamp_decode, xmix_sae_encode_candidates,
+               xmix_sae_encode_topk, xmix_sae_encode_topk_ring, xmix_sae_fold_bias,
+               xmix_sae_merge_topk, xmix_sae_merge_topk_ring, xmix_sae_pack_encoder,
+               xmix_steer_apply)
 
 
 def to_device_bits(a: np.ndarray, device) -> torch.Tensor:
@@ -151,15 +152,31 @@ class HookStep:
         for lay in self.layers:
             lay.h.copy_(lay.h_in)
 
-    def run(self, stream=None):
-        """Enqueue one full hook step (all layers) on `stream`."""
+    def run(self, stream=None, marks=None):
+        """Enqueue one full hook step (all layers) on `stream`.  `marks`, if
+        given, is a pair of host callables invoked while enqueueing, right
+        before and right after the encode GEMM stage of each SAE app (e.g. to
+        record timing events); the SAE call is then issued as its two stages,
+        which enqueues the same kernels."""
         xmix_route_build(self.req, self.T_valid, self.sub, self.route, self.err, stream)
         for lay in self.layers:
             for p in lay.probes:
                 xmix_probe_score(lay.h, self.route, p.w, p.b, p.bits, p.mode, p.logit, p.score,
                                  cu_seqlens=self.cu, ws=p.ws, stream=stream)
             for s in lay.saes:
-                if s.ring is not None and self.fuse_readback:
+                if marks is not None:
+                    marks[0]()
+                    xmix_sae_encode_candidates(lay.h, self.route, s.bit, s.W_enc, s.b_enc,
+                                               s.b_dec, s.c_fold, s.k, s.ws, stream)
+                    marks[1]()
+                    if s.ring is not None and self.fuse_readback:
+                        xmix_sae_merge_topk_ring(lay.h, self.route, s.bit, s.W_enc, s.c_fold,
+                                                 s.k, s.idx, s.val, s.ws, self.req,
+                                                 lay.layer_id, s.bit, s.ring, stream)
+                    else:
+                        xmix_sae_merge_topk(lay.h, self.route, s.bit, s.W_enc, s.c_fold, s.k,
+                                            s.idx, s.val, s.ws, stream)
+                elif s.ring is not None and self.fuse_readback:
                     # the merge writes the ring rows itself
                     xmix_sae_encode_topk_ring(lay.h, self.route, s.bit, s.W_enc, s.b_enc, s.b_dec,
                                               s.c_fold, s.k, s.idx, s.val, s.ws, self.req,
