@@ -1,9 +1,11 @@
 // Readback compaction into a fixed-capacity device ring.  One wave per row of
 // the app's token list (the list is already ascending and compact, built by
 // the routing kernel's ballot/prefix pass); slot = (head + i) mod capacity.
-// Every workgroup reads head[0] before it takes a ticket from head[1]; the
-// workgroup drawing the last ticket has therefore seen every other read, and
-// it alone advances head[0] and returns the ticket counter to zero.
+// Every workgroup that holds a row reads head[0] before it takes a ticket
+// from head[1]; the one drawing the last ticket has therefore seen every
+// other read, and it alone advances head[0] and returns the ticket counter
+// to zero.  Workgroups without a row take no ticket, so a step with no
+// subscriber costs no atomics.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "launch.hpp"
@@ -27,6 +29,8 @@ compact_kernel(Segments segs, const int32_t* __restrict__ app_count,
     __syncthreads();
     const uint64_t h0 = h0_s;
     const int32_t cnt = cnt_s;
+    const int32_t n_active = (cnt + kRowsPerBlock - 1) / kRowsPerBlock;
+    if (static_cast<int32_t>(blockIdx.x) >= n_active) return;  // uniform
 
     const int wave = threadIdx.x / kWave, lane = lane_id();
     const int32_t i = blockIdx.x * kRowsPerBlock + wave;
@@ -51,7 +55,7 @@ compact_kernel(Segments segs, const int32_t* __restrict__ app_count,
     if (threadIdx.x == 0) {
         __threadfence();
         const uint64_t ticket = atomicAdd(reinterpret_cast<unsigned long long*>(&head[1]), 1ull);
-        if (ticket == gridDim.x - 1) {
+        if (ticket == static_cast<uint64_t>(n_active) - 1u) {
             __atomic_store_n(&head[0], h0 + static_cast<uint64_t>(cnt), __ATOMIC_RELAXED);
             atomicExch(reinterpret_cast<unsigned long long*>(&head[1]), 0ull);
         }

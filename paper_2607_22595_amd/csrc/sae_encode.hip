@@ -961,12 +961,14 @@ struct RingOut {
     int32_t layer_id, app_id;
 };
 
-// The workgroup's ticket; the last of gridDim.x advances the head by `cnt`
-// (every workgroup read the head before its ticket) and resets the counter.
+// The workgroup's ticket; the last of the `cnt` workgroups that hold a token
+// advances the head by `cnt` (each read the head before its ticket) and
+// resets the counter.  Workgroups without a token take no ticket, so a step
+// with no subscriber costs no atomics.
 __device__ __forceinline__ void ring_ticket(const RingOut& ring, uint64_t h0, int cnt) {
     __threadfence();
     const uint64_t ticket = atomicAdd(reinterpret_cast<unsigned long long*>(&ring.head[1]), 1ull);
-    if (ticket == gridDim.x - 1) {
+    if (ticket == static_cast<uint64_t>(cnt) - 1u) {
         __atomic_store_n(&ring.head[0], h0 + static_cast<uint64_t>(cnt), __ATOMIC_RELAXED);
         atomicExch(reinterpret_cast<unsigned long long*>(&ring.head[1]), 0ull);
     }
@@ -1038,14 +1040,11 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
     const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
     const int n = blockIdx.x;
     const int cnt = *app_count;
-    // readback ring (optional): every workgroup reads the head before it
-    // takes a ticket; the one drawing the last ticket advances the head
+    if (n >= cnt) return;  // uniform: no token, no ring row, no ticket
+    // readback ring (optional): each workgroup with a token reads the head
+    // before it takes a ticket; the one drawing the last ticket advances it
     uint64_t h0 = 0;
     if (ring.slots && tid == 0) h0 = __atomic_load_n(&ring.head[0], __ATOMIC_RELAXED);
-    if (n >= cnt) {  // uniform over the workgroup
-        if (ring.slots && tid == 0) ring_ticket(ring, h0, cnt);
-        return;
-    }
     const int32_t t = tok_list[n];
     const int64_t row0 = static_cast<int64_t>(n) * n_mt;
 
