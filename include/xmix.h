@@ -17,15 +17,16 @@
  * --------------------------------
  * - All data pointers are DEVICE pointers unless the comment says "host".
  *   The caller allocates and owns every buffer; the library keeps no
- *   per-call state and allocates nothing.
+ *   per-call state and allocates nothing (the one exception is the step
+ *   graph executor, xmix_graph_*, which owns the graphs it instantiates).
  * - bf16 values travel as their raw 16-bit patterns (uint16_t).
  * - Activations are row-major [T_max, d]: one row per token slot of the
  *   continuous batch.  T_max is the static batch capacity; the number of
  *   live tokens, T_valid, lives in device memory, so one captured graph
  *   serves every batch.
- * - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
- *   stream), never synchronises, never copies between host and device, and
- *   can be captured into a HIP graph.  Per-step data (T_valid, subscription
+ * - Every hook-step call is asynchronous on `stream` (a hipStream_t; NULL =
+ *   the null stream), never synchronises, never copies between host and
+ *   device, and can be captured into a HIP graph.  Per-step data (T_valid, subscription
  *   masks, alpha, clamp values, ring heads) is read from device memory at
  *   run time, so a graph can be replayed with new requests without
  *   recapture.
@@ -36,6 +37,14 @@
  * - Rows of unsubscribed tokens or requests are never written in any
  *   output ("don't use, don't pay").
  * - No C++ exception crosses this interface.
+ *
+ * Calls, in the order of one layer's step: routing (xmix_route_build) and
+ * its conditional filters (xmix_route_gate, xmix_route_trigger); the reads
+ * (xmix_probe_score, xmix_sae_encode_topk and its stages); the writes
+ * (xmix_steer_apply, xmix_sae_clamp_decode, xmix_router_write); readback
+ * (xmix_readback_compact, or fused into the SAE merge with the _ring
+ * variants).  Step graphs (xmix_graph_*) capture and replay such a
+ * sequence.
  */
 #ifndef XMIX_H
 #define XMIX_H
