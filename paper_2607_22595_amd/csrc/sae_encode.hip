@@ -1289,7 +1289,7 @@ static EmitPlan emit_plan(int32_t m, int32_t k) {
     e.target = (2 * k * kBM + m - 1) / m + 1;
     e.target = e.target < 2 ? 2 : (e.target > 64 ? 64 : e.target);
     e.cap = 4 * e.target;
-    e.cap = e.cap < 16 ? 16 : (e.cap > 64 ? 64 : e.cap);
+    e.cap = e.cap < 8 ? 8 : (e.cap > 64 ? 64 : e.cap);
     e.lo = (n_mt * e.target >= 4 * k) ? 0 : (k < e.cap ? k : e.cap);
     const double want = e.lo ? 0.5 * (e.lo + e.cap) : e.target;
     // upper-tail quantile: 0.5 * erfc(z / sqrt 2) = want / 256, by bisection

@@ -72,12 +72,12 @@ def test_workspace_queries(lib):
     lib.xmix_probe_workspace.restype = ctypes.c_size_t
     # decode SAE: 256 token slots, m = 65536 (256 slices), k = 64: the
     # folded bias, then per (token, slice) a block of `cap` candidate pairs
-    # (8 bytes each) plus a count and a threshold, 16 <= cap <= 64
+    # (8 bytes each) plus a count and a threshold, 8 <= cap <= 64
     fold = 65536 * 4
     ws = lib.xmix_sae_encode_workspace(256, 4096, 65536, 64)
     per_slot, rem = divmod(ws - fold, 256 * 256)
     assert rem == 0 and (per_slot - 8) % 8 == 0
-    assert 16 <= (per_slot - 8) // 8 <= 64
+    assert 8 <= (per_slot - 8) // 8 <= 64
     assert lib.xmix_probe_workspace(8192, 4, 1) == 8192 * 4 * 4
     assert lib.xmix_probe_workspace(8192, 4, 0) == 0
 
