@@ -981,17 +981,21 @@ constexpr int kMaxRepair = 16;                     // slices one repair redoes
 constexpr int kRepairR = 6;                        // repair pool entries per lane
 constexpr int kRepairPool = kRepairR * kWave;      // 384 >= k + one slice
 
-// The k best of the pool key[0..n) (k <= n <= kPoolMax), by wave 0, with a
-// register footprint matched to the pool size; the 64 entries past
-// kPoolMax are the staging area.
-__device__ __forceinline__ void pool_select(uint32_t* K, int32_t* I, int n, int k,
-                                            uint32_t* tau, uint32_t* wk, int32_t* wi) {
-    uint32_t* sk = K + kPoolMax;
-    int32_t* si = I + kPoolMax;
-    if (n <= 4 * kWave) wave_select_take<4>(K, I, n, k, sk, si, tau, wk, wi);
-    else if (n <= 8 * kWave) wave_select_take<8>(K, I, n, k, sk, si, tau, wk, wi);
-    else if (n <= 16 * kWave) wave_select_take<16>(K, I, n, k, sk, si, tau, wk, wi);
-    else wave_select_take<kMergeR>(K, I, n, k, sk, si, tau, wk, wi);
+// The k best of key[0..n) / idx[0..n) (k <= n <= 8 * 64) by one wave, with
+// a register footprint matched to n; sk / si is that wave's 64-entry
+// staging area.
+constexpr int kDirectSelect = 4 * kWave;  // pools up to this go to one wave
+__device__ __forceinline__ void small_select(const uint32_t* K, const int32_t* I, int n, int k,
+                                             uint32_t* sk, int32_t* si, uint32_t* tau,
+                                             uint32_t* wk, int32_t* wi) {
+    if (n <= kDirectSelect) wave_select_take<4>(K, I, n, k, sk, si, tau, wk, wi);
+    else wave_select_take<8>(K, I, n, k, sk, si, tau, wk, wi);
+}
+
+// Entries of quarter w of a pool of `total` cut into four.
+__device__ __forceinline__ int quarter_size(int total, int w) {
+    const int q = (total + 3) / 4;
+    return max(0, min(q, total - w * q));
 }
 
 // pre-activation of latent j without the bias: plain fp32 dot product of
@@ -1032,6 +1036,10 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
                  RingOut ring) {
     __shared__ uint32_t K[kPoolMax + kWave];
     __shared__ int32_t I[kPoolMax + kWave];
+    __shared__ uint32_t K2[5 * kWave];  // the four waves' winners, then a staging area
+    __shared__ int32_t I2[5 * kWave];
+    __shared__ uint32_t SK[kMergeThreads / kWave][kWave];  // per-wave staging areas
+    __shared__ int32_t SI[kMergeThreads / kWave][kWave];
     __shared__ int scan_s[kMergeThreads / kWave];
     __shared__ uint32_t tmax_s[kMergeThreads / kWave];
     __shared__ int pool_n_s, nfail_s, fix_s;
@@ -1120,18 +1128,42 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
         }
     }
     __syncthreads();
-    // wave 0 selects the k best of the pool and checks the certificate
+    // Selection.  A large pool is cut into quarters: each wave keeps the k
+    // best of its quarter, and wave 0 selects from those (an entry of the
+    // pool's top k, in the order key descending, latent ascending, is in its
+    // quarter's top k, so nothing is lost, ties included); a small pool goes
+    // to wave 0 directly.  Then wave 0 checks the certificate.
     uint32_t wk = 0;
     int32_t wi = 0x7FFFFFFF;
-    if (wave == 0) {
-        const bool fits = total <= kPoolMax && total >= k;
-        uint32_t tau = 0;
-        if (fits) pool_select(K, I, total, k, &tau, &wk, &wi);
-        if (lane == 0) {
-            sel_tau_s = tau;
-            fix_s = !fits ? 2 : (tau_tiles <= tau ? 0 : 1);
-            nfail_s = 0;
+    const bool fits = total <= kPoolMax && total >= k;  // uniform
+    uint32_t tau = 0;
+    if (fits && total > kDirectSelect) {
+        const int q = (total + 3) / 4, nw = quarter_size(total, wave), kw = min(k, nw);
+        int off = 0, total2 = 0;
+        for (int w = 0; w < kMergeThreads / kWave; ++w) {
+            const int kq = min(k, quarter_size(total, w));
+            off += w < wave ? kq : 0;
+            total2 += kq;
         }
+        if (nw > 0) {
+            uint32_t tw, a;
+            int32_t b;
+            small_select(K + wave * q, I + wave * q, nw, kw, SK[wave], SI[wave], &tw, &a, &b);
+            if (lane < kw) {
+                K2[off + lane] = a;
+                I2[off + lane] = b;
+            }
+        }
+        __syncthreads();
+        if (wave == 0)
+            small_select(K2, I2, total2, k, K2 + 4 * kWave, I2 + 4 * kWave, &tau, &wk, &wi);
+    } else if (fits && wave == 0) {
+        small_select(K, I, total, k, K + kPoolMax, I + kPoolMax, &tau, &wk, &wi);
+    }
+    if (wave == 0 && lane == 0) {
+        sel_tau_s = tau;
+        fix_s = !fits ? 2 : (tau_tiles <= tau ? 0 : 1);
+        nfail_s = 0;
     }
     __syncthreads();
     if (fix_s != 0) {  // uniform
