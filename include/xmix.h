@@ -59,7 +59,7 @@ extern "C" {
 typedef enum {
     XMIX_OK = 0,
     XMIX_E_INVAL = 1,        /* bad pointer, size or combination of sizes */
-    XMIX_E_UNSUPPORTED = 2,  /* valid request outside what this build supports */
+    XMIX_E_UNSUPPORTED = 2,  /* valid request outside what the library supports */
     XMIX_E_WORKSPACE = 3,    /* workspace missing or smaller than required */
     XMIX_E_LAUNCH = 4        /* the HIP runtime rejected a launch */
 } xmix_status;
