@@ -18,6 +18,9 @@
 // mean + z * stdev of the tile's 256 values, then bisection on the value if
 // needed); every latent with pre >= tau is emitted as a candidate, and tau
 // and the count are recorded for the tile.  This costs O(1) work per value.
+// The decode kernel stages the candidates in LDS with its first guess and
+// takes the counts from the staging atomics; only a tile with a token
+// outside the window stages again.
 //
 // Stage 2 (sae_merge_kernel): one workgroup per subscribed token gathers the
 // candidates of all tiles and selects the exact top-k of that pool (key
@@ -54,15 +57,26 @@ constexpr int kBK = 64;   // K chunk
 constexpr int kEncWaves = 8;
 constexpr int kEncThreads = kEncWaves * kWave;
 constexpr int kRefineIters = 24;
+constexpr int kMaxCap = 64;  // most candidate pairs one slice may emit
 // Values above mean + kTrimZ * stdev of a tile's 256 pre-activations are left
-// out of the statistics behind the first threshold guess (one strong latent
-// would otherwise raise the guess for its whole tile); kTrimCount packs
-// their number into the count reduction.
+// out of the statistics behind the decode kernel's first threshold guess
+// (one strong latent would otherwise raise the guess for its whole tile).
 constexpr float kTrimZ = 5.0f;
-constexpr float kTrimCount = 512.0f;
 constexpr int kLatentFastTiles = 4;  // token tiles up to which the latent tile runs fastest
 constexpr int kBlkTok = 8;           // prefill block: token tiles
 constexpr int kBlkLat = 4;           // prefill block: latent tiles
+
+// v[r] for a lane-varying r in [0, 16), by a select tree on the bits of r
+// (registers cannot be indexed per lane)
+__device__ __forceinline__ float pick16(const f32x16_t& v, int r) {
+    const bool b0 = r & 1, b1 = r & 2, b2 = r & 4, b3 = r & 8;
+    const float a0 = b0 ? v[1] : v[0], a1 = b0 ? v[3] : v[2], a2 = b0 ? v[5] : v[4],
+                a3 = b0 ? v[7] : v[6], a4 = b0 ? v[9] : v[8], a5 = b0 ? v[11] : v[10],
+                a6 = b0 ? v[13] : v[12], a7 = b0 ? v[15] : v[14];
+    const float c0 = b1 ? a1 : a0, c1 = b1 ? a3 : a2, c2 = b1 ? a5 : a4, c3 = b1 ? a7 : a6;
+    const float d0 = b2 ? c1 : c0, d1 = b2 ? c3 : c2;
+    return b3 ? d1 : d0;
+}
 
 // mean + z * stdev of n values with sum s1 and sum of squares s2
 __device__ __forceinline__ float trimmed_guess(float s1, float s2, int n, float z) {
@@ -141,8 +155,12 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     __shared__ uint4 xs[2][kBN * 8];          // 2 x 16 KiB token chunks
     __shared__ float red1[kEncWaves][kBN];    // per-wave partials of the epilogue
     __shared__ float red2[kEncWaves][kBN];
-    __shared__ float red3[kEncWaves][kBN];
+    __shared__ float red3[kEncWaves][kBN];    // trim partials (not read by the statistics)
+    __shared__ float red4[kEncWaves][kBN];
     __shared__ int cnt_s[kBN];
+    __shared__ int ne_s[kBN];
+    __shared__ float tau_s[kBN];
+    __shared__ uint4 stage4[kBN * kMaxCap / 2];  // per token: up to kMaxCap pairs
 
     // Tile order.  Few token tiles (decode): latent tile fastest, so the
     // workgroups of the first token tile, the ones with live tokens, are
@@ -293,6 +311,10 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     }
     // per-token mean and variance over the tile's 256 latents (and this
     // lane's largest value, which tells whether it holds any to trim)
+    if (tid < kBN) {
+        cnt_s[tid] = 0;
+        ne_s[tid] = 0;
+    }
     float mx[4];
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
@@ -313,7 +335,6 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     }
     __syncthreads();
     float tau[4], lo_b[4], hi_b[4], sum1[4], sum2[4], cut[4];
-    bool bad[4];
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
         const int n = 32 * nb + j32;
@@ -331,80 +352,106 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
         cut[nb] = mu + kTrimZ * sd;
         lo_b[nb] = -INFINITY;  // count(lo_b) > cap
         hi_b[nb] = INFINITY;   // count(hi_b) < lo_cnt (or 0)
-        bad[nb] = false;
     }
-    // count(pre >= tau) per token; refine tau until lo_cnt <= count <= cap.
-    // The first count also sums the values above the trim cut, and a token
-    // that has any takes its guess again from the statistics without them.
-    for (int it = 0; it < kRefineIters; ++it) {
-        __syncthreads();  // red1 is reused
+    // Emission passes.  Each pass places every latent with pre >= tau in its
+    // token's LDS staging block (one LDS atomic per lane and token reserves
+    // the slots, so the atomics also count the token over all eight waves).
+    // The first pass also sums, per token, the values above the trim cut.
+    // Then every token checks its count against [lo_cnt, cap]; a token
+    // outside it, or one with values above the cut (it takes its guess
+    // again from the statistics without them), moves its tau, and the pass
+    // is repeated for the whole tile.  Usually the first guess holds and one
+    // pass is all.
+    uint2* stage = reinterpret_cast<uint2*>(stage4);
+    for (int it = 0;; ++it) {
+        if (it > 0) {
+            // every thread read the last pass's counts before the barrier
+            // that ended it
+            if (tid < kBN) cnt_s[tid] = 0;
+            __syncthreads();
+        }
 #pragma unroll
         for (int nb = 0; nb < 4; ++nb) {
-            float c = 0.0f;
+            const int n = 32 * nb + j32;
+            // bit r: acc[nb][r] >= tau; the selected values are then taken
+            // one per round by a select tree on the bits of r (no dynamic
+            // register indexing), so a lane with none does no further work
+            uint32_t m = 0;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) c += acc[nb][r] >= tau[nb] ? 1.0f : 0.0f;
+            for (int r = 0; r < 16; ++r) m |= (acc[nb][r] >= tau[nb] ? 1u : 0u) << r;
+            if (n >= ntok) m = 0;
+            if (m != 0) {
+                int slot = atomicAdd(&cnt_s[n], __popc(m));
+                uint2* dst = stage + n * cap;
+                while (m != 0) {
+                    const int r = __builtin_ctz(m);
+                    m &= m - 1;
+                    const float val = pick16(acc[nb], r);
+                    if (slot < cap)
+                        dst[slot] = make_uint2(__float_as_uint(val),
+                                               static_cast<uint32_t>(mt * kBM + 32 * wave +
+                                                                     8 * (r >> 2) + 4 * g + (r & 3)));
+                    ++slot;
+                }
+            }
             if (it == 0) {
                 float e1 = 0.0f, e2 = 0.0f;
+                int ne = 0;
                 if (mx[nb] > cut[nb]) {
 #pragma unroll
                     for (int r = 0; r < 16; ++r) {
                         const bool o = acc[nb][r] > cut[nb];
-                        c += o ? kTrimCount : 0.0f;
+                        ne += o ? 1 : 0;
                         e1 += o ? acc[nb][r] : 0.0f;
                         e2 = fmaf(o ? acc[nb][r] : 0.0f, acc[nb][r], e2);
                     }
+                    if (ne > 0) atomicAdd(&ne_s[n], ne);
                 }
                 e1 += __shfl_xor(e1, 32, kWave);
                 e2 += __shfl_xor(e2, 32, kWave);
                 if (g == 0) {
-                    red2[wave][32 * nb + j32] = e1;
-                    red3[wave][32 * nb + j32] = e2;
+                    red3[wave][n] = e1;
+                    red4[wave][n] = e2;
                 }
             }
-            c += __shfl_xor(c, 32, kWave);
-            if (g == 0) red1[wave][32 * nb + j32] = c;
+            if (wave == 0 && g == 0) tau_s[n] = tau[nb];
         }
         __syncthreads();
         bool any_bad = false;
 #pragma unroll
         for (int nb = 0; nb < 4; ++nb) {
             const int n = 32 * nb + j32;
-            float c = 0.0f;
-#pragma unroll
-            for (int w = 0; w < kEncWaves; ++w) c += red1[w][n];
-            int cn = static_cast<int>(c);
-            int ne = 0;
-            if (it == 0) {
-                ne = cn / static_cast<int>(kTrimCount);
-                cn -= ne * static_cast<int>(kTrimCount);
-            }
-            bad[nb] = false;
-            if (n < ntok) {
-                if (cn > cap) {
-                    lo_b[nb] = tau[nb];
-                    bad[nb] = true;
-                } else if (cn < lo_cnt) {
-                    hi_b[nb] = tau[nb];
-                    bad[nb] = true;
-                }
-            }
-            if (ne > 0 && n < ntok) {
+            if (n >= ntok) continue;
+            const int cn = cnt_s[n];
+            if (it == 0 && ne_s[n] > 0) {
                 float e1 = 0.0f, e2 = 0.0f;
 #pragma unroll
                 for (int w = 0; w < kEncWaves; ++w) {
-                    e1 += red2[w][n];
-                    e2 += red3[w][n];
+                    e1 += red3[w][n];
+                    e2 += red4[w][n];
                 }
-                const float t = trimmed_guess(sum1[nb] - e1, sum2[nb] - e2, kBM - ne, z_guess);
+                const float t = trimmed_guess(sum1[nb] - e1, sum2[nb] - e2, kBM - ne_s[n], z_guess);
                 if (t > lo_b[nb] && t < hi_b[nb]) {
                     tau[nb] = t;
                     any_bad = true;
                     continue;
                 }
             }
-            if (bad[nb]) {
+            bool bad = false;
+            if (cn > cap) {
+                lo_b[nb] = tau[nb];
+                bad = true;
+            } else if (cn < lo_cnt) {
+                hi_b[nb] = tau[nb];
+                bad = true;
+            }
+            if (bad) {
                 any_bad = true;
-                if (isfinite(lo_b[nb]) && isfinite(hi_b[nb])) {
+                if (it >= kRefineIters - 1) {
+                    // out of passes: a threshold whose count is known to be
+                    // <= cap (the merge then checks exactness)
+                    tau[nb] = hi_b[nb];
+                } else if (isfinite(lo_b[nb]) && isfinite(hi_b[nb])) {
                     tau[nb] = 0.5f * (lo_b[nb] + hi_b[nb]);
                 } else {
                     // step away from the bad side by a growing fraction of |tau|+1
@@ -414,45 +461,25 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
             }
         }
         if (!__syncthreads_or(any_bad)) break;
-        if (it == kRefineIters - 1) {
-            // give up on the window: fall back to a threshold whose count is
-            // known to be <= cap (the merge then checks exactness)
-#pragma unroll
-            for (int nb = 0; nb < 4; ++nb)
-                if (bad[nb]) tau[nb] = hi_b[nb];
-        }
+        if (it >= kRefineIters) break;  // the pass with tau = hi_b was the last
     }
-    // emit every latent with pre >= tau: one LDS atomic per lane and token
-    // reserves the lane's slots, then (value, latent) pairs are stored
-    __syncthreads();
-    if (tid < kBN) cnt_s[tid] = 0;
-    __syncthreads();
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb) {
-        const int n = 32 * nb + j32;
-        if (n >= ntok) continue;
-        const int64_t row = static_cast<int64_t>(n0 + n) * n_mt + mt;
-        int c = 0;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) c += acc[nb][r] >= tau[nb] ? 1 : 0;
-        if (c > 0) {
-            int slot = atomicAdd(&cnt_s[n], c);
-            uint2* dst = cand + row * cap;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                if (acc[nb][r] >= tau[nb]) {
-                    if (slot < cap)
-                        dst[slot] = make_uint2(__float_as_uint(acc[nb][r]),
-                                               static_cast<uint32_t>(mt * kBM + 32 * wave +
-                                                                     8 * (r / 4) + 4 * g + (r % 4)));
-                    ++slot;
-                }
+    // write-out: four threads per token, 16-byte stores (two pairs each), and
+    // the count and threshold beside the block
+    static_assert(kEncThreads == 4 * kBN, "four threads per token");
+    {
+        const int n = tid >> 2, part = tid & 3;
+        if (n < ntok) {
+            const int c = min(cnt_s[n], cap);
+            const int64_t row = static_cast<int64_t>(n0 + n) * n_mt + mt;
+            const uint4* src = stage4 + n * (cap / 2);
+            uint4* dst = reinterpret_cast<uint4*>(cand + row * cap);
+            for (int q = part; 2 * q < c; q += 4) dst[q] = src[q];
+            if (part == 0) {
+                tile_cnt[row] = c;
+                tile_tau[row] = tau_s[n];
             }
         }
-        if (wave == 0 && g == 0) tile_tau[row] = tau[nb];
     }
-    __syncthreads();
-    if (tid < ntok) tile_cnt[static_cast<int64_t>(n0 + tid) * n_mt + mt] = min(cnt_s[tid], cap);
 }
 
 // ------------------------------------------ prefill GEMM + candidate emission
@@ -1321,7 +1348,7 @@ static EmitPlan emit_plan(int32_t m, int32_t k) {
     e.target = (2 * k * kBM + m - 1) / m + 1;
     e.target = e.target < 2 ? 2 : (e.target > 64 ? 64 : e.target);
     e.cap = 4 * e.target;
-    e.cap = e.cap < 8 ? 8 : (e.cap > 64 ? 64 : e.cap);
+    e.cap = e.cap < 8 ? 8 : (e.cap > kMaxCap ? kMaxCap : e.cap);
     e.lo = (n_mt * e.target >= 4 * k) ? 0 : (k < e.cap ? k : e.cap);
     const double want = e.lo ? 0.5 * (e.lo + e.cap) : e.target;
     // upper-tail quantile: 0.5 * erfc(z / sqrt 2) = want / 256, by bisection
