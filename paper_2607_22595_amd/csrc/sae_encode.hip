@@ -228,10 +228,11 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     }
 
     f32x16_t acc[4];
+    // the accumulators start from the folded bias
 #pragma unroll
     for (int b = 0; b < 4; ++b)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[b][r] = 0.0f;
+        for (int r = 0; r < 16; ++r) acc[b][r] = cfv[r];
 
     uint4 wa0[4], wa1[4], wa2[4], wa3[4];   // W ring: 4 chunks, 3 in flight
     uint4 xv0[2], xv1[2];                   // token ring: 2 chunks in flight
@@ -304,11 +305,6 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     // acc[nb][r] holds latent 32*wave + 8*(r/4) + 4*g + r%4 of token
     // 32*nb + j32 (the 32x32 MFMA output layout).  Lanes j32 and j32 + 32 of
     // all eight waves together hold the 256 latents of one token.
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-#pragma unroll
-        for (int nb = 0; nb < 4; ++nb) acc[nb][r] += cfv[r];
-    }
     // per-token mean and variance over the tile's 256 latents (and this
     // lane's largest value, which tells whether it holds any to trim)
     if (tid < kBN) {
