@@ -259,6 +259,21 @@ def test_encode_all_tokens_many_token_tiles(px):
     _check_encode(wl, sae, wl.layers[0].h, idx, val, np.arange(300))
 
 
+def test_encode_decode_kernel_blocked_tile_order(px):
+    """Between 513 and 1024 token slots the decode kernel walks its tiles in
+    XCD blocks of 8 token tiles x 4 latent tiles (more than 4 token tiles);
+    900 slots with 777 subscribed leave a ragged last token tile."""
+    wl = synth.make("c3", d=256, m=2048, k=16, T=900, n_sub=777)
+    sae = wl.layers[0].saes[0]
+    rt, idx, val = _encode(px, wl, sae, wl.layers[0].h)
+    tm, cnt, lists, _ = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    toks = lists[0, :cnt[0]]
+    assert len(toks) == 777
+    _check_encode(wl, sae, wl.layers[0].h, idx, val, toks)
+    off = np.setdiff1d(np.arange(900), toks)
+    assert np.all(idx[off] == -7)
+
+
 @pytest.mark.parametrize("d,m,k,T,n_sub", [(256, 1024, 16, 1500, 1100), (512, 2048, 32, 2100, 2100),
                                            (256, 2560, 64, 1025, 700)])
 def test_encode_prefill_gemm_path(px, d, m, k, T, n_sub):
