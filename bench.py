@@ -83,23 +83,55 @@ def measured_traffic(workload):
     return float(v) if v else None
 
 
-class Rotation:
-    """Graphs of one callable, one per dictionary copy, replayed in turn."""
+STEPS_PER_GRAPH = 4
 
-    def __init__(self, torch, fn, copies, set_copy):
-        self.graphs = []
-        for c in copies:
-            set_copy(c)
+
+class MultiStep:
+    """One graph of `per_graph` consecutive steps (as consecutive hooked
+    layers sit in one forward-pass graph), dictionary copies rotating from
+    step to step, plus a graph of `rest` steps for a count that is not a
+    multiple of it."""
+
+    def __init__(self, torch, fn, copies, set_copy, per_graph, rest):
+        def capture(n):
             torch.cuda.synchronize()
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g):
-                fn()
-            self.graphs.append(g)
-        self.i = 0
+                for i in range(n):
+                    set_copy(copies[i % len(copies)])
+                    fn()
+            return g
+        self.per_graph = per_graph
+        self.full = capture(per_graph)
+        self.rest = capture(rest) if rest else None
+        set_copy(copies[0])
 
-    def replay(self):
-        self.graphs[self.i].replay()
-        self.i = (self.i + 1) % len(self.graphs)
+
+def time_step_runs(torch, ms, n_steps, runs=7):
+    """Exactly n_steps steps: n_steps // per_graph replays of the full graph
+    and one of the rest graph, in `runs` consecutive runs with one HIP event
+    between runs on the current stream (the stream the kernels run on).
+    Returns the average ms per step and the per-run averages and sizes."""
+    n_full = n_steps // ms.per_graph
+    runs = max(1, min(runs, n_full)) if n_full else 1
+    sizes = [n_full // runs + (1 if i < n_full % runs else 0) for i in range(runs)]
+    s = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(runs + 1)]
+    torch.cuda.synchronize()
+    ev[0].record(s)
+    steps = []
+    for i, k in enumerate(sizes):
+        for _ in range(k):
+            ms.full.replay()
+        n = k * ms.per_graph
+        if i == runs - 1 and ms.rest is not None:
+            ms.rest.replay()
+            n += n_steps - n_full * ms.per_graph
+        steps.append(n)
+        ev[i + 1].record(s)
+    ev[-1].synchronize()
+    per_run = [ev[i].elapsed_time(ev[i + 1]) / steps[i] for i in range(runs)]
+    return ev[0].elapsed_time(ev[-1]) / n_steps, per_run, steps
 
 
 def time_replays(torch, rot, n):
@@ -117,26 +149,6 @@ def time_replays(torch, rot, n):
     return e0.elapsed_time(e1) / n
 
 
-def time_replay_runs(torch, rot, n, runs=7):
-    """n replays of `rot` in `runs` consecutive runs, one HIP event between
-    runs on the current stream (the stream the kernels run on).  Returns the
-    average ms per replay over all n and the per-run averages."""
-    runs = max(1, min(runs, n))
-    sizes = [n // runs + (1 if i < n % runs else 0) for i in range(runs)]
-    s = torch.cuda.current_stream()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(runs + 1)]
-    torch.cuda.synchronize()
-    ev[0].record(s)
-    for i, k in enumerate(sizes):
-        for _ in range(k):
-            rot.replay()
-        ev[i + 1].record(s)
-    ev[-1].synchronize()
-    per_run = [ev[i].elapsed_time(ev[i + 1]) / sizes[i] for i in range(runs)]
-    total = ev[0].elapsed_time(ev[-1])
-    return total / n, per_run, sizes
-
-
 def run_stats(per_run, sizes, tokens_per_step, seed=0):
     """Median and p10/p90 of the per-run latency; the throughput over all
     runs (total tokens / total time, the harmonic mean of the per-run
@@ -151,14 +163,15 @@ def run_stats(per_run, sizes, tokens_per_step, seed=0):
         i = rng.integers(0, len(ms), len(ms))
         boot.append(tokens_per_step * w[i].sum() / (ms[i] * w[i]).sum() * 1e3)
     lo, hi = np.percentile(boot, [2.5, 97.5])
-    return {"runs": len(ms), "replays_per_run": [int(x) for x in sizes],
+    return {"runs": len(ms), "steps_per_run": [int(x) for x in sizes],
+            "steps_per_graph": STEPS_PER_GRAPH,
             "ms_median": float(np.median(ms)), "ms_p10": float(np.percentile(ms, 10)),
             "ms_p90": float(np.percentile(ms, 90)), "tokens_per_s": float(thr),
             "tokens_per_s_ci95": [float(lo), float(hi)]}
 
 
 def dictionary_copies(torch, W, min_bytes=1.5 * 2 ** 30):
-    n = max(2, int(np.ceil(min_bytes / (W.numel() * W.element_size()))))
+    n = max(STEPS_PER_GRAPH, int(np.ceil(min_bytes / (W.numel() * W.element_size()))))
     return [W] + [W.clone() for _ in range(n - 1)]
 
 
@@ -174,11 +187,11 @@ def bench_workload(torch, px, step, sae_layer, sae_idx, steps, warmup, encode=Tr
     step.reset()
     step.run()   # eager run once (also checks the arguments)
     torch.cuda.synchronize()
-    full = Rotation(torch, step.run, copies, set_copy)
-    for _ in range(warmup):
-        full.replay()
+    multi = MultiStep(torch, step.run, copies, set_copy, STEPS_PER_GRAPH, steps % STEPS_PER_GRAPH)
+    for _ in range(max(1, warmup // STEPS_PER_GRAPH)):
+        multi.full.replay()
     torch.cuda.synchronize()
-    ms_step, per_run, sizes = time_replay_runs(torch, full, steps)
+    ms_step, per_run, sizes = time_step_runs(torch, multi, steps)
     stats = run_stats(per_run, sizes, step.wl.T_valid)
     ms_enc = encode_in_step(torch, step, copies, set_copy, steps) if encode else None
     set_copy(copies[0])
