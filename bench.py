@@ -218,6 +218,48 @@ def encode_in_step(torch, step, copies, set_copy, n):
     return sum(a.elapsed_time(b) for a, b in pairs) / n
 
 
+def read_ceiling(torch, nbytes, n_bufs=4, runs=7, per_run=20):
+    """The device's measured HBM read ceiling: a plain stream of nontemporal
+    16-byte loads (libxmix_ceiling) over `n_bufs` rotating buffers of the
+    dictionary's size, back-to-back launches; median GB/s over the runs."""
+    from paper_2607_22595_amd import ceiling
+    bufs = [torch.empty(nbytes, dtype=torch.uint8, device="cuda") for _ in range(n_bufs)]
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for i in range(2 * n_bufs):
+        ceiling.read(bufs[i % n_bufs], sink)
+    rates = []
+    for _ in range(runs):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(per_run):
+            ceiling.read(bufs[i % n_bufs], sink)
+        e1.record()
+        e1.synchronize()
+        rates.append(nbytes * per_run / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    del bufs
+    torch.cuda.empty_cache()
+    return float(np.median(rates))
+
+
+def mfma_ceiling(torch, iters=4000, runs=7, per_run=3):
+    """The device's measured bf16 MFMA ceiling (libxmix_ceiling): register
+    operands only, one workgroup of four waves per CU; median TFLOP/s."""
+    from paper_2607_22595_amd import ceiling
+    sink = torch.zeros(1, dtype=torch.float32, device="cuda")
+    flops = ceiling.mfma(iters, sink)
+    torch.cuda.synchronize()
+    rates = []
+    for _ in range(runs):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(per_run):
+            ceiling.mfma(iters, sink)
+        e1.record()
+        e1.synchronize()
+        rates.append(flops * per_run / (e0.elapsed_time(e1) * 1e-3) / 1e12)
+    return float(np.median(rates))
+
+
 def cpu_baseline_decode(wl, budget_s):
     """The oracle on this host's cores: one full decode SAE step is routing,
     the encode of every subscribed token and the ring compaction; the encode
@@ -319,6 +361,12 @@ def run_decode(torch, px, synth, HookStep, args):
                      "timing": "HIP events around the encode stage inside back-to-back steps"},
     }
     out["step_stats"] = stats
+    log("measuring the HBM read ceiling")
+    ceil = read_ceiling(torch, s.m * wl.d * 2)
+    out["roofline"].update({
+        "achievable_peak": ceil, "achievable_frac": achieved / ceil,
+        "achievable_how": "nontemporal 16-byte read stream over 4 rotating buffers of the "
+                          "dictionary's size, back-to-back launches (libxmix_ceiling)"})
     # "don't use, don't pay": the same captured step with no subscriber
     sub_saved = step.sub.clone()
     step.sub.zero_()
@@ -584,6 +632,12 @@ def run_prefill(torch, px, synth, HookStep, args):
         "step_stats": stats4}
     del step4
     torch.cuda.empty_cache()
+    log("measuring the MFMA ceiling")
+    ceil = mfma_ceiling(torch)
+    res["roofline"].update({
+        "achievable_peak": ceil, "achievable_frac": tf / ceil,
+        "achievable_how": "32x32x16 bf16 MFMAs with register operands, 8 chains per wave, "
+                          "4 waves per CU (libxmix_ceiling)"})
     return res
 
 

@@ -1,8 +1,10 @@
 """Build libxmix.so (HIP for gfx950) in-tree.
 
 Each source under csrc/ is compiled by hipcc into _build/, then linked into
-paper_2607_22595_amd/libxmix.so.  Packed-fp32 instruction selection is
-switched off for device code."""
+paper_2607_22595_amd/libxmix.so.  The measured-ceiling kernels under
+ceiling/ (a benchmark aid, no part of the hook step) become
+libxmix_ceiling.so.  Packed-fp32 instruction selection is switched off for
+device code."""
 import concurrent.futures as cf
 import glob
 import os
@@ -29,20 +31,28 @@ def _compile(src: str, obj: str, extra) -> None:
         sys.stderr.write("\n".join(noise) + "\n")
 
 
-def build(extra=(), jobs: int = 8) -> str:
-    out_dir = os.path.join(ROOT, "_build")
-    os.makedirs(out_dir, exist_ok=True)
-    srcs = sorted(glob.glob(os.path.join(HERE, "csrc", "*.hip")))
-    objs = [os.path.join(out_dir, os.path.basename(s) + ".o") for s in srcs]
-    with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
-        list(ex.map(lambda so: _compile(so[0], so[1], list(extra)), zip(srcs, objs)))
-    lib = os.path.join(HERE, "libxmix.so")
+def _link(objs, lib: str) -> None:
     tmp = lib + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
     os.replace(tmp, lib)
+
+
+def build(extra=(), jobs: int = 8) -> str:
+    out_dir = os.path.join(ROOT, "_build")
+    os.makedirs(out_dir, exist_ok=True)
+    srcs = sorted(glob.glob(os.path.join(HERE, "csrc", "*.hip")))
+    objs = [os.path.join(out_dir, os.path.basename(s) + ".o") for s in srcs]
+    ceil_src = os.path.join(HERE, "ceiling", "ceiling.hip")
+    ceil_obj = os.path.join(out_dir, "ceiling.hip.o")
+    pairs = list(zip(srcs, objs)) + [(ceil_src, ceil_obj)]
+    with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
+        list(ex.map(lambda so: _compile(so[0], so[1], list(extra)), pairs))
+    lib = os.path.join(HERE, "libxmix.so")
+    _link(objs, lib)
+    _link([ceil_obj], os.path.join(HERE, "libxmix_ceiling.so"))
     return lib
 
 

@@ -103,3 +103,26 @@ def test_encode_rejects_unsupported_shapes_on_the_host(lib):
     assert call(app_bit=1) == 1        # bit outside the route's apps
     assert call(m=262144, k=64) == 2   # too many merge candidates per token
     assert call(ws_bytes=1024) == 3    # workspace too small
+
+
+CEIL_HEADER = os.path.join(ROOT, "include", "xmix_ceiling.h")
+CEIL_LIB = os.path.join(ROOT, "paper_2607_22595_amd", "libxmix_ceiling.so")
+
+
+def test_ceiling_library_exports_its_header():
+    """The measured-ceiling aid (a benchmark tool beside the hook step)."""
+    if not os.path.exists(CEIL_LIB):
+        import __graft_entry__
+        __graft_entry__.build()
+    text = re.sub(r"/\*.*?\*/", "", open(CEIL_HEADER).read(), flags=re.S)
+    declared = sorted(set(re.findall(r"\b(xmix_[a-z_0-9]+)\s*\(", text)))
+    assert declared == ["xmix_ceiling_mfma", "xmix_ceiling_read"]
+    out = subprocess.run(["nm", "-D", "--defined-only", CEIL_LIB], capture_output=True,
+                         text=True, check=True).stdout
+    assert sorted(set(re.findall(r"\bT\s+(xmix_\w+)", out))) == declared
+    lib = ctypes.CDLL(CEIL_LIB)
+    lib.xmix_ceiling_read.restype = ctypes.c_int
+    lib.xmix_ceiling_mfma.restype = ctypes.c_int
+    # invalid arguments are rejected before any device call
+    assert lib.xmix_ceiling_read(None, ctypes.c_uint64(16), None, None) == 1
+    assert lib.xmix_ceiling_mfma(0, None, None, None) == 1
