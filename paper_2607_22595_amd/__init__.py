@@ -13,6 +13,7 @@ point to.
 from __future__ import annotations
 
 import ctypes
+import gc
 import os
 from typing import Optional, Sequence
 
@@ -239,12 +240,22 @@ class Graph:
             raise ValueError("capture needs a torch.cuda.Stream (not the null stream)")
         self.stream = stream
         self._h = ctypes.c_void_p()
-        _check("xmix_graph_begin", _lib.xmix_graph_begin(_stream(stream)))
+        # An object collected during the capture (a torch CUDA graph, say)
+        # could make a HIP call that is not allowed while the stream
+        # captures: collect first and keep the collector off until the end.
+        gc_was_on = gc.isenabled()
+        gc.collect()
+        gc.disable()
         try:
-            record()
+            _check("xmix_graph_begin", _lib.xmix_graph_begin(_stream(stream)))
+            try:
+                record()
+            finally:
+                st = _lib.xmix_graph_end(_stream(stream), ctypes.byref(self._h))
+            _check("xmix_graph_end", st)
         finally:
-            st = _lib.xmix_graph_end(_stream(stream), ctypes.byref(self._h))
-        _check("xmix_graph_end", st)
+            if gc_was_on:
+                gc.enable()
 
     @property
     def kernel_nodes(self) -> int:
