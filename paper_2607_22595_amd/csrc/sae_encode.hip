@@ -1077,14 +1077,29 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
     __shared__ int fail_s[kMaxRepair];
     const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
     const int n = blockIdx.x;
+    const int64_t row0 = static_cast<int64_t>(n) * n_mt;
+    // The first round of the gather below does not depend on the token
+    // count: its loads go out before the count is read (the slot's area
+    // exists for every slot below T_max; a slot past the count leaves
+    // without using them).
+    const int last = cap / 2 - 1;
+    uint4 v0[4];
+    int c0 = 0;
+    float tf0 = 0.0f;
+    {
+        const bool own = tid < n_mt;
+        const int64_t row = row0 + (own ? tid : 0);
+        const uint4* src = reinterpret_cast<const uint4*>(cand + row * cap);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v0[u] = src[min(u, last)];
+        if (own) {
+            c0 = tile_cnt[row];
+            tf0 = tile_tau[row];
+        }
+    }
+    const int32_t t = tok_list[n];
     const int cnt = *app_count;
     if (n >= cnt) return;  // uniform: no token, no ring row, no ticket
-    // readback ring (optional): each workgroup with a token reads the head
-    // before it takes a ticket; the one drawing the last ticket advances it
-    uint64_t h0 = 0;
-    if (ring.slots && tid == 0) h0 = __atomic_load_n(&ring.head[0], __ATOMIC_RELAXED);
-    const int32_t t = tok_list[n];
-    const int64_t row0 = static_cast<int64_t>(n) * n_mt;
 
     int total = 0;
     uint32_t tau_tiles = 0;
@@ -1095,12 +1110,20 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
         // count, threshold and the first 8 pairs of the slice, in one round
         // (a slice holds about 2-3 candidates; more are fetched below)
         const uint4* src = reinterpret_cast<const uint4*>(cand + row * cap);
-        const int last = cap / 2 - 1;
         uint4 v[4];
+        int c;
+        uint32_t tk;
+        if (t0 == 0) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u) v[u] = src[min(u, last)];
-        const int c = own ? tile_cnt[row] : 0;
-        const uint32_t tk = own ? f32_key(tile_tau[row]) : 0u;
+            for (int u = 0; u < 4; ++u) v[u] = v0[u];
+            c = c0;
+            tk = own ? f32_key(tf0) : 0u;
+        } else {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) v[u] = src[min(u, last)];
+            c = own ? tile_cnt[row] : 0;
+            tk = own ? f32_key(tile_tau[row]) : 0u;
+        }
         // workgroup prefix of the counts
         int incl = c;
 #pragma unroll
@@ -1158,6 +1181,13 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
         }
     }
     __syncthreads();
+    // readback ring (optional): each workgroup with a token reads the head
+    // before it takes a ticket; the one drawing the last ticket advances it
+    // (read here, after the gather's loads, so that no wait for those waits
+    // for this one)
+    uint64_t h0 = 0;
+    if (ring.slots && tid == 0)
+        h0 = __hip_atomic_load(&ring.head[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     // Selection.  A large pool is cut into quarters: each wave keeps the k
     // best of its quarter, and wave 0 selects from those (an entry of the
     // pool's top k, in the order key descending, latent ascending, is in its
