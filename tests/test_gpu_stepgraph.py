@@ -138,3 +138,28 @@ def test_redirect_subscriptions_and_unknown_buffer(captured):
     assert g.redirect(sub1, sub0) == 1
     other = torch.zeros(16, dtype=torch.float32, device="cuda")
     assert g.redirect(other, torch.zeros_like(other)) == 0
+
+
+def test_capture_after_dropping_a_torch_graph_in_a_cycle(captured):
+    """A torch CUDA graph left in a reference cycle is collected before the
+    library's capture starts, not during it (collected during the capture,
+    its teardown would make a HIP call that capture forbids)."""
+    import gc
+    import paper_2607_22595_amd as px
+    wl, step, _ = captured
+    x = torch.zeros(1024, device="cuda")
+    tg = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(tg):
+        x.add_(1.0)
+    holder = {"graph": tg}
+    holder["self"] = holder  # a cycle: only the collector frees it
+    del tg, holder
+    stream = torch.cuda.Stream()
+    g = px.Graph(lambda: step.run(stream), stream)
+    try:
+        assert gc.isenabled()
+        ref = _eager(step)
+        assert all(np.array_equal(a, b) for a, b in zip(_replay(step, g), ref))
+    finally:
+        torch.cuda.synchronize()
+        g.close()
