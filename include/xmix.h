@@ -183,6 +183,30 @@ xmix_status xmix_steer_apply(void *h, xmix_dtype dt, int32_t d, const xmix_route
                              const int32_t *app_bits, const float *alpha,
                              int32_t n_steer, int32_t R_max, void *stream);
 
+/* ------------------------------------------------- probes + steering, fused
+ * Reads and writes composed at one hook (Sec. 4.2: several apps on the same
+ * layer; reads see the activation as the model produced it, then writes
+ * apply): token-mode probes and the steering add in one pass over each row.
+ * The result is bit-identical to
+ *   xmix_probe_score(h, ..., probe_bits, n_probe, XMIX_PROBE_TOKEN, ...)
+ * followed by
+ *   xmix_steer_apply(h, ..., steer_bits, alpha, n_steer, R_max, ...)
+ * (same arithmetic in the same order): the probes read each row before the
+ * steering rewrites it, and each row is read from HBM once instead of twice.
+ * Arguments are those of the two calls: h [T_max, d] of dtype `dt`, updated
+ * in place; vecs [n_steer, d] and w [n_probe, d] of dtype `dt`; alpha
+ * [R_max][n_steer] fp32; b [n_probe] fp32; logit_out and score_out
+ * [n_probe][T_max] fp32, written only for tokens with the probe's bit.
+ * steer_bits and probe_bits are host arrays.
+ * Requires 1 <= n_steer <= 32, 1 <= n_probe <= 32, d % 8 == 0 (bf16) or
+ * d % 4 == 0 (fp32).  Errors: XMIX_E_INVAL as for the two calls. */
+xmix_status xmix_steer_probe(void *h, xmix_dtype dt, int32_t d, const xmix_route *rt,
+                             const int32_t *req_of_token, const void *vecs,
+                             const int32_t *steer_bits, const float *alpha, int32_t n_steer,
+                             int32_t R_max, const void *w, const float *b,
+                             const int32_t *probe_bits, int32_t n_probe, float *logit_out,
+                             float *score_out, void *stream);
+
 /* ------------------------------------------------------ router-logit write
  * Expert (de)activation on a mixture-of-experts router, a write whose locus
  * is the router logits (Table 1, App-7).  For each token t with at least one

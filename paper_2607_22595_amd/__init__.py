@@ -66,6 +66,8 @@ _sigs = {
                           _st),
     "xmix_steer_apply": ([_vp, _st, _i32, ctypes.POINTER(XmixRoute), _vp, _vp, _vp, _vp, _i32,
                           _i32, _vp], _st),
+    "xmix_steer_probe": ([_vp, _st, _i32, ctypes.POINTER(XmixRoute), _vp, _vp, _vp, _vp, _i32,
+                          _i32, _vp, _vp, _vp, _i32, _vp, _vp, _vp], _st),
     "xmix_probe_workspace": ([_i32, _i32, _i32], _sz),
     "xmix_probe_score": ([_vp, _st, _i32, ctypes.POINTER(XmixRoute), _vp, _vp, _vp, _i32, _i32,
                           _vp, _i32, _vp, _vp, _vp, _sz, _vp], _st),
@@ -211,6 +213,24 @@ def xmix_steer_apply(h, route: Route, req_of_token, vecs, app_bits: Sequence[int
     _check("xmix_steer_apply", _lib.xmix_steer_apply(
         _ptr(h), _dt(h), d, ctypes.byref(route.struct), _ptr(req_of_token), _ptr(vecs), bits,
         _ptr(alpha), n, alpha.shape[0], _stream(stream)))
+
+
+def xmix_steer_probe(h, route: Route, req_of_token, vecs, steer_bits: Sequence[int], alpha,
+                     w, b, probe_bits: Sequence[int], logit_out, score_out, stream=None):
+    """Token-mode probes and the steering add in one pass: the same results
+    as xmix_probe_score(mode TOKEN) followed by xmix_steer_apply."""
+    T_max, d = h.shape
+    assert T_max == route.T_max and vecs.dtype == h.dtype and vecs.shape[-1] == d
+    ns, npb = len(steer_bits), len(probe_bits)
+    assert alpha.dtype == torch.float32 and alpha.dim() == 2 and alpha.shape[1] == ns
+    assert w.dtype == h.dtype and w.shape == (npb, d) and b.dtype == torch.float32
+    assert logit_out.shape == (npb, T_max) and score_out.shape == (npb, T_max)
+    sb = (ctypes.c_int32 * ns)(*steer_bits)
+    pb = (ctypes.c_int32 * npb)(*probe_bits)
+    _check("xmix_steer_probe", _lib.xmix_steer_probe(
+        _ptr(h), _dt(h), d, ctypes.byref(route.struct), _ptr(req_of_token), _ptr(vecs), sb,
+        _ptr(alpha), ns, alpha.shape[0], _ptr(w), _ptr(b), pb, npb, _ptr(logit_out),
+        _ptr(score_out), _stream(stream)))
 
 
 def xmix_router_write(logits, route: Route, app_bits: Sequence[int], offsets, stream=None):

@@ -101,6 +101,26 @@ xmix_status xmix_steer_apply(void* h, xmix_dtype dt, int32_t d, const xmix_route
                                  vecs, bits, alpha, n_steer, as_stream(stream)));
 }
 
+xmix_status xmix_steer_probe(void* h, xmix_dtype dt, int32_t d, const xmix_route* rt,
+                             const int32_t* req_of_token, const void* vecs,
+                             const int32_t* steer_bits, const float* alpha, int32_t n_steer,
+                             int32_t R_max, const void* w, const float* b,
+                             const int32_t* probe_bits, int32_t n_probe, float* logit_out,
+                             float* score_out, void* stream) {
+    if (!h || !req_of_token || !vecs || !alpha || !w || !b || !logit_out || !score_out ||
+        !route_ok(rt) || R_max < 1 || d < 1)
+        return XMIX_E_INVAL;
+    if (dt != XMIX_BF16 && dt != XMIX_F32) return XMIX_E_INVAL;
+    if (d % (dt == XMIX_BF16 ? 8 : 4) != 0 || !aligned16(h) || !aligned16(vecs) || !aligned16(w))
+        return XMIX_E_INVAL;
+    BitList sbits, pbits;
+    if (!bits_ok(steer_bits, n_steer, rt->n_apps, &sbits)) return XMIX_E_INVAL;
+    if (!bits_ok(probe_bits, n_probe, rt->n_apps, &pbits)) return XMIX_E_INVAL;
+    return launched(launch_steer_probe(h, dt == XMIX_BF16, d, rt->T_max, rt->tok_mask,
+                                       req_of_token, vecs, sbits, alpha, n_steer, w, b, pbits,
+                                       n_probe, logit_out, score_out, as_stream(stream)));
+}
+
 xmix_status xmix_router_write(void* logits, xmix_dtype dt, int32_t n_experts,
                               const xmix_route* rt, const int32_t* app_bits,
                               const float* offsets, int32_t n_router, void* stream) {

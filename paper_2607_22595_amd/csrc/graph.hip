@@ -44,6 +44,7 @@ const std::vector<KernelInfo>& kernel_table() {
         std::vector<KernelInfo> t;
         add_route_kernels(t);
         add_steer_kernels(t);
+        add_steer_probe_kernels(t);
         add_probe_kernels(t);
         add_router_kernels(t);
         add_sae_kernels(t);

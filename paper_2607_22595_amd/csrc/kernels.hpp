@@ -29,6 +29,7 @@ KernelInfo kernel_info(void (*f)(A...)) {
 // One per kernel source: appends the kernels that file launches.
 void add_route_kernels(std::vector<KernelInfo>& t);
 void add_steer_kernels(std::vector<KernelInfo>& t);
+void add_steer_probe_kernels(std::vector<KernelInfo>& t);
 void add_probe_kernels(std::vector<KernelInfo>& t);
 void add_router_kernels(std::vector<KernelInfo>& t);
 void add_sae_kernels(std::vector<KernelInfo>& t);

@@ -1,0 +1,185 @@
+// Per-token probes and the steering add in one pass over each row: a hook
+// where apps read and write (probes and steering vectors composed at one
+// layer).  The row is read once in 16-byte slices; the probes take their
+// dot products from the values as read (the activation as the model
+// produced it), the steering sum is added in fp64 and the row written back
+// rounded once.  The arithmetic and its order are those of the separate
+// probe and steering kernels (same slicing, same per-thread accumulation,
+// same reductions), so the results are bit-identical to a token-mode probe
+// call followed by a steering call.  One workgroup per token slot; a row
+// with neither kind of bit returns after reading its mask word.
+#include "common.hpp"
+#include "kernels.hpp"
+#include "launch.hpp"
+
+namespace xmix {
+
+constexpr int kFuseThreads = 256;
+constexpr int kFuseWaves = kFuseThreads / kWave;
+
+template <bool BF16, int MAXP>
+__global__ void __launch_bounds__(kFuseThreads)
+steer_probe_kernel(void* __restrict__ h, int32_t d, int32_t T_max,
+                   const uint32_t* __restrict__ tok_mask, const int32_t* __restrict__ req,
+                   const void* __restrict__ vecs, BitList sbits, const float* __restrict__ alpha,
+                   int32_t n_steer, const void* __restrict__ w, const float* __restrict__ b,
+                   BitList pbits, int32_t n_probe, float* __restrict__ logit,
+                   float* __restrict__ score) {
+    __shared__ float red[kFuseWaves][MAXP];
+    const int32_t t = blockIdx.x;
+    const uint32_t mask = tok_mask[t];
+    uint32_t ss = 0, sp = 0;
+    for (int s = 0; s < n_steer; ++s) ss |= ((mask >> sbits.bit[s]) & 1u) << s;
+    for (int p = 0; p < n_probe; ++p) sp |= ((mask >> pbits.bit[p]) & 1u) << p;
+    if ((ss | sp) == 0) return;
+    const float* a_row = ss ? alpha + static_cast<int64_t>(req[t]) * n_steer : alpha;
+
+    constexpr int EPV = BF16 ? 8 : 4;  // elements per 16-byte vector
+    const int32_t nvec = d / EPV;
+    uint4* row = reinterpret_cast<uint4*>(h) + static_cast<int64_t>(t) * nvec;
+    const uint4* V = reinterpret_cast<const uint4*>(vecs);
+    const uint4* W = reinterpret_cast<const uint4*>(w);
+    float part[MAXP];
+#pragma unroll
+    for (int p = 0; p < MAXP; ++p) part[p] = 0.0f;
+
+    for (int32_t i = threadIdx.x; i < nvec; i += kFuseThreads) {
+        const uint4 hv = row[i];
+        const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w};
+        // probes, on the row as read
+        float x[EPV];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            if constexpr (BF16) {
+                x[2 * e] = lo_bf16(hw[e]);
+                x[2 * e + 1] = hi_bf16(hw[e]);
+            } else {
+                x[e] = __uint_as_float(hw[e]);
+            }
+        }
+#pragma unroll
+        for (int p = 0; p < MAXP; ++p) {
+            if (!((sp >> p) & 1u)) continue;
+            const uint4 wv = W[static_cast<int64_t>(p) * nvec + i];
+            const uint32_t ww[4] = {wv.x, wv.y, wv.z, wv.w};
+            float acc = part[p];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if constexpr (BF16) {
+                    acc = fmaf(lo_bf16(ww[e]), x[2 * e], acc);
+                    acc = fmaf(hi_bf16(ww[e]), x[2 * e + 1], acc);
+                } else {
+                    acc = fmaf(__uint_as_float(ww[e]), x[e], acc);
+                }
+            }
+            part[p] = acc;
+        }
+        // steering, written back
+        if (ss) {
+            double acc[EPV];
+#pragma unroll
+            for (int e = 0; e < EPV; ++e) acc[e] = x[e];
+            for (uint32_t rest = ss; rest; rest &= rest - 1) {
+                const int s = __builtin_ctz(rest);
+                const double a = a_row[s];
+                const uint4 vv = V[static_cast<int64_t>(s) * nvec + i];
+                const uint32_t vw[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    if constexpr (BF16) {
+                        acc[2 * e] = fma(a, static_cast<double>(lo_bf16(vw[e])), acc[2 * e]);
+                        acc[2 * e + 1] =
+                            fma(a, static_cast<double>(hi_bf16(vw[e])), acc[2 * e + 1]);
+                    } else {
+                        acc[e] = fma(a, static_cast<double>(__uint_as_float(vw[e])), acc[e]);
+                    }
+                }
+            }
+            uint4 out;
+            if constexpr (BF16) {
+                out.x = pack_bf16_from_f64(acc[0], acc[1]);
+                out.y = pack_bf16_from_f64(acc[2], acc[3]);
+                out.z = pack_bf16_from_f64(acc[4], acc[5]);
+                out.w = pack_bf16_from_f64(acc[6], acc[7]);
+            } else {
+                out.x = __float_as_uint(static_cast<float>(acc[0]));
+                out.y = __float_as_uint(static_cast<float>(acc[1]));
+                out.z = __float_as_uint(static_cast<float>(acc[2]));
+                out.w = __float_as_uint(static_cast<float>(acc[3]));
+            }
+            row[i] = out;
+        }
+    }
+    if (sp == 0) return;  // uniform over the block
+
+    const int wave = threadIdx.x / kWave;
+#pragma unroll
+    for (int p = 0; p < MAXP; ++p) {
+        if (!((sp >> p) & 1u)) continue;
+        const float s = wave_sum(part[p]);
+        if (lane_id() == 0) red[wave][p] = s;
+    }
+    __syncthreads();
+    const int p = threadIdx.x;
+    if (p < n_probe && ((sp >> p) & 1u)) {
+        float dot = 0.0f;
+#pragma unroll
+        for (int wv = 0; wv < kFuseWaves; ++wv) dot += red[wv][p];
+        const int64_t o = static_cast<int64_t>(p) * T_max + t;
+        const float l = b[p] + dot;
+        logit[o] = l;
+        score[o] = logistic(l);
+    }
+}
+
+template <bool BF16>
+static hipError_t launch_steer_probe_t(void* h, int32_t d, int32_t T_max,
+                                       const uint32_t* tok_mask, const int32_t* req,
+                                       const void* vecs, const BitList& sbits,
+                                       const float* alpha, int32_t n_steer, const void* w,
+                                       const float* b, const BitList& pbits, int32_t n_probe,
+                                       float* logit, float* score, hipStream_t stream) {
+    dim3 g(T_max), blk(kFuseThreads);
+    if (n_probe <= 4)
+        hipLaunchKernelGGL((steer_probe_kernel<BF16, 4>), g, blk, 0, stream, h, d, T_max,
+                           tok_mask, req, vecs, sbits, alpha, n_steer, w, b, pbits, n_probe,
+                           logit, score);
+    else if (n_probe <= 8)
+        hipLaunchKernelGGL((steer_probe_kernel<BF16, 8>), g, blk, 0, stream, h, d, T_max,
+                           tok_mask, req, vecs, sbits, alpha, n_steer, w, b, pbits, n_probe,
+                           logit, score);
+    else if (n_probe <= 16)
+        hipLaunchKernelGGL((steer_probe_kernel<BF16, 16>), g, blk, 0, stream, h, d, T_max,
+                           tok_mask, req, vecs, sbits, alpha, n_steer, w, b, pbits, n_probe,
+                           logit, score);
+    else
+        hipLaunchKernelGGL((steer_probe_kernel<BF16, 32>), g, blk, 0, stream, h, d, T_max,
+                           tok_mask, req, vecs, sbits, alpha, n_steer, w, b, pbits, n_probe,
+                           logit, score);
+    return hipGetLastError();
+}
+
+hipError_t launch_steer_probe(void* h, bool bf16, int32_t d, int32_t T_max,
+                              const uint32_t* tok_mask, const int32_t* req, const void* vecs,
+                              const BitList& sbits, const float* alpha, int32_t n_steer,
+                              const void* w, const float* b, const BitList& pbits,
+                              int32_t n_probe, float* logit, float* score, hipStream_t stream) {
+    return bf16 ? launch_steer_probe_t<true>(h, d, T_max, tok_mask, req, vecs, sbits, alpha,
+                                             n_steer, w, b, pbits, n_probe, logit, score, stream)
+                : launch_steer_probe_t<false>(h, d, T_max, tok_mask, req, vecs, sbits, alpha,
+                                              n_steer, w, b, pbits, n_probe, logit, score,
+                                              stream);
+}
+
+void add_steer_probe_kernels(std::vector<KernelInfo>& t) {
+    t.push_back(kernel_info(steer_probe_kernel<true, 4>));
+    t.push_back(kernel_info(steer_probe_kernel<true, 8>));
+    t.push_back(kernel_info(steer_probe_kernel<true, 16>));
+    t.push_back(kernel_info(steer_probe_kernel<true, 32>));
+    t.push_back(kernel_info(steer_probe_kernel<false, 4>));
+    t.push_back(kernel_info(steer_probe_kernel<false, 8>));
+    t.push_back(kernel_info(steer_probe_kernel<false, 16>));
+    t.push_back(kernel_info(steer_probe_kernel<false, 32>));
+}
+
+}  // namespace xmix

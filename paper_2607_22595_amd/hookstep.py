@@ -10,6 +10,9 @@ order for every layer:
   2. reads of the activation as the model produced it: per-token probes,
      mean-pooled probes, SAE encodes;
   3. writes: steering, then each SAE app's clamp-decode;
+     (by default a layer's per-token probes run fused with its steering,
+     after the other reads: one pass reads each row, probes it as read and
+     writes the steered row, with the same results as the separate calls);
   4. readback of SAE results into each app's ring (by default fused into
      the encode's merge, which writes the ring rows itself).
 
@@ -31,7 +34,7 @@ from . import (XMIX_PROBE_LAST, XMIX_PROBE_MEAN, XMIX_PROBE_TOKEN, Ring, Route, 
                xmix_route_build, xmix_sae_clamp_decode, xmix_sae_encode_candidates,
                xmix_sae_encode_topk, xmix_sae_encode_topk_ring, xmix_sae_fold_bias,
                xmix_sae_merge_topk, xmix_sae_merge_topk_ring, xmix_sae_pack_encoder,
-               xmix_steer_apply)
+               xmix_steer_apply, xmix_steer_probe)
 
 
 def to_device_bits(a: np.ndarray, device) -> torch.Tensor:
@@ -88,10 +91,12 @@ class _Layer:
 
 
 class HookStep:
-    def __init__(self, wl, device="cuda", fold_bias: bool = True, fuse_readback: bool = True):
+    def __init__(self, wl, device="cuda", fold_bias: bool = True, fuse_readback: bool = True,
+                 fuse_steer_probe: bool = True):
         dev = torch.device(device)
         self.wl = wl
         self.fuse_readback = fuse_readback
+        self.fuse_steer_probe = fuse_steer_probe
         self.device = dev
         act = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
         self.req = to_device(wl.req, torch.int32, dev)
@@ -160,7 +165,12 @@ class HookStep:
         which enqueues the same kernels."""
         xmix_route_build(self.req, self.T_valid, self.sub, self.route, self.err, stream)
         for lay in self.layers:
+            fused = None  # the token probes that run in one pass with the steering
+            if self.fuse_steer_probe and lay.steer_v is not None:
+                fused = next((p for p in lay.probes if p.mode == XMIX_PROBE_TOKEN), None)
             for p in lay.probes:
+                if p is fused:
+                    continue
                 xmix_probe_score(lay.h, self.route, p.w, p.b, p.bits, p.mode, p.logit, p.score,
                                  cu_seqlens=self.cu, ws=p.ws, stream=stream)
             for s in lay.saes:
@@ -184,7 +194,11 @@ class HookStep:
                 else:
                     xmix_sae_encode_topk(lay.h, self.route, s.bit, s.W_enc, s.b_enc, s.b_dec,
                                          s.c_fold, s.k, s.idx, s.val, s.ws, stream)
-            if lay.steer_v is not None:
+            if fused is not None:
+                xmix_steer_probe(lay.h, self.route, self.req, lay.steer_v, lay.steer_bits,
+                                 self.alpha, fused.w, fused.b, fused.bits, fused.logit,
+                                 fused.score, stream)
+            elif lay.steer_v is not None:
                 xmix_steer_apply(lay.h, self.route, self.req, lay.steer_v, lay.steer_bits,
                                  self.alpha, stream)
             for s in lay.saes:

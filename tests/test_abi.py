@@ -64,6 +64,9 @@ def test_host_validation_rejects_before_launch(lib):
     assert lib.xmix_readback_compact(None, None, 1, None, 0, None, 0, 0, None, None) == 1
     lib.xmix_router_write.restype = ctypes.c_int
     assert lib.xmix_router_write(None, 0, 8, None, None, None, 1, None) == 1
+    lib.xmix_steer_probe.restype = ctypes.c_int
+    assert lib.xmix_steer_probe(None, 1, 64, None, None, None, None, None, 1, 1, None, None,
+                                None, 1, None, None, None) == 1
     assert lib.xmix_status_string(3) == b"workspace missing or too small"
 
 

@@ -200,6 +200,71 @@ def test_probe_70b_shape(px):
     _probe_case(px, synth.make("c5", m=256, k=8))
 
 
+# ------------------------------------------------- probes + steering, fused
+
+def _steer_probe_case(px, wl, layer=0):
+    """One fused pass against the two separate calls (bit-identical rows and
+    probe outputs) and against the oracle (the probes see the row as read)."""
+    L = wl.layers[layer]
+    tm, _, _, _ = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    rt, _ = gpu_route(px, wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    bf = wl.dtype == "bf16"
+    put = (lambda a: dev_bits(a)) if bf else (lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda())
+    ps = [p for p in L.probes if p.mode == "token"]
+    sbits, pbits = [s.bit for s in L.steer], [p.bit for p in ps]
+    v, w = np.stack([s.v for s in L.steer]), np.stack([p.w for p in ps])
+    b = np.array([p.b for p in ps], np.float32)
+    vd, wd, bd = put(v), put(w), torch.from_numpy(b).cuda()
+    alpha, req = torch.from_numpy(wl.alpha).cuda(), dev_i32(wl.req)
+    nan = lambda: torch.full((len(ps), wl.T_max), float("nan"), device="cuda")
+    # separate calls: probes first (they read the activation as produced)
+    h1, l1, s1 = put(L.h), nan(), nan()
+    px.xmix_probe_score(h1, rt, wd, bd, pbits, px.XMIX_PROBE_TOKEN, l1, s1)
+    px.xmix_steer_apply(h1, rt, req, vd, sbits, alpha)
+    h2, l2, s2 = put(L.h), nan(), nan()
+    px.xmix_steer_probe(h2, rt, req, vd, sbits, alpha, wd, bd, pbits, l2, s2)
+    torch.cuda.synchronize()
+    g1 = torch_bits(h1) if bf else h1.cpu().numpy()
+    g2 = torch_bits(h2) if bf else h2.cpu().numpy()
+    assert np.array_equal(g1.view(np.uint8), g2.view(np.uint8))
+    for a, c in ((l1, l2), (s1, s2)):
+        a, c = a.cpu().numpy(), c.cpu().numpy()
+        assert np.array_equal(np.isnan(a), np.isnan(c))
+        assert np.array_equal(a[~np.isnan(a)].view(np.uint32), c[~np.isnan(c)].view(np.uint32))
+    # against the oracle
+    ref = oracle.steer(L.h, tm, wl.req, v, sbits, wl.alpha)
+    rows = (tm & np.uint32(sum(1 << q for q in sbits))) != 0
+    check_steer(g2, ref, L.h, rows, bf)
+    lr, sr = oracle.probe_token(L.h, tm, w, b, pbits)
+    hv = bf16_f64(L.h) if bf else L.h.astype(np.float64)
+    wv = bf16_f64(w) if bf else w.astype(np.float64)
+    written = ~np.isnan(lr)
+    lg, sg = l2.cpu().numpy(), s2.cpu().numpy()
+    assert np.all(np.isnan(lg[~written])), "unsubscribed outputs were written"
+    check_probe(lg, sg, lr, sr, written, np.abs(wv) @ np.abs(hv).T)
+
+
+def test_steer_probe_fused_toy_fp32(px):
+    _steer_probe_case(px, synth.make("c1"))
+
+
+def test_steer_probe_fused_decode_8b_shape(px):
+    wl = synth.make("c2", n_layers=2)
+    for layer in range(2):
+        _steer_probe_case(px, wl, layer)
+
+
+def test_steer_probe_fused_padding_and_ragged(px):
+    wl = synth.make("c2", d=264 - 8, T=77, n_layers=1)
+    wl.req[70:] = -1
+    wl.T_valid = 70
+    _steer_probe_case(px, wl)
+
+
+def test_steer_probe_fused_70b_shape(px):
+    _steer_probe_case(px, synth.make("c5", m=256, k=8))
+
+
 # --------------------------------------------------------------- SAE encode
 
 def _encode(px, wl, sae, h_bits, fold=True):
