@@ -24,8 +24,8 @@
 // outside the window stages again.
 //
 // Stage 2 (sae_merge_kernel): one workgroup per subscribed token gathers the
-// candidates of all tiles and selects the exact top-k of that pool (key
-// bisection, ties to the lower latent).  The result is the exact top-k of
+// candidates of all tiles and selects the exact top-k of that pool (a radix
+// select over (value, latent) composites, ties to the lower latent).  The result is the exact top-k of
 // all m latents whenever the k-th selected value is >= every tile's tau,
 // because a latent that was not emitted lies below its tile's tau.  When
 // that certificate fails (only for inputs whose best latents crowd into a
@@ -1011,21 +1011,10 @@ constexpr int kMaxRepair = 16;                     // slices one repair redoes
 constexpr int kRepairR = 6;                        // repair pool entries per lane
 constexpr int kRepairPool = kRepairR * kWave;      // 384 >= k + one slice
 
-// The k best of key[0..n) / idx[0..n) (k <= n <= 8 * 64) by one wave, with
-// a register footprint matched to n; sk / si is that wave's 64-entry
-// staging area.
-constexpr int kDirectSelect = 4 * kWave;  // pools up to this go to one wave
-__device__ __forceinline__ void small_select(const uint32_t* K, const int32_t* I, int n, int k,
-                                             uint32_t* sk, int32_t* si, uint32_t* tau,
-                                             uint32_t* wk, int32_t* wi) {
-    if (n <= kDirectSelect) wave_select_take<4>(K, I, n, k, sk, si, tau, wk, wi);
-    else wave_select_take<8>(K, I, n, k, sk, si, tau, wk, wi);
-}
-
-// Entries of quarter w of a pool of `total` cut into four.
-__device__ __forceinline__ int quarter_size(int total, int w) {
-    const int q = (total + 3) / 4;
-    return max(0, min(q, total - w * q));
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
+    const uint32_t lo = static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), m, kWave));
+    const uint32_t hi = static_cast<uint32_t>(__shfl_xor(static_cast<int>(v >> 32), m, kWave));
+    return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
 // pre-activation of latent j without the bias: plain fp32 dot product of
@@ -1053,9 +1042,9 @@ __device__ __forceinline__ float latent_dot(const uint16_t* __restrict__ Wp,
 // One workgroup per subscribed token.  Every thread gathers the candidates
 // of the slices it owns (count, threshold and the slice's pair block are
 // loaded together, so the gather costs one memory round trip), a prefix
-// over the workgroup places them in an LDS pool, and wave 0 selects and
-// checks the certificate; a failed check is repaired by the whole
-// workgroup; wave 0 then sorts and writes.
+// over the workgroup places them in an LDS pool, the workgroup selects the
+// k best of it (radix select) and wave 0 checks the certificate; a failed
+// check is repaired by the whole workgroup; wave 0 then sorts and writes.
 __global__ void __launch_bounds__(kMergeThreads)
 sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ tile_cnt,
                  const float* __restrict__ tile_tau, int32_t n_mt, int32_t cap,
@@ -1066,10 +1055,11 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
                  RingOut ring) {
     __shared__ uint32_t K[kPoolMax + kWave];
     __shared__ int32_t I[kPoolMax + kWave];
-    __shared__ uint32_t K2[5 * kWave];  // the four waves' winners, then a staging area
-    __shared__ int32_t I2[5 * kWave];
-    __shared__ uint32_t SK[kMergeThreads / kWave][kWave];  // per-wave staging areas
-    __shared__ int32_t SI[kMergeThreads / kWave][kWave];
+    __shared__ uint32_t K2[kWave];  // the selected k entries (k <= 64)
+    __shared__ int32_t I2[kWave];
+    __shared__ int hist_s[2][256];  // radix-select digit counts (two rounds in flight)
+    __shared__ uint64_t cmin_s[kMergeThreads / kWave], cmax_s[kMergeThreads / kWave];
+    __shared__ int dig_s, gt_s, hb_s, sel_n_s;
     __shared__ int scan_s[kMergeThreads / kWave];
     __shared__ uint32_t tmax_s[kMergeThreads / kWave];
     __shared__ int pool_n_s, nfail_s, fix_s;
@@ -1188,42 +1178,124 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
     uint64_t h0 = 0;
     if (ring.slots && tid == 0)
         h0 = __hip_atomic_load(&ring.head[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    // Selection.  A large pool is cut into quarters: each wave keeps the k
-    // best of its quarter, and wave 0 selects from those (an entry of the
-    // pool's top k, in the order key descending, latent ascending, is in its
-    // quarter's top k, so nothing is lost, ties included); a small pool goes
-    // to wave 0 directly.  Then wave 0 checks the certificate.
+    // Selection: a radix select over the pool by the whole workgroup.  An
+    // entry's rank is its 64-bit composite (key, ~latent), so the order key
+    // descending, latent ascending has no ties and exactly k entries lie at
+    // or above the k-th composite.  Starting at the 8-bit digit that holds
+    // the highest bit in which the pool's composites differ, each round
+    // counts (LDS atomics) the digits of the entries that match the prefix
+    // found so far, and wave 0 finds the digit that holds the k-th entry;
+    // the rounds end as soon as that digit's whole bin is needed.  The k
+    // entries at or above the prefix then go to wave 0.  The pool itself is
+    // left as it was (the repair below reads it).
     uint32_t wk = 0;
     int32_t wi = 0x7FFFFFFF;
     const bool fits = total <= kPoolMax && total >= k;  // uniform
-    uint32_t tau = 0;
-    if (fits && total > kDirectSelect) {
-        const int q = (total + 3) / 4, nw = quarter_size(total, wave), kw = min(k, nw);
-        int off = 0, total2 = 0;
-        for (int w = 0; w < kMergeThreads / kWave; ++w) {
-            const int kq = min(k, quarter_size(total, w));
-            off += w < wave ? kq : 0;
-            total2 += kq;
+    if (fits) {
+        // composite of pool entry i (read from LDS where needed)
+        auto comp = [&](int i) __attribute__((always_inline)) {
+            return (static_cast<uint64_t>(K[i]) << 32) | static_cast<uint32_t>(~I[i]);
+        };
+        uint64_t cmin = ~0ull, cmax = 0ull;
+        for (int i = tid; i < total; i += kMergeThreads) {
+            const uint64_t c = comp(i);
+            cmin = min(cmin, c);
+            cmax = max(cmax, c);
         }
-        if (nw > 0) {
-            uint32_t tw, a;
-            int32_t b;
-            small_select(K + wave * q, I + wave * q, nw, kw, SK[wave], SI[wave], &tw, &a, &b);
-            if (lane < kw) {
-                K2[off + lane] = a;
-                I2[off + lane] = b;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+            cmin = min(cmin, shfl_xor_u64(cmin, off));
+            cmax = max(cmax, shfl_xor_u64(cmax, off));
+        }
+        hist_s[0][tid] = 0;
+        hist_s[1][tid] = 0;
+        if (lane == 0) {
+            cmin_s[wave] = cmin;
+            cmax_s[wave] = cmax;
+        }
+        if (tid == 0) sel_n_s = 0;
+        __syncthreads();
+#pragma unroll
+        for (int w = 0; w < kMergeThreads / kWave; ++w) {
+            cmin = min(cmin, cmin_s[w]);
+            cmax = max(cmax, cmax_s[w]);
+        }
+        const uint64_t diff = cmin ^ cmax;
+        int shift = diff ? ((63 - __clzll(static_cast<long long>(diff))) & ~7) : 0;
+        // bits above the first digit are common to every entry
+        uint64_t prefix = shift < 56 ? cmin & ~((1ull << (shift + 8)) - 1ull) : 0ull;
+        int need = k;
+        for (int round = 0;; ++round) {
+            int* hc = hist_s[round & 1];
+            const uint64_t hi = shift < 56 ? prefix >> (shift + 8) : 0ull;
+            for (int i = tid; i < total; i += kMergeThreads) {
+                const uint64_t c = comp(i);
+                if (shift >= 56 || (c >> (shift + 8)) == hi)
+                    atomicAdd(&hc[static_cast<int>(c >> shift) & 255], 1);
+            }
+            // the other buffer was last read before the previous round's
+            // second barrier
+            hist_s[(round + 1) & 1][tid] = 0;
+            __syncthreads();
+            if (wave == 0) {
+                int h4[4], ls = 0;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    h4[j] = hc[4 * lane + j];
+                    ls += h4[j];
+                }
+                int sfx = ls;  // entries in this lane's bins and every higher lane's
+#pragma unroll
+                for (int off = 1; off < kWave; off <<= 1) {
+                    const int y = __shfl_down(sfx, off, kWave);
+                    if (lane + off < kWave) sfx += y;
+                }
+                int above = sfx - ls;
+#pragma unroll
+                for (int j = 3; j >= 0; --j) {
+                    if (above < need && need <= above + h4[j]) {
+                        dig_s = 4 * lane + j;
+                        gt_s = above;
+                        hb_s = h4[j];
+                    }
+                    above += h4[j];
+                }
+            }
+            __syncthreads();
+            const int D = dig_s, gt = gt_s, hb = hb_s;
+            need -= gt;
+            prefix |= static_cast<uint64_t>(D) << shift;
+            if (hb == need || shift == 0) break;  // uniform
+            shift -= 8;
+        }
+        const uint64_t cut = prefix >> shift;
+        for (int i = tid; i < total; i += kMergeThreads) {
+            const uint64_t c = comp(i);
+            if ((c >> shift) >= cut) {
+                const int pos = atomicAdd(&sel_n_s, 1);  // exactly k entries
+                if (pos < kWave) {
+                    K2[pos] = static_cast<uint32_t>(c >> 32);
+                    I2[pos] = static_cast<int32_t>(~static_cast<uint32_t>(c));
+                }
             }
         }
         __syncthreads();
-        if (wave == 0)
-            small_select(K2, I2, total2, k, K2 + 4 * kWave, I2 + 4 * kWave, &tau, &wk, &wi);
-    } else if (fits && wave == 0) {
-        small_select(K, I, total, k, K + kPoolMax, I + kPoolMax, &tau, &wk, &wi);
+        if (wave == 0 && lane < k) {
+            wk = K2[lane];
+            wi = I2[lane];
+        }
     }
-    if (wave == 0 && lane == 0) {
-        sel_tau_s = tau;
-        fix_s = !fits ? 2 : (tau_tiles <= tau ? 0 : 1);
-        nfail_s = 0;
+    if (wave == 0) {
+        // the k-th key: the smallest of the selected
+        uint32_t tau = lane < k ? wk : 0xFFFFFFFFu;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1)
+            tau = min(tau, static_cast<uint32_t>(__shfl_xor(static_cast<int>(tau), off, kWave)));
+        if (lane == 0) {
+            sel_tau_s = tau;
+            fix_s = !fits ? 2 : (tau_tiles <= tau ? 0 : 1);
+            nfail_s = 0;
+        }
     }
     __syncthreads();
     if (fix_s != 0) {  // uniform
