@@ -385,6 +385,28 @@ def test_encode_exact_ties_take_lower_index(px):
                 assert lo_ in s, f"token {t}: {hi_} selected without its lower twin {lo_}"
 
 
+@pytest.mark.parametrize("shift", [-60.0, -12.0])
+def test_encode_negative_pre_activations(px, shift):
+    """b_enc moved down so that every pre-activation is negative (-60), or so
+    that fewer than k are positive (-12): the k largest are still taken by
+    value (ties to the lower latent) and the negative ones come out as 0."""
+    wl = synth.make("c3", d=256, m=1024, k=16, T=40)
+    sae = wl.layers[0].saes[0]
+    b = torch.from_numpy(bf16_f64(sae.b_enc) + shift).float().to(torch.bfloat16)
+    sae.b_enc = b.view(torch.int16).numpy().view(np.uint16)
+    rt, idx, val = _encode(px, wl, sae, wl.layers[0].h)
+    tm, cnt, lists, _ = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    toks = lists[0, :cnt[0]]
+    _check_encode(wl, sae, wl.layers[0].h, idx, val, toks)
+    _, _, _, pre = oracle.sae_encode(wl.layers[0].h, toks, sae.W_enc, sae.b_enc, sae.b_dec,
+                                     sae.k, want_pre=True)
+    n_pos = (pre > 0).sum(axis=1)
+    if shift == -60.0:
+        assert n_pos.max() == 0 and np.all(val[toks] == 0)
+    else:
+        assert n_pos.min() < sae.k  # the k-th value is negative for some tokens
+
+
 def test_encode_clustered_winners_in_one_tile(px):
     """All k winners planted in one 256-latent tile."""
     d, m, k = 256, 1024, 64
