@@ -385,12 +385,15 @@ def test_encode_exact_ties_take_lower_index(px):
                 assert lo_ in s, f"token {t}: {hi_} selected without its lower twin {lo_}"
 
 
-@pytest.mark.parametrize("shift", [-60.0, -12.0])
-def test_encode_negative_pre_activations(px, shift):
+@pytest.mark.parametrize("shift,T,n_sub", [(-60.0, 40, None), (-12.0, 40, None),
+                                           (-60.0, 1100, 1100), (-12.0, 1100, 1000)])
+def test_encode_negative_pre_activations(px, shift, T, n_sub):
     """b_enc moved down so that every pre-activation is negative (-60), or so
     that fewer than k are positive (-12): the k largest are still taken by
     value (ties to the lower latent) and the negative ones come out as 0."""
-    wl = synth.make("c3", d=256, m=1024, k=16, T=40)
+    # 40 token slots run the decode kernel; 1100 run the prefill GEMM
+    kw = {} if n_sub is None else {"n_sub": n_sub}
+    wl = synth.make("c3", d=256, m=1024, k=16, T=T, **kw)
     sae = wl.layers[0].saes[0]
     b = torch.from_numpy(bf16_f64(sae.b_enc) + shift).float().to(torch.bfloat16)
     sae.b_enc = b.view(torch.int16).numpy().view(np.uint16)
