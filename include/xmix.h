@@ -313,6 +313,28 @@ xmix_status xmix_sae_merge_topk(const uint16_t *h, int32_t d, const xmix_route *
                                 int32_t *idx_out, uint16_t *val_out,
                                 void *ws, size_t ws_bytes, void *stream);
 
+/* Route build and the candidates stage in one launch, for a step whose
+ * first consumer of the routing is an SAE encode (per-request toggling
+ * inside the batch, Sec. 4.2-4.3; the first stage of the encode above).
+ * Same effect as
+ *   xmix_route_build(req_of_token, T_valid, sub_mask, R_max, rt, err_word)
+ * followed by
+ *   xmix_sae_encode_candidates(h, d, rt, app_bit, W_packed, ...):
+ * the route's tok_mask, app_count, app_tokens and err_word hold exactly what
+ * the route build writes, and the candidates are the same.  Up to 1024
+ * token slots the encode kernel builds the routing itself (every workgroup
+ * lists its app's tokens in LDS; the separate launch and its kernel
+ * boundary are saved); above that the two launches are made.  Arguments are
+ * those of the two calls; errors as for them. */
+xmix_status xmix_route_sae_encode_candidates(const int32_t *req_of_token, const int32_t *T_valid,
+                                             const uint32_t *sub_mask, int32_t R_max,
+                                             const xmix_route *rt, uint32_t *err_word,
+                                             const uint16_t *h, int32_t d, int32_t app_bit,
+                                             const uint16_t *W_packed, const uint16_t *b_enc,
+                                             const uint16_t *b_dec, const float *c_fold,
+                                             int32_t m, int32_t k, void *ws, size_t ws_bytes,
+                                             void *stream);
+
 /* Encode + TopK with the readback of each encoded row fused in (the merge
  * writes the ring rows itself, saving the separate compaction pass).  Same
  * arguments and results as xmix_sae_encode_topk / xmix_sae_merge_topk, plus

@@ -76,6 +76,9 @@ _sigs = {
                               _i32, _i32, _vp, _vp, _vp, _sz, _vp], _st),
     "xmix_sae_encode_candidates": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _vp,
                                     _vp, _i32, _i32, _vp, _sz, _vp], _st),
+    "xmix_route_sae_encode_candidates": ([_vp, _vp, _vp, _i32, ctypes.POINTER(XmixRoute), _vp,
+                                          _vp, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _i32, _vp,
+                                          _sz, _vp], _st),
     "xmix_sae_merge_topk": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32, _i32,
                              _vp, _vp, _vp, _sz, _vp], _st),
     "xmix_sae_encode_topk_ring": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _vp,
@@ -396,6 +399,22 @@ def xmix_sae_merge_topk_ring(h, route: Route, app_bit: int, W_enc, c_fold, k: in
         _ptr(h), d, ctypes.byref(route.struct), app_bit, _ptr(W_enc), _ptr(c_fold), m, k,
         _ptr(idx_out), _ptr(val_out), _ptr(ws), ws.numel() * ws.element_size(),
         _ptr(req_of_token), layer_id, app_id, ctypes.byref(ring.struct), _stream(stream)))
+
+
+def xmix_route_sae_encode_candidates(req_of_token, T_valid, sub_mask, route: Route, err_word, h,
+                                     app_bit: int, W_enc, b_enc, b_dec, c_fold, k: int, ws,
+                                     stream=None):
+    """Route build and the encode's candidates stage in one launch (up to
+    1024 token slots): the same results as xmix_route_build followed by
+    xmix_sae_encode_candidates."""
+    T_max, d = h.shape
+    m = W_enc.shape[0]
+    assert T_max == route.T_max and h.dtype == torch.bfloat16 and W_enc.dtype == torch.bfloat16
+    _check("xmix_route_sae_encode_candidates", _lib.xmix_route_sae_encode_candidates(
+        _ptr(req_of_token), _ptr(T_valid), _ptr(sub_mask), sub_mask.numel(),
+        ctypes.byref(route.struct), _ptr(err_word), _ptr(h), d, app_bit, _ptr(W_enc),
+        _ptr(b_enc), _ptr(b_dec), _ptr(c_fold), m, k, _ptr(ws), ws.numel() * ws.element_size(),
+        _stream(stream)))
 
 
 def xmix_sae_encode_candidates(h, route: Route, app_bit: int, W_enc, b_enc, b_dec, c_fold,

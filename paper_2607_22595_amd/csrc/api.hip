@@ -234,6 +234,42 @@ xmix_status xmix_sae_encode_candidates(const uint16_t* h, int32_t d, const xmix_
                                           app_list(rt, app_bit), W_enc, c_fold, m, k, cand, s));
 }
 
+xmix_status xmix_route_sae_encode_candidates(const int32_t* req_of_token, const int32_t* T_valid,
+                                             const uint32_t* sub_mask, int32_t R_max,
+                                             const xmix_route* rt, uint32_t* err_word,
+                                             const uint16_t* h, int32_t d, int32_t app_bit,
+                                             const uint16_t* W_enc, const uint16_t* b_enc,
+                                             const uint16_t* b_dec, const float* c_fold,
+                                             int32_t m, int32_t k, void* ws, size_t ws_bytes,
+                                             void* stream) {
+    if (!req_of_token || !T_valid || !sub_mask || !err_word || R_max < 1) return XMIX_E_INVAL;
+    if (!h || !W_enc) return XMIX_E_INVAL;
+    if (!c_fold && (!b_enc || !b_dec || !aligned16(b_dec))) return XMIX_E_INVAL;
+    float* fold;
+    void* cand;
+    const xmix_status st = encode_args(h, d, rt, app_bit, W_enc, m, k, ws, ws_bytes, &fold, &cand);
+    if (st != XMIX_OK) return st;
+    hipStream_t s = as_stream(stream);
+    if (!c_fold) {
+        if (launch_sae_fold(W_enc, b_enc, b_dec, m, d, fold, s) != hipSuccess) return XMIX_E_LAUNCH;
+        c_fold = fold;
+    }
+    RouteIn r;
+    r.req = req_of_token;
+    r.T_valid = T_valid;
+    r.sub = sub_mask;
+    r.R_max = R_max;
+    r.n_apps = rt->n_apps;
+    r.app_bit = app_bit;
+    r.tok_mask = rt->tok_mask;
+    r.app_count = rt->app_count;
+    r.app_tokens = rt->app_tokens;
+    r.err_word = err_word;
+    return launched(launch_sae_candidates(h, d, rt->T_max, rt->app_count + app_bit,
+                                          app_list(rt, app_bit), W_enc, c_fold, m, k, cand, s,
+                                          &r));
+}
+
 xmix_status xmix_sae_merge_topk(const uint16_t* h, int32_t d, const xmix_route* rt,
                                 int32_t app_bit, const uint16_t* W_packed, const float* c_fold,
                                 int32_t m, int32_t k, int32_t* idx_out, uint16_t* val_out,

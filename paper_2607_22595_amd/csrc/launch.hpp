@@ -50,10 +50,24 @@ hipError_t launch_sae_pack(const uint16_t* W_enc, int32_t m, int32_t d, uint16_t
                            hipStream_t stream);
 hipError_t launch_sae_fold(const uint16_t* W_enc, const uint16_t* b_enc, const uint16_t* b_dec,
                            int32_t m, int32_t d, float* c_fold, hipStream_t stream);
+// Routing inputs and outputs for an encode launch that also builds the
+// step's routing (see xmix_route_sae_encode_candidates).
+struct RouteIn {
+    const int32_t* req = nullptr;
+    const int32_t* T_valid = nullptr;
+    const uint32_t* sub = nullptr;
+    int32_t R_max = 0, n_apps = 0, app_bit = 0;
+    uint32_t* tok_mask = nullptr;
+    int32_t* app_count = nullptr;
+    int32_t* app_tokens = nullptr;
+    uint32_t* err_word = nullptr;
+};
+
 hipError_t launch_sae_candidates(const uint16_t* h, int32_t d, int32_t T_max,
                                  const int32_t* app_count, const int32_t* tok_list,
                                  const uint16_t* W_enc, const float* c_fold, int32_t m,
-                                 int32_t k, void* cand, hipStream_t stream);
+                                 int32_t k, void* cand, hipStream_t stream,
+                                 const RouteIn* route = nullptr);
 struct MergeRing {  // readback of the merged rows into a ring
     uint8_t* slots;
     uint64_t* head;

@@ -146,6 +146,55 @@ sae_fold_kernel(const uint16_t* __restrict__ Wp, const uint16_t* __restrict__ b_
     if (lane_id() == 0) c_fold[j] = bf16_to_f32(b_enc[j]) - acc;
 }
 
+// In-kernel route build, for up to kRouteMaxT token slots (the decode
+// kernel below can take the place of the route-build launch of a step).
+// Same rules as the route-build kernel: T_valid is clamped to [0, T_max]
+// (error bit 2), a request id >= R_max routes nowhere (error bit 1).  The
+// ascending list of the tokens that carry `bit` is written to list_s and its
+// length returned; `mask_out`, if given, receives every slot's mask.  Every
+// thread of the workgroup takes part (two barriers per 512 slots).
+constexpr int kRouteMaxT = 1024;
+__device__ int32_t build_token_list(const int32_t* __restrict__ req, int32_t tv,
+                                    const uint32_t* __restrict__ sub, int32_t R_max,
+                                    uint32_t keep, int bit, int32_t T_max, int32_t* list_s,
+                                    int32_t* wtot, uint32_t* __restrict__ mask_out,
+                                    uint32_t& err) {
+    const int tid = threadIdx.x, wave = tid / kWave;
+    int32_t base = 0;
+    for (int32_t c0 = 0; c0 < T_max; c0 += kEncThreads) {
+        const int32_t t = c0 + tid;
+        uint32_t mask = 0;
+        if (t < tv) {
+            const int32_t r = req[t];
+            if (r >= R_max) err |= 1u;
+            else if (r >= 0) mask = sub[r] & keep;
+        }
+        if (mask_out && t < T_max) mask_out[t] = mask;
+        const bool has = (mask >> bit) & 1u;
+        const uint64_t bal = wave_ballot(has);
+        if (lane_id() == 0) wtot[wave] = __popcll(bal);
+        __syncthreads();
+        int32_t before = 0, total = 0;
+#pragma unroll
+        for (int w = 0; w < kEncWaves; ++w) {
+            const int32_t c = wtot[w];
+            before += (w < wave) ? c : 0;
+            total += c;
+        }
+        if (has) list_s[base + before + lanes_below(bal)] = t;
+        base += total;
+        __syncthreads();  // wtot is rewritten by the next chunk
+    }
+    return base;
+}
+
+// Publishes one app's list (padded with -1) and count, as the route build does.
+__device__ void publish_token_list(const int32_t* list_s, int32_t n, int32_t T_max,
+                                   int32_t* __restrict__ list_g, int32_t* __restrict__ count_g) {
+    for (int32_t i = threadIdx.x; i < T_max; i += kEncThreads) list_g[i] = i < n ? list_s[i] : -1;
+    if (threadIdx.x == 0) *count_g = n;
+}
+
 // ---------------------------------------------- GEMM + candidate emission
 __global__ void __launch_bounds__(kEncThreads, 1)
 sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
@@ -153,8 +202,14 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
                   const uint16_t* __restrict__ W, const float* __restrict__ c_fold,
                   int32_t n_mt, int32_t n_nt, float z_guess, int32_t lo_cnt, int32_t cap,
                   uint2* __restrict__ cand, int32_t* __restrict__ tile_cnt,
-                  float* __restrict__ tile_tau) {
+                  float* __restrict__ tile_tau, const int32_t* __restrict__ r_req,
+                  const int32_t* __restrict__ r_tvalid, const uint32_t* __restrict__ r_sub,
+                  int32_t r_Rmax, int32_t r_Tmax, int32_t r_napps, int32_t r_bit,
+                  uint32_t* __restrict__ r_mask, int32_t* __restrict__ r_count,
+                  int32_t* __restrict__ r_lists, uint32_t* __restrict__ r_err) {
     __shared__ uint4 xs[2][kBN * 8];          // 2 x 16 KiB token chunks
+    __shared__ int32_t list_s[kRouteMaxT];    // the app's token list (in-kernel route build)
+    __shared__ int32_t rtot_s[kEncWaves];
     __shared__ float red1[kEncWaves][kBN];    // per-wave partials of the epilogue
     __shared__ float red2[kEncWaves][kBN];
     __shared__ float red3[kEncWaves][kBN];    // trim partials (not read by the statistics)
@@ -163,6 +218,46 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     __shared__ int ne_s[kBN];
     __shared__ float tau_s[kBN];
     __shared__ uint4 stage4[kBN * kMaxCap / 2];  // per token: up to kMaxCap pairs
+
+    // With r_req given, the kernel also builds the step's routing (in place
+    // of a route-build launch): every workgroup builds its app's token list
+    // in LDS; workgroup a < n_apps publishes app a's list and count, and
+    // workgroup 0 the token masks and the error word.
+    const int32_t* tl = tok_list;
+    int cnt = 0;
+    if (r_req) {  // uniform
+        int32_t tv = *r_tvalid;
+        uint32_t err = 0;
+        if (tv < 0 || tv > r_Tmax) {
+            err |= 2u;
+            tv = tv < 0 ? 0 : r_Tmax;
+        }
+        const uint32_t keep = r_napps >= 32 ? 0xFFFFFFFFu : ((1u << r_napps) - 1u);
+        const int own = blockIdx.x;
+        uint32_t* masks = own == 0 ? r_mask : nullptr;
+        if (own < r_napps && own != r_bit) {
+            const int32_t n = build_token_list(r_req, tv, r_sub, r_Rmax, keep, own, r_Tmax,
+                                               list_s, rtot_s, masks, err);
+            masks = nullptr;
+            publish_token_list(list_s, n, r_Tmax, r_lists + static_cast<int64_t>(own) * r_Tmax,
+                               r_count + own);
+            __syncthreads();  // list_s is rebuilt below
+        }
+        cnt = build_token_list(r_req, tv, r_sub, r_Rmax, keep, r_bit, r_Tmax, list_s, rtot_s,
+                               masks, err);
+        if (own == r_bit)
+            publish_token_list(list_s, cnt, r_Tmax, r_lists + static_cast<int64_t>(r_bit) * r_Tmax,
+                               r_count + r_bit);
+        if (own == 0) {
+            uint32_t e = err;
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) e |= __shfl_xor(e, off, kWave);
+            if (lane_id() == 0 && e != 0) atomicOr(r_err, e);
+        }
+        tl = list_s;
+    } else {
+        cnt = *app_count;
+    }
 
     // Tile order.  Few token tiles (decode): latent tile fastest, so the
     // workgroups of the first token tile, the ones with live tokens, are
@@ -193,7 +288,6 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
         mt = xcd * m8 + lt;
     }
     if (mt >= n_mt) return;
-    const int cnt = *app_count;
     const int n0 = nt * kBN;
     if (n0 >= cnt) return;
     const int ntok = min(kBN, cnt - n0);
@@ -218,7 +312,7 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
         const int n = xr + 64 * p;
         const bool ok = n < ntok;
         xmask[p] = ok ? 0xFFFFFFFFu : 0u;
-        xrow[p] = h + static_cast<int64_t>(tok_list[n0 + (ok ? n : 0)]) * d + 8 * xc;
+        xrow[p] = h + static_cast<int64_t>(tl[n0 + (ok ? n : 0)]) * d + 8 * xc;
     }
 
     // folded bias of this lane's 16 latents, fetched before the K loop
@@ -1518,10 +1612,22 @@ hipError_t launch_sae_fold(const uint16_t* W_enc, const uint16_t* b_enc, const u
 hipError_t launch_sae_candidates(const uint16_t* h, int32_t d, int32_t T_max,
                                  const int32_t* app_count, const int32_t* tok_list,
                                  const uint16_t* W_enc, const float* c_fold, int32_t m,
-                                 int32_t k, void* cand, hipStream_t stream) {
+                                 int32_t k, void* cand, hipStream_t stream,
+                                 const RouteIn* route) {
     const int32_t n_mt = m / kBM;
     const EmitPlan e = emit_plan(m, k);
     const CandArea a = cand_area(cand, T_max, n_mt, e.cap);
+    // the decode kernel routes when the batch fits its LDS list and its grid
+    // has a workgroup for every app to publish
+    if (route && (T_max > kRouteMaxT ||
+                  enc_grid(n_mt, (T_max + kBN - 1) / kBN) < route->n_apps)) {
+        const hipError_t r = launch_route_build(route->req, route->T_valid, route->sub,
+                                                route->R_max, T_max, route->n_apps,
+                                                route->tok_mask, route->app_count,
+                                                route->app_tokens, route->err_word, stream);
+        if (r != hipSuccess) return r;
+        route = nullptr;
+    }
     if (T_max >= kPrefillMinT) {
         const int32_t n_pad = stage_tokens(T_max);
         uint16_t* xs = reinterpret_cast<uint16_t*>(
@@ -1539,9 +1645,13 @@ hipError_t launch_sae_candidates(const uint16_t* h, int32_t d, int32_t T_max,
         return hipGetLastError();
     }
     const int32_t n_nt = (T_max + kBN - 1) / kBN;
+    const RouteIn none{};
+    const RouteIn& ri = route ? *route : none;
     hipLaunchKernelGGL(sae_stream_kernel, dim3(enc_grid(n_mt, n_nt)), dim3(kEncThreads), 0,
                        stream, h, d, app_count, tok_list, W_enc, c_fold, n_mt, n_nt, e.z, e.lo,
-                       e.cap, a.cand, a.cnt, a.tau);
+                       e.cap, a.cand, a.cnt, a.tau, ri.req, ri.T_valid, ri.sub, ri.R_max, T_max,
+                       ri.n_apps, ri.app_bit, ri.tok_mask, ri.app_count, ri.app_tokens,
+                       ri.err_word);
     return hipGetLastError();
 }
 

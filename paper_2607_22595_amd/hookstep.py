@@ -6,7 +6,9 @@ buffers of static shape and runs the step through the C ABI, in this
 order for every layer:
 
   1. route build (once per step: the batch and subscriptions are shared by
-     all hooked layers);
+     all hooked layers; when the first layer's first consumer of the routing
+     is an SAE encode and the batch has at most 1024 slots, that encode's
+     kernel builds the routing itself, one launch instead of two);
   2. reads of the activation as the model produced it: per-token probes,
      mean-pooled probes, SAE encodes;
   3. writes: steering, then each SAE app's clamp-decode;
@@ -33,8 +35,9 @@ from . import (XMIX_PROBE_LAST, XMIX_PROBE_MEAN, XMIX_PROBE_TOKEN, Ring, Route, 
                sae_encode_workspace, xmix_probe_score, xmix_readback_compact,
                xmix_route_build, xmix_sae_clamp_decode, xmix_sae_encode_candidates,
                xmix_sae_encode_topk, xmix_sae_encode_topk_ring, xmix_sae_fold_bias,
-               xmix_sae_merge_topk, xmix_sae_merge_topk_ring, xmix_sae_pack_encoder,
-               xmix_steer_apply, xmix_steer_probe)
+               xmix_route_sae_encode_candidates, xmix_sae_merge_topk,
+               xmix_sae_merge_topk_ring, xmix_sae_pack_encoder, xmix_steer_apply,
+               xmix_steer_probe)
 
 
 def to_device_bits(a: np.ndarray, device) -> torch.Tensor:
@@ -92,11 +95,12 @@ class _Layer:
 
 class HookStep:
     def __init__(self, wl, device="cuda", fold_bias: bool = True, fuse_readback: bool = True,
-                 fuse_steer_probe: bool = True):
+                 fuse_steer_probe: bool = True, fuse_route: bool = True):
         dev = torch.device(device)
         self.wl = wl
         self.fuse_readback = fuse_readback
         self.fuse_steer_probe = fuse_steer_probe
+        self.fuse_route = fuse_route
         self.device = dev
         act = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
         self.req = to_device(wl.req, torch.int32, dev)
@@ -163,8 +167,12 @@ class HookStep:
         before and right after the encode GEMM stage of each SAE app (e.g. to
         record timing events); the SAE call is then issued as its two stages,
         which enqueues the same kernels."""
-        xmix_route_build(self.req, self.T_valid, self.sub, self.route, self.err, stream)
-        for lay in self.layers:
+        first = self.layers[0] if self.layers else None
+        route_in_encode = (self.fuse_route and first is not None and not first.probes
+                           and len(first.saes) > 0 and self.wl.T_max <= 1024)
+        if not route_in_encode:
+            xmix_route_build(self.req, self.T_valid, self.sub, self.route, self.err, stream)
+        for li, lay in enumerate(self.layers):
             fused = None  # the token probes that run in one pass with the steering
             if self.fuse_steer_probe and lay.steer_v is not None:
                 fused = next((p for p in lay.probes if p.mode == XMIX_PROBE_TOKEN), None)
@@ -173,12 +181,21 @@ class HookStep:
                     continue
                 xmix_probe_score(lay.h, self.route, p.w, p.b, p.bits, p.mode, p.logit, p.score,
                                  cu_seqlens=self.cu, ws=p.ws, stream=stream)
-            for s in lay.saes:
-                if marks is not None:
-                    marks[0]()
-                    xmix_sae_encode_candidates(lay.h, self.route, s.bit, s.W_enc, s.b_enc,
-                                               s.b_dec, s.c_fold, s.k, s.ws, stream)
-                    marks[1]()
+            for i, s in enumerate(lay.saes):
+                routed = route_in_encode and li == 0 and i == 0
+                if marks is not None or routed:
+                    if marks is not None:
+                        marks[0]()
+                    if routed:
+                        xmix_route_sae_encode_candidates(self.req, self.T_valid, self.sub,
+                                                         self.route, self.err, lay.h, s.bit,
+                                                         s.W_enc, s.b_enc, s.b_dec, s.c_fold,
+                                                         s.k, s.ws, stream)
+                    else:
+                        xmix_sae_encode_candidates(lay.h, self.route, s.bit, s.W_enc, s.b_enc,
+                                                   s.b_dec, s.c_fold, s.k, s.ws, stream)
+                    if marks is not None:
+                        marks[1]()
                     if s.ring is not None and self.fuse_readback:
                         xmix_sae_merge_topk_ring(lay.h, self.route, s.bit, s.W_enc, s.c_fold,
                                                  s.k, s.idx, s.val, s.ws, self.req,

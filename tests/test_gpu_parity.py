@@ -410,6 +410,66 @@ def test_encode_negative_pre_activations(px, shift, T, n_sub):
         assert n_pos.min() < sae.k  # the k-th value is negative for some tokens
 
 
+@pytest.mark.parametrize("T,n_apps,bit,t_valid,bad_ids,m", [
+    (256, 1, 0, 256, False, 1024),    # the decode SAE step: one app
+    (300, 3, 2, 290, True, 1024),     # the SAE on bit 2 of 3, padding and bad ids
+    (40, 2, 0, 45, False, 1024),      # T_valid above T_max (error bit 2)
+    (1000, 5, 1, 1000, True, 1024),   # up to the in-kernel limit
+    (40, 3, 1, 40, False, 256),       # one workgroup, three apps: a route launch
+    (1100, 2, 0, 1100, False, 1024)])  # over 1024 slots: a route launch
+def test_route_built_inside_the_encode(px, T, n_apps, bit, t_valid, bad_ids, m):
+    """xmix_route_sae_encode_candidates leaves the route, the error word and
+    (after the merge) the top-k exactly as xmix_route_build followed by the
+    candidates stage does; the routing is also checked against the oracle."""
+    wl = synth.make("c3", d=256, m=m, k=16, T=T)
+    sae = wl.layers[0].saes[0]
+    rng = np.random.default_rng(T + n_apps)
+    sub = (wl.sub & np.uint32(1)) << np.uint32(bit)
+    for a in range(n_apps):
+        if a != bit:
+            sub |= (rng.random(wl.sub.size) < 0.4).astype(np.uint32) << np.uint32(a)
+    sub |= np.uint32(1 << 31)     # a bit beyond n_apps is dropped
+    req = wl.req.copy()
+    if bad_ids:
+        req[rng.choice(T, 7, replace=False)] = wl.sub.size + 3   # >= R_max
+        req[rng.choice(T, 5, replace=False)] = -1
+    h = dev_bits(wl.layers[0].h)
+    W = px.xmix_sae_pack_encoder(dev_bits(sae.W_enc))
+    be, bd = dev_bits(sae.b_enc), dev_bits(sae.b_dec)
+    c = torch.empty(sae.m, dtype=torch.float32, device="cuda")
+    px.xmix_sae_fold_bias(W, be, bd, c)
+    tv = torch.tensor([t_valid], dtype=torch.int32, device="cuda")
+    reqd, subd = dev_i32(req), dev_i32(sub)
+    outs = []
+    for fused in (False, True):
+        rt = px.Route(T, n_apps)
+        rt.tok_mask.fill_(-5)
+        rt.app_count.fill_(-5)
+        rt.app_tokens.fill_(-5)
+        err = torch.zeros(1, dtype=torch.int32, device="cuda")
+        ws = torch.empty(px.sae_encode_workspace(T, wl.d, sae.m, sae.k), dtype=torch.uint8,
+                         device="cuda")
+        idx = torch.full((T, sae.k), -7, dtype=torch.int32, device="cuda")
+        val = torch.zeros((T, sae.k), dtype=torch.bfloat16, device="cuda")
+        if fused:
+            px.xmix_route_sae_encode_candidates(reqd, tv, subd, rt, err, h, bit, W, be, bd, c,
+                                                sae.k, ws)
+        else:
+            px.xmix_route_build(reqd, tv, subd, rt, err)
+            px.xmix_sae_encode_candidates(h, rt, bit, W, be, bd, c, sae.k, ws)
+        px.xmix_sae_merge_topk(h, rt, bit, W, c, sae.k, idx, val, ws)
+        torch.cuda.synchronize()
+        outs.append((rt.tok_mask.cpu().numpy().view(np.uint32), rt.app_count.cpu().numpy(),
+                     rt.app_tokens.cpu().numpy(), int(err.item()), idx.cpu().numpy(),
+                     torch_bits(val)))
+    for a, b in zip(*outs):
+        assert np.array_equal(np.asarray(a), np.asarray(b))
+    tm, cnt, lists, e = oracle.route(req, t_valid, sub, n_apps)
+    assert np.array_equal(outs[1][0], tm) and np.array_equal(outs[1][1], cnt)
+    assert np.array_equal(outs[1][2], lists) and outs[1][3] == e
+    assert cnt[bit] > 0
+
+
 def test_encode_clustered_winners_in_one_tile(px):
     """All k winners planted in one 256-latent tile."""
     d, m, k = 256, 1024, 64
