@@ -64,6 +64,10 @@ def test_host_validation_rejects_before_launch(lib):
     assert lib.xmix_readback_compact(None, None, 1, None, 0, None, 0, 0, None, None) == 1
     lib.xmix_router_write.restype = ctypes.c_int
     assert lib.xmix_router_write(None, 0, 8, None, None, None, 1, None) == 1
+    lib.xmix_route_sae_encode_candidates.restype = ctypes.c_int
+    assert lib.xmix_route_sae_encode_candidates(None, None, None, 1, None, None, None, 256, 0,
+                                                None, None, None, None, 1024, 8, None,
+                                                ctypes.c_size_t(0), None) == 1
     lib.xmix_steer_probe.restype = ctypes.c_int
     assert lib.xmix_steer_probe(None, 1, 64, None, None, None, None, None, 1, 1, None, None,
                                 None, 1, None, None, None) == 1
