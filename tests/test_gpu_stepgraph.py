@@ -164,3 +164,46 @@ def test_capture_after_dropping_a_torch_graph_in_a_cycle(captured):
     finally:
         torch.cuda.synchronize()
         g.close()
+
+
+def test_decode_sae_step_graph_with_routing_in_the_encode():
+    """A decode SAE step whose routing is built inside the encode launch:
+    the captured step replays like the eager one, and redirecting the
+    subscription buffer reaches the encode kernel (no token encoded, the
+    ring head unchanged), and back."""
+    import paper_2607_22595_amd as px
+    from paper_2607_22595_amd.hookstep import HookStep
+    wl = synth.make("c3", d=512, m=2048, k=16, T=200, ring_capacity=256)
+    step = HookStep(wl)
+    s = step.layers[0].saes[0]
+    step.run()
+    torch.cuda.synchronize()
+    n = int(step.route.app_count[0].item())
+    toks = step.route.app_tokens[0, :n].long()
+    assert n > 0
+    idx_ref, val_ref = s.idx[toks].clone(), s.val[toks].clone()
+    stream = torch.cuda.Stream()
+    g = px.Graph(lambda: step.run(stream), stream)
+
+    def replay():
+        s.idx.fill_(-3)
+        torch.cuda.synchronize()
+        g.launch()
+        g.stream.synchronize()
+
+    try:
+        assert g.kernel_nodes == 2  # the encode (with the routing) and the merge
+        replay()
+        assert torch.equal(s.idx[toks], idx_ref) and torch.equal(s.val[toks], val_ref)
+        head = int(s.ring.head[0].item())
+        sub1 = torch.zeros_like(step.sub)
+        assert g.redirect(step.sub, sub1) == 1   # read once, by the encode
+        replay()
+        assert bool((s.idx == -3).all()) and int(s.ring.head[0].item()) == head
+        assert int(step.route.app_count[0].item()) == 0
+        assert g.redirect(sub1, step.sub) == 1
+        replay()
+        assert torch.equal(s.idx[toks], idx_ref)
+    finally:
+        torch.cuda.synchronize()
+        g.close()
