@@ -207,6 +207,23 @@ xmix_status xmix_steer_probe(void *h, xmix_dtype dt, int32_t d, const xmix_route
                              const int32_t *probe_bits, int32_t n_probe, float *logit_out,
                              float *score_out, void *stream);
 
+/* Route build and the pass above in one launch, for a step whose first
+ * consumer of the routing is this pass (per-request toggling inside the
+ * batch, Sec. 4.2-4.3).  Same effect as
+ *   xmix_route_build(req_of_token, T_valid, sub_mask, R_max, rt, err_word)
+ * followed by xmix_steer_probe(h, ...): the route holds exactly what the
+ * route build writes.  Up to 1024 token slots (and at least one slot per
+ * app) the kernel builds the routing itself: each workgroup computes its
+ * token's mask, workgroup a publishes app a's list.  Otherwise the two
+ * launches are made.  Arguments are those of the two calls. */
+xmix_status xmix_route_steer_probe(const int32_t *req_of_token, const int32_t *T_valid,
+                                   const uint32_t *sub_mask, int32_t R_max, const xmix_route *rt,
+                                   uint32_t *err_word, void *h, xmix_dtype dt, int32_t d,
+                                   const void *vecs, const int32_t *steer_bits,
+                                   const float *alpha, int32_t n_steer, const void *w,
+                                   const float *b, const int32_t *probe_bits, int32_t n_probe,
+                                   float *logit_out, float *score_out, void *stream);
+
 /* ------------------------------------------------------ router-logit write
  * Expert (de)activation on a mixture-of-experts router, a write whose locus
  * is the router logits (Table 1, App-7).  For each token t with at least one

@@ -68,6 +68,9 @@ _sigs = {
                           _i32, _vp], _st),
     "xmix_steer_probe": ([_vp, _st, _i32, ctypes.POINTER(XmixRoute), _vp, _vp, _vp, _vp, _i32,
                           _i32, _vp, _vp, _vp, _i32, _vp, _vp, _vp], _st),
+    "xmix_route_steer_probe": ([_vp, _vp, _vp, _i32, ctypes.POINTER(XmixRoute), _vp, _vp, _st,
+                                _i32, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _i32, _vp, _vp, _vp],
+                               _st),
     "xmix_probe_workspace": ([_i32, _i32, _i32], _sz),
     "xmix_probe_score": ([_vp, _st, _i32, ctypes.POINTER(XmixRoute), _vp, _vp, _vp, _i32, _i32,
                           _vp, _i32, _vp, _vp, _vp, _sz, _vp], _st),
@@ -234,6 +237,28 @@ def xmix_steer_probe(h, route: Route, req_of_token, vecs, steer_bits: Sequence[i
         _ptr(h), _dt(h), d, ctypes.byref(route.struct), _ptr(req_of_token), _ptr(vecs), sb,
         _ptr(alpha), ns, alpha.shape[0], _ptr(w), _ptr(b), pb, npb, _ptr(logit_out),
         _ptr(score_out), _stream(stream)))
+
+
+def xmix_route_steer_probe(req_of_token, T_valid, sub_mask, route: Route, err_word, h, vecs,
+                           steer_bits: Sequence[int], alpha, w, b, probe_bits: Sequence[int],
+                           logit_out, score_out, stream=None):
+    """Route build and the fused probes + steering pass in one launch (up to
+    1024 token slots): the same results as xmix_route_build followed by
+    xmix_steer_probe."""
+    T_max, d = h.shape
+    assert T_max == route.T_max and vecs.dtype == h.dtype and vecs.shape[-1] == d
+    ns, npb = len(steer_bits), len(probe_bits)
+    assert alpha.dtype == torch.float32 and alpha.dim() == 2 and alpha.shape[1] == ns
+    assert w.dtype == h.dtype and w.shape == (npb, d) and b.dtype == torch.float32
+    assert logit_out.shape == (npb, T_max) and score_out.shape == (npb, T_max)
+    assert req_of_token.dtype == torch.int32 and req_of_token.numel() == T_max
+    sb = (ctypes.c_int32 * ns)(*steer_bits)
+    pb = (ctypes.c_int32 * npb)(*probe_bits)
+    _check("xmix_route_steer_probe", _lib.xmix_route_steer_probe(
+        _ptr(req_of_token), _ptr(T_valid), _ptr(sub_mask), sub_mask.numel(),
+        ctypes.byref(route.struct), _ptr(err_word), _ptr(h), _dt(h), d, _ptr(vecs), sb,
+        _ptr(alpha), ns, _ptr(w), _ptr(b), pb, npb, _ptr(logit_out), _ptr(score_out),
+        _stream(stream)))
 
 
 def xmix_router_write(logits, route: Route, app_bits: Sequence[int], offsets, stream=None):

@@ -121,6 +121,37 @@ xmix_status xmix_steer_probe(void* h, xmix_dtype dt, int32_t d, const xmix_route
                                        n_probe, logit_out, score_out, as_stream(stream)));
 }
 
+xmix_status xmix_route_steer_probe(const int32_t* req_of_token, const int32_t* T_valid,
+                                   const uint32_t* sub_mask, int32_t R_max, const xmix_route* rt,
+                                   uint32_t* err_word, void* h, xmix_dtype dt, int32_t d,
+                                   const void* vecs, const int32_t* steer_bits,
+                                   const float* alpha, int32_t n_steer, const void* w,
+                                   const float* b, const int32_t* probe_bits, int32_t n_probe,
+                                   float* logit_out, float* score_out, void* stream) {
+    if (!req_of_token || !T_valid || !sub_mask || !err_word || R_max < 1) return XMIX_E_INVAL;
+    if (!h || !vecs || !alpha || !w || !b || !logit_out || !score_out || !route_ok(rt) || d < 1)
+        return XMIX_E_INVAL;
+    if (dt != XMIX_BF16 && dt != XMIX_F32) return XMIX_E_INVAL;
+    if (d % (dt == XMIX_BF16 ? 8 : 4) != 0 || !aligned16(h) || !aligned16(vecs) || !aligned16(w))
+        return XMIX_E_INVAL;
+    BitList sbits, pbits;
+    if (!bits_ok(steer_bits, n_steer, rt->n_apps, &sbits)) return XMIX_E_INVAL;
+    if (!bits_ok(probe_bits, n_probe, rt->n_apps, &pbits)) return XMIX_E_INVAL;
+    RouteIn r;
+    r.req = req_of_token;
+    r.T_valid = T_valid;
+    r.sub = sub_mask;
+    r.R_max = R_max;
+    r.n_apps = rt->n_apps;
+    r.tok_mask = rt->tok_mask;
+    r.app_count = rt->app_count;
+    r.app_tokens = rt->app_tokens;
+    r.err_word = err_word;
+    return launched(launch_steer_probe(h, dt == XMIX_BF16, d, rt->T_max, rt->tok_mask,
+                                       req_of_token, vecs, sbits, alpha, n_steer, w, b, pbits,
+                                       n_probe, logit_out, score_out, as_stream(stream), &r));
+}
+
 xmix_status xmix_router_write(void* logits, xmix_dtype dt, int32_t n_experts,
                               const xmix_route* rt, const int32_t* app_bits,
                               const float* offsets, int32_t n_router, void* stream) {

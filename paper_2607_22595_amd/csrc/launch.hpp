@@ -29,11 +29,6 @@ hipError_t launch_steer(void* h, bool bf16, int32_t d, int32_t T_max, const uint
                         const int32_t* req, const void* vecs, const BitList& bits,
                         const float* alpha, int32_t n_steer, hipStream_t stream);
 
-hipError_t launch_steer_probe(void* h, bool bf16, int32_t d, int32_t T_max,
-                              const uint32_t* tok_mask, const int32_t* req, const void* vecs,
-                              const BitList& sbits, const float* alpha, int32_t n_steer,
-                              const void* w, const float* b, const BitList& pbits,
-                              int32_t n_probe, float* logit, float* score, hipStream_t stream);
 
 hipError_t launch_router_write(void* logits, bool bf16, int32_t n_experts, int32_t T_max,
                                const uint32_t* tok_mask, const BitList& bits,
@@ -62,6 +57,13 @@ struct RouteIn {
     int32_t* app_tokens = nullptr;
     uint32_t* err_word = nullptr;
 };
+
+hipError_t launch_steer_probe(void* h, bool bf16, int32_t d, int32_t T_max,
+                              const uint32_t* tok_mask, const int32_t* req, const void* vecs,
+                              const BitList& sbits, const float* alpha, int32_t n_steer,
+                              const void* w, const float* b, const BitList& pbits,
+                              int32_t n_probe, float* logit, float* score, hipStream_t stream,
+                              const RouteIn* route = nullptr);
 
 hipError_t launch_sae_candidates(const uint16_t* h, int32_t d, int32_t T_max,
                                  const int32_t* app_count, const int32_t* tok_list,

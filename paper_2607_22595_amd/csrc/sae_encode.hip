@@ -46,6 +46,7 @@
 #include "common.hpp"
 #include "kernels.hpp"
 #include "launch.hpp"
+#include "route_list.hpp"
 
 namespace xmix {
 
@@ -146,55 +147,6 @@ sae_fold_kernel(const uint16_t* __restrict__ Wp, const uint16_t* __restrict__ b_
     if (lane_id() == 0) c_fold[j] = bf16_to_f32(b_enc[j]) - acc;
 }
 
-// In-kernel route build, for up to kRouteMaxT token slots (the decode
-// kernel below can take the place of the route-build launch of a step).
-// Same rules as the route-build kernel: T_valid is clamped to [0, T_max]
-// (error bit 2), a request id >= R_max routes nowhere (error bit 1).  The
-// ascending list of the tokens that carry `bit` is written to list_s and its
-// length returned; `mask_out`, if given, receives every slot's mask.  Every
-// thread of the workgroup takes part (two barriers per 512 slots).
-constexpr int kRouteMaxT = 1024;
-__device__ int32_t build_token_list(const int32_t* __restrict__ req, int32_t tv,
-                                    const uint32_t* __restrict__ sub, int32_t R_max,
-                                    uint32_t keep, int bit, int32_t T_max, int32_t* list_s,
-                                    int32_t* wtot, uint32_t* __restrict__ mask_out,
-                                    uint32_t& err) {
-    const int tid = threadIdx.x, wave = tid / kWave;
-    int32_t base = 0;
-    for (int32_t c0 = 0; c0 < T_max; c0 += kEncThreads) {
-        const int32_t t = c0 + tid;
-        uint32_t mask = 0;
-        if (t < tv) {
-            const int32_t r = req[t];
-            if (r >= R_max) err |= 1u;
-            else if (r >= 0) mask = sub[r] & keep;
-        }
-        if (mask_out && t < T_max) mask_out[t] = mask;
-        const bool has = (mask >> bit) & 1u;
-        const uint64_t bal = wave_ballot(has);
-        if (lane_id() == 0) wtot[wave] = __popcll(bal);
-        __syncthreads();
-        int32_t before = 0, total = 0;
-#pragma unroll
-        for (int w = 0; w < kEncWaves; ++w) {
-            const int32_t c = wtot[w];
-            before += (w < wave) ? c : 0;
-            total += c;
-        }
-        if (has) list_s[base + before + lanes_below(bal)] = t;
-        base += total;
-        __syncthreads();  // wtot is rewritten by the next chunk
-    }
-    return base;
-}
-
-// Publishes one app's list (padded with -1) and count, as the route build does.
-__device__ void publish_token_list(const int32_t* list_s, int32_t n, int32_t T_max,
-                                   int32_t* __restrict__ list_g, int32_t* __restrict__ count_g) {
-    for (int32_t i = threadIdx.x; i < T_max; i += kEncThreads) list_g[i] = i < n ? list_s[i] : -1;
-    if (threadIdx.x == 0) *count_g = n;
-}
-
 // ---------------------------------------------- GEMM + candidate emission
 __global__ void __launch_bounds__(kEncThreads, 1)
 sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
@@ -226,34 +178,27 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     const int32_t* tl = tok_list;
     int cnt = 0;
     if (r_req) {  // uniform
-        int32_t tv = *r_tvalid;
         uint32_t err = 0;
-        if (tv < 0 || tv > r_Tmax) {
-            err |= 2u;
-            tv = tv < 0 ? 0 : r_Tmax;
-        }
+        const int32_t tv = clamp_t_valid(*r_tvalid, r_Tmax, err);
         const uint32_t keep = r_napps >= 32 ? 0xFFFFFFFFu : ((1u << r_napps) - 1u);
         const int own = blockIdx.x;
         uint32_t* masks = own == 0 ? r_mask : nullptr;
         if (own < r_napps && own != r_bit) {
-            const int32_t n = build_token_list(r_req, tv, r_sub, r_Rmax, keep, own, r_Tmax,
-                                               list_s, rtot_s, masks, err);
+            const int32_t n = build_token_list<kEncThreads>(r_req, tv, r_sub, r_Rmax, keep, own,
+                                                            r_Tmax, list_s, rtot_s, masks, err);
             masks = nullptr;
-            publish_token_list(list_s, n, r_Tmax, r_lists + static_cast<int64_t>(own) * r_Tmax,
-                               r_count + own);
+            publish_token_list<kEncThreads>(list_s, n, r_Tmax,
+                                            r_lists + static_cast<int64_t>(own) * r_Tmax,
+                                            r_count + own);
             __syncthreads();  // list_s is rebuilt below
         }
-        cnt = build_token_list(r_req, tv, r_sub, r_Rmax, keep, r_bit, r_Tmax, list_s, rtot_s,
-                               masks, err);
+        cnt = build_token_list<kEncThreads>(r_req, tv, r_sub, r_Rmax, keep, r_bit, r_Tmax,
+                                            list_s, rtot_s, masks, err);
         if (own == r_bit)
-            publish_token_list(list_s, cnt, r_Tmax, r_lists + static_cast<int64_t>(r_bit) * r_Tmax,
-                               r_count + r_bit);
-        if (own == 0) {
-            uint32_t e = err;
-#pragma unroll
-            for (int off = 32; off >= 1; off >>= 1) e |= __shfl_xor(e, off, kWave);
-            if (lane_id() == 0 && e != 0) atomicOr(r_err, e);
-        }
+            publish_token_list<kEncThreads>(list_s, cnt, r_Tmax,
+                                            r_lists + static_cast<int64_t>(r_bit) * r_Tmax,
+                                            r_count + r_bit);
+        if (own == 0) publish_error(err, r_err);
         tl = list_s;
     } else {
         cnt = *app_count;

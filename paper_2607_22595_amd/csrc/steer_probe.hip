@@ -8,9 +8,15 @@
 // same reductions), so the results are bit-identical to a token-mode probe
 // call followed by a steering call.  One workgroup per token slot; a row
 // with neither kind of bit returns after reading its mask word.
+//
+// With r_tvalid given, the kernel also builds the step's routing (in place
+// of a route-build launch): each workgroup computes its token's mask
+// itself and writes it, and workgroup a < n_apps publishes app a's token
+// list and count (workgroup 0 also the error word).
 #include "common.hpp"
 #include "kernels.hpp"
 #include "launch.hpp"
+#include "route_list.hpp"
 
 namespace xmix {
 
@@ -24,10 +30,33 @@ steer_probe_kernel(void* __restrict__ h, int32_t d, int32_t T_max,
                    const void* __restrict__ vecs, BitList sbits, const float* __restrict__ alpha,
                    int32_t n_steer, const void* __restrict__ w, const float* __restrict__ b,
                    BitList pbits, int32_t n_probe, float* __restrict__ logit,
-                   float* __restrict__ score) {
+                   float* __restrict__ score, const int32_t* __restrict__ r_tvalid,
+                   const uint32_t* __restrict__ r_sub, int32_t r_Rmax, int32_t r_napps,
+                   uint32_t* __restrict__ r_mask, int32_t* __restrict__ r_count,
+                   int32_t* __restrict__ r_lists, uint32_t* __restrict__ r_err) {
     __shared__ float red[kFuseWaves][MAXP];
+    __shared__ int32_t list_s[kRouteMaxT];
+    __shared__ int32_t rtot_s[kFuseWaves];
     const int32_t t = blockIdx.x;
-    const uint32_t mask = tok_mask[t];
+    uint32_t mask;
+    if (r_tvalid) {  // uniform
+        uint32_t err = 0;
+        const int32_t tv = clamp_t_valid(*r_tvalid, T_max, err);
+        const uint32_t keep = r_napps >= 32 ? 0xFFFFFFFFu : ((1u << r_napps) - 1u);
+        if (t < r_napps) {
+            const int32_t n = build_token_list<kFuseThreads>(req, tv, r_sub, r_Rmax, keep, t,
+                                                             T_max, list_s, rtot_s, nullptr, err);
+            publish_token_list<kFuseThreads>(list_s, n, T_max,
+                                             r_lists + static_cast<int64_t>(t) * T_max,
+                                             r_count + t);
+            if (t == 0) publish_error(err, r_err);  // its pass saw every slot
+        }
+        uint32_t unused = 0;
+        mask = slot_mask(req, t, tv, r_sub, r_Rmax, keep, unused);
+        if (threadIdx.x == 0) r_mask[t] = mask;
+    } else {
+        mask = tok_mask[t];
+    }
     uint32_t ss = 0, sp = 0;
     for (int s = 0; s < n_steer; ++s) ss |= ((mask >> sbits.bit[s]) & 1u) << s;
     for (int p = 0; p < n_probe; ++p) sp |= ((mask >> pbits.bit[p]) & 1u) << p;
@@ -138,24 +167,29 @@ static hipError_t launch_steer_probe_t(void* h, int32_t d, int32_t T_max,
                                        const void* vecs, const BitList& sbits,
                                        const float* alpha, int32_t n_steer, const void* w,
                                        const float* b, const BitList& pbits, int32_t n_probe,
-                                       float* logit, float* score, hipStream_t stream) {
+                                       float* logit, float* score, const RouteIn& r,
+                                       hipStream_t stream) {
     dim3 g(T_max), blk(kFuseThreads);
     if (n_probe <= 4)
         hipLaunchKernelGGL((steer_probe_kernel<BF16, 4>), g, blk, 0, stream, h, d, T_max,
                            tok_mask, req, vecs, sbits, alpha, n_steer, w, b, pbits, n_probe,
-                           logit, score);
+                           logit, score, r.T_valid, r.sub, r.R_max, r.n_apps, r.tok_mask,
+                           r.app_count, r.app_tokens, r.err_word);
     else if (n_probe <= 8)
         hipLaunchKernelGGL((steer_probe_kernel<BF16, 8>), g, blk, 0, stream, h, d, T_max,
                            tok_mask, req, vecs, sbits, alpha, n_steer, w, b, pbits, n_probe,
-                           logit, score);
+                           logit, score, r.T_valid, r.sub, r.R_max, r.n_apps, r.tok_mask,
+                           r.app_count, r.app_tokens, r.err_word);
     else if (n_probe <= 16)
         hipLaunchKernelGGL((steer_probe_kernel<BF16, 16>), g, blk, 0, stream, h, d, T_max,
                            tok_mask, req, vecs, sbits, alpha, n_steer, w, b, pbits, n_probe,
-                           logit, score);
+                           logit, score, r.T_valid, r.sub, r.R_max, r.n_apps, r.tok_mask,
+                           r.app_count, r.app_tokens, r.err_word);
     else
         hipLaunchKernelGGL((steer_probe_kernel<BF16, 32>), g, blk, 0, stream, h, d, T_max,
                            tok_mask, req, vecs, sbits, alpha, n_steer, w, b, pbits, n_probe,
-                           logit, score);
+                           logit, score, r.T_valid, r.sub, r.R_max, r.n_apps, r.tok_mask,
+                           r.app_count, r.app_tokens, r.err_word);
     return hipGetLastError();
 }
 
@@ -163,11 +197,26 @@ hipError_t launch_steer_probe(void* h, bool bf16, int32_t d, int32_t T_max,
                               const uint32_t* tok_mask, const int32_t* req, const void* vecs,
                               const BitList& sbits, const float* alpha, int32_t n_steer,
                               const void* w, const float* b, const BitList& pbits,
-                              int32_t n_probe, float* logit, float* score, hipStream_t stream) {
+                              int32_t n_probe, float* logit, float* score, hipStream_t stream,
+                              const RouteIn* route) {
+    RouteIn r{};
+    if (route) {
+        if (T_max > kRouteMaxT || T_max < route->n_apps) {
+            // the kernel cannot route this batch: the route-build launch first
+            const hipError_t e = launch_route_build(route->req, route->T_valid, route->sub,
+                                                    route->R_max, T_max, route->n_apps,
+                                                    route->tok_mask, route->app_count,
+                                                    route->app_tokens, route->err_word, stream);
+            if (e != hipSuccess) return e;
+        } else {
+            r = *route;
+        }
+    }
     return bf16 ? launch_steer_probe_t<true>(h, d, T_max, tok_mask, req, vecs, sbits, alpha,
-                                             n_steer, w, b, pbits, n_probe, logit, score, stream)
+                                             n_steer, w, b, pbits, n_probe, logit, score, r,
+                                             stream)
                 : launch_steer_probe_t<false>(h, d, T_max, tok_mask, req, vecs, sbits, alpha,
-                                              n_steer, w, b, pbits, n_probe, logit, score,
+                                              n_steer, w, b, pbits, n_probe, logit, score, r,
                                               stream);
 }
 

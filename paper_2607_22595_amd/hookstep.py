@@ -7,8 +7,8 @@ order for every layer:
 
   1. route build (once per step: the batch and subscriptions are shared by
      all hooked layers; when the first layer's first consumer of the routing
-     is an SAE encode and the batch has at most 1024 slots, that encode's
-     kernel builds the routing itself, one launch instead of two);
+     is an SAE encode, or its fused probes + steering pass, that kernel
+     builds the routing itself: one launch instead of two);
   2. reads of the activation as the model produced it: per-token probes,
      mean-pooled probes, SAE encodes;
   3. writes: steering, then each SAE app's clamp-decode;
@@ -35,7 +35,7 @@ from . import (XMIX_PROBE_LAST, XMIX_PROBE_MEAN, XMIX_PROBE_TOKEN, Ring, Route, 
                sae_encode_workspace, xmix_probe_score, xmix_readback_compact,
                xmix_route_build, xmix_sae_clamp_decode, xmix_sae_encode_candidates,
                xmix_sae_encode_topk, xmix_sae_encode_topk_ring, xmix_sae_fold_bias,
-               xmix_route_sae_encode_candidates, xmix_sae_merge_topk,
+               xmix_route_sae_encode_candidates, xmix_route_steer_probe, xmix_sae_merge_topk,
                xmix_sae_merge_topk_ring, xmix_sae_pack_encoder, xmix_steer_apply,
                xmix_steer_probe)
 
@@ -167,10 +167,17 @@ class HookStep:
         before and right after the encode GEMM stage of each SAE app (e.g. to
         record timing events); the SAE call is then issued as its two stages,
         which enqueues the same kernels."""
+        # the kernel that first reads the routing builds it when it can: the
+        # first layer's first SAE encode, or its fused probes + steering pass
+        # when that is the layer's only read
         first = self.layers[0] if self.layers else None
         route_in_encode = (self.fuse_route and first is not None and not first.probes
                            and len(first.saes) > 0 and self.wl.T_max <= 1024)
-        if not route_in_encode:
+        route_in_pass = (self.fuse_route and self.fuse_steer_probe and first is not None
+                         and not first.saes and first.steer_v is not None
+                         and len(first.probes) == 1
+                         and first.probes[0].mode == XMIX_PROBE_TOKEN)
+        if not (route_in_encode or route_in_pass):
             xmix_route_build(self.req, self.T_valid, self.sub, self.route, self.err, stream)
         for li, lay in enumerate(self.layers):
             fused = None  # the token probes that run in one pass with the steering
@@ -211,7 +218,11 @@ class HookStep:
                 else:
                     xmix_sae_encode_topk(lay.h, self.route, s.bit, s.W_enc, s.b_enc, s.b_dec,
                                          s.c_fold, s.k, s.idx, s.val, s.ws, stream)
-            if fused is not None:
+            if fused is not None and route_in_pass and li == 0:
+                xmix_route_steer_probe(self.req, self.T_valid, self.sub, self.route, self.err,
+                                       lay.h, lay.steer_v, lay.steer_bits, self.alpha, fused.w,
+                                       fused.b, fused.bits, fused.logit, fused.score, stream)
+            elif fused is not None:
                 xmix_steer_probe(lay.h, self.route, self.req, lay.steer_v, lay.steer_bits,
                                  self.alpha, fused.w, fused.b, fused.bits, fused.logit,
                                  fused.score, stream)

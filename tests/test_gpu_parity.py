@@ -244,6 +244,59 @@ def _steer_probe_case(px, wl, layer=0):
     check_probe(lg, sg, lr, sr, written, np.abs(wv) @ np.abs(hv).T)
 
 
+@pytest.mark.parametrize("d,T,t_valid,bad_ids", [
+    (4096, 256, 256, False),    # the 8B-shaped decode layer
+    (256, 300, 290, True),      # padding and bad request ids
+    (256, 40, 45, False),       # T_valid above T_max (error bit 2)
+    (256, 6, 6, False),         # fewer slots than apps: a route launch first
+    (256, 1100, 1100, True)])   # over 1024 slots: a route launch first
+def test_route_built_inside_the_steer_probe_pass(px, d, T, t_valid, bad_ids):
+    """xmix_route_steer_probe leaves the route, the error word, the rows and
+    the probe outputs exactly as xmix_route_build followed by
+    xmix_steer_probe; the routing is also checked against the oracle."""
+    wl = synth.make("c2", d=d, T=T, n_layers=1)
+    L = wl.layers[0]
+    rng = np.random.default_rng(T)
+    req = wl.req.copy()
+    if bad_ids:
+        req[rng.choice(T, 7, replace=False)] = wl.sub.size + 3
+        req[rng.choice(T, 5, replace=False)] = -1
+    sub = wl.sub | np.uint32(1 << 30)   # a bit beyond n_apps is dropped
+    ps = [p for p in L.probes if p.mode == "token"]
+    sbits, pbits = [q.bit for q in L.steer], [q.bit for q in ps]
+    vd = dev_bits(np.stack([q.v for q in L.steer]))
+    wd = dev_bits(np.stack([q.w for q in ps]))
+    bd = torch.tensor([q.b for q in ps], dtype=torch.float32, device="cuda")
+    alpha = torch.from_numpy(wl.alpha).cuda()
+    tv = torch.tensor([t_valid], dtype=torch.int32, device="cuda")
+    reqd, subd = dev_i32(req), dev_i32(sub)
+    outs = []
+    for fused in (False, True):
+        rt = px.Route(T, wl.n_apps)
+        rt.tok_mask.fill_(-5)
+        rt.app_count.fill_(-5)
+        rt.app_tokens.fill_(-5)
+        err = torch.zeros(1, dtype=torch.int32, device="cuda")
+        h = dev_bits(L.h)
+        lo = torch.full((len(ps), T), float("nan"), device="cuda")
+        so = torch.full((len(ps), T), float("nan"), device="cuda")
+        if fused:
+            px.xmix_route_steer_probe(reqd, tv, subd, rt, err, h, vd, sbits, alpha, wd, bd, pbits,
+                                      lo, so)
+        else:
+            px.xmix_route_build(reqd, tv, subd, rt, err)
+            px.xmix_steer_probe(h, rt, reqd, vd, sbits, alpha, wd, bd, pbits, lo, so)
+        torch.cuda.synchronize()
+        outs.append((rt.tok_mask.cpu().numpy().view(np.uint32), rt.app_count.cpu().numpy(),
+                     rt.app_tokens.cpu().numpy(), int(err.item()), torch_bits(h),
+                     lo.cpu().numpy().view(np.uint32), so.cpu().numpy().view(np.uint32)))
+    for a, b in zip(*outs):
+        assert np.array_equal(np.asarray(a), np.asarray(b))
+    tm, cnt, lists, e = oracle.route(req, t_valid, sub, wl.n_apps)
+    assert np.array_equal(outs[1][0], tm) and np.array_equal(outs[1][1], cnt)
+    assert np.array_equal(outs[1][2], lists) and outs[1][3] == e
+
+
 def test_steer_probe_fused_toy_fp32(px):
     _steer_probe_case(px, synth.make("c1"))
 
