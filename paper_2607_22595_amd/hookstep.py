@@ -171,8 +171,13 @@ class HookStep:
         # first layer's first SAE encode, or its fused probes + steering pass
         # when that is the layer's only read
         first = self.layers[0] if self.layers else None
-        route_in_encode = (self.fuse_route and first is not None and not first.probes
-                           and len(first.saes) > 0 and self.wl.T_max <= 1024)
+        # the first layer's token probes, when they run fused with its
+        # steering, come after its SAE encodes
+        fused_only = first is not None and (not first.probes or (
+            self.fuse_steer_probe and first.steer_v is not None and len(first.probes) == 1
+            and first.probes[0].mode == XMIX_PROBE_TOKEN))
+        route_in_encode = (self.fuse_route and fused_only and len(first.saes) > 0
+                           and self.wl.T_max <= 1024)
         route_in_pass = (self.fuse_route and self.fuse_steer_probe and first is not None
                          and not first.saes and first.steer_v is not None
                          and len(first.probes) == 1
