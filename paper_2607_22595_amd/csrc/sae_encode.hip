@@ -998,28 +998,6 @@ __device__ __forceinline__ void wave_select_take(const uint32_t* key, const int3
     *wi = lane < base ? stage_i[lane] : 0x7FFFFFFF;
 }
 
-// Sorts one (key, latent) pair per lane across the wave: key descending,
-// latent ascending (bitonic network over shuffles).
-__device__ __forceinline__ void wave_sort_desc(uint32_t& key, int32_t& idx) {
-    const int lane = lane_id();
-#pragma unroll
-    for (int size = 2; size <= kWave; size <<= 1) {
-#pragma unroll
-        for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            const uint32_t ok = static_cast<uint32_t>(__shfl_xor(static_cast<int>(key), stride, kWave));
-            const int32_t oi = __shfl_xor(idx, stride, kWave);
-            const bool mine_better = key > ok || (key == ok && idx < oi);
-            const bool first_half = (lane & stride) == 0;
-            const bool descending = (lane & size) == 0;
-            const bool keep_better = first_half == descending;
-            if (keep_better != mine_better) {
-                key = ok;
-                idx = oi;
-            }
-        }
-    }
-}
-
 // Optional readback of the merged rows into a ring (same row format and
 // head protocol as the readback compaction).
 struct RingOut {
@@ -1083,7 +1061,8 @@ __device__ __forceinline__ float latent_dot(const uint16_t* __restrict__ Wp,
 // loaded together, so the gather costs one memory round trip), a prefix
 // over the workgroup places them in an LDS pool, the workgroup selects the
 // k best of it (radix select) and wave 0 checks the certificate; a failed
-// check is repaired by the whole workgroup; wave 0 then sorts and writes.
+// check is repaired by the whole workgroup; wave 0 then writes each winner
+// at its rank.
 __global__ void __launch_bounds__(kMergeThreads)
 sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ tile_cnt,
                  const float* __restrict__ tile_tau, int32_t n_mt, int32_t cap,
@@ -1437,11 +1416,23 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
         }
     }
     if (wave != 0) return;
-    // order the k winners by (value desc, index asc) and write them
-    wave_sort_desc(wk, wi);
+    // write the k winners in the order (value desc, index asc): each lane
+    // counts the winners that come before its own (the entries are
+    // distinct), reading them back from LDS in broadcast
+    if (lane < k) {
+        K2[lane] = wk;
+        I2[lane] = wi;
+    }
+    wave_sync();
+    const uint64_t mine = (static_cast<uint64_t>(wk) << 32) | static_cast<uint32_t>(~wi);
+    int rank = 0;
+    for (int j = 0; j < k; ++j) {
+        const uint64_t other = (static_cast<uint64_t>(K2[j]) << 32) | static_cast<uint32_t>(~I2[j]);
+        rank += other > mine ? 1 : 0;
+    }
     const uint16_t vb = f32_to_bf16_rne(fmaxf(key_f32(wk), 0.0f));
     if (lane < k) {
-        const int64_t o = static_cast<int64_t>(t) * k + lane;
+        const int64_t o = static_cast<int64_t>(t) * k + rank;
         idx_out[o] = wi;
         val_out[o] = vb;
     }
@@ -1459,8 +1450,8 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
                 reinterpret_cast<int32_t*>(row)[lane] = hdr;
             }
             if (lane < k) {
-                reinterpret_cast<int32_t*>(row + 16)[lane] = wi;
-                reinterpret_cast<uint16_t*>(row + 16 + 4 * k)[lane] = vb;
+                reinterpret_cast<int32_t*>(row + 16)[rank] = wi;
+                reinterpret_cast<uint16_t*>(row + 16 + 4 * k)[rank] = vb;
             }
         }
         if (lane == 0) ring_ticket(ring, h0, cnt);
