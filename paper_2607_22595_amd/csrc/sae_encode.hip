@@ -588,6 +588,7 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
     __shared__ float red1[2][kGemmTok];
     __shared__ float red2[2][kGemmTok];
     __shared__ int cnt_s[kGemmTok];
+    __shared__ int cnt2_s[2][kGemmTok];
 
     // Tile order: launch slot L runs on XCD L % 8, which owns the latent
     // tiles [x*M8, (x+1)*M8) and walks them in blocks of 8 token tiles x 4
@@ -769,108 +770,144 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
     // ---------------------------------------------------------- epilogue
     // acc[a][nb][r] holds latent 128*wm + 32*a + 8*(r/4) + 4*g + r%4 of
     // token 128*wn + 32*nb + j32; lanes j32 and j32 + 32 of waves (0, wn)
-    // and (1, wn) together hold the 256 latents of one token.  The tokens of
-    // one nb are finished at a time, so only their 64 values per lane need
-    // vector registers.  The count pass keeps a bit mask of the lane's
-    // values >= tau; the values are parked in the (now idle) stage buffers
-    // so that the few selected ones are fetched by index, one per round.
+    // and (1, wn) together hold the 256 latents of one token.  The four
+    // token groups nb of a wave go through each phase together, so the
+    // waves meet once for the statistics and twice per refinement round
+    // (not once per group) and the groups' independent work fills the gaps
+    // of a wave that has its SIMD to itself.  Each token's threshold follows
+    // the same sequence of guesses as when its group is finished alone: the
+    // rounds go on while any token of the tile is outside the window, and a
+    // token inside it keeps its threshold.  The count pass keeps a bit mask
+    // of the lane's values >= tau; for the emission a group's values are
+    // parked in the wave's own part of the (now idle) stage buffers, so that
+    // the few selected ones are fetched by index.
     cnt_s[tid] = 0;
-    float* park = reinterpret_cast<float*>(wave == 0 ? wsA : wave == 1 ? wsB : wave == 2 ? wsC : wsD);
+    float* park[2] = {reinterpret_cast<float*>(wave == 0 ? wsA : wave == 1 ? wsB : wave == 2 ? wsC : wsD),
+                      reinterpret_cast<float*>(wave == 0 ? xsA : wave == 1 ? xsB : wave == 2 ? xsC : xsD)};
+    // park the values of group nb in buffer nb % 2 (16-byte groups,
+    // lane-contiguous, so the stores are conflict-free)
+    auto park_group = [&](int nb) __attribute__((always_inline)) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+            reinterpret_cast<float4*>(park[nb & 1])[q * 64 + lane] =
+                make_float4(acc[q >> 2][nb][4 * (q & 3)], acc[q >> 2][nb][4 * (q & 3) + 1],
+                            acc[q >> 2][nb][4 * (q & 3) + 2], acc[q >> 2][nb][4 * (q & 3) + 3]);
+    };
+    park_group(0);
+    park_group(1);
+    // mean and variance over the tile's 256 latents, per token
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
-        const int n = 128 * wn + 32 * nb + j32;
-        float v[64];
+        float s1 = 0.0f, s2 = 0.0f;
 #pragma unroll
         for (int a = 0; a < 4; ++a)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) v[16 * a + r] = acc[a][nb][r];
-        // park the values in LDS (16-byte groups, lane-contiguous, so the
-        // stores are conflict-free) for the emission below
-#pragma unroll
-        for (int q = 0; q < 16; ++q)
-            reinterpret_cast<float4*>(park)[q * 64 + lane] =
-                make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
-        // mean and variance over the tile's 256 latents
-        float s1 = 0.0f, s2 = 0.0f;
-#pragma unroll
-        for (int i = 0; i < 64; ++i) {
-            s1 += v[i];
-            s2 = fmaf(v[i], v[i], s2);
-        }
+            for (int r = 0; r < 16; ++r) {
+                s1 += acc[a][nb][r];
+                s2 = fmaf(acc[a][nb][r], acc[a][nb][r], s2);
+            }
         s1 += __shfl_xor(s1, 32, kWave);
         s2 += __shfl_xor(s2, 32, kWave);
-        __syncthreads();  // red1/red2 and the parked values are reused
         if (g == 0) {
-            red1[wm][n] = s1;
-            red2[wm][n] = s2;
+            red1[wm][128 * wn + 32 * nb + j32] = s1;
+            red2[wm][128 * wn + 32 * nb + j32] = s2;
         }
-        __syncthreads();
+    }
+    __syncthreads();
+    float tau[4], lo_b[4], hi_b[4];
+    uint32_t m0[4], m1[4];  // bit i: value i >= tau (m1: value 32 + i)
+    bool bad[4];
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+        const int n = 128 * wn + 32 * nb + j32;
         const float mu = (red1[0][n] + red1[1][n]) * (1.0f / 256.0f);
         const float sd = sqrtf(fmaxf((red2[0][n] + red2[1][n]) * (1.0f / 256.0f) - mu * mu, 0.0f));
-        float tau = mu + z_guess * sd;
-        float lo_b = -INFINITY, hi_b = INFINITY;
-        uint32_t m0 = 0, m1 = 0;  // bit i: v[i] >= tau (m1: v[32 + i])
-        bool gave_up = false;
-        auto count_at = [&](float t) __attribute__((always_inline)) {
-            m0 = 0;
-            m1 = 0;
+        tau[nb] = mu + z_guess * sd;
+        lo_b[nb] = -INFINITY;
+        hi_b[nb] = INFINITY;
+        bad[nb] = false;
+    }
+    auto count_at = [&](int nb) __attribute__((always_inline)) {
+        uint32_t b0 = 0, b1 = 0;
 #pragma unroll
-            for (int i = 0; i < 32; ++i) {
-                m0 |= (v[i] >= t ? 1u : 0u) << i;
-                m1 |= (v[32 + i] >= t ? 1u : 0u) << i;
-            }
-            return __popc(m0) + __popc(m1);
-        };
-        // count(pre >= tau) per token; refine tau until lo_cnt <= count <= cap
-        for (int it = 0; it < kRefineIters; ++it) {
-            const int c_lane = count_at(tau);
-            const float c = static_cast<float>(c_lane + __shfl_xor(c_lane, 32, kWave));
-            __syncthreads();  // red1 is reused
-            if (g == 0) red1[wm][n] = c;
-            __syncthreads();
-            const int cn = static_cast<int>(red1[0][n] + red1[1][n]);
-            bool bad = false;
+        for (int i = 0; i < 32; ++i) {
+            b0 |= (acc[i >> 4][nb][i & 15] >= tau[nb] ? 1u : 0u) << i;
+            b1 |= (acc[2 + (i >> 4)][nb][i & 15] >= tau[nb] ? 1u : 0u) << i;
+        }
+        m0[nb] = b0;
+        m1[nb] = b1;
+        return __popc(b0) + __popc(b1);
+    };
+    // count(pre >= tau) per token; refine tau until lo_cnt <= count <= cap.
+    // cnt2_s is written before the round's first barrier and read before its
+    // second, so one buffer serves every round.
+    bool gave_up = false;
+    for (int it = 0; it < kRefineIters; ++it) {
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) {
+            const int c_lane = count_at(nb);
+            const int c = c_lane + __shfl_xor(c_lane, 32, kWave);
+            if (g == 0) cnt2_s[wm][128 * wn + 32 * nb + j32] = c;
+        }
+        __syncthreads();
+        bool any_bad = false;
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) {
+            const int n = 128 * wn + 32 * nb + j32;
+            const int cn = cnt2_s[0][n] + cnt2_s[1][n];
+            bad[nb] = false;
             if (n < ntok) {
                 if (cn > cap) {
-                    lo_b = tau;
-                    bad = true;
+                    lo_b[nb] = tau[nb];
+                    bad[nb] = true;
                 } else if (cn < lo_cnt) {
-                    hi_b = tau;
-                    bad = true;
+                    hi_b[nb] = tau[nb];
+                    bad[nb] = true;
                 }
             }
-            if (bad) {
-                if (isfinite(lo_b) && isfinite(hi_b)) {
-                    tau = 0.5f * (lo_b + hi_b);
+            if (bad[nb]) {
+                if (isfinite(lo_b[nb]) && isfinite(hi_b[nb])) {
+                    tau[nb] = 0.5f * (lo_b[nb] + hi_b[nb]);
                 } else {
-                    const float step = ldexpf(0.25f * (fabsf(tau) + 1.0f), it);
-                    tau = isfinite(hi_b) ? tau - step : tau + step;
+                    const float step = ldexpf(0.25f * (fabsf(tau[nb]) + 1.0f), it);
+                    tau[nb] = isfinite(hi_b[nb]) ? tau[nb] - step : tau[nb] + step;
                 }
             }
-            if (!__syncthreads_or(bad)) break;
-            // out of iterations: a threshold whose count is known to be <= cap
-            if (it == kRefineIters - 1) {
-                if (bad) tau = hi_b;
-                gave_up = true;
-            }
+            any_bad = any_bad || bad[nb];
         }
-        if (gave_up) count_at(tau);
-        // emit every latent with pre >= tau: reserve the lane's slots with
-        // one LDS atomic, then write one selected (value, latent) pair per
-        // round, the value read back from where it was parked
-        if (n >= ntok) m0 = m1 = 0;
-        const int c = __popc(m0) + __popc(m1);
+        if (!__syncthreads_or(any_bad)) break;
+        // out of rounds: a threshold whose count is known to be <= cap
+        if (it == kRefineIters - 1) {
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb)
+                if (bad[nb]) tau[nb] = hi_b[nb];
+            gave_up = true;
+        }
+    }
+    if (gave_up) {
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) count_at(nb);
+    }
+    // emit every latent with pre >= tau: reserve the lane's slots with one
+    // LDS atomic, then write one selected (value, latent) pair per round,
+    // the value read back from where it was parked
+    const int lat0 = mt * 256 + 128 * wm + 4 * g;
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+        const int n = 128 * wn + 32 * nb + j32;
+        const float* pk = park[nb & 1];
+        uint32_t b0 = n < ntok ? m0[nb] : 0u, b1 = n < ntok ? m1[nb] : 0u;
+        const int c = __popc(b0) + __popc(b1);
         int slot = 0;
         if (c > 0) slot = atomicAdd(&cnt_s[n], c);
         const int64_t row = static_cast<int64_t>(n0 + n) * n_mt + mt;
         uint2* dst = cand + row * cap;
-        const int lat0 = mt * 256 + 128 * wm + 4 * g;
-        while (__builtin_amdgcn_read_exec() & wave_ballot((m0 | m1) != 0)) {
-            if ((m0 | m1) != 0) {
-                const int i = m0 ? __builtin_ctz(m0) : 32 + __builtin_ctz(m1);
-                if (m0) m0 &= m0 - 1;
-                else m1 &= m1 - 1;
-                const float val = park[((i >> 2) * 64 + lane) * 4 + (i & 3)];
+        while (__builtin_amdgcn_read_exec() & wave_ballot((b0 | b1) != 0)) {
+            if ((b0 | b1) != 0) {
+                const int i = b0 ? __builtin_ctz(b0) : 32 + __builtin_ctz(b1);
+                if (b0) b0 &= b0 - 1;
+                else b1 &= b1 - 1;
+                const float val = pk[((i >> 2) * 64 + lane) * 4 + (i & 3)];
                 if (slot < cap)
                     dst[slot] = make_uint2(__float_as_uint(val),
                                            static_cast<uint32_t>(lat0 + 32 * (i >> 4) +
@@ -878,7 +915,9 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
                 ++slot;
             }
         }
-        if (n < ntok && wm == 0 && g == 0) tile_tau[row] = tau;
+        if (n < ntok && wm == 0 && g == 0) tile_tau[row] = tau[nb];
+        // the wave's reads of this buffer precede these stores in its LDS queue
+        if (nb < 2) park_group(nb + 2);
     }
     __syncthreads();
     if (tid < ntok) tile_cnt[static_cast<int64_t>(n0 + tid) * n_mt + mt] = min(cnt_s[tid], cap);
