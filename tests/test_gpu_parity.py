@@ -416,10 +416,12 @@ def test_encode_prefill_gemm_no_subscribers(px):
     assert np.all(idx == -7)
 
 
-def test_encode_exact_ties_take_lower_index(px):
+@pytest.mark.parametrize("T", [40, 1100])
+def test_encode_exact_ties_take_lower_index(px, T):
     """Duplicated dictionary rows give bit-identical pre-activations; the
-    lower latent index must win, across tiles and inside one tile."""
-    wl = synth.make("c3", d=256, m=1024, k=16, T=40)
+    lower latent index must win, across tiles and inside one tile (40 token
+    slots run the decode kernel, 1100 the prefill GEMM)."""
+    wl = synth.make("c3", d=256, m=1024, k=16, T=T)
     sae = wl.layers[0].saes[0]
     W = sae.W_enc.copy()
     b = sae.b_enc.copy()
@@ -691,16 +693,18 @@ def to_bf16_bits(a):
         .numpy().view(np.uint16)
 
 
-@pytest.mark.parametrize("n_tied", [10, 20, 64])
-def test_encode_repair_of_tied_slices(px, n_tied):
+@pytest.mark.parametrize("n_tied,T", [(10, 6), (20, 6), (64, 6), (10, 1100), (64, 1100)])
+def test_encode_repair_of_tied_slices(px, n_tied, T):
     """n_tied slices whose 256 pre-activations are all exactly 40 (zero
     dictionary rows, bias 40), far above every other latent.  No threshold
     splits a tie, so these slices emit nothing and fail the certificate.
     10: the merge recomputes them one by one and its pool overflows on the
     way (compaction to the k best); 20: more than it repairs slice by
     slice, so every slice is recomputed; 64: nothing is emitted at all.
-    The k lowest latents of the tie win."""
-    d, m, k, T = 256, 16384, 64, 6
+    The k lowest latents of the tie win.  With 1100 token slots the prefill
+    GEMM runs, whose threshold search on a tied slice uses every refinement
+    round and then gives up."""
+    d, m, k = 256, 16384, 64
     wl = synth.make("c3", d=d, m=m, k=k, T=T, n_sub=T)
     sae = wl.layers[0].saes[0]
     W, b = sae.W_enc.copy(), sae.b_enc.copy()
