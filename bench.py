@@ -171,7 +171,9 @@ def run_stats(per_run, sizes, tokens_per_step, seed=0):
 
 
 def dictionary_copies(torch, W, min_bytes=1.5 * 2 ** 30):
-    n = max(STEPS_PER_GRAPH, int(np.ceil(min_bytes / (W.numel() * W.element_size()))))
+    """W (a packed dictionary) and enough device copies of it that a
+    rotation over them exceeds every cache."""
+    n = max(STEPS_PER_GRAPH, int(np.ceil(min_bytes / W.nbytes)))
     return [W] + [W.clone() for _ in range(n - 1)]
 
 

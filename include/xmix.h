@@ -109,6 +109,22 @@ typedef struct {
     int32_t row_bytes;
 } xmix_ring;
 
+/* Encoder dictionary of one SAE app in the library's tiled HBM layout
+ * (host struct; `pieces` is caller-owned device memory of m * d bf16).
+ * Only xmix_sae_pack_encoder fills it: it permutes a row-major [m, d]
+ * matrix into `pieces` and sets m, d and layout = XMIX_SAE_DICT_TILED.
+ * Every call that reads a dictionary takes this struct, never a bare
+ * pointer, and rejects (XMIX_E_INVAL) a struct whose layout tag is not
+ * XMIX_SAE_DICT_TILED or whose d differs from the activation width, so a
+ * row-major matrix cannot be passed by mistake. */
+#define XMIX_SAE_DICT_TILED 0x31504D58u  /* "XMP1" */
+typedef struct {
+    const uint16_t *pieces;
+    int32_t m;
+    int32_t d;
+    uint32_t layout;
+} xmix_sae_dict;
+
 const char *xmix_status_string(xmix_status s);
 const char *xmix_version(void);
 
@@ -258,15 +274,19 @@ xmix_status xmix_router_write(void *logits, xmix_dtype dt, int32_t n_experts,
  *   bit app_bits[p]:
  *   logit_out[p][r] = b[p] + mean_{t in span} (w[p,:] . h[t,:]) (the probe of
  *   the span's mean activation), score as above; outputs are [n_probe][R_max].
- *   The span sums are reduced in a fixed order (bit-reproducible).
+ *   Every token of the span counts, whatever its own mask holds (a
+ *   conditional filter may have cleared the bit on later tokens, or the span
+ *   may run past T_valid).  The span sums are reduced in a fixed order
+ *   (bit-reproducible).
  * mode XMIX_PROBE_LAST: the "last token" condition of a read (Sec. 4.1):
  *   for each request r with a non-empty span whose first token has bit
  *   app_bits[p], logit_out[p][r] = b[p] + w[p,:] . h[cu_seqlens[r+1]-1,:],
  *   score as above; outputs are [n_probe][R_max].
  * h [T_max, d] and w [n_probe, d] of dtype dt; b [n_probe] fp32;
- * app_bits host [n_probe]; cu_seqlens [R_max + 1] int32 (MEAN and LAST,
- * spans contiguous and inside [0, T_max]); the probe reads h as given (call
- * it before any write at the same hook).
+ * app_bits host [n_probe]; cu_seqlens [R_max + 1] int32 (MEAN and LAST:
+ * non-decreasing, spans contiguous; a span outside [0, T_max] is not
+ * written); the probe reads h as given (call it before any write at the
+ * same hook).
  * ws: device workspace of at least xmix_probe_workspace(...) bytes (may be
  * NULL when that is 0).  Requires 1 <= n_probe <= 32. */
 size_t xmix_probe_workspace(int32_t T_max, int32_t n_probe, int32_t mode);
@@ -285,8 +305,8 @@ xmix_status xmix_probe_score(const void *h, xmix_dtype dt, int32_t d, const xmix
  *   descending;  idx_out[t][q] = j,  val_out[t][q] = bf16(max(pre_j, 0)).
  * Rows t of idx_out/val_out ([T_max, k]) are written only for subscribed t.
  * h [T_max, d] bf16; b_enc [m], b_dec [d] bf16.
- * W_packed: the encoder dictionary in the library's tiled HBM layout, made
- * once per app by xmix_sae_pack_encoder from the row-major [m, d] matrix.
+ * dict: the encoder dictionary (m latents of width d) as packed once per app
+ * by xmix_sae_pack_encoder; dict->d must equal d.
  * c_fold [m] fp32, nullable: b_enc - W_enc . b_dec as produced by
  * xmix_sae_fold_bias.  With c_fold the call never reads b_enc or b_dec and
  * streams the dictionary once; with NULL it folds into the workspace first
@@ -295,12 +315,15 @@ xmix_status xmix_probe_score(const void *h, xmix_dtype dt, int32_t d, const xmix
  * exact.
  * Requires d % 256 == 0, m % 256 == 0, 1 <= k <= min(64, m),
  * (m / 256) * k <= 16384.
- * ws: at least xmix_sae_encode_workspace(T_max, d, m, k) bytes. */
+ * ws: at least xmix_sae_encode_workspace(T_max, d, m, k) bytes.
+ * Errors: XMIX_E_INVAL (null pointer, bad size, a dictionary struct not made
+ * by xmix_sae_pack_encoder or of another width), XMIX_E_UNSUPPORTED (too
+ * many candidates per token), XMIX_E_WORKSPACE. */
 size_t xmix_sae_encode_workspace(int32_t T_max, int32_t d, int32_t m, int32_t k);
 xmix_status xmix_sae_encode_topk(const uint16_t *h, int32_t d, const xmix_route *rt,
-                                 int32_t app_bit, const uint16_t *W_packed,
+                                 int32_t app_bit, const xmix_sae_dict *dict,
                                  const uint16_t *b_enc, const uint16_t *b_dec,
-                                 const float *c_fold, int32_t m, int32_t k,
+                                 const float *c_fold, int32_t k,
                                  int32_t *idx_out, uint16_t *val_out,
                                  void *ws, size_t ws_bytes, void *stream);
 
@@ -314,19 +337,20 @@ xmix_status xmix_sae_encode_topk(const uint16_t *h, int32_t d, const xmix_route 
  *               The top-k of the kept latents is the top-k of all m
  *               latents when its k-th value is >= every slice's tau (a
  *               latent left out lies below its slice's tau); otherwise the
- *               merge recomputes that token's m pre-activations and selects
- *               from them (same result, slower; it happens only when the
+ *               merge recomputes the slices that can hide a winner (those
+ *               whose tau lies above the k-th selected value) and selects
+ *               again (same result, slower; it happens only when the
  *               winners crowd into a few slices).
  * The same certificate lets a dictionary be split across devices by latent
  * slices: exchange the kept candidates and thresholds, then merge. */
 xmix_status xmix_sae_encode_candidates(const uint16_t *h, int32_t d, const xmix_route *rt,
-                                       int32_t app_bit, const uint16_t *W_packed,
+                                       int32_t app_bit, const xmix_sae_dict *dict,
                                        const uint16_t *b_enc, const uint16_t *b_dec,
-                                       const float *c_fold, int32_t m, int32_t k,
+                                       const float *c_fold, int32_t k,
                                        void *ws, size_t ws_bytes, void *stream);
 xmix_status xmix_sae_merge_topk(const uint16_t *h, int32_t d, const xmix_route *rt,
-                                int32_t app_bit, const uint16_t *W_packed,
-                                const float *c_fold, int32_t m, int32_t k,
+                                int32_t app_bit, const xmix_sae_dict *dict,
+                                const float *c_fold, int32_t k,
                                 int32_t *idx_out, uint16_t *val_out,
                                 void *ws, size_t ws_bytes, void *stream);
 
@@ -336,7 +360,7 @@ xmix_status xmix_sae_merge_topk(const uint16_t *h, int32_t d, const xmix_route *
  * Same effect as
  *   xmix_route_build(req_of_token, T_valid, sub_mask, R_max, rt, err_word)
  * followed by
- *   xmix_sae_encode_candidates(h, d, rt, app_bit, W_packed, ...):
+ *   xmix_sae_encode_candidates(h, d, rt, app_bit, dict, ...):
  * the route's tok_mask, app_count, app_tokens and err_word hold exactly what
  * the route build writes, and the candidates are the same.  Up to 1024
  * token slots the encode kernel builds the routing itself (every workgroup
@@ -347,9 +371,9 @@ xmix_status xmix_route_sae_encode_candidates(const int32_t *req_of_token, const 
                                              const uint32_t *sub_mask, int32_t R_max,
                                              const xmix_route *rt, uint32_t *err_word,
                                              const uint16_t *h, int32_t d, int32_t app_bit,
-                                             const uint16_t *W_packed, const uint16_t *b_enc,
+                                             const xmix_sae_dict *dict, const uint16_t *b_enc,
                                              const uint16_t *b_dec, const float *c_fold,
-                                             int32_t m, int32_t k, void *ws, size_t ws_bytes,
+                                             int32_t k, void *ws, size_t ws_bytes,
                                              void *stream);
 
 /* Encode + TopK with the readback of each encoded row fused in (the merge
@@ -362,32 +386,33 @@ xmix_status xmix_route_sae_encode_candidates(const int32_t *req_of_token, const 
  * ring->row_bytes must equal 16 + 6 * k.  Calls that overlap on one ring
  * race, as for xmix_readback_compact. */
 xmix_status xmix_sae_encode_topk_ring(const uint16_t *h, int32_t d, const xmix_route *rt,
-                                      int32_t app_bit, const uint16_t *W_packed,
+                                      int32_t app_bit, const xmix_sae_dict *dict,
                                       const uint16_t *b_enc, const uint16_t *b_dec,
-                                      const float *c_fold, int32_t m, int32_t k,
+                                      const float *c_fold, int32_t k,
                                       int32_t *idx_out, uint16_t *val_out, void *ws,
                                       size_t ws_bytes, const int32_t *req_of_token,
                                       int32_t layer_id, int32_t app_id, const xmix_ring *ring,
                                       void *stream);
 xmix_status xmix_sae_merge_topk_ring(const uint16_t *h, int32_t d, const xmix_route *rt,
-                                     int32_t app_bit, const uint16_t *W_packed,
-                                     const float *c_fold, int32_t m, int32_t k,
+                                     int32_t app_bit, const xmix_sae_dict *dict,
+                                     const float *c_fold, int32_t k,
                                      int32_t *idx_out, uint16_t *val_out, void *ws,
                                      size_t ws_bytes, const int32_t *req_of_token,
                                      int32_t layer_id, int32_t app_id, const xmix_ring *ring,
                                      void *stream);
 
 /* One-time repack of a row-major encoder dictionary W_enc [m, d] (bf16)
- * into the tiled layout the encode kernels stream (same bytes, permuted).
- * W_packed must not overlap W_enc.  Requires m % 256 == 0, d % 256 == 0. */
+ * into the tiled layout the encode kernels stream (same bytes, permuted),
+ * written to W_packed (device, m * d bf16, caller-owned, not overlapping
+ * W_enc).  *dict (host) is filled to describe W_packed; it stays valid as
+ * long as W_packed does.  Requires m % 256 == 0, d % 256 == 0. */
 xmix_status xmix_sae_pack_encoder(const uint16_t *W_enc, int32_t m, int32_t d,
-                                  uint16_t *W_packed, void *stream);
+                                  uint16_t *W_packed, xmix_sae_dict *dict, void *stream);
 
 /* One-time fold of the encoder biases, run when an SAE app is loaded:
- *   c_fold[j] = b_enc[j] - W_enc[j,:] . b_dec   (fp32, W given packed). */
-xmix_status xmix_sae_fold_bias(const uint16_t *W_packed, const uint16_t *b_enc,
-                               const uint16_t *b_dec, int32_t m, int32_t d,
-                               float *c_fold, void *stream);
+ *   c_fold[j] = b_enc[j] - W_enc[j,:] . b_dec   (fp32), c_fold [dict->m]. */
+xmix_status xmix_sae_fold_bias(const xmix_sae_dict *dict, const uint16_t *b_enc,
+                               const uint16_t *b_dec, float *c_fold, void *stream);
 
 /* ------------------------------------------------------- SAE clamp-decode
  * Feature clamp with the decoded delta added back (a Write whose payload
@@ -421,9 +446,11 @@ xmix_status xmix_sae_clamp_decode(uint16_t *h, int32_t d, const xmix_route *rt,
  * `capacity` rows of one call are written).
  * seg_rows  host [n_seg] device pointers; segment s of row t starts at
  *           seg_rows[s] + t * seg_bytes[s].
- * seg_bytes host [n_seg], each a positive multiple of 4;
+ * seg_bytes host [n_seg], each a positive even number (rows of any k:
+ *           an SAE row is idx[k] int32 then val[k] bf16);
  *           16 + sum(seg_bytes) must equal ring->row_bytes.
- * ring      host struct; slots 16-byte aligned, row_bytes % 16 == 0.
+ * ring      host struct; slots 4-byte aligned, head 8-byte aligned,
+ *           row_bytes even.  Segment rows must be 2-byte aligned.
  * Requires 1 <= n_seg <= 4. */
 xmix_status xmix_readback_compact(const void *const *seg_rows, const int32_t *seg_bytes,
                                   int32_t n_seg, const xmix_route *rt, int32_t app_bit,

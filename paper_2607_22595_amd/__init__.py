@@ -48,7 +48,16 @@ class XmixRing(ctypes.Structure):
                 ("capacity", ctypes.c_int32), ("row_bytes", ctypes.c_int32)]
 
 
+XMIX_SAE_DICT_TILED = 0x31504D58
+
+
+class XmixSaeDict(ctypes.Structure):
+    _fields_ = [("pieces", ctypes.c_void_p), ("m", ctypes.c_int32), ("d", ctypes.c_int32),
+                ("layout", ctypes.c_uint32)]
+
+
 _vp, _i32, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+_dp = ctypes.POINTER(XmixSaeDict)
 _st = ctypes.c_int
 _sigs = {
     "xmix_status_string": ([_st], ctypes.c_char_p),
@@ -75,23 +84,23 @@ _sigs = {
     "xmix_probe_score": ([_vp, _st, _i32, ctypes.POINTER(XmixRoute), _vp, _vp, _vp, _i32, _i32,
                           _vp, _i32, _vp, _vp, _vp, _sz, _vp], _st),
     "xmix_sae_encode_workspace": ([_i32, _i32, _i32, _i32], _sz),
-    "xmix_sae_encode_topk": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _vp, _vp,
-                              _i32, _i32, _vp, _vp, _vp, _sz, _vp], _st),
-    "xmix_sae_encode_candidates": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _vp,
-                                    _vp, _i32, _i32, _vp, _sz, _vp], _st),
+    "xmix_sae_encode_topk": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _dp, _vp, _vp, _vp,
+                              _i32, _vp, _vp, _vp, _sz, _vp], _st),
+    "xmix_sae_encode_candidates": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _dp, _vp, _vp,
+                                    _vp, _i32, _vp, _sz, _vp], _st),
     "xmix_route_sae_encode_candidates": ([_vp, _vp, _vp, _i32, ctypes.POINTER(XmixRoute), _vp,
-                                          _vp, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _i32, _vp,
-                                          _sz, _vp], _st),
-    "xmix_sae_merge_topk": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32, _i32,
-                             _vp, _vp, _vp, _sz, _vp], _st),
-    "xmix_sae_encode_topk_ring": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _vp,
-                                   _vp, _i32, _i32, _vp, _vp, _vp, _sz, _vp, _i32, _i32,
+                                          _vp, _i32, _i32, _dp, _vp, _vp, _vp, _i32, _vp, _sz,
+                                          _vp], _st),
+    "xmix_sae_merge_topk": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _dp, _vp, _i32, _vp,
+                             _vp, _vp, _sz, _vp], _st),
+    "xmix_sae_encode_topk_ring": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _dp, _vp, _vp,
+                                   _vp, _i32, _vp, _vp, _vp, _sz, _vp, _i32, _i32,
                                    ctypes.POINTER(XmixRing), _vp], _st),
-    "xmix_sae_merge_topk_ring": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32,
-                                  _i32, _vp, _vp, _vp, _sz, _vp, _i32, _i32,
+    "xmix_sae_merge_topk_ring": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _dp, _vp, _i32,
+                                  _vp, _vp, _vp, _sz, _vp, _i32, _i32,
                                   ctypes.POINTER(XmixRing), _vp], _st),
-    "xmix_sae_pack_encoder": ([_vp, _i32, _i32, _vp, _vp], _st),
-    "xmix_sae_fold_bias": ([_vp, _vp, _vp, _i32, _i32, _vp, _vp], _st),
+    "xmix_sae_pack_encoder": ([_vp, _i32, _i32, _vp, _dp, _vp], _st),
+    "xmix_sae_fold_bias": ([_dp, _vp, _vp, _vp, _vp], _st),
     "xmix_sae_clamp_decode": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32, _vp,
                                _i32, _vp, _vp, _i32, _vp, _vp], _st),
     "xmix_readback_compact": ([_vp, _vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _i32, _i32,
@@ -362,104 +371,135 @@ def sae_encode_workspace(T_max: int, d: int, m: int, k: int) -> int:
     return int(_lib.xmix_sae_encode_workspace(T_max, d, m, k))
 
 
-def xmix_sae_pack_encoder(W_enc, W_packed=None, stream=None):
+class SaeDict:
+    """An encoder dictionary packed by xmix_sae_pack_encoder: the device
+    buffer of m * d bf16 in the library's tiled layout (``packed``) and the
+    C descriptor that points at it (``struct``)."""
+
+    def __init__(self, packed: torch.Tensor, struct: XmixSaeDict):
+        self.packed = packed
+        self.struct = struct
+        self.m, self.d = int(struct.m), int(struct.d)
+
+    @property
+    def nbytes(self) -> int:
+        return self.packed.numel() * self.packed.element_size()
+
+    def clone(self) -> "SaeDict":
+        """A second device copy of the packed bytes with its own descriptor."""
+        p = self.packed.clone()
+        return SaeDict(p, XmixSaeDict(p.data_ptr(), self.m, self.d, self.struct.layout))
+
+    def ref(self):
+        return ctypes.byref(self.struct)
+
+
+def _dict(W) -> SaeDict:
+    if not isinstance(W, SaeDict):
+        raise TypeError("the encoder dictionary must come from xmix_sae_pack_encoder")
+    return W
+
+
+def xmix_sae_pack_encoder(W_enc, W_packed=None, stream=None) -> SaeDict:
     """Row-major bf16 W_enc [m, d] -> the tiled layout the encode streams.
-    Returns W_packed (same shape and dtype; only the byte order differs)."""
+    Returns the packed dictionary (a new device buffer unless W_packed, a
+    bf16 tensor of m * d elements, is given)."""
     m, d = W_enc.shape
     assert W_enc.dtype == torch.bfloat16
     if W_packed is None:
         W_packed = torch.empty_like(W_enc)
+    assert W_packed.dtype == torch.bfloat16 and W_packed.numel() == m * d
+    st = XmixSaeDict()
     _check("xmix_sae_pack_encoder", _lib.xmix_sae_pack_encoder(
-        _ptr(W_enc), m, d, _ptr(W_packed), _stream(stream)))
-    return W_packed
+        _ptr(W_enc), m, d, _ptr(W_packed), ctypes.byref(st), _stream(stream)))
+    return SaeDict(W_packed, st)
 
 
-def xmix_sae_fold_bias(W_enc, b_enc, b_dec, c_fold, stream=None):
-    """W_enc: the packed dictionary."""
-    m, d = W_enc.shape
-    assert W_enc.dtype == torch.bfloat16 and c_fold.dtype == torch.float32 and c_fold.numel() == m
+def xmix_sae_fold_bias(W: SaeDict, b_enc, b_dec, c_fold, stream=None):
+    W = _dict(W)
+    assert c_fold.dtype == torch.float32 and c_fold.numel() == W.m
     _check("xmix_sae_fold_bias", _lib.xmix_sae_fold_bias(
-        _ptr(W_enc), _ptr(b_enc), _ptr(b_dec), m, d, _ptr(c_fold), _stream(stream)))
+        W.ref(), _ptr(b_enc), _ptr(b_dec), _ptr(c_fold), _stream(stream)))
 
 
-def xmix_sae_encode_topk(h, route: Route, app_bit: int, W_enc, b_enc, b_dec, c_fold, k: int,
-                         idx_out, val_out, ws, stream=None):
-    """h bf16 [T_max, d]; W_enc bf16 [m, d] packed; c_fold fp32 [m] or None;
+def xmix_sae_encode_topk(h, route: Route, app_bit: int, W: SaeDict, b_enc, b_dec, c_fold,
+                         k: int, idx_out, val_out, ws, stream=None):
+    """h bf16 [T_max, d]; W the packed dictionary; c_fold fp32 [m] or None;
     idx_out int32 [T_max, k]; val_out bf16 [T_max, k]; ws uint8 workspace."""
     T_max, d = h.shape
-    m = W_enc.shape[0]
-    assert h.dtype == torch.bfloat16 and W_enc.dtype == torch.bfloat16
+    W = _dict(W)
+    assert h.dtype == torch.bfloat16
     assert idx_out.dtype == torch.int32 and idx_out.shape == (T_max, k)
     assert val_out.dtype == torch.bfloat16 and val_out.shape == (T_max, k)
     ws_bytes = ws.numel() * ws.element_size()
     _check("xmix_sae_encode_topk", _lib.xmix_sae_encode_topk(
-        _ptr(h), d, ctypes.byref(route.struct), app_bit, _ptr(W_enc), _ptr(b_enc), _ptr(b_dec),
-        _ptr(c_fold), m, k, _ptr(idx_out), _ptr(val_out), _ptr(ws), ws_bytes, _stream(stream)))
+        _ptr(h), d, ctypes.byref(route.struct), app_bit, W.ref(), _ptr(b_enc), _ptr(b_dec),
+        _ptr(c_fold), k, _ptr(idx_out), _ptr(val_out), _ptr(ws), ws_bytes, _stream(stream)))
 
 
-def xmix_sae_encode_topk_ring(h, route: Route, app_bit: int, W_enc, b_enc, b_dec, c_fold,
+def xmix_sae_encode_topk_ring(h, route: Route, app_bit: int, W: SaeDict, b_enc, b_dec, c_fold,
                               k: int, idx_out, val_out, ws, req_of_token, layer_id: int,
                               app_id: int, ring: Ring, stream=None):
     """xmix_sae_encode_topk with the ring readback of (idx, val) rows fused
     into the merge; ring.row_bytes must be 16 + 6 k."""
     T_max, d = h.shape
-    m = W_enc.shape[0]
-    assert h.dtype == torch.bfloat16 and W_enc.dtype == torch.bfloat16
+    W = _dict(W)
+    assert h.dtype == torch.bfloat16
     assert idx_out.dtype == torch.int32 and idx_out.shape == (T_max, k)
     assert val_out.dtype == torch.bfloat16 and val_out.shape == (T_max, k)
     assert req_of_token.dtype == torch.int32 and req_of_token.numel() == T_max
     _check("xmix_sae_encode_topk_ring", _lib.xmix_sae_encode_topk_ring(
-        _ptr(h), d, ctypes.byref(route.struct), app_bit, _ptr(W_enc), _ptr(b_enc), _ptr(b_dec),
-        _ptr(c_fold), m, k, _ptr(idx_out), _ptr(val_out), _ptr(ws), ws.numel() * ws.element_size(),
+        _ptr(h), d, ctypes.byref(route.struct), app_bit, W.ref(), _ptr(b_enc), _ptr(b_dec),
+        _ptr(c_fold), k, _ptr(idx_out), _ptr(val_out), _ptr(ws), ws.numel() * ws.element_size(),
         _ptr(req_of_token), layer_id, app_id, ctypes.byref(ring.struct), _stream(stream)))
 
 
-def xmix_sae_merge_topk_ring(h, route: Route, app_bit: int, W_enc, c_fold, k: int, idx_out,
+def xmix_sae_merge_topk_ring(h, route: Route, app_bit: int, W: SaeDict, c_fold, k: int, idx_out,
                              val_out, ws, req_of_token, layer_id: int, app_id: int, ring: Ring,
                              stream=None):
     """Stage 2 of the encode with the fused ring readback."""
     T_max, d = h.shape
-    m = W_enc.shape[0]
+    W = _dict(W)
     _check("xmix_sae_merge_topk_ring", _lib.xmix_sae_merge_topk_ring(
-        _ptr(h), d, ctypes.byref(route.struct), app_bit, _ptr(W_enc), _ptr(c_fold), m, k,
+        _ptr(h), d, ctypes.byref(route.struct), app_bit, W.ref(), _ptr(c_fold), k,
         _ptr(idx_out), _ptr(val_out), _ptr(ws), ws.numel() * ws.element_size(),
         _ptr(req_of_token), layer_id, app_id, ctypes.byref(ring.struct), _stream(stream)))
 
 
 def xmix_route_sae_encode_candidates(req_of_token, T_valid, sub_mask, route: Route, err_word, h,
-                                     app_bit: int, W_enc, b_enc, b_dec, c_fold, k: int, ws,
+                                     app_bit: int, W: SaeDict, b_enc, b_dec, c_fold, k: int, ws,
                                      stream=None):
     """Route build and the encode's candidates stage in one launch (up to
     1024 token slots): the same results as xmix_route_build followed by
     xmix_sae_encode_candidates."""
     T_max, d = h.shape
-    m = W_enc.shape[0]
-    assert T_max == route.T_max and h.dtype == torch.bfloat16 and W_enc.dtype == torch.bfloat16
+    W = _dict(W)
+    assert T_max == route.T_max and h.dtype == torch.bfloat16
     _check("xmix_route_sae_encode_candidates", _lib.xmix_route_sae_encode_candidates(
         _ptr(req_of_token), _ptr(T_valid), _ptr(sub_mask), sub_mask.numel(),
-        ctypes.byref(route.struct), _ptr(err_word), _ptr(h), d, app_bit, _ptr(W_enc),
-        _ptr(b_enc), _ptr(b_dec), _ptr(c_fold), m, k, _ptr(ws), ws.numel() * ws.element_size(),
+        ctypes.byref(route.struct), _ptr(err_word), _ptr(h), d, app_bit, W.ref(),
+        _ptr(b_enc), _ptr(b_dec), _ptr(c_fold), k, _ptr(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
 
 
-def xmix_sae_encode_candidates(h, route: Route, app_bit: int, W_enc, b_enc, b_dec, c_fold,
+def xmix_sae_encode_candidates(h, route: Route, app_bit: int, W: SaeDict, b_enc, b_dec, c_fold,
                                k: int, ws, stream=None):
     """Stage 1 of the encode: per-slice top-k candidates into `ws`."""
     T_max, d = h.shape
-    m = W_enc.shape[0]
-    assert h.dtype == torch.bfloat16 and W_enc.dtype == torch.bfloat16
+    W = _dict(W)
+    assert h.dtype == torch.bfloat16
     _check("xmix_sae_encode_candidates", _lib.xmix_sae_encode_candidates(
-        _ptr(h), d, ctypes.byref(route.struct), app_bit, _ptr(W_enc), _ptr(b_enc), _ptr(b_dec),
-        _ptr(c_fold), m, k, _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+        _ptr(h), d, ctypes.byref(route.struct), app_bit, W.ref(), _ptr(b_enc), _ptr(b_dec),
+        _ptr(c_fold), k, _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
-def xmix_sae_merge_topk(h, route: Route, app_bit: int, W_enc, c_fold, k: int, idx_out, val_out,
-                        ws, stream=None):
+def xmix_sae_merge_topk(h, route: Route, app_bit: int, W: SaeDict, c_fold, k: int, idx_out,
+                        val_out, ws, stream=None):
     """Stage 2 of the encode: exact top-k per token from the candidates."""
     T_max, d = h.shape
-    m = W_enc.shape[0]
+    W = _dict(W)
     _check("xmix_sae_merge_topk", _lib.xmix_sae_merge_topk(
-        _ptr(h), d, ctypes.byref(route.struct), app_bit, _ptr(W_enc), _ptr(c_fold), m, k,
+        _ptr(h), d, ctypes.byref(route.struct), app_bit, W.ref(), _ptr(c_fold), k,
         _ptr(idx_out), _ptr(val_out), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 

@@ -32,6 +32,14 @@ bool bits_ok(const int32_t* bits, int32_t n, int32_t n_apps, BitList* out) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// A dictionary struct made by xmix_sae_pack_encoder, of width d (d < 0:
+// any width).
+bool dict_ok(const xmix_sae_dict* w, int32_t d) {
+    return w && w->layout == XMIX_SAE_DICT_TILED && w->pieces && aligned16(w->pieces) &&
+           w->m >= 256 && w->m % 256 == 0 && w->d >= 256 && w->d % 256 == 0 &&
+           (d < 0 || w->d == d);
+}
+
 const int32_t* app_list(const xmix_route* rt, int32_t a) {
     return rt->app_tokens + static_cast<int64_t>(a) * rt->T_max;
 }
@@ -202,20 +210,28 @@ size_t xmix_sae_encode_workspace(int32_t T_max, int32_t d, int32_t m, int32_t k)
 }
 
 xmix_status xmix_sae_pack_encoder(const uint16_t* W_enc, int32_t m, int32_t d,
-                                  uint16_t* W_packed, void* stream) {
-    if (!W_enc || !W_packed || W_enc == W_packed || m < 256 || m % 256 != 0 || d < 256 ||
-        d % 256 != 0 || !aligned16(W_enc) || !aligned16(W_packed))
+                                  uint16_t* W_packed, xmix_sae_dict* dict, void* stream) {
+    if (!W_enc || !W_packed || !dict || W_enc == W_packed || m < 256 || m % 256 != 0 ||
+        d < 256 || d % 256 != 0 || !aligned16(W_enc) || !aligned16(W_packed))
         return XMIX_E_INVAL;
-    return launched(launch_sae_pack(W_enc, m, d, W_packed, as_stream(stream)));
+    const int64_t bytes = static_cast<int64_t>(m) * d * 2;
+    const char *a = reinterpret_cast<const char*>(W_enc), *b = reinterpret_cast<char*>(W_packed);
+    if (a < b + bytes && b < a + bytes) return XMIX_E_INVAL;  // overlap
+    const xmix_status st = launched(launch_sae_pack(W_enc, m, d, W_packed, as_stream(stream)));
+    if (st != XMIX_OK) return st;
+    dict->pieces = W_packed;
+    dict->m = m;
+    dict->d = d;
+    dict->layout = XMIX_SAE_DICT_TILED;
+    return XMIX_OK;
 }
 
-xmix_status xmix_sae_fold_bias(const uint16_t* W_enc, const uint16_t* b_enc,
-                               const uint16_t* b_dec, int32_t m, int32_t d, float* c_fold,
-                               void* stream) {
-    if (!W_enc || !b_enc || !b_dec || !c_fold || m < 256 || m % 256 != 0 || d < 256 ||
-        d % 256 != 0 || !aligned16(W_enc) || !aligned16(b_dec))
+xmix_status xmix_sae_fold_bias(const xmix_sae_dict* dict, const uint16_t* b_enc,
+                               const uint16_t* b_dec, float* c_fold, void* stream) {
+    if (!dict_ok(dict, -1) || !b_enc || !b_dec || !c_fold || !aligned16(b_dec))
         return XMIX_E_INVAL;
-    return launched(launch_sae_fold(W_enc, b_enc, b_dec, m, d, c_fold, as_stream(stream)));
+    return launched(launch_sae_fold(dict->pieces, b_enc, b_dec, dict->m, dict->d, c_fold,
+                                    as_stream(stream)));
 }
 
 }  // extern "C"
@@ -225,12 +241,13 @@ namespace {
 // Checks shared by the encode entry points; returns the folded-bias area
 // and the candidate area of the workspace.
 xmix_status encode_args(const uint16_t* h, int32_t d, const xmix_route* rt, int32_t app_bit,
-                        const uint16_t* W_enc, int32_t m, int32_t k, void* ws, size_t ws_bytes,
+                        const xmix_sae_dict* dict, int32_t k, void* ws, size_t ws_bytes,
                         float** fold, void** cand) {
     if (!route_ok(rt) || app_bit < 0 || app_bit >= rt->n_apps) return XMIX_E_INVAL;
-    if (h && (!aligned16(h) || d < 256 || d % 256 != 0)) return XMIX_E_INVAL;
-    if (W_enc && !aligned16(W_enc)) return XMIX_E_INVAL;
-    if (m < 256 || m % 256 != 0 || k < 1 || k > XMIX_MAX_TOPK || k > m) return XMIX_E_INVAL;
+    if (!h || !aligned16(h) || d < 256 || d % 256 != 0) return XMIX_E_INVAL;
+    if (!dict_ok(dict, d)) return XMIX_E_INVAL;
+    const int32_t m = dict->m;
+    if (k < 1 || k > XMIX_MAX_TOPK || k > m) return XMIX_E_INVAL;
     // the merge keeps (m / 256) * k candidates per token in registers
     if (static_cast<int64_t>(m / 256) * k > 64 * 256) return XMIX_E_UNSUPPORTED;
     const size_t need = xmix_sae_encode_workspace(rt->T_max, d, m, k);
@@ -246,43 +263,46 @@ xmix_status encode_args(const uint16_t* h, int32_t d, const xmix_route* rt, int3
 extern "C" {
 
 xmix_status xmix_sae_encode_candidates(const uint16_t* h, int32_t d, const xmix_route* rt,
-                                       int32_t app_bit, const uint16_t* W_enc,
+                                       int32_t app_bit, const xmix_sae_dict* dict,
                                        const uint16_t* b_enc, const uint16_t* b_dec,
-                                       const float* c_fold, int32_t m, int32_t k, void* ws,
+                                       const float* c_fold, int32_t k, void* ws,
                                        size_t ws_bytes, void* stream) {
-    if (!h || !W_enc) return XMIX_E_INVAL;
     if (!c_fold && (!b_enc || !b_dec || !aligned16(b_dec))) return XMIX_E_INVAL;
     float* fold;
     void* cand;
-    const xmix_status st = encode_args(h, d, rt, app_bit, W_enc, m, k, ws, ws_bytes, &fold, &cand);
+    const xmix_status st = encode_args(h, d, rt, app_bit, dict, k, ws, ws_bytes, &fold, &cand);
     if (st != XMIX_OK) return st;
     hipStream_t s = as_stream(stream);
+    const int32_t m = dict->m;
     if (!c_fold) {
-        if (launch_sae_fold(W_enc, b_enc, b_dec, m, d, fold, s) != hipSuccess) return XMIX_E_LAUNCH;
+        if (launch_sae_fold(dict->pieces, b_enc, b_dec, m, d, fold, s) != hipSuccess)
+            return XMIX_E_LAUNCH;
         c_fold = fold;
     }
     return launched(launch_sae_candidates(h, d, rt->T_max, rt->app_count + app_bit,
-                                          app_list(rt, app_bit), W_enc, c_fold, m, k, cand, s));
+                                          app_list(rt, app_bit), dict->pieces, c_fold, m, k,
+                                          cand, s));
 }
 
 xmix_status xmix_route_sae_encode_candidates(const int32_t* req_of_token, const int32_t* T_valid,
                                              const uint32_t* sub_mask, int32_t R_max,
                                              const xmix_route* rt, uint32_t* err_word,
                                              const uint16_t* h, int32_t d, int32_t app_bit,
-                                             const uint16_t* W_enc, const uint16_t* b_enc,
+                                             const xmix_sae_dict* dict, const uint16_t* b_enc,
                                              const uint16_t* b_dec, const float* c_fold,
-                                             int32_t m, int32_t k, void* ws, size_t ws_bytes,
+                                             int32_t k, void* ws, size_t ws_bytes,
                                              void* stream) {
     if (!req_of_token || !T_valid || !sub_mask || !err_word || R_max < 1) return XMIX_E_INVAL;
-    if (!h || !W_enc) return XMIX_E_INVAL;
     if (!c_fold && (!b_enc || !b_dec || !aligned16(b_dec))) return XMIX_E_INVAL;
     float* fold;
     void* cand;
-    const xmix_status st = encode_args(h, d, rt, app_bit, W_enc, m, k, ws, ws_bytes, &fold, &cand);
+    const xmix_status st = encode_args(h, d, rt, app_bit, dict, k, ws, ws_bytes, &fold, &cand);
     if (st != XMIX_OK) return st;
     hipStream_t s = as_stream(stream);
+    const int32_t m = dict->m;
     if (!c_fold) {
-        if (launch_sae_fold(W_enc, b_enc, b_dec, m, d, fold, s) != hipSuccess) return XMIX_E_LAUNCH;
+        if (launch_sae_fold(dict->pieces, b_enc, b_dec, m, d, fold, s) != hipSuccess)
+            return XMIX_E_LAUNCH;
         c_fold = fold;
     }
     RouteIn r;
@@ -297,41 +317,39 @@ xmix_status xmix_route_sae_encode_candidates(const int32_t* req_of_token, const 
     r.app_tokens = rt->app_tokens;
     r.err_word = err_word;
     return launched(launch_sae_candidates(h, d, rt->T_max, rt->app_count + app_bit,
-                                          app_list(rt, app_bit), W_enc, c_fold, m, k, cand, s,
-                                          &r));
+                                          app_list(rt, app_bit), dict->pieces, c_fold, m, k,
+                                          cand, s, &r));
 }
 
 xmix_status xmix_sae_merge_topk(const uint16_t* h, int32_t d, const xmix_route* rt,
-                                int32_t app_bit, const uint16_t* W_packed, const float* c_fold,
-                                int32_t m, int32_t k, int32_t* idx_out, uint16_t* val_out,
-                                void* ws, size_t ws_bytes, void* stream) {
-    if (!h || !W_packed || !idx_out || !val_out) return XMIX_E_INVAL;
+                                int32_t app_bit, const xmix_sae_dict* dict, const float* c_fold,
+                                int32_t k, int32_t* idx_out, uint16_t* val_out, void* ws,
+                                size_t ws_bytes, void* stream) {
+    if (!idx_out || !val_out) return XMIX_E_INVAL;
     float* fold;
     void* cand;
-    const xmix_status st =
-        encode_args(h, d, rt, app_bit, W_packed, m, k, ws, ws_bytes, &fold, &cand);
+    const xmix_status st = encode_args(h, d, rt, app_bit, dict, k, ws, ws_bytes, &fold, &cand);
     if (st != XMIX_OK) return st;
     return launched(launch_sae_merge(h, d, rt->T_max, rt->app_count + app_bit,
-                                     app_list(rt, app_bit), W_packed, c_fold ? c_fold : fold, m,
-                                     k, idx_out, val_out, cand, nullptr, as_stream(stream)));
+                                     app_list(rt, app_bit), dict->pieces,
+                                     c_fold ? c_fold : fold, dict->m, k, idx_out, val_out, cand,
+                                     nullptr, as_stream(stream)));
 }
 
 xmix_status xmix_sae_merge_topk_ring(const uint16_t* h, int32_t d, const xmix_route* rt,
-                                     int32_t app_bit, const uint16_t* W_packed,
-                                     const float* c_fold, int32_t m, int32_t k,
-                                     int32_t* idx_out, uint16_t* val_out, void* ws,
-                                     size_t ws_bytes, const int32_t* req_of_token,
-                                     int32_t layer_id, int32_t app_id, const xmix_ring* ring,
-                                     void* stream) {
-    if (!h || !W_packed || !idx_out || !val_out || !req_of_token || !ring) return XMIX_E_INVAL;
+                                     int32_t app_bit, const xmix_sae_dict* dict,
+                                     const float* c_fold, int32_t k, int32_t* idx_out,
+                                     uint16_t* val_out, void* ws, size_t ws_bytes,
+                                     const int32_t* req_of_token, int32_t layer_id,
+                                     int32_t app_id, const xmix_ring* ring, void* stream) {
+    if (!idx_out || !val_out || !req_of_token || !ring) return XMIX_E_INVAL;
     if (!ring->slots || !ring->head || ring->capacity < 1 ||
         ring->row_bytes != 16 + 6 * k || (reinterpret_cast<uintptr_t>(ring->slots) & 3u) != 0 ||
         (reinterpret_cast<uintptr_t>(ring->head) & 7u) != 0)
         return XMIX_E_INVAL;
     float* fold;
     void* cand;
-    const xmix_status st =
-        encode_args(h, d, rt, app_bit, W_packed, m, k, ws, ws_bytes, &fold, &cand);
+    const xmix_status st = encode_args(h, d, rt, app_bit, dict, k, ws, ws_bytes, &fold, &cand);
     if (st != XMIX_OK) return st;
     MergeRing r;
     r.slots = ring->slots;
@@ -342,37 +360,37 @@ xmix_status xmix_sae_merge_topk_ring(const uint16_t* h, int32_t d, const xmix_ro
     r.layer_id = layer_id;
     r.app_id = app_id;
     return launched(launch_sae_merge(h, d, rt->T_max, rt->app_count + app_bit,
-                                     app_list(rt, app_bit), W_packed, c_fold ? c_fold : fold, m,
-                                     k, idx_out, val_out, cand, &r, as_stream(stream)));
+                                     app_list(rt, app_bit), dict->pieces,
+                                     c_fold ? c_fold : fold, dict->m, k, idx_out, val_out, cand,
+                                     &r, as_stream(stream)));
 }
 
 xmix_status xmix_sae_encode_topk_ring(const uint16_t* h, int32_t d, const xmix_route* rt,
-                                      int32_t app_bit, const uint16_t* W_enc,
+                                      int32_t app_bit, const xmix_sae_dict* dict,
                                       const uint16_t* b_enc, const uint16_t* b_dec,
-                                      const float* c_fold, int32_t m, int32_t k,
-                                      int32_t* idx_out, uint16_t* val_out, void* ws,
-                                      size_t ws_bytes, const int32_t* req_of_token,
-                                      int32_t layer_id, int32_t app_id, const xmix_ring* ring,
-                                      void* stream) {
+                                      const float* c_fold, int32_t k, int32_t* idx_out,
+                                      uint16_t* val_out, void* ws, size_t ws_bytes,
+                                      const int32_t* req_of_token, int32_t layer_id,
+                                      int32_t app_id, const xmix_ring* ring, void* stream) {
     if (!idx_out || !val_out || !req_of_token || !ring || ring->row_bytes != 16 + 6 * k)
         return XMIX_E_INVAL;
-    const xmix_status st = xmix_sae_encode_candidates(h, d, rt, app_bit, W_enc, b_enc, b_dec,
-                                                      c_fold, m, k, ws, ws_bytes, stream);
+    const xmix_status st = xmix_sae_encode_candidates(h, d, rt, app_bit, dict, b_enc, b_dec,
+                                                      c_fold, k, ws, ws_bytes, stream);
     if (st != XMIX_OK) return st;
-    return xmix_sae_merge_topk_ring(h, d, rt, app_bit, W_enc, c_fold, m, k, idx_out, val_out,
-                                    ws, ws_bytes, req_of_token, layer_id, app_id, ring, stream);
+    return xmix_sae_merge_topk_ring(h, d, rt, app_bit, dict, c_fold, k, idx_out, val_out, ws,
+                                    ws_bytes, req_of_token, layer_id, app_id, ring, stream);
 }
 
 xmix_status xmix_sae_encode_topk(const uint16_t* h, int32_t d, const xmix_route* rt,
-                                 int32_t app_bit, const uint16_t* W_enc, const uint16_t* b_enc,
-                                 const uint16_t* b_dec, const float* c_fold, int32_t m,
-                                 int32_t k, int32_t* idx_out, uint16_t* val_out, void* ws,
-                                 size_t ws_bytes, void* stream) {
+                                 int32_t app_bit, const xmix_sae_dict* dict,
+                                 const uint16_t* b_enc, const uint16_t* b_dec,
+                                 const float* c_fold, int32_t k, int32_t* idx_out,
+                                 uint16_t* val_out, void* ws, size_t ws_bytes, void* stream) {
     if (!idx_out || !val_out) return XMIX_E_INVAL;
-    const xmix_status st = xmix_sae_encode_candidates(h, d, rt, app_bit, W_enc, b_enc, b_dec,
-                                                      c_fold, m, k, ws, ws_bytes, stream);
+    const xmix_status st = xmix_sae_encode_candidates(h, d, rt, app_bit, dict, b_enc, b_dec,
+                                                      c_fold, k, ws, ws_bytes, stream);
     if (st != XMIX_OK) return st;
-    return xmix_sae_merge_topk(h, d, rt, app_bit, W_enc, c_fold, m, k, idx_out, val_out, ws,
+    return xmix_sae_merge_topk(h, d, rt, app_bit, dict, c_fold, k, idx_out, val_out, ws,
                                ws_bytes, stream);
 }
 
@@ -401,18 +419,18 @@ xmix_status xmix_readback_compact(const void* const* seg_rows, const int32_t* se
     if (n_seg < 1 || n_seg > XMIX_MAX_SEGMENTS) return XMIX_E_INVAL;
     if (app_bit < 0 || app_bit >= rt->n_apps) return XMIX_E_INVAL;
     if (!ring->slots || !ring->head || ring->capacity < 1 || ring->row_bytes < 16 ||
-        ring->row_bytes % 16 != 0 || !aligned16(ring->slots) ||
+        ring->row_bytes % 2 != 0 || (reinterpret_cast<uintptr_t>(ring->slots) & 3u) != 0 ||
         (reinterpret_cast<uintptr_t>(ring->head) & 7u) != 0)
         return XMIX_E_INVAL;
     Segments segs;
     memset(&segs, 0, sizeof(segs));
     int64_t total = 16;
     for (int s = 0; s < n_seg; ++s) {
-        if (!seg_rows[s] || seg_bytes[s] < 4 || seg_bytes[s] % 4 != 0 ||
-            (reinterpret_cast<uintptr_t>(seg_rows[s]) & 3u) != 0)
+        if (!seg_rows[s] || seg_bytes[s] < 2 || seg_bytes[s] % 2 != 0 ||
+            (reinterpret_cast<uintptr_t>(seg_rows[s]) & 1u) != 0)
             return XMIX_E_INVAL;
         segs.ptr[s] = static_cast<const uint8_t*>(seg_rows[s]);
-        segs.words[s] = seg_bytes[s] / 4;
+        segs.bytes[s] = seg_bytes[s];
         total += seg_bytes[s];
     }
     segs.n = n_seg;

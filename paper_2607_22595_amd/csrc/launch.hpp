@@ -91,7 +91,7 @@ hipError_t launch_clamp_decode(uint16_t* h, int32_t d, const int32_t* app_count,
 
 struct Segments {
     const uint8_t* ptr[4];
-    int32_t words[4];  // 4-byte words per row of each segment
+    int32_t bytes[4];  // bytes per row of each segment (even)
     int32_t n;
 };
 hipError_t launch_compact(const Segments& segs, const int32_t* app_count,

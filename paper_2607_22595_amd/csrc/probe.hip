@@ -7,7 +7,12 @@
 //
 // Mean pooling is a segmented reduction in two launches: the token pass
 // writes each token's dot products (without bias) to the workspace, then one
-// workgroup per request sums its contiguous span in a fixed order.
+// workgroup per request sums its contiguous span in a fixed order.  Whether
+// a request is pooled is decided at the first token of its span, so in this
+// mode the token pass finds each token's span and takes the subscription of
+// the span's first token: every token of a pooled span gets its dots, also
+// where its own mask lacks the bit (a conditional filter narrowed it, or the
+// span runs past T_valid).
 //
 // Last-token mode runs the token pass with one workgroup per request on the
 // last token of its span, writing [n_probe][R_max].
@@ -20,25 +25,48 @@ namespace xmix {
 constexpr int kProbeThreads = 256;
 constexpr int kProbeWaves = kProbeThreads / kWave;
 
+// The request whose span [cu[r], cu[r+1]) holds token t, or -1: with cu
+// non-decreasing, r + 1 is the number of entries cu[0..R] that are <= t.
+// Called by every thread of the workgroup (the count is a barrier).
+__device__ __forceinline__ int32_t span_of_token(const int32_t* __restrict__ cu, int32_t R,
+                                                 int32_t t) {
+    int c = 0;
+    for (int32_t i0 = 0; i0 <= R; i0 += kProbeThreads) {
+        const int32_t i = i0 + static_cast<int32_t>(threadIdx.x);
+        c += __syncthreads_count(i <= R && cu[i] <= t);
+    }
+    const int32_t r = c - 1;
+    if (r < 0 || r >= R) return -1;
+    return t < cu[r + 1] ? r : -1;
+}
+
 template <bool BF16, int MAXP>
 __global__ void __launch_bounds__(kProbeThreads)
 probe_token_kernel(const void* __restrict__ h, int32_t d, int32_t T_max,
                    const uint32_t* __restrict__ tok_mask, const void* __restrict__ w,
                    const float* __restrict__ b, BitList bits, int32_t n_probe,
-                   const int32_t* __restrict__ cu, float* __restrict__ logit,
-                   float* __restrict__ score, float* __restrict__ dots) {
+                   const int32_t* __restrict__ cu, int32_t R, int32_t mode,
+                   float* __restrict__ logit, float* __restrict__ score,
+                   float* __restrict__ dots) {
     __shared__ float red[kProbeWaves][MAXP];
-    // token mode: slot = token; last-token mode (cu given): slot = request,
-    // reading the last token of its span (subscription of its first token)
+    // token mode: slot = token; last-token mode: slot = request, reading the
+    // last token of its span (subscription of its first token); mean mode:
+    // slot = token, subscription of the first token of its span
     int32_t t = blockIdx.x;
     int32_t out_len = T_max;
     uint32_t mask;
-    if (cu) {
+    if (mode == 2) {
         const int32_t lo = cu[blockIdx.x], hi = cu[blockIdx.x + 1];
         if (hi <= lo || lo < 0 || hi > T_max) return;
         t = hi - 1;
         mask = tok_mask[lo];
         out_len = static_cast<int32_t>(gridDim.x);
+    } else if (mode == 1) {
+        const int32_t r = span_of_token(cu, R, t);
+        if (r < 0) return;
+        const int32_t lo = cu[r], hi = cu[r + 1];
+        if (lo < 0 || hi > T_max) return;  // the pooling skips such a span too
+        mask = tok_mask[lo];
     } else {
         mask = tok_mask[t];
     }
@@ -149,21 +177,21 @@ template <bool BF16>
 static hipError_t launch_probe_t(const void* h, int32_t d, int32_t T_max,
                                  const uint32_t* tok_mask, const void* w, const float* b,
                                  const BitList& bits, int32_t n_probe, const int32_t* cu,
-                                 int32_t slots, float* logit, float* score, float* dots,
-                                 hipStream_t stream) {
+                                 int32_t R, int32_t mode, int32_t slots, float* logit,
+                                 float* score, float* dots, hipStream_t stream) {
     dim3 g(slots), blk(kProbeThreads);
     if (n_probe <= 4)
         hipLaunchKernelGGL((probe_token_kernel<BF16, 4>), g, blk, 0, stream, h, d, T_max,
-                           tok_mask, w, b, bits, n_probe, cu, logit, score, dots);
+                           tok_mask, w, b, bits, n_probe, cu, R, mode, logit, score, dots);
     else if (n_probe <= 8)
         hipLaunchKernelGGL((probe_token_kernel<BF16, 8>), g, blk, 0, stream, h, d, T_max,
-                           tok_mask, w, b, bits, n_probe, cu, logit, score, dots);
+                           tok_mask, w, b, bits, n_probe, cu, R, mode, logit, score, dots);
     else if (n_probe <= 16)
         hipLaunchKernelGGL((probe_token_kernel<BF16, 16>), g, blk, 0, stream, h, d, T_max,
-                           tok_mask, w, b, bits, n_probe, cu, logit, score, dots);
+                           tok_mask, w, b, bits, n_probe, cu, R, mode, logit, score, dots);
     else
         hipLaunchKernelGGL((probe_token_kernel<BF16, 32>), g, blk, 0, stream, h, d, T_max,
-                           tok_mask, w, b, bits, n_probe, cu, logit, score, dots);
+                           tok_mask, w, b, bits, n_probe, cu, R, mode, logit, score, dots);
     return hipGetLastError();
 }
 
@@ -173,12 +201,12 @@ hipError_t launch_probe(const void* h, bool bf16, int32_t d, int32_t T_max,
                         const int32_t* cu_seqlens, int32_t R_max, float* logit, float* score,
                         float* ws, hipStream_t stream) {
     float* dots = mode == 1 ? ws : nullptr;
-    const int32_t* cu = mode == 2 ? cu_seqlens : nullptr;  // last-token mode
+    const int32_t* cu = mode == 0 ? nullptr : cu_seqlens;
     const int32_t slots = mode == 2 ? R_max : T_max;
     hipError_t e = bf16 ? launch_probe_t<true>(h, d, T_max, tok_mask, w, b, bits, n_probe, cu,
-                                               slots, logit, score, dots, stream)
+                                               R_max, mode, slots, logit, score, dots, stream)
                         : launch_probe_t<false>(h, d, T_max, tok_mask, w, b, bits, n_probe, cu,
-                                                slots, logit, score, dots, stream);
+                                                R_max, mode, slots, logit, score, dots, stream);
     if (e != hipSuccess || mode != 1) return e;
     hipLaunchKernelGGL(probe_pool_kernel, dim3(R_max), dim3(kProbeThreads), 0, stream, ws, T_max,
                        tok_mask, cu_seqlens, b, bits, n_probe, R_max, logit, score);

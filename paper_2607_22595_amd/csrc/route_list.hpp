@@ -1,7 +1,8 @@
 // In-kernel route build for a kernel that takes the place of the route-build
 // launch (internal).  The rules are the route-build kernel's: T_valid is
-// clamped to [0, T_max] (error bit 2); a request id >= R_max routes nowhere
-// (error bit 1); a negative id is padding.
+// clamped to [0, T_max] (error value XMIX_ERR_T_VALID = 2); a request id >=
+// R_max routes nowhere (XMIX_ERR_REQUEST_RANGE = 1); a negative id is
+// padding.
 #pragma once
 
 #include "common.hpp"
@@ -10,7 +11,7 @@ namespace xmix {
 
 constexpr int kRouteMaxT = 1024;  // most token slots a kernel routes itself
 
-// T_valid clamped to [0, T_max]; error bit 2 when it was outside.
+// T_valid clamped to [0, T_max]; XMIX_ERR_T_VALID (2) when it was outside.
 __device__ __forceinline__ int32_t clamp_t_valid(int32_t tv, int32_t T_max, uint32_t& err) {
     if (tv < 0 || tv > T_max) {
         err |= 2u;
@@ -19,7 +20,8 @@ __device__ __forceinline__ int32_t clamp_t_valid(int32_t tv, int32_t T_max, uint
     return tv;
 }
 
-// The mask of token slot t (0 past T_valid or for a bad id, with error bit 1).
+// The mask of token slot t (0 past T_valid, or for a bad id with
+// XMIX_ERR_REQUEST_RANGE (1)).
 __device__ __forceinline__ uint32_t slot_mask(const int32_t* __restrict__ req, int32_t t,
                                               int32_t tv, const uint32_t* __restrict__ sub,
                                               int32_t R_max, uint32_t keep, uint32_t& err) {

@@ -1483,14 +1483,20 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
             uint8_t* row = ring.slots + static_cast<int64_t>((h0 + static_cast<uint64_t>(n)) %
                                                              static_cast<uint64_t>(ring.capacity)) *
                                             ring.row_bytes;
-            if (lane < 4) {
-                const int32_t hdr = lane == 0 ? t : lane == 1 ? ring.req[t]
-                                  : lane == 2 ? ring.layer_id : ring.app_id;
-                reinterpret_cast<int32_t*>(row)[lane] = hdr;
+            // 16-bit stores: with k odd, every other row starts 2 bytes
+            // past a 4-byte boundary
+            uint16_t* row16 = reinterpret_cast<uint16_t*>(row);
+            if (lane < 8) {
+                const int f = lane >> 1;
+                const uint32_t hdr = static_cast<uint32_t>(
+                    f == 0 ? t : f == 1 ? ring.req[t] : f == 2 ? ring.layer_id : ring.app_id);
+                row16[lane] = static_cast<uint16_t>((lane & 1) ? hdr >> 16 : hdr & 0xFFFFu);
             }
             if (lane < k) {
-                reinterpret_cast<int32_t*>(row + 16)[rank] = wi;
-                reinterpret_cast<uint16_t*>(row + 16 + 4 * k)[rank] = vb;
+                const uint32_t iv = static_cast<uint32_t>(wi);
+                row16[8 + 2 * rank] = static_cast<uint16_t>(iv & 0xFFFFu);
+                row16[8 + 2 * rank + 1] = static_cast<uint16_t>(iv >> 16);
+                row16[8 + 2 * k + rank] = vb;
             }
         }
         if (lane == 0) ring_ticket(ring, h0, cnt);

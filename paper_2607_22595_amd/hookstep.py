@@ -31,8 +31,8 @@ from typing import List, Optional
 import numpy as np
 import torch
 
-from . import (XMIX_PROBE_LAST, XMIX_PROBE_MEAN, XMIX_PROBE_TOKEN, Ring, Route, probe_workspace,
-               sae_encode_workspace, xmix_probe_score, xmix_readback_compact,
+from . import (XMIX_PROBE_LAST, XMIX_PROBE_MEAN, XMIX_PROBE_TOKEN, Ring, Route, SaeDict,
+               probe_workspace, sae_encode_workspace, xmix_probe_score, xmix_readback_compact,
                xmix_route_build, xmix_sae_clamp_decode, xmix_sae_encode_candidates,
                xmix_sae_encode_topk, xmix_sae_encode_topk_ring, xmix_sae_fold_bias,
                xmix_route_sae_encode_candidates, xmix_route_steer_probe, xmix_sae_merge_topk,
@@ -69,7 +69,7 @@ class _Sae:
     bit: int
     m: int
     k: int
-    W_enc: torch.Tensor
+    W_enc: SaeDict
     b_enc: torch.Tensor
     b_dec: torch.Tensor
     c_fold: Optional[torch.Tensor]
@@ -135,10 +135,10 @@ class HookStep:
                 d = wl.d
                 # the dictionary is packed once into the layout the encode streams
                 W_row = to_device_bits(s.W_enc, dev)
-                W_packed = xmix_sae_pack_encoder(W_row)
+                W_dict = xmix_sae_pack_encoder(W_row)
                 del W_row
                 sae = _Sae(
-                    s.bit, s.m, s.k, W_packed, to_device_bits(s.b_enc, dev),
+                    s.bit, s.m, s.k, W_dict, to_device_bits(s.b_enc, dev),
                     to_device_bits(s.b_dec, dev), None,
                     torch.zeros((wl.T_max, s.k), dtype=torch.int32, device=dev),
                     torch.zeros((wl.T_max, s.k), dtype=torch.bfloat16, device=dev),

@@ -59,14 +59,14 @@ def test_host_validation_rejects_before_launch(lib):
     # null pointers and missing route -> XMIX_E_INVAL (1), nothing launched
     assert lib.xmix_route_build(None, None, None, 1, None, None, None) == 1
     assert lib.xmix_steer_apply(None, 1, 64, None, None, None, None, None, 1, 1, None) == 1
-    assert lib.xmix_sae_encode_topk(None, 64, None, 0, None, None, None, None, 256, 8,
+    assert lib.xmix_sae_encode_topk(None, 64, None, 0, None, None, None, None, 8,
                                     None, None, None, ctypes.c_size_t(0), None) == 1
     assert lib.xmix_readback_compact(None, None, 1, None, 0, None, 0, 0, None, None) == 1
     lib.xmix_router_write.restype = ctypes.c_int
     assert lib.xmix_router_write(None, 0, 8, None, None, None, 1, None) == 1
     lib.xmix_route_sae_encode_candidates.restype = ctypes.c_int
     assert lib.xmix_route_sae_encode_candidates(None, None, None, 1, None, None, None, 256, 0,
-                                                None, None, None, None, 1024, 8, None,
+                                                None, None, None, None, 8, None,
                                                 ctypes.c_size_t(0), None) == 1
     lib.xmix_steer_probe.restype = ctypes.c_int
     assert lib.xmix_steer_probe(None, 1, 64, None, None, None, None, None, 1, 1, None, None,
@@ -95,12 +95,15 @@ def test_encode_rejects_unsupported_shapes_on_the_host(lib):
     import paper_2607_22595_amd as px
     f = lib.xmix_sae_encode_topk
     f.restype = ctypes.c_int
+    f.argtypes = None
     rt = px.XmixRoute(0x10000, 0x20000, 0x30000, 256, 1)
     A = 0x100000   # 16-byte aligned fake address
 
-    def call(d=4096, m=65536, k=64, ws_bytes=1 << 40, app_bit=0, c_fold=A):
-        return f(ctypes.c_void_p(A), d, ctypes.byref(rt), app_bit, ctypes.c_void_p(A),
-                 ctypes.c_void_p(A), ctypes.c_void_p(A), ctypes.c_void_p(c_fold), m, k,
+    def call(d=4096, m=65536, k=64, ws_bytes=1 << 40, app_bit=0, c_fold=A, dict_d=None,
+             layout=px.XMIX_SAE_DICT_TILED):
+        w = px.XmixSaeDict(A, m, d if dict_d is None else dict_d, layout)
+        return f(ctypes.c_void_p(A), d, ctypes.byref(rt), app_bit, ctypes.byref(w),
+                 ctypes.c_void_p(A), ctypes.c_void_p(A), ctypes.c_void_p(c_fold), k,
                  ctypes.c_void_p(A), ctypes.c_void_p(A), ctypes.c_void_p(A),
                  ctypes.c_size_t(ws_bytes), None)
     assert call(d=320) == 1            # d must be a multiple of 256
@@ -110,6 +113,45 @@ def test_encode_rejects_unsupported_shapes_on_the_host(lib):
     assert call(app_bit=1) == 1        # bit outside the route's apps
     assert call(m=262144, k=64) == 2   # too many merge candidates per token
     assert call(ws_bytes=1024) == 3    # workspace too small
+
+
+def test_dictionary_must_come_from_the_packer(lib):
+    """A row-major matrix cannot reach the encode in place of the packed
+    dictionary: the calls take a descriptor that only xmix_sae_pack_encoder
+    fills, and refuse one without its layout tag or of another width."""
+    import paper_2607_22595_amd as px
+    A = 0x100000
+    rt = px.XmixRoute(0x10000, 0x20000, 0x30000, 256, 1)
+    enc = lib.xmix_sae_encode_topk
+    enc.restype = ctypes.c_int
+    enc.argtypes = None
+    fold = lib.xmix_sae_fold_bias
+    fold.restype = ctypes.c_int
+    fold.argtypes = None
+
+    def call(w):
+        return enc(ctypes.c_void_p(A), 4096, ctypes.byref(rt), 0,
+                   None if w is None else ctypes.byref(w), ctypes.c_void_p(A),
+                   ctypes.c_void_p(A), ctypes.c_void_p(A), 64, ctypes.c_void_p(A),
+                   ctypes.c_void_p(A), ctypes.c_void_p(A), ctypes.c_size_t(1 << 40), None)
+    # a descriptor filled by hand around a row-major matrix has no layout tag
+    assert call(px.XmixSaeDict(A, 65536, 4096, 0)) == 1
+    assert call(px.XmixSaeDict(A, 65536, 4096, px.XMIX_SAE_DICT_TILED ^ 1)) == 1
+    assert call(px.XmixSaeDict(A, 65536, 2048, px.XMIX_SAE_DICT_TILED)) == 1  # width
+    assert call(px.XmixSaeDict(0, 65536, 4096, px.XMIX_SAE_DICT_TILED)) == 1  # no pieces
+    assert call(None) == 1
+    assert fold(ctypes.byref(px.XmixSaeDict(A, 65536, 4096, 0)), ctypes.c_void_p(A),
+                ctypes.c_void_p(A), ctypes.c_void_p(A), None) == 1
+    # the binding refuses anything but a packed dictionary object
+    with pytest.raises(TypeError):
+        px._dict(object())
+    # the C prototypes take the descriptor, not a bare pointer
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    for fn in ("xmix_sae_encode_topk", "xmix_sae_encode_candidates", "xmix_sae_merge_topk",
+               "xmix_route_sae_encode_candidates", "xmix_sae_encode_topk_ring",
+               "xmix_sae_merge_topk_ring", "xmix_sae_fold_bias"):
+        proto = re.search(fn + r"\s*\(([^;]*)\)\s*;", text).group(1)
+        assert "const xmix_sae_dict *dict" in proto and "W_packed" not in proto, fn
 
 
 CEIL_HEADER = os.path.join(ROOT, "include", "xmix_ceiling.h")

@@ -1,8 +1,10 @@
 """Full-size hook steps in the launch configuration the benchmark times
 (HookStep.run, static shapes), checked against the oracle on every output
-the oracle can afford: all of routing, steering, probes and readback, and a
-seeded sample of tokens for the SAE encode (each sampled token is checked
-over all m latents).  Clamp-decode and readback are stage-isolated: the
+the oracle can afford: all of routing, steering, probes and readback; the
+SAE encode on every subscribed token of the decode shape, on one token per
+32-token group of every GEMM tile of the prefill shape and on 16 tokens of
+each of the eight clamp apps of the 70B-shaped step (each checked over all m
+latents).  Clamp-decode and readback are stage-isolated: the
 oracle consumes the GPU's own encode results."""
 import numpy as np
 import pytest
@@ -86,10 +88,10 @@ def test_decode_sae_with_ring(HookStep):
                                      tm, s.bit, wl.req, 0, s.bit, slots, head)
         assert int(sd.ring.head[0].item()) == head
         assert np.array_equal(sd.ring.slots.cpu().numpy(), slots)
-    sample = _sample(toks, 32, "c3")
-    idx_ref, _, _, pre = oracle.sae_encode(L.h, sample, s.W_enc, s.b_enc, s.b_dec, s.k,
+    # every subscribed token, over all m latents
+    idx_ref, _, _, pre = oracle.sae_encode(L.h, toks, s.W_enc, s.b_enc, s.b_dec, s.k,
                                            want_pre=True)
-    for q, t in enumerate(sample):
+    for q, t in enumerate(toks):
         check_topk(idx[t], val[t], idx_ref[q], pre[q], s.k)
 
 
@@ -104,9 +106,15 @@ def test_prefill_sae_and_probes(HookStep):
     s, sd = L.saes[0], lay.saes[0]
     idx = sd.idx.cpu().numpy()
     val = torch_bits(sd.val)
-    # a sample spanning the first, last and a middle token-tile of every request
-    sample = np.unique(np.concatenate([wl.cu_seqlens[:-1][:4], [8191, 4095],
-                                       _sample(np.arange(wl.T_max), 4, "c4")]))
+    # one token in every 32-token group of every 256-token GEMM tile (the
+    # group fixes the wave's token half and accumulator block that hold the
+    # token; the lane within the group varies with tile and group), plus the
+    # first token of every request and the batch's last token
+    tiles = np.arange(wl.T_max // 256)
+    groups = np.arange(8)
+    lane = (tiles[:, None] * 7 + groups[None, :] * 13) % 32
+    grid = (tiles[:, None] * 256 + groups[None, :] * 32 + lane).ravel()
+    sample = np.unique(np.concatenate([grid, wl.cu_seqlens[:-1], [wl.T_max - 1]]))
     idx_ref, _, _, pre = oracle.sae_encode(L.h, sample, s.W_enc, s.b_enc, s.b_dec, s.k,
                                            want_pre=True)
     for q, t in enumerate(sample):
@@ -121,10 +129,11 @@ def test_prefill_sae_and_probes(HookStep):
 
 
 def test_decode_70b_shape_steer_probe_clamp(HookStep):
-    # the first two of the eight clamp apps (same seeds and bits as the full
-    # 32-app workload), steering and probes at full size
+    # the full 32-app workload: 16 steering, 8 probe and 8 clamp apps, each
+    # clamp app with its own 65536 x 8192 dictionary
     from parity import bf16_ulp
-    wl = synth.make("c5", n_clamp_apps=2)
+    wl = synth.make("c5")
+    assert len(wl.layers[0].saes) == 8 and wl.n_apps == 32
     step = HookStep(wl)
     step.run()
     torch.cuda.synchronize()
@@ -142,7 +151,7 @@ def test_decode_70b_shape_steer_probe_clamp(HookStep):
         idx = sd.idx.cpu().numpy()
         val = torch_bits(sd.val)
         toks = lists[s.bit, :cnt[s.bit]]
-        sample = _sample(toks, 4, f"c5/{s.bit}")
+        sample = _sample(toks, 16, f"c5/{s.bit}")
         idx_ref, _, _, pre = oracle.sae_encode(L.h, sample, s.W_enc, s.b_enc, s.b_dec, s.k,
                                                want_pre=True)
         for q, t in enumerate(sample):

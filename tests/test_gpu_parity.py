@@ -200,6 +200,90 @@ def test_probe_70b_shape(px):
     _probe_case(px, synth.make("c5", m=256, k=8))
 
 
+def _pooled_case(px, wl, narrow=None):
+    """Mean-pooled probes of wl's layer 0 against the oracle on a route that
+    `narrow(rt, tm, cnt, lists)` may narrow first (GPU) and returns the
+    oracle's narrowed mask for.  The workspace starts as NaN bit patterns, so
+    a span sum that read a token the pass skipped is NaN."""
+    L = wl.layers[0]
+    tm, cnt, lists, _ = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    rt, _ = gpu_route(px, wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    if narrow is not None:
+        tm = narrow(rt, tm, cnt, lists)
+    ps = [p for p in L.probes if p.mode == "mean"]
+    w = np.stack([p.w for p in ps])
+    b = np.array([p.b for p in ps], np.float32)
+    bits = [p.bit for p in ps]
+    lo = torch.full((len(ps), wl.R_max), float("nan"), device="cuda")
+    so = torch.full((len(ps), wl.R_max), float("nan"), device="cuda")
+    ws = torch.full((px.probe_workspace(wl.T_max, len(ps), px.XMIX_PROBE_MEAN),), 0xFF,
+                    dtype=torch.uint8, device="cuda")
+    px.xmix_probe_score(dev_bits(L.h), rt, dev_bits(w), torch.from_numpy(b).cuda(), bits,
+                        px.XMIX_PROBE_MEAN, lo, so, cu_seqlens=dev_i32(wl.cu_seqlens), ws=ws)
+    torch.cuda.synchronize()
+    lr, sr = oracle.probe_mean(L.h, tm, w, b, bits, wl.cu_seqlens)
+    cu = wl.cu_seqlens
+    absdot = np.abs(bf16_f64(w)) @ np.abs(bf16_f64(L.h)).T
+    floor = np.stack([[absdot[q, cu[r]:cu[r + 1]].mean() if cu[r + 1] > cu[r] else 0.0
+                       for r in range(wl.R_max)] for q in range(len(ps))])
+    written = ~np.isnan(lr)
+    lg, sg = lo.cpu().numpy(), so.cpu().numpy()
+    assert np.array_equal(np.isnan(lg), ~written), "written set differs from the oracle's"
+    check_probe(lg, sg, lr, sr, written, floor)
+    return written
+
+
+def _small_prefill():
+    return synth.make("c4", d=512, T=2000, R=5, len_lo=100, len_hi=700, m=256, k=8)
+
+
+def test_probe_mean_span_past_t_valid(px):
+    """T_valid ends inside the last span: the request is pooled (its first
+    token is live) over its whole span, tokens past T_valid included."""
+    wl = _small_prefill()
+    cu = wl.cu_seqlens
+    wl.T_valid = int(cu[-2] + (cu[-1] - cu[-2]) // 3)
+    written = _pooled_case(px, wl)
+    assert written[:, -1].all()
+
+
+def test_probe_mean_with_padding_inside_a_span(px):
+    """Padding slots (request -1, mask 0) inside a span still count."""
+    wl = _small_prefill()
+    cu = wl.cu_seqlens
+    wl.req[cu[1] + 5:cu[1] + 40] = -1
+    wl.req[cu[3] - 3:cu[3]] = -1
+    written = _pooled_case(px, wl)
+    assert written[:, 1].all() and written[:, 2].all()
+
+
+def test_probe_mean_after_a_trigger_clears_the_bit_mid_span(px):
+    """A token-driven filter clears a pooled probe's bit on some tokens of a
+    span: a request whose first token keeps the bit is pooled over its whole
+    span; one whose first token loses it is not written."""
+    wl = _small_prefill()
+    cu, T = wl.cu_seqlens, wl.T_max
+    bit = [p.bit for p in wl.layers[0].probes if p.mode == "mean"][1]
+    V = 1000
+    rng = np.random.default_rng(7)
+    ids = rng.integers(0, V, T).astype(np.int32)
+    trig = np.arange(0, V, 2)                      # even ids pass
+    vocab = np.zeros((V + 31) // 32, np.uint32)
+    np.bitwise_or.at(vocab, trig >> 5, (np.uint32(1) << (trig & 31).astype(np.uint32)))
+    ids[cu[0]] = 4                                  # request 0: first token passes
+    ids[cu[1]] = 3                                  # request 1: first token fails
+    ids[cu[2]] = 10
+    ids[cu[2] + 1:cu[3]] = 11                       # request 2: only its first token passes
+
+    def narrow(rt, tm, cnt, lists):
+        px.xmix_route_trigger(rt, bit, dev_i32(ids), dev_i32(vocab), V)
+        return oracle.route_trigger(tm, cnt, lists, bit, ids, vocab, V)[0]
+
+    written = _pooled_case(px, wl, narrow)
+    q = [p.bit for p in wl.layers[0].probes if p.mode == "mean"].index(bit)
+    assert written[q, 0] and not written[q, 1] and written[q, 2]
+
+
 # ------------------------------------------------- probes + steering, fused
 
 def _steer_probe_case(px, wl, layer=0):
@@ -598,13 +682,16 @@ def test_clamp_to_current_value_leaves_h(px):
 
 # ---------------------------------------------------------------- readback
 
-def test_readback_ring_bit_exact_with_wraparound(px):
-    wl = synth.make("c3", d=256, m=512, k=16, T=100, ring_capacity=64)
+@pytest.mark.parametrize("k", [16, 5])
+def test_readback_ring_bit_exact_with_wraparound(px, k):
+    """Odd k: rows of 16 + 6 k bytes, every other one 2 bytes past a 4-byte
+    boundary."""
+    wl = synth.make("c3", d=256, m=512, k=k, T=100, ring_capacity=64)
     sae = wl.layers[0].saes[0]
     rt, idx, val = _encode(px, wl, sae, wl.layers[0].h)
-    ring = px.Ring(64, 16 + 16 * 6)
+    ring = px.Ring(64, 16 + k * 6)
     tm = rt.tok_mask.cpu().numpy().view(np.uint32)
-    slots = np.zeros((64, 16 + 16 * 6), np.uint8)
+    slots = np.zeros((64, 16 + k * 6), np.uint8)
     head = 0
     idx_d, val_d = torch.from_numpy(idx).cuda(), dev_bits(val)
     for step in range(3):   # 3 x 50 rows into 64 slots: wraps and overwrites
@@ -633,7 +720,8 @@ def test_readback_more_rows_than_capacity(px):
     assert np.array_equal(ring.slots.cpu().numpy(), slots)
 
 
-@pytest.mark.parametrize("T,n_sub,cap,k", [(100, 50, 64, 16), (1500, 1100, 500, 8)])
+@pytest.mark.parametrize("T,n_sub,cap,k", [(100, 50, 64, 16), (1500, 1100, 500, 8),
+                                           (100, 50, 64, 7)])
 def test_encode_with_fused_readback_bit_exact(px, T, n_sub, cap, k):
     """The merge writes the ring rows itself: same rows and head as the
     compaction of the encode's own outputs (3 calls: wrap-around and, in the

@@ -232,6 +232,33 @@ def test_probe_closed_forms():
     assert np.all(logit[1] == 0.0) and np.all(score[1] == 0.5)
 
 
+def test_probe_logistic_closed_forms():
+    """The score's orientation and scale, from values whose logistic is known
+    in closed form: sigma(ln 3) = 3/4, sigma(-ln 3) = 1/4, sigma(ln 9) = 9/10,
+    sigma(0) = 1/2 and sigma(-x) = 1 - sigma(x).  A probe with w = e_0 and
+    b = 0 on fp32 rows makes the logit exactly the row's first value."""
+    d = 8
+    xs = np.array([math.log(3.0), -math.log(3.0), math.log(9.0), 0.0, 2.5, -2.5, 17.0, -17.0],
+                  np.float32)
+    h = np.zeros((xs.size, d), np.float32)
+    h[:, 0] = xs
+    w = np.zeros((1, d), np.float32)
+    w[0, 0] = 1.0
+    logit, score = oracle.probe_token(h, np.ones(xs.size, np.uint32), w,
+                                      np.zeros(1, np.float32), [0])
+    assert np.array_equal(logit[0], xs.astype(np.float64))
+    # float32(ln 3) differs from ln 3 by < 2^-24 relative; sigma' <= 1/4
+    assert abs(score[0, 0] - 0.75) <= 1e-7
+    assert abs(score[0, 1] - 0.25) <= 1e-7
+    assert abs(score[0, 2] - 0.9) <= 1e-7
+    assert score[0, 3] == 0.5
+    assert score[0, 4] + score[0, 5] == pytest.approx(1.0, abs=1e-15)
+    assert score[0, 4] > 0.5 > score[0, 5]
+    assert score[0, 6] + score[0, 7] == pytest.approx(1.0, abs=1e-15)
+    assert 1.0 - score[0, 6] == pytest.approx(math.exp(-17.0) / (1 + math.exp(-17.0)),
+                                              rel=1e-6)
+
+
 def test_probe_mean_pins():
     d, R = 32, 4
     lens = [1, 3, 0, 5]
