@@ -327,6 +327,27 @@ xmix_status xmix_sae_encode_topk(const uint16_t *h, int32_t d, const xmix_route 
                                  int32_t *idx_out, uint16_t *val_out,
                                  void *ws, size_t ws_bytes, void *stream);
 
+/* xmix_sae_encode_topk without a workspace argument, for callers that
+ * cannot allocate device memory (code under graph capture, tight serving
+ * loops, harnesses that forbid allocation).  Same arguments minus ws and
+ * ws_bytes, same kernels and results.  The workspace is a device array of
+ * XMIX_STATIC_SCRATCH_BYTES inside the library, one per GPU, held until the
+ * process ends; the call itself allocates nothing.
+ * Limit: xmix_sae_encode_workspace(rt->T_max, d, dict->m, k) must not exceed
+ * XMIX_STATIC_SCRATCH_BYTES (16 MiB: e.g. up to 512 token slots at
+ * m = 65536, k = 64); larger calls return XMIX_E_UNSUPPORTED and launch
+ * nothing.  All calls on one GPU share the array: calls that overlap in
+ * time on one GPU (other streams, other threads) race and must be ordered by
+ * the caller.  Nothing in the array has to start at zero.
+ * Errors: as xmix_sae_encode_topk; XMIX_E_LAUNCH if the array's device
+ * address cannot be obtained. */
+#define XMIX_STATIC_SCRATCH_BYTES (16 << 20)
+xmix_status xmix_sae_encode_topk_noalloc(const uint16_t *h, int32_t d, const xmix_route *rt,
+                                         int32_t app_bit, const xmix_sae_dict *dict,
+                                         const uint16_t *b_enc, const uint16_t *b_dec,
+                                         const float *c_fold, int32_t k, int32_t *idx_out,
+                                         uint16_t *val_out, void *stream);
+
 /* The two stages of xmix_sae_encode_topk, callable on their own (same
  * arguments and workspace; run them in this order on one stream):
  *   candidates: the GEMM; for every 256-latent slice of the dictionary and

@@ -86,6 +86,8 @@ _sigs = {
     "xmix_sae_encode_workspace": ([_i32, _i32, _i32, _i32], _sz),
     "xmix_sae_encode_topk": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _dp, _vp, _vp, _vp,
                               _i32, _vp, _vp, _vp, _sz, _vp], _st),
+    "xmix_sae_encode_topk_noalloc": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _dp, _vp,
+                                      _vp, _vp, _i32, _vp, _vp, _vp], _st),
     "xmix_sae_encode_candidates": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _dp, _vp, _vp,
                                     _vp, _i32, _vp, _sz, _vp], _st),
     "xmix_route_sae_encode_candidates": ([_vp, _vp, _vp, _i32, ctypes.POINTER(XmixRoute), _vp,
@@ -435,6 +437,23 @@ def xmix_sae_encode_topk(h, route: Route, app_bit: int, W: SaeDict, b_enc, b_dec
     _check("xmix_sae_encode_topk", _lib.xmix_sae_encode_topk(
         _ptr(h), d, ctypes.byref(route.struct), app_bit, W.ref(), _ptr(b_enc), _ptr(b_dec),
         _ptr(c_fold), k, _ptr(idx_out), _ptr(val_out), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+XMIX_STATIC_SCRATCH_BYTES = 16 << 20
+
+
+def xmix_sae_encode_topk_noalloc(h, route: Route, app_bit: int, W: SaeDict, b_enc, b_dec,
+                                 c_fold, k: int, idx_out, val_out, stream=None):
+    """xmix_sae_encode_topk with the library's own per-GPU static workspace
+    (no workspace argument, nothing allocated by the call)."""
+    T_max, d = h.shape
+    W = _dict(W)
+    assert h.dtype == torch.bfloat16
+    assert idx_out.dtype == torch.int32 and idx_out.shape == (T_max, k)
+    assert val_out.dtype == torch.bfloat16 and val_out.shape == (T_max, k)
+    _check("xmix_sae_encode_topk_noalloc", _lib.xmix_sae_encode_topk_noalloc(
+        _ptr(h), d, ctypes.byref(route.struct), app_bit, W.ref(), _ptr(b_enc), _ptr(b_dec),
+        _ptr(c_fold), k, _ptr(idx_out), _ptr(val_out), _stream(stream)))
 
 
 def xmix_sae_encode_topk_ring(h, route: Route, app_bit: int, W: SaeDict, b_enc, b_dec, c_fold,
