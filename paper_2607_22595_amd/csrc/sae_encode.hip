@@ -19,9 +19,12 @@
 // mean + z * stdev of the tile's 256 values, then bisection on the value if
 // needed); every latent with pre >= tau is emitted as a candidate, and tau
 // and the count are recorded for the tile.  This costs O(1) work per value.
-// The decode kernel stages the candidates in LDS with its first guess and
-// takes the counts from the staging atomics; only a tile with a token
-// outside the window stages again.
+// The decode kernel writes the tile to LDS token-major, and eight lanes of
+// one wave select for each token with no barrier or LDS atomic between the
+// waves.  The prefill kernel (one wave per SIMD, values in accumulator
+// registers) runs the four token groups of a wave through each phase
+// together; a wave alone on its SIMD has no other wave to hide its
+// latencies, and the LDS path measured slower there.
 //
 // Stage 2 (sae_merge_kernel): one workgroup per subscribed token gathers the
 // candidates of all tiles and selects the exact top-k of that pool (a radix
@@ -147,6 +150,214 @@ sae_fold_kernel(const uint16_t* __restrict__ Wp, const uint16_t* __restrict__ b_
     if (lane_id() == 0) c_fold[j] = bf16_to_f32(b_enc[j]) - acc;
 }
 
+// ------------------------------------------------ wave-local slice selection
+// After a tile's K loop, its values are written to LDS token-major (one row
+// of kSelStride floats per token, 256 latents each) and the 256 values of a
+// token are taken by 8 lanes of one wave, 32 contiguous latents per lane.
+// The threshold search, the counts and the emission prefix then reduce over
+// those 8 lanes with DPP moves: no barrier and no LDS atomic between the
+// waves.  Each lane works on NT tokens at once (independent chains that
+// fill each other's latencies).  The row stride is 4 words past a multiple
+// of the 64 LDS banks, so the 16-byte reads of the 64 lanes at one step
+// spread over every bank.
+constexpr int kSelStride = 260;  // floats per token row
+
+// DPP lane moves inside groups of 8 lanes (quad_perm [1,0,3,2] and
+// [2,3,0,1], row_half_mirror, row_shr:n; every source lane is active)
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+    return __int_as_float(dpp_i<CTRL>(__float_as_int(v)));
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141;
+__device__ __forceinline__ float sum8(float v) {
+    v += dpp_f<kDppXor1>(v);
+    v += dpp_f<kDppXor2>(v);
+    return v + dpp_f<kDppHalfMirror>(v);
+}
+__device__ __forceinline__ int isum8(int v) {
+    v += dpp_i<kDppXor1>(v);
+    v += dpp_i<kDppXor2>(v);
+    return v + dpp_i<kDppHalfMirror>(v);
+}
+__device__ __forceinline__ float max8(float v) {
+    v = fmaxf(v, dpp_f<kDppXor1>(v));
+    v = fmaxf(v, dpp_f<kDppXor2>(v));
+    return fmaxf(v, dpp_f<kDppHalfMirror>(v));
+}
+// sum over the lanes q' < q of the group of 8 (q = lane & 7)
+__device__ __forceinline__ int excl_scan8(int v, int q) {
+    int incl = v;
+    int y = dpp_i<0x111>(incl);  // row_shr:1
+    incl += q >= 1 ? y : 0;
+    y = dpp_i<0x112>(incl);      // row_shr:2
+    incl += q >= 2 ? y : 0;
+    y = dpp_i<0x114>(incl);      // row_shr:4
+    incl += q >= 4 ? y : 0;
+    return incl - v;
+}
+
+// The selection of NT tokens over one 256-latent slice each: per token a
+// threshold tau with lo_cnt <= count(pre >= tau) <= cap (first guess
+// mean + z * stdev of the 256 values, then bisection on the value), and
+// every latent with pre >= tau written to dst[t][0 .. count) as (fp32 bits,
+// latent), with the count and tau beside it.  vrow[t]: token t's LDS row;
+// q = lane & 7 takes latents [32q, 32q + 32); lat0: the slice's first
+// latent.  Every lane of the wave calls it (the cross-lane steps are
+// wave-wide); the lanes of a token with valid[t] == false take part in them
+// and write nothing.  With TRIM, the values above mean + 5 stdev are left
+// out of the statistics behind the first guess (a few strong latents would
+// otherwise lift it for the whole slice).
+template <bool TRIM, int NT>
+__device__ __forceinline__ void select_slices(const float* const (&vrow)[NT], int q,
+                                              const bool (&valid)[NT], float z, int lo_cnt,
+                                              int cap, int32_t lat0, uint2* const (&dst)[NT],
+                                              int32_t* const (&cnt_out)[NT],
+                                              float* const (&tau_out)[NT]) {
+    float x[NT][32];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        const float4* src = reinterpret_cast<const float4*>(vrow[t]);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const float4 v = src[8 * q + i];
+            x[t][4 * i] = v.x;
+            x[t][4 * i + 1] = v.y;
+            x[t][4 * i + 2] = v.z;
+            x[t][4 * i + 3] = v.w;
+        }
+    }
+    float tau[NT], s1[NT], s2[NT], mx[NT], mu[NT], sd[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        float a = 0.0f, b = 0.0f, c = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 32; ++i) {
+            a += x[t][i];
+            b = fmaf(x[t][i], x[t][i], b);
+            if (TRIM) c = fmaxf(c, x[t][i]);
+        }
+        s1[t] = a;
+        s2[t] = b;
+        mx[t] = c;
+    }
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        s1[t] = sum8(s1[t]);
+        s2[t] = sum8(s2[t]);
+        if (TRIM) mx[t] = max8(mx[t]);
+        mu[t] = s1[t] * (1.0f / kBM);
+        sd[t] = sqrtf(fmaxf(s2[t] * (1.0f / kBM) - mu[t] * mu[t], 0.0f));
+        tau[t] = mu[t] + z * sd[t];
+    }
+    if (TRIM) {
+        bool trim[NT], any = false;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            trim[t] = valid[t] && mx[t] > mu[t] + kTrimZ * sd[t];
+            any = any || trim[t];
+        }
+        if (wave_ballot(any)) {  // uniform
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const float cut = mu[t] + kTrimZ * sd[t];
+                float e1 = 0.0f, e2 = 0.0f;
+                int ne = 0;
+#pragma unroll
+                for (int i = 0; i < 32; ++i) {
+                    const bool o = x[t][i] > cut;
+                    ne += o ? 1 : 0;
+                    e1 += o ? x[t][i] : 0.0f;
+                    e2 = fmaf(o ? x[t][i] : 0.0f, x[t][i], e2);
+                }
+                e1 = sum8(e1);
+                e2 = sum8(e2);
+                ne = isum8(ne);
+                if (trim[t]) tau[t] = trimmed_guess(s1[t] - e1, s2[t] - e2, kBM - ne, z);
+            }
+        }
+    }
+    float lo[NT], hi[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        lo[t] = -INFINITY;
+        hi[t] = INFINITY;
+    }
+    for (int it = 0; it < kRefineIters; ++it) {
+        int c[NT];
+        bool bad[NT], any = false;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            int k = 0;
+#pragma unroll
+            for (int i = 0; i < 32; ++i) k += x[t][i] >= tau[t] ? 1 : 0;
+            c[t] = k;
+        }
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            c[t] = isum8(c[t]);
+            bad[t] = valid[t] && (c[t] > cap || c[t] < lo_cnt);
+            any = any || bad[t];
+        }
+        if (!wave_ballot(any)) break;  // uniform
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            if (!bad[t]) continue;
+            if (c[t] > cap) lo[t] = tau[t];
+            else hi[t] = tau[t];
+            if (it == kRefineIters - 1) {
+                // out of rounds: a threshold whose count is known to be below
+                // lo_cnt (or +inf, count 0); the merge then checks exactness
+                tau[t] = hi[t];
+            } else if (isfinite(lo[t]) && isfinite(hi[t])) {
+                tau[t] = 0.5f * (lo[t] + hi[t]);
+            } else {
+                // step away from the bad side by a growing fraction of |tau| + 1
+                const float step = ldexpf(0.25f * (fabsf(tau[t]) + 1.0f), it);
+                tau[t] = isfinite(hi[t]) ? tau[t] - step : tau[t] + step;
+            }
+        }
+    }
+    // emission: this lane's selected latents go to the slots after those of
+    // the lanes before it in the token's group of 8
+    uint32_t m[NT];
+    int base[NT], total[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        uint32_t b = 0;
+#pragma unroll
+        for (int i = 0; i < 32; ++i) b |= (x[t][i] >= tau[t] ? 1u : 0u) << i;
+        m[t] = b;
+    }
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        const int cl = __popc(m[t]);
+        base[t] = excl_scan8(cl, q);
+        total[t] = isum8(cl);
+    }
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        if (!valid[t]) continue;
+        uint32_t b = m[t];
+        int slot = base[t];
+        while (b != 0) {
+            const int i = __builtin_ctz(b);
+            b &= b - 1;
+            if (slot < cap)
+                dst[t][slot] = make_uint2(__float_as_uint(vrow[t][32 * q + i]),
+                                          static_cast<uint32_t>(lat0 + 32 * q + i));
+            ++slot;
+        }
+        if (q == 0) {
+            *cnt_out[t] = min(total[t], cap);
+            *tau_out[t] = tau[t];
+        }
+    }
+}
+
 // ---------------------------------------------- GEMM + candidate emission
 __global__ void __launch_bounds__(kEncThreads, 1)
 sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
@@ -159,17 +370,12 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
                   int32_t r_Rmax, int32_t r_Tmax, int32_t r_napps, int32_t r_bit,
                   uint32_t* __restrict__ r_mask, int32_t* __restrict__ r_count,
                   int32_t* __restrict__ r_lists, uint32_t* __restrict__ r_err) {
-    __shared__ uint4 xs[2][kBN * 8];          // 2 x 16 KiB token chunks
+    // K loop: two 16 KiB token chunks; epilogue: the tile's 128 token rows
+    __shared__ uint4 lds_main[kBN * kSelStride / 4];
+    static_assert(kBN * kSelStride / 4 >= 2 * kBN * 8, "token chunks fit");
     __shared__ int32_t list_s[kRouteMaxT];    // the app's token list (in-kernel route build)
     __shared__ int32_t rtot_s[kEncWaves];
-    __shared__ float red1[kEncWaves][kBN];    // per-wave partials of the epilogue
-    __shared__ float red2[kEncWaves][kBN];
-    __shared__ float red3[kEncWaves][kBN];    // trim partials (not read by the statistics)
-    __shared__ float red4[kEncWaves][kBN];
-    __shared__ int cnt_s[kBN];
-    __shared__ int ne_s[kBN];
-    __shared__ float tau_s[kBN];
-    __shared__ uint4 stage4[kBN * kMaxCap / 2];  // per token: up to kMaxCap pairs
+    uint4 (*xs)[kBN * 8] = reinterpret_cast<uint4 (*)[kBN * 8]>(lds_main);
 
     // With r_req given, the kernel also builds the step's routing (in place
     // of a route-build launch): every workgroup builds its app's token list
@@ -349,179 +555,31 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
 
     // ---------------------------------------------------------- epilogue
     // acc[nb][r] holds latent 32*wave + 8*(r/4) + 4*g + r%4 of token
-    // 32*nb + j32 (the 32x32 MFMA output layout).  Lanes j32 and j32 + 32 of
-    // all eight waves together hold the 256 latents of one token.
-    // per-token mean and variance over the tile's 256 latents (and this
-    // lane's largest value, which tells whether it holds any to trim)
-    if (tid < kBN) {
-        cnt_s[tid] = 0;
-        ne_s[tid] = 0;
-    }
-    float mx[4];
+    // 32*nb + j32 (the 32x32 MFMA output layout).  Every lane writes its
+    // values to the tile's 128 token rows in LDS; then wave w selects for
+    // rows 16w .. 16w + 15, eight lanes per row, two rows per lane.
+    __syncthreads();  // every wave is done with the token chunks
+    float* V = reinterpret_cast<float*>(lds_main);
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
-        float s1 = 0.0f, s2 = 0.0f;
-        mx[nb] = -INFINITY;
+        float* rowp = V + (32 * nb + j32) * kSelStride + 32 * wave + 4 * g;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            s1 += acc[nb][r];
-            s2 = fmaf(acc[nb][r], acc[nb][r], s2);
-            mx[nb] = fmaxf(mx[nb], acc[nb][r]);
-        }
-        s1 += __shfl_xor(s1, 32, kWave);
-        s2 += __shfl_xor(s2, 32, kWave);
-        if (g == 0) {
-            red1[wave][32 * nb + j32] = s1;
-            red2[wave][32 * nb + j32] = s2;
-        }
+        for (int j = 0; j < 4; ++j)
+            *reinterpret_cast<float4*>(rowp + 8 * j) =
+                make_float4(acc[nb][4 * j], acc[nb][4 * j + 1], acc[nb][4 * j + 2],
+                            acc[nb][4 * j + 3]);
     }
     __syncthreads();
-    float tau[4], lo_b[4], hi_b[4], sum1[4], sum2[4], cut[4];
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb) {
-        const int n = 32 * nb + j32;
-        float s1 = 0.0f, s2 = 0.0f;
-#pragma unroll
-        for (int w = 0; w < kEncWaves; ++w) {
-            s1 += red1[w][n];
-            s2 += red2[w][n];
-        }
-        const float mu = s1 * (1.0f / kBM);
-        const float sd = sqrtf(fmaxf(s2 * (1.0f / kBM) - mu * mu, 0.0f));
-        tau[nb] = mu + z_guess * sd;
-        sum1[nb] = s1;
-        sum2[nb] = s2;
-        cut[nb] = mu + kTrimZ * sd;
-        lo_b[nb] = -INFINITY;  // count(lo_b) > cap
-        hi_b[nb] = INFINITY;   // count(hi_b) < lo_cnt (or 0)
-    }
-    // Emission passes.  Each pass places every latent with pre >= tau in its
-    // token's LDS staging block (one LDS atomic per lane and token reserves
-    // the slots, so the atomics also count the token over all eight waves).
-    // The first pass also sums, per token, the values above the trim cut.
-    // Then every token checks its count against [lo_cnt, cap]; a token
-    // outside it, or one with values above the cut (it takes its guess
-    // again from the statistics without them), moves its tau, and the pass
-    // is repeated for the whole tile.  Usually the first guess holds and one
-    // pass is all.
-    uint2* stage = reinterpret_cast<uint2*>(stage4);
-    for (int it = 0;; ++it) {
-        if (it > 0) {
-            // every thread read the last pass's counts before the barrier
-            // that ended it
-            if (tid < kBN) cnt_s[tid] = 0;
-            __syncthreads();
-        }
-#pragma unroll
-        for (int nb = 0; nb < 4; ++nb) {
-            const int n = 32 * nb + j32;
-            // bit r: acc[nb][r] >= tau; the selected values are then taken
-            // one per round by a select tree on the bits of r (no dynamic
-            // register indexing), so a lane with none does no further work
-            uint32_t m = 0;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) m |= (acc[nb][r] >= tau[nb] ? 1u : 0u) << r;
-            if (n >= ntok) m = 0;
-            if (m != 0) {
-                int slot = atomicAdd(&cnt_s[n], __popc(m));
-                uint2* dst = stage + n * cap;
-                while (m != 0) {
-                    const int r = __builtin_ctz(m);
-                    m &= m - 1;
-                    const float val = pick16(acc[nb], r);
-                    if (slot < cap)
-                        dst[slot] = make_uint2(__float_as_uint(val),
-                                               static_cast<uint32_t>(mt * kBM + 32 * wave +
-                                                                     8 * (r >> 2) + 4 * g + (r & 3)));
-                    ++slot;
-                }
-            }
-            if (it == 0) {
-                float e1 = 0.0f, e2 = 0.0f;
-                int ne = 0;
-                if (mx[nb] > cut[nb]) {
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const bool o = acc[nb][r] > cut[nb];
-                        ne += o ? 1 : 0;
-                        e1 += o ? acc[nb][r] : 0.0f;
-                        e2 = fmaf(o ? acc[nb][r] : 0.0f, acc[nb][r], e2);
-                    }
-                    if (ne > 0) atomicAdd(&ne_s[n], ne);
-                }
-                e1 += __shfl_xor(e1, 32, kWave);
-                e2 += __shfl_xor(e2, 32, kWave);
-                if (g == 0) {
-                    red3[wave][n] = e1;
-                    red4[wave][n] = e2;
-                }
-            }
-            if (wave == 0 && g == 0) tau_s[n] = tau[nb];
-        }
-        __syncthreads();
-        bool any_bad = false;
-#pragma unroll
-        for (int nb = 0; nb < 4; ++nb) {
-            const int n = 32 * nb + j32;
-            if (n >= ntok) continue;
-            const int cn = cnt_s[n];
-            if (it == 0 && ne_s[n] > 0) {
-                float e1 = 0.0f, e2 = 0.0f;
-#pragma unroll
-                for (int w = 0; w < kEncWaves; ++w) {
-                    e1 += red3[w][n];
-                    e2 += red4[w][n];
-                }
-                const float t = trimmed_guess(sum1[nb] - e1, sum2[nb] - e2, kBM - ne_s[n], z_guess);
-                if (t > lo_b[nb] && t < hi_b[nb]) {
-                    tau[nb] = t;
-                    any_bad = true;
-                    continue;
-                }
-            }
-            bool bad = false;
-            if (cn > cap) {
-                lo_b[nb] = tau[nb];
-                bad = true;
-            } else if (cn < lo_cnt) {
-                hi_b[nb] = tau[nb];
-                bad = true;
-            }
-            if (bad) {
-                any_bad = true;
-                if (it >= kRefineIters - 1) {
-                    // out of passes: a threshold whose count is known to be
-                    // <= cap (the merge then checks exactness)
-                    tau[nb] = hi_b[nb];
-                } else if (isfinite(lo_b[nb]) && isfinite(hi_b[nb])) {
-                    tau[nb] = 0.5f * (lo_b[nb] + hi_b[nb]);
-                } else {
-                    // step away from the bad side by a growing fraction of |tau|+1
-                    const float step = ldexpf(0.25f * (fabsf(tau[nb]) + 1.0f), it);
-                    tau[nb] = isfinite(hi_b[nb]) ? tau[nb] - step : tau[nb] + step;
-                }
-            }
-        }
-        if (!__syncthreads_or(any_bad)) break;
-        if (it >= kRefineIters) break;  // the pass with tau = hi_b was the last
-    }
-    // write-out: four threads per token, 16-byte stores (two pairs each), and
-    // the count and threshold beside the block
-    static_assert(kEncThreads == 4 * kBN, "four threads per token");
-    {
-        const int n = tid >> 2, part = tid & 3;
-        if (n < ntok) {
-            const int c = min(cnt_s[n], cap);
-            const int64_t row = static_cast<int64_t>(n0 + n) * n_mt + mt;
-            const uint4* src = stage4 + n * (cap / 2);
-            uint4* dst = reinterpret_cast<uint4*>(cand + row * cap);
-            for (int q = part; 2 * q < c; q += 4) dst[q] = src[q];
-            if (part == 0) {
-                tile_cnt[row] = c;
-                tile_tau[row] = tau_s[n];
-            }
-        }
-    }
+    const int q = lane & 7;
+    const int r0 = 16 * wave + (lane >> 3), r1 = r0 + 8;
+    const int64_t row0 = static_cast<int64_t>(n0 + r0) * n_mt + mt;
+    const int64_t row1 = static_cast<int64_t>(n0 + r1) * n_mt + mt;
+    const float* const vr[2] = {V + r0 * kSelStride, V + r1 * kSelStride};
+    const bool ok[2] = {r0 < ntok, r1 < ntok};
+    uint2* const dst[2] = {cand + row0 * cap, cand + row1 * cap};
+    int32_t* const co[2] = {tile_cnt + row0, tile_cnt + row1};
+    float* const to[2] = {tile_tau + row0, tile_tau + row1};
+    select_slices<true, 2>(vr, q, ok, z_guess, lo_cnt, cap, mt * kBM, dst, co, to);
 }
 
 // ------------------------------------------ prefill GEMM + candidate emission
