@@ -1,21 +1,24 @@
 #!/usr/bin/env python3
 """Benchmark of the per-layer MI hook step on one MI355X.
 
-Default workload: the decode-shaped SAE hook step (d=4096, m=65536 latents,
-TopK k=64, 256 decode tokens of which 128 requests subscribe, readback into
-a 256-row ring): routing, SAE encode + top-k, ring compaction.  A step is
-one full pass of that hook step, captured once as a HIP graph and replayed;
-inputs are resident in HBM before timing starts.  The prefill-shaped SAE
-step (8192 tokens, m=131072, k=32, plus 4 per-token and 4 pooled probes) is
-timed in the same run and reported under "prefill".
+Headline (`value`): the decode-shaped SAE hook step (d=4096, m=65536
+latents, TopK k=64, 256 decode tokens of which 128 requests subscribe,
+readback into a 256-row ring): routing, SAE encode + top-k, ring readback.
+A step is one full pass of that hook step, captured as a HIP graph and
+replayed; inputs are resident in HBM before timing starts.  The dictionary
+(0.5 GiB) is larger than the 256 MB last-level cache and each timed step
+uses one of several copies in rotation, so every step streams it from HBM.
 
-The dictionaries (0.5 GiB and 1 GiB) are larger than the 256 MB
-last-level cache, and each timed replay uses one of several copies in
-rotation, so every replay streams its dictionary from HBM.
+Timed in the same run, each in its own sub-record: the toy step (c1), the
+4-layer steering + probe decode step (c2, hot and cold caches, conditional
+filters, parameter updates on a step graph), the prefill step (c4), the
+70B-shaped decode step with 8 SAE clamp apps (c5), the merge's repair path
+on adversarial inputs, per-stage times of every step, and the CPU oracle on
+this host's cores for every configuration.
 
 Prints one JSON line: hooked tokens/s per layer, the roofline fraction of
 the dominant kernel (the encode GEMM, timed live with HIP events on the
-stream it runs on) and the CPU oracle's rate on this host's cores.
+stream it runs on) and the CPU oracle's rate.
 """
 import argparse
 import json
@@ -28,8 +31,9 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
+SETTLE_S = 0.3                  # untimed replays before the warmup steps
 
 
 def parse():
@@ -40,13 +44,11 @@ def parse():
     ap.add_argument("--prefill-steps", type=int, default=20)
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--no-decode", action="store_true",
-                    help="profile only the prefill step (the JSON line then has no value)")
+                    help="skip the decode steps (the JSON line then has no value)")
+    ap.add_argument("--no-c5", action="store_true",
+                    help="skip the 70B-shaped decode step (8 dictionaries of 1 GiB)")
+    ap.add_argument("--no-repair", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0,
-                    help="target CPU time of the oracle sample")
-    ap.add_argument("--c5", action="store_true",
-                    help="also time the 70B-shaped decode step (d=8192, T=R=512, 16 steering, "
-                         "8 probe and 8 SAE clamp apps with 1 GiB dictionaries each)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run three device copies of 512 MiB, the known-size reference "
                          "for scaling HBM counter readings")
@@ -83,6 +85,8 @@ def measured_traffic(workload):
     return float(v) if v else None
 
 
+# ------------------------------------------------------------------ timing
+
 STEPS_PER_GRAPH = 4
 
 
@@ -105,6 +109,22 @@ class MultiStep:
         self.full = capture(per_graph)
         self.rest = capture(rest) if rest else None
         set_copy(copies[0])
+
+
+def settle(torch, replay, seconds=SETTLE_S):
+    """Untimed replays for `seconds`, so that the timed steps run at the
+    device's steady clocks (generating the inputs leaves the GPU idle
+    beforehand)."""
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    n = 0
+    while time.perf_counter() - t0 < seconds:
+        replay()
+        n += 1
+        if n % 8 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    return n
 
 
 def time_step_runs(torch, ms, n_steps, runs=7):
@@ -134,8 +154,8 @@ def time_step_runs(torch, ms, n_steps, runs=7):
     return ev[0].elapsed_time(ev[-1]) / n_steps, per_run, steps
 
 
-def time_replays(torch, rot, n):
-    """Average ms per replay of `rot` over n replays, HIP events on the
+def time_replays(torch, replay, n):
+    """Average ms per call of `replay` over n calls, HIP events on the
     current stream (the stream the kernels run on)."""
     s = torch.cuda.current_stream()
     e0 = torch.cuda.Event(enable_timing=True)
@@ -143,7 +163,7 @@ def time_replays(torch, rot, n):
     torch.cuda.synchronize()
     e0.record(s)
     for _ in range(n):
-        rot.replay()
+        replay()
     e1.record(s)
     e1.synchronize()
     return e0.elapsed_time(e1) / n
@@ -170,6 +190,66 @@ def run_stats(per_run, sizes, tokens_per_step, seed=0):
             "tokens_per_s_ci95": [float(lo), float(hi)]}
 
 
+def stage_times(torch, step, n, before=None, warm=3):
+    """Average time (us) of each stage of a hook step: n steps enqueued
+    eagerly, back to back, with a HIP event recorded on the step's stream
+    right before each stage and after the last (HookStep.run's `mark`).  A
+    stage's time runs from its event to the next one: its kernels and the
+    dispatch gap before them.  The host enqueues far faster than the GPU
+    runs a step, so the GPU sees the same back-to-back sequence as in the
+    captured step.  `before(i)` runs ahead of step i, outside every stage
+    (dictionary rotation, restore copies)."""
+    recs = []
+    for i in range(n + warm):
+        if before is not None:
+            before(i)
+        evs = []
+
+        def mark(name, evs=evs):
+            e = torch.cuda.Event(enable_timing=True)
+            e.record()
+            evs.append((name, e))
+        step.run(mark=mark)
+        if i >= warm:
+            recs.append(evs)
+    torch.cuda.synchronize()
+    acc = {}
+    for evs in recs:
+        for (name, ea), (_, eb) in zip(evs[:-1], evs[1:]):
+            acc.setdefault(name, []).append(ea.elapsed_time(eb) * 1e3)
+    return {k: round(float(np.mean(v)), 3) for k, v in acc.items()}
+
+
+def stage_times_graph(torch, step, n=10, before=None):
+    """Per stage of a hook step: the GPU time (us) of one launch of that
+    stage alone, from a graph of R back-to-back launches of it (the same
+    arguments as in the step; the device state it reads is the one a full
+    step left) replayed n times, divided by R.  R is 20 for stages under
+    0.2 ms, else 1.  This is the time the stage takes inside a captured
+    step, launch of its kernels in the graph included; unlike events
+    between eager launches, it does not depend on the host's enqueue rate
+    for short kernels.  `before()` runs ahead of the full step (restore
+    copies)."""
+    names = step.stage_names()
+    if before is not None:
+        before()
+    step.run()
+    torch.cuda.synchronize()
+    out = {}
+    for name in names:
+        reps = 1
+        for _ in range(2):
+            g = graph_of(torch, lambda: step.run(only=name, repeat=reps))
+            g.replay()
+            ms = time_replays(torch, g.replay, n) / reps
+            del g
+            if reps > 1 or ms > 0.2:
+                break
+            reps = 20
+        out[name] = round(ms * 1e3, 3)
+    return out
+
+
 def dictionary_copies(torch, W, min_bytes=1.5 * 2 ** 30):
     """W (a packed dictionary) and enough device copies of it that a
     rotation over them exceeds every cache."""
@@ -177,10 +257,11 @@ def dictionary_copies(torch, W, min_bytes=1.5 * 2 ** 30):
     return [W] + [W.clone() for _ in range(n - 1)]
 
 
-def bench_workload(torch, px, step, sae_layer, sae_idx, steps, warmup, encode=True):
-    """Times the full step and the encode GEMM (candidates stage)."""
-    lay = step.layers[sae_layer]
-    sae = lay.saes[sae_idx]
+def timed_sae_step(torch, step, steps, warmup, n_stage):
+    """Times a step whose first layer holds one SAE app: the step graphs
+    with the dictionary rotating over copies (settle, W warmup steps, then
+    exactly `steps` timed steps), and the per-stage times."""
+    sae = step.layers[0].saes[0]
     copies = dictionary_copies(torch, sae.W_enc)
 
     def set_copy(W):
@@ -190,34 +271,17 @@ def bench_workload(torch, px, step, sae_layer, sae_idx, steps, warmup, encode=Tr
     step.run()   # eager run once (also checks the arguments)
     torch.cuda.synchronize()
     multi = MultiStep(torch, step.run, copies, set_copy, STEPS_PER_GRAPH, steps % STEPS_PER_GRAPH)
+    settle(torch, multi.full.replay)
     for _ in range(max(1, warmup // STEPS_PER_GRAPH)):
         multi.full.replay()
     torch.cuda.synchronize()
     ms_step, per_run, sizes = time_step_runs(torch, multi, steps)
     stats = run_stats(per_run, sizes, step.wl.T_valid)
-    ms_enc = encode_in_step(torch, step, copies, set_copy, steps) if encode else None
+    stages = stage_times(torch, step, n_stage,
+                         before=lambda i: set_copy(copies[i % len(copies)]))
     set_copy(copies[0])
-    return ms_step, ms_enc, stats
-
-
-def encode_in_step(torch, step, copies, set_copy, n):
-    """Average duration of the encode GEMM stage inside the step: n steps
-    enqueued eagerly, back to back, with HIP events recorded on the step's
-    stream right before and right after that stage (the step's other
-    kernels run around it in the same order as in the captured step; the
-    host enqueues far faster than the GPU runs a step, so the GPU sees the
-    same back-to-back sequence)."""
-    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-             for _ in range(n)]
-    for i in range(3):
-        set_copy(copies[i % len(copies)])
-        step.run()
-    torch.cuda.synchronize()
-    for i, (e0, e1) in enumerate(pairs):
-        set_copy(copies[i % len(copies)])
-        step.run(marks=(e0.record, e1.record))
-    torch.cuda.synchronize()
-    return sum(a.elapsed_time(b) for a, b in pairs) / n
+    stages["graph"] = stage_times_graph(torch, step)
+    return ms_step, stats, stages, multi
 
 
 def read_ceiling(torch, nbytes, n_bufs=4, runs=7, per_run=20):
@@ -262,83 +326,28 @@ def mfma_ceiling(torch, iters=4000, runs=7, per_run=3):
     return float(np.median(rates))
 
 
-def cpu_baseline_decode(wl, budget_s):
-    """The oracle on this host's cores: one full decode SAE step is routing,
-    the encode of every subscribed token and the ring compaction; the encode
-    dominates, so a sample of subscribed tokens is encoded and the step time
-    is scaled from it."""
-    import oracle
-    L = wl.layers[0]
-    s = L.saes[0]
-    t0 = time.perf_counter()
-    tm, cnt, lists, err = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
-    t_route = time.perf_counter() - t0
-    toks = lists[0, :cnt[0]]
-    t0 = time.perf_counter()
-    oracle.sae_encode(L.h, toks[:4], s.W_enc, s.b_enc, s.b_dec, s.k)
-    per_tok = (time.perf_counter() - t0) / 4
-    n = int(min(len(toks), max(4, budget_s / max(per_tok, 1e-9))))
-    t0 = time.perf_counter()
-    idx, val, _, _ = oracle.sae_encode(L.h, toks[:n], s.W_enc, s.b_enc, s.b_dec, s.k)
-    t_enc = (time.perf_counter() - t0) / n * len(toks)
-    idx_full = np.zeros((wl.T_max, s.k), np.int32)
-    val_full = np.zeros((wl.T_max, s.k), np.uint16)
-    t0 = time.perf_counter()
-    oracle.compact([idx_full.view(np.uint8).reshape(wl.T_max, -1),
-                    val_full.view(np.uint8).reshape(wl.T_max, -1)], tm, 0, wl.req, 0, 0,
-                   np.zeros((s.ring_capacity, 16 + s.k * 6), np.uint8), 0)
-    t_compact = time.perf_counter() - t0
-    t_step = t_route + t_enc + t_compact
-    return {"value": wl.T_valid / t_step, "unit": "tokens/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": f"{n} of {len(toks)} subscribed tokens encoded over all m latents "
-                      f"(fp64), scaled to the full step; routing and compaction timed whole"}
+def graph_of(torch, fn):
+    fn()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    return g
 
 
-def main():
-    args = parse()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "the hook step runs on one GPU; sharding across GPUs is "
-                                   "described, not implemented", "n_gpus": args.gpus}))
-        sys.exit(2)
-    import torch
-    import synth
-    import paper_2607_22595_amd as px
-    from paper_2607_22595_amd.hookstep import HookStep
+# ----------------------------------------------------------- workloads
 
-    torch.cuda.set_device(0)
-    if args.calibrate_copy:
-        src = torch.empty(512 * 2 ** 20, dtype=torch.uint8, device="cuda")
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
-    out = {}
-    if not args.no_decode:
-        out, wl = run_decode(torch, px, synth, HookStep, args)
-    if not args.no_decode:
-        out["steer_probe"] = run_steer_probe(torch, synth, HookStep, args)
-    if not args.no_prefill:
-        out["prefill"] = run_prefill(torch, px, synth, HookStep, args)
-    if args.c5:
-        out["decode_70b"] = run_c5(torch, synth, HookStep, args)
-    if not args.no_cpu_baseline and not args.no_decode:
-        log("timing the CPU oracle")
-        out["cpu_baseline"] = cpu_baseline_decode(wl, args.cpu_seconds)
-    print(json.dumps(out), flush=True)
-
-
-def run_decode(torch, px, synth, HookStep, args):
-    log("generating the decode SAE workload")
+def run_decode(torch, synth, HookStep, args):
+    log("generating the decode SAE workload (c3)")
     wl = synth.make("c3")
     step = HookStep(wl)
     log("timing the decode step")
-    ms_step, ms_enc, stats = bench_workload(torch, px, step, 0, 0, args.steps, args.warmup)
+    n_stage = max(200, args.steps)
+    ms_step, stats, stages, multi = timed_sae_step(torch, step, args.steps, args.warmup, n_stage)
     s = wl.layers[0].saes[0]
     n_sub = int(np.count_nonzero(wl.sub & 1))
     enc_bytes = s.m * wl.d * 2 + s.m * 4 + n_sub * wl.d * 2   # W_enc + folded bias + tokens
+    ms_enc = stages["L0/sae0/route+encode"] * 1e-3
     achieved = enc_bytes / (ms_enc * 1e-3) / 1e9
     out = {
         "metric": "hooked tokens/sec per layer + % HBM/MFMA roofline (decode & prefill shapes)",
@@ -356,28 +365,54 @@ def run_decode(torch, px, synth, HookStep, args):
         "config": {"workload": "decode SAE hook step: route + encode/top-k + ring readback, "
                                "d=4096 m=65536 k=64 T=256 T_sub=128 ring=256",
                    "global_batch": wl.T_valid, "seq_len": 1, "parallelism": "none (1 GPU)"},
-        "roofline": {"bound": "hbm", "kernel": "sae_stream_kernel (encode GEMM)",
+        "roofline": {"bound": "hbm", "kernel": "sae_stream_kernel (encode GEMM, routing built "
+                                               "in the same launch)",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic("decode"),
-                     "ms_per_launch": ms_enc, "algorithmic_bytes": enc_bytes,
-                     "timing": "HIP events around the encode stage inside back-to-back steps"},
+                     "ms_per_launch": ms_enc, "launches_timed": n_stage,
+                     "algorithmic_bytes": enc_bytes,
+                     "timing": "HIP events on the step's stream around the encode stage, "
+                               "back-to-back eager steps, dictionary copies rotating"},
+        "settle_s": SETTLE_S,
     }
     out["step_stats"] = stats
+    out["stages_us"] = stages.pop("graph")
+    out["stages_eager_us"] = stages
     log("measuring the HBM read ceiling")
     ceil = read_ceiling(torch, s.m * wl.d * 2)
     out["roofline"].update({
         "achievable_peak": ceil, "achievable_frac": achieved / ceil,
         "achievable_how": "nontemporal 16-byte read stream over 4 rotating buffers of the "
                           "dictionary's size, back-to-back launches (libxmix_ceiling)"})
-    # "don't use, don't pay": the same captured step with no subscriber
+    # "don't use, don't pay": the same captured steps with no subscriber
     sub_saved = step.sub.clone()
     step.sub.zero_()
-    ms_zero, _, _ = bench_workload(torch, px, step, 0, 0, args.steps, args.warmup, encode=False)
+    settle(torch, multi.full.replay, 0.1)
+    ms_zero, _, _ = time_step_runs(torch, multi, max(args.steps, 100))
     step.sub.copy_(sub_saved)
+    torch.cuda.synchronize()
     out["zero_mask_step_us"] = ms_zero * 1e3
-    del step
+    del multi, step
     torch.cuda.empty_cache()
     return out, wl
+
+
+def run_toy(torch, synth, HookStep, args):
+    """c1: 16 tokens of 4 requests, fp32, one steering and one probe app."""
+    log("timing the toy step (c1)")
+    wl = synth.make("c1")
+    step = HookStep(wl)
+    g = graph_of(torch, step.run)
+    settle(torch, g.replay, 0.05)
+    ms = time_replays(torch, g.replay, max(50, args.steps))
+    res = {"workload": "toy step, 1 layer, fp32: d=256 T=16 R=4, 1 steering + 1 probe app "
+                       "(routing built inside the fused probe + steering pass: one kernel)",
+           "us_per_step": ms * 1e3,
+           "value": wl.T_valid / (ms * 1e-3), "unit": "hooked tokens/s per layer",
+           "note": "one graph launch per step: the graph's launch latency is most of it",
+           "stages_us": stage_times_graph(torch, step)}
+    del step
+    return res, wl
 
 
 def time_conditional(torch, step, wl, args):
@@ -400,20 +435,10 @@ def time_conditional(torch, step, wl, args):
     reps = 20
 
     def timed(fn):
-        fn()
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            for _ in range(reps):
-                fn()
-
-        class One:
-            def replay(self):
-                g.replay()
-        one = One()
+        g = graph_of(torch, lambda: [fn() for _ in range(reps)])
         for _ in range(args.warmup):
-            one.replay()
-        return time_replays(torch, one, args.steps) * 1e3 / reps
+            g.replay()
+        return time_replays(torch, g.replay, args.steps) * 1e3 / reps
 
     # router-logit write on a Mixtral-shaped router (8 experts, bf16 logits),
     # bits 0-3 as four router apps; -inf offsets remove experts
@@ -442,7 +467,6 @@ def time_step_graph(torch, step, args):
     zero-mask step (subscriptions buffer redirected to zeros); and a graph of
     one kernel that finds nothing to do, the floor of any graph launch."""
     import ctypes
-    import time
     import paper_2607_22595_amd as px
     hip = ctypes.CDLL("libamdhip64.so")
     hip.hipMemcpyAsync.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
@@ -531,34 +555,43 @@ def time_step_graph(torch, step, args):
 
 def run_steer_probe(torch, synth, HookStep, args):
     """The 4-layer decode step of steering and probe apps (d=4096, T=R=256,
-    bits 0-3 steer, bits 4-7 probe), captured as one graph."""
-    log("timing the 4-layer steering + probe decode step")
+    bits 0-3 steer, bits 4-7 probe), captured as one graph.  Hot: replays
+    back to back, so each step finds its rows in the caches as a layer does
+    right after the model wrote them.  Cold: before each timed step a 512 MiB
+    write evicts the caches (outside the timed interval)."""
+    log("timing the 4-layer steering + probe decode step (c2)")
     wl = synth.make("c2")
     step = HookStep(wl)
-    step.run()
-    torch.cuda.synchronize()
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
-        step.run()
-
-    class One:
-        def replay(self):
-            g.replay()
-    one = One()
+    g = graph_of(torch, step.run)
+    settle(torch, g.replay, 0.1)
     for _ in range(args.warmup):
-        one.replay()
-    ms = time_replays(torch, one, args.steps)
+        g.replay()
+    ms = time_replays(torch, g.replay, args.steps)
+    flush = torch.empty(512 * 2 ** 20, dtype=torch.uint8, device="cuda")
+    cold = []
+    for _ in range(max(20, args.steps // 4)):
+        flush.zero_()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        cold.append((e0, e1))
+    torch.cuda.synchronize()
+    ms_cold = float(np.mean([a.elapsed_time(b) for a, b in cold]))
+    del flush
     res = {"workload": "decode steering + probe step, 4 hooked layers, d=4096 T=R=256, "
                        "4 steering + 4 probe apps, subscriptions Bernoulli(0.3)",
            "us_per_step": ms * 1e3, "us_per_layer": ms * 1e3 / len(wl.layers),
+           "cold_us_per_step": ms_cold * 1e3,
            "value": wl.T_valid * len(wl.layers) / (ms * 1e-3), "unit": "hooked tokens/s per layer",
-           "hbm_bytes": step.hbm_bytes()}
+           "hbm_bytes": step.hbm_bytes(),
+           "stages_us": stage_times_graph(torch, step)}
     res["conditional_us"] = time_conditional(torch, step, wl, args)
     log("timing parameter updates on the step graph")
     res["step_graph"] = time_step_graph(torch, step, args)
-    del step
+    del step, g
     torch.cuda.empty_cache()
-    return res
+    return res, wl
 
 
 def run_c5(torch, synth, HookStep, args):
@@ -566,33 +599,22 @@ def run_c5(torch, synth, HookStep, args):
     each encoding its subscribers over its own 1 GiB dictionary, captured as
     one graph.  The eight dictionaries (8 GiB) exceed every cache, so each
     replay streams them from HBM."""
-    log("generating the 70B-shaped decode workload (8 dictionaries)")
+    log("generating the 70B-shaped decode workload (c5, 8 dictionaries)")
     wl = synth.make("c5")
     step = HookStep(wl)
     step.run()
     torch.cuda.synchronize()
     # every replay starts from the same residual rows (steering and clamping
     # write them), restored by a device copy that is timed on its own too
-    graphs = {}
-    for name, body in (("step", lambda: (step.reset(), step.run())), ("restore", step.reset)):
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            body()
-        graphs[name] = g
-
-    class One:
-        def __init__(self, g):
-            self.g = g
-
-        def replay(self):
-            self.g.replay()
+    graphs = {"step": graph_of(torch, lambda: (step.reset(), step.run())),
+              "restore": graph_of(torch, step.reset)}
     log("timing the 70B-shaped decode step")
+    settle(torch, graphs["step"].replay, 0.2)
     times = {}
     for name, g in graphs.items():
-        one = One(g)
         for _ in range(3):
-            one.replay()
-        times[name] = time_replays(torch, one, max(10, args.steps // 10))
+            g.replay()
+        times[name] = time_replays(torch, g.replay, max(10, args.steps // 10))
     ms = times["step"] - times["restore"]
     nbytes = step.hbm_bytes()
     res = {"workload": "decode step d=8192 T=R=512: 16 steering, 8 probe and 8 SAE clamp apps "
@@ -600,24 +622,26 @@ def run_c5(torch, synth, HookStep, args):
            "ms_per_step": ms, "restore_ms": times["restore"],
            "value": wl.T_valid / (ms * 1e-3), "unit": "tokens/s",
            "algorithmic_bytes": nbytes, "achieved_GBps": nbytes / (ms * 1e-3) / 1e9,
-           "frac_of_hbm_peak": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+           "frac_of_hbm_peak": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+           "stages_us": stage_times_graph(torch, step, n=3, before=step.reset)}
     del graphs
     log("timing parameter updates on the 70B-shaped step graph")
     res["step_graph"] = time_step_graph(torch, step, args)
     del step
     torch.cuda.empty_cache()
-    return res
+    return res, wl
 
 
-def run_prefill(torch, px, synth, HookStep, args):
-    log("generating the prefill workload")
+def run_prefill(torch, synth, HookStep, args):
+    log("generating the prefill workload (c4)")
     wl4 = synth.make("c4")
     step4 = HookStep(wl4)
     log("timing the prefill step")
-    ms4, ms4_enc, stats4 = bench_workload(torch, px, step4, 0, 0, args.prefill_steps,
-                                          max(2, args.warmup // 10))
+    ms4, stats4, stages4, multi = timed_sae_step(torch, step4, args.prefill_steps,
+                                                  max(2, args.warmup // 10), args.prefill_steps)
     s4 = wl4.layers[0].saes[0]
     flops = 2.0 * wl4.T_valid * s4.m * wl4.d
+    ms4_enc = stages4["L0/sae0/encode"] * 1e-3
     tf = flops / (ms4_enc * 1e-3) / 1e12
     res = {
         "workload": "prefill hook step: route + 4 token probes + 4 pooled probes + SAE "
@@ -628,11 +652,12 @@ def run_prefill(torch, px, synth, HookStep, args):
                      "kernel": "sae_xstage_kernel + sae_gemm_kernel (encode GEMM)",
                      "achieved": tf, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": tf / MFMA_BF16_PEAK_TFLOPS, "ms_per_launch": ms4_enc,
-                     "timing": "HIP events around the encode stage inside back-to-back steps",
+                     "timing": "HIP events on the step's stream around the encode stage, "
+                               "back-to-back eager steps, dictionary copies rotating",
                      "algorithmic_flops": flops,
                      "traffic": measured_traffic("prefill")},
-        "step_stats": stats4}
-    del step4
+        "step_stats": stats4, "stages_us": stages4.pop("graph"), "stages_eager_us": stages4}
+    del multi, step4
     torch.cuda.empty_cache()
     log("measuring the MFMA ceiling")
     ceil = mfma_ceiling(torch)
@@ -640,7 +665,227 @@ def run_prefill(torch, px, synth, HookStep, args):
         "achievable_peak": ceil, "achievable_frac": tf / ceil,
         "achievable_how": "32x32x16 bf16 MFMAs with register operands, 8 chains per wave, "
                           "4 waves per CU (libxmix_ceiling)"})
+    return res, wl4
+
+
+# ------------------------------------------------- repair path, worst cases
+
+def _strong_latents(synth, wl, scale=60.0):
+    """Every subscribed token's row moved along three dictionary rows, so
+    that those latents stand far above the token's others (as clamping
+    features high leaves them)."""
+    s = wl.layers[0].saes[0]
+    h = synth.bf16_bits_to_f32(wl.layers[0].h).astype(np.float64)
+    T = wl.T_max
+    picks = synth.randint("bench/strong_latents", 3 * T, 0, s.m - 1).reshape(T, 3)
+    for t in range(T):
+        for j in picks[t]:
+            w = synth.bf16_bits_to_f32(s.W_enc[j]).astype(np.float64)
+            h[t] += scale * w / np.dot(w, w)
+    u = h.astype(np.float32).view(np.uint32).astype(np.uint64)
+    wl.layers[0].h = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)  # to bf16, RNE
+
+
+def _tied_slices(wl, n_tied):
+    """n_tied 256-latent slices whose pre-activations are all exactly 40:
+    zero dictionary rows with bias 40, far above every other latent.  No
+    threshold splits a tie, so those slices emit nothing and the merge must
+    recompute them."""
+    s = wl.layers[0].saes[0]
+    n_mt = s.m // 256
+    slices = np.arange(n_mt) if n_tied >= n_mt else 1 + (n_mt // n_tied) * np.arange(n_tied)
+    W, b = s.W_enc.copy(), s.b_enc.copy()
+    for sl in slices:
+        W[256 * sl:256 * (sl + 1)] = 0
+        b[256 * sl:256 * (sl + 1)] = 0x4220  # 40.0
+    s.W_enc, s.b_enc = W, b
+
+
+def run_repair(torch, synth, HookStep, args):
+    """The merge's repair path on inputs built to defeat the candidate
+    thresholds, at the decode SAE shape (c3) and with the prefill GEMM
+    (1100 token slots, d=4096, m=131072, k=32): per case the encode and
+    merge stage times of the step."""
+    log("timing the repair path on adversarial inputs")
+    cases = [("c3 plain", {}, None, 10),
+             ("c3 strong latents (3 per token)", {}, "strong", 10),
+             ("c3 10 tied slices", {}, 10, 10),
+             ("c3 20 tied slices", {}, 20, 5),
+             ("c3 every slice tied", {}, 256, 3),
+             ("prefill GEMM, 1100 tokens, strong latents", {"T": 1100, "n_sub": 1100,
+                                                            "m": 131072, "k": 32}, "strong", 5)]
+    res = {}
+    for name, kw, kind, n in cases:
+        wl = synth.make("c3", ring_capacity=0, **kw)
+        if kind == "strong":
+            _strong_latents(synth, wl)
+        elif kind is not None:
+            _tied_slices(wl, kind)
+        step = HookStep(wl)
+        st = stage_times(torch, step, n, warm=1)
+        enc = next(v for k, v in st.items() if k.endswith("encode"))
+        res[name] = {"encode_us": enc, "merge_us": st["L0/sae0/merge"],
+                     "tokens": int(np.count_nonzero(wl.sub & 1))}
+        del step
+        torch.cuda.empty_cache()
     return res
+
+
+# ------------------------------------------------------------ CPU oracle
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _timed(fn):
+    t0 = time.perf_counter()
+    fn()
+    return time.perf_counter() - t0
+
+
+def _encode_rate(oracle, L, s, toks, n):
+    """Seconds per token of the oracle's encode over a sample of n tokens."""
+    n = max(1, min(n, len(toks)))
+    return _timed(lambda: oracle.sae_encode(L.h, toks[:n], s.W_enc, s.b_enc, s.b_dec, s.k)) / n
+
+
+def _cpu_config(oracle, name, wl, n_all, n_one):
+    """One configuration's oracle step on the host: the parts that are cheap
+    are timed whole, the SAE encodes on token samples (n_all tokens with all
+    threads, n_one single-threaded) and scaled to the full step.  Returns
+    (seconds all-core, seconds single-thread, sample description)."""
+    t = {}
+    for label, threads, n_enc in (("all", oracle_threads(oracle), n_all), ("one", 1, n_one)):
+        oracle.set_num_threads(threads)
+        total = 0.0
+        t0 = time.perf_counter()
+        tm, cnt, lists, _ = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+        total += time.perf_counter() - t0
+        for L in wl.layers:
+            if L.steer:
+                bits = [s.bit for s in L.steer]
+                v = np.stack([s.v for s in L.steer])
+                total += _timed(lambda: oracle.steer(L.h, tm, wl.req, v, bits, wl.alpha))
+            for mode in ("token", "mean"):
+                ps = [p for p in L.probes if p.mode == mode]
+                if not ps:
+                    continue
+                w = np.stack([p.w for p in ps])
+                b = np.array([p.b for p in ps], np.float32)
+                bits = [p.bit for p in ps]
+                if mode == "token":
+                    total += _timed(lambda: oracle.probe_token(L.h, tm, w, b, bits))
+                else:
+                    total += _timed(lambda: oracle.probe_mean(L.h, tm, w, b, bits,
+                                                              wl.cu_seqlens))
+            for s in L.saes:
+                toks = lists[s.bit, :cnt[s.bit]]
+                if len(toks) == 0:
+                    continue
+                total += _encode_rate(oracle, L, s, toks, n_enc) * len(toks)
+                if s.W_dec is not None:
+                    idx = np.zeros((wl.T_max, s.k), np.int32)
+                    val = np.zeros((wl.T_max, s.k), np.uint16)
+                    total += _timed(lambda: oracle.clamp_decode(L.h, tm, s.bit, idx, val,
+                                                                s.W_dec, s.clamp_ids,
+                                                                s.clamp_vals))
+                if s.ring_capacity:
+                    idx = np.zeros((wl.T_max, s.k), np.int32)
+                    val = np.zeros((wl.T_max, s.k), np.uint16)
+                    slots = np.zeros((s.ring_capacity, 16 + 6 * s.k), np.uint8)
+                    total += _timed(lambda: oracle.compact(
+                        [idx.view(np.uint8).reshape(wl.T_max, -1),
+                         val.view(np.uint8).reshape(wl.T_max, -1)], tm, s.bit, wl.req, 0,
+                        s.bit, slots, 0))
+        t[label] = total
+    oracle.set_num_threads(oracle_threads(oracle))
+    n_sae = sum(len(L.saes) for L in wl.layers)
+    sample = ("whole step" if n_sae == 0 else
+              f"whole step except the SAE encodes: {n_all} tokens per SAE app with all "
+              f"threads, {n_one} single-threaded, each over all m latents, scaled to every "
+              f"subscribed token")
+    return t["all"], t["one"], sample
+
+
+_THREADS = []
+
+
+def oracle_threads(oracle):
+    if not _THREADS:
+        _THREADS.append(oracle.num_threads())
+    return _THREADS[0]
+
+
+def cpu_baseline(wls):
+    """The CPU oracle (plain fp64 C, OpenMP over tokens) on this host: per
+    configuration, tokens per second per hooked layer with all threads and
+    with one thread.  The headline figure is the decode SAE step (c3)."""
+    import oracle
+    threads = oracle_threads(oracle)
+    plan = {"c1": (0, 0), "c2": (0, 0), "c3": (128, 6), "c4": (48, 2), "c5": (8, 1)}
+    per = {}
+    for name, wl in wls.items():
+        if wl is None:
+            continue
+        n_all, n_one = plan[name]
+        log(f"timing the CPU oracle on {name}")
+        t_all, t_one, sample = _cpu_config(oracle, name, wl, n_all, n_one)
+        layers = len(wl.layers)
+        per[name] = {"tokens_per_s_all_threads": wl.T_valid * layers / t_all,
+                     "tokens_per_s_single_thread": wl.T_valid * layers / t_one,
+                     "step_s_all_threads": t_all, "step_s_single_thread": t_one,
+                     "single_thread": "measured" if name in ("c1", "c2") else
+                     "extrapolated from the sample",
+                     "sample": sample}
+    head = per.get("c3") or next(iter(per.values()))
+    return {"value": head["tokens_per_s_all_threads"], "unit": "tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": "decode SAE step (c3): " + head["sample"],
+            "cpu_model": _cpu_model(), "nproc": os.cpu_count(), "per_config": per}
+
+
+# ------------------------------------------------------------------ main
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "the hook step runs on one GPU; sharding across GPUs is "
+                                   "described, not implemented", "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    import synth
+    from paper_2607_22595_amd.hookstep import HookStep
+
+    torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        src = torch.empty(512 * 2 ** 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    out = {}
+    wls = {}
+    if not args.no_decode:
+        out, wls["c3"] = run_decode(torch, synth, HookStep, args)
+        out["steer_probe"], wls["c2"] = run_steer_probe(torch, synth, HookStep, args)
+        out["toy"], wls["c1"] = run_toy(torch, synth, HookStep, args)
+    if not args.no_prefill:
+        out["prefill"], wls["c4"] = run_prefill(torch, synth, HookStep, args)
+    if not args.no_decode and not args.no_c5:
+        out["decode_70b"], wls["c5"] = run_c5(torch, synth, HookStep, args)
+    if not args.no_repair:
+        out["repair"] = run_repair(torch, synth, HookStep, args)
+    if not args.no_cpu_baseline and wls:
+        out["cpu_baseline"] = cpu_baseline(wls)
+    print(json.dumps(out), flush=True)
 
 
 if __name__ == "__main__":

@@ -33,6 +33,8 @@ def _load():
     lib.oracle_round_bf16.argtypes = [ctypes.c_double]
     lib.oracle_round_bf16.restype = ctypes.c_uint16
     lib.oracle_num_threads.restype = ctypes.c_int
+    lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
+    lib.oracle_set_num_threads.restype = None
     lib.oracle_route.argtypes = [vp, i32, i32, vp, i32, i32, vp, vp, vp, vp]
     lib.oracle_steer.argtypes = [vp, ctypes.c_int, i32, i32, vp, vp, vp, vp, vp, i32]
     lib.oracle_router_write.argtypes = [vp, ctypes.c_int, i32, i32, vp, vp, vp, i32]
@@ -65,6 +67,11 @@ def _p(a):
 
 def num_threads() -> int:
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads the oracle's parallel loops use from now on."""
+    _load().oracle_set_num_threads(int(n))
 
 
 def round_bf16(x: float) -> int:

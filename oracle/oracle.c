@@ -74,6 +74,16 @@ int oracle_num_threads(void) {
 #endif
 }
 
+/* Threads of the parallel loops below (n < 1: leave unchanged); for timing
+ * the oracle single-threaded beside its all-core runs. */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* ----------------------------------------------------------------- routing
  * Token -> request -> app bitmask (Sec. 4.2 "Toggling semantics": an app is
  * deployed for every request but active only for the requests that turned it

@@ -161,12 +161,28 @@ class HookStep:
         for lay in self.layers:
             lay.h.copy_(lay.h_in)
 
-    def run(self, stream=None, marks=None):
-        """Enqueue one full hook step (all layers) on `stream`.  `marks`, if
-        given, is a pair of host callables invoked while enqueueing, right
-        before and right after the encode GEMM stage of each SAE app (e.g. to
-        record timing events); the SAE call is then issued as its two stages,
-        which enqueues the same kernels."""
+    def run(self, stream=None, mark=None, only=None, repeat=1):
+        """Enqueue one full hook step (all layers) on `stream`.
+
+        mark: a host callable invoked while enqueueing with the name of each
+        stage right before its launch, and with "end" after the last one
+        (e.g. to record timing events between the stages); an SAE encode is
+        then issued as its two stages ("...encode" and "merge"), which
+        enqueues the same kernels.
+        only, repeat: enqueue only the stage named `only` (same arguments as
+        in the full step; the device state it reads, such as the routing or
+        the encode's candidates, is whatever an earlier step left), `repeat`
+        times in a row, to time one stage on its own (repeat=0 launches
+        nothing)."""
+        def issue(name, call):
+            if only is not None and name != only:
+                return
+            if mark is not None:
+                mark(name)
+            for _ in range(repeat):
+                call()
+
+        split = mark is not None or only is not None
         # the kernel that first reads the routing builds it when it can: the
         # first layer's first SAE encode, or its fused probes + steering pass
         # when that is the layer's only read
@@ -183,7 +199,9 @@ class HookStep:
                          and len(first.probes) == 1
                          and first.probes[0].mode == XMIX_PROBE_TOKEN)
         if not (route_in_encode or route_in_pass):
-            xmix_route_build(self.req, self.T_valid, self.sub, self.route, self.err, stream)
+            issue("route", lambda: xmix_route_build(self.req, self.T_valid, self.sub, self.route,
+                                                    self.err, stream))
+        modes = {XMIX_PROBE_TOKEN: "token", XMIX_PROBE_MEAN: "mean", XMIX_PROBE_LAST: "last"}
         for li, lay in enumerate(self.layers):
             fused = None  # the token probes that run in one pass with the steering
             if self.fuse_steer_probe and lay.steer_v is not None:
@@ -191,57 +209,78 @@ class HookStep:
             for p in lay.probes:
                 if p is fused:
                     continue
-                xmix_probe_score(lay.h, self.route, p.w, p.b, p.bits, p.mode, p.logit, p.score,
-                                 cu_seqlens=self.cu, ws=p.ws, stream=stream)
+                issue(f"L{li}/probe_{modes[p.mode]}",
+                      lambda p=p, lay=lay: xmix_probe_score(
+                          lay.h, self.route, p.w, p.b, p.bits, p.mode, p.logit, p.score,
+                          cu_seqlens=self.cu, ws=p.ws, stream=stream))
             for i, s in enumerate(lay.saes):
                 routed = route_in_encode and li == 0 and i == 0
-                if marks is not None or routed:
-                    if marks is not None:
-                        marks[0]()
+                name = f"L{li}/sae{s.bit}"
+                if split or routed:
                     if routed:
-                        xmix_route_sae_encode_candidates(self.req, self.T_valid, self.sub,
-                                                         self.route, self.err, lay.h, s.bit,
-                                                         s.W_enc, s.b_enc, s.b_dec, s.c_fold,
-                                                         s.k, s.ws, stream)
+                        issue(f"{name}/route+encode",
+                              lambda s=s, lay=lay: xmix_route_sae_encode_candidates(
+                                  self.req, self.T_valid, self.sub, self.route, self.err, lay.h,
+                                  s.bit, s.W_enc, s.b_enc, s.b_dec, s.c_fold, s.k, s.ws, stream))
                     else:
-                        xmix_sae_encode_candidates(lay.h, self.route, s.bit, s.W_enc, s.b_enc,
-                                                   s.b_dec, s.c_fold, s.k, s.ws, stream)
-                    if marks is not None:
-                        marks[1]()
+                        issue(f"{name}/encode",
+                              lambda s=s, lay=lay: xmix_sae_encode_candidates(
+                                  lay.h, self.route, s.bit, s.W_enc, s.b_enc, s.b_dec, s.c_fold,
+                                  s.k, s.ws, stream))
                     if s.ring is not None and self.fuse_readback:
-                        xmix_sae_merge_topk_ring(lay.h, self.route, s.bit, s.W_enc, s.c_fold,
-                                                 s.k, s.idx, s.val, s.ws, self.req,
-                                                 lay.layer_id, s.bit, s.ring, stream)
+                        issue(f"{name}/merge",
+                              lambda s=s, lay=lay: xmix_sae_merge_topk_ring(
+                                  lay.h, self.route, s.bit, s.W_enc, s.c_fold, s.k, s.idx, s.val,
+                                  s.ws, self.req, lay.layer_id, s.bit, s.ring, stream))
                     else:
-                        xmix_sae_merge_topk(lay.h, self.route, s.bit, s.W_enc, s.c_fold, s.k,
-                                            s.idx, s.val, s.ws, stream)
+                        issue(f"{name}/merge",
+                              lambda s=s, lay=lay: xmix_sae_merge_topk(
+                                  lay.h, self.route, s.bit, s.W_enc, s.c_fold, s.k, s.idx, s.val,
+                                  s.ws, stream))
                 elif s.ring is not None and self.fuse_readback:
                     # the merge writes the ring rows itself
-                    xmix_sae_encode_topk_ring(lay.h, self.route, s.bit, s.W_enc, s.b_enc, s.b_dec,
-                                              s.c_fold, s.k, s.idx, s.val, s.ws, self.req,
-                                              lay.layer_id, s.bit, s.ring, stream)
+                    issue(name, lambda s=s, lay=lay: xmix_sae_encode_topk_ring(
+                        lay.h, self.route, s.bit, s.W_enc, s.b_enc, s.b_dec, s.c_fold, s.k, s.idx,
+                        s.val, s.ws, self.req, lay.layer_id, s.bit, s.ring, stream))
                 else:
-                    xmix_sae_encode_topk(lay.h, self.route, s.bit, s.W_enc, s.b_enc, s.b_dec,
-                                         s.c_fold, s.k, s.idx, s.val, s.ws, stream)
+                    issue(name, lambda s=s, lay=lay: xmix_sae_encode_topk(
+                        lay.h, self.route, s.bit, s.W_enc, s.b_enc, s.b_dec, s.c_fold, s.k, s.idx,
+                        s.val, s.ws, stream))
             if fused is not None and route_in_pass and li == 0:
-                xmix_route_steer_probe(self.req, self.T_valid, self.sub, self.route, self.err,
-                                       lay.h, lay.steer_v, lay.steer_bits, self.alpha, fused.w,
-                                       fused.b, fused.bits, fused.logit, fused.score, stream)
+                issue(f"L{li}/route+steer_probe",
+                      lambda lay=lay, fused=fused: xmix_route_steer_probe(
+                          self.req, self.T_valid, self.sub, self.route, self.err, lay.h,
+                          lay.steer_v, lay.steer_bits, self.alpha, fused.w, fused.b, fused.bits,
+                          fused.logit, fused.score, stream))
             elif fused is not None:
-                xmix_steer_probe(lay.h, self.route, self.req, lay.steer_v, lay.steer_bits,
-                                 self.alpha, fused.w, fused.b, fused.bits, fused.logit,
-                                 fused.score, stream)
+                issue(f"L{li}/steer_probe",
+                      lambda lay=lay, fused=fused: xmix_steer_probe(
+                          lay.h, self.route, self.req, lay.steer_v, lay.steer_bits, self.alpha,
+                          fused.w, fused.b, fused.bits, fused.logit, fused.score, stream))
             elif lay.steer_v is not None:
-                xmix_steer_apply(lay.h, self.route, self.req, lay.steer_v, lay.steer_bits,
-                                 self.alpha, stream)
+                issue(f"L{li}/steer", lambda lay=lay: xmix_steer_apply(
+                    lay.h, self.route, self.req, lay.steer_v, lay.steer_bits, self.alpha, stream))
             for s in lay.saes:
                 if s.W_dec is not None:
-                    xmix_sae_clamp_decode(lay.h, self.route, s.bit, s.idx, s.val, s.W_dec,
-                                          s.clamp_ids, s.clamp_vals, stream=stream)
+                    issue(f"L{li}/sae{s.bit}/clamp",
+                          lambda s=s, lay=lay: xmix_sae_clamp_decode(
+                              lay.h, self.route, s.bit, s.idx, s.val, s.W_dec, s.clamp_ids,
+                              s.clamp_vals, stream=stream))
             for s in lay.saes:
                 if s.ring is not None and not self.fuse_readback:
-                    xmix_readback_compact([s.idx, s.val], self.route, s.bit, self.req,
-                                          lay.layer_id, s.bit, s.ring, stream)
+                    issue(f"L{li}/sae{s.bit}/compact",
+                          lambda s=s, lay=lay: xmix_readback_compact(
+                              [s.idx, s.val], self.route, s.bit, self.req, lay.layer_id, s.bit,
+                              s.ring, stream))
+        if mark is not None:
+            mark("end")
+
+    def stage_names(self):
+        """The names of the step's stages, in launch order (as `run` reports
+        them to `mark`)."""
+        names = []
+        self.run(mark=names.append, repeat=0)
+        return names[:-1]
 
     def hbm_bytes(self) -> int:
         """Algorithmic bytes of one step: what the method must touch."""

@@ -12,6 +12,7 @@
 #include <string.h>
 
 uint16_t oracle_round_bf16(double x);
+void oracle_set_num_threads(int n);
 int oracle_num_threads(void);
 void oracle_route(const int32_t *req, int32_t T_valid, int32_t T_max, const uint32_t *sub,
                   int32_t R_max, int32_t n_apps, uint32_t *tok_mask, int32_t *count,
@@ -176,6 +177,9 @@ int main(void) {
     for (int rep = 0; rep < 3; ++rep)
         oracle_compact(segs, seg_bytes, 2, tm, T, 1, req, 7, 1, slots, cap, row, &head);
 
+    oracle_set_num_threads(1);
+    oracle_sae_encode(hb, d, toks, 3, W, be, bd, m, k, idx, val, vx, pre);
+    oracle_set_num_threads(4);
     printf("sanitized oracle and generator ok (threads %d)\n", oracle_num_threads());
     free(hb); free(hf); free(cs); free(uf); free(ud); free(bits); free(req); free(sub);
     free(tm); free(cnt); free(lists); free(sig); free(ids); free(vocab); free(vb); free(vf);
