@@ -647,6 +647,7 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
     __shared__ float red2[2][kGemmTok];
     __shared__ int cnt_s[kGemmTok];
     __shared__ int cnt2_s[2][kGemmTok];
+    __shared__ float red3[2][kGemmTok];  // per-token maxima
 
     // Tile order: launch slot L runs on XCD L % 8, which owns the latent
     // tiles [x*M8, (x+1)*M8) and walks them in blocks of 8 token tiles x 4
@@ -853,22 +854,26 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
     };
     park_group(0);
     park_group(1);
-    // mean and variance over the tile's 256 latents, per token
+    // mean and variance over the tile's 256 latents, per token, and the
+    // largest value
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
-        float s1 = 0.0f, s2 = 0.0f;
+        float s1 = 0.0f, s2 = 0.0f, mx = -INFINITY;
 #pragma unroll
         for (int a = 0; a < 4; ++a)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 s1 += acc[a][nb][r];
                 s2 = fmaf(acc[a][nb][r], acc[a][nb][r], s2);
+                mx = fmaxf(mx, acc[a][nb][r]);
             }
         s1 += __shfl_xor(s1, 32, kWave);
         s2 += __shfl_xor(s2, 32, kWave);
+        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
         if (g == 0) {
             red1[wm][128 * wn + 32 * nb + j32] = s1;
             red2[wm][128 * wn + 32 * nb + j32] = s2;
+            red3[wm][128 * wn + 32 * nb + j32] = mx;
         }
     }
     __syncthreads();
@@ -878,9 +883,17 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
         const int n = 128 * wn + 32 * nb + j32;
-        const float mu = (red1[0][n] + red1[1][n]) * (1.0f / 256.0f);
-        const float sd = sqrtf(fmaxf((red2[0][n] + red2[1][n]) * (1.0f / 256.0f) - mu * mu, 0.0f));
-        tau[nb] = mu + z_guess * sd;
+        const float s1 = red1[0][n] + red1[1][n], s2 = red2[0][n] + red2[1][n];
+        const float mu = s1 * (1.0f / 256.0f);
+        const float sd = sqrtf(fmaxf(s2 * (1.0f / 256.0f) - mu * mu, 0.0f));
+        const float mx = fmaxf(red3[0][n], red3[1][n]);
+        // a strong latent (above mean + 5 stdev, such as a feature clamped
+        // high at an earlier layer) would lift the guess for its whole
+        // slice: the guess leaves the slice's largest value out then (the
+        // decode kernel leaves out every value above the cut; here a second
+        // pass over the accumulators would not fit the register file)
+        tau[nb] = mx > mu + kTrimZ * sd ? trimmed_guess(s1 - mx, s2 - mx * mx, kBM - 1, z_guess)
+                                        : mu + z_guess * sd;
         lo_b[nb] = -INFINITY;
         hi_b[nb] = INFINITY;
         bad[nb] = false;
@@ -1119,11 +1132,13 @@ __device__ __forceinline__ void ring_ticket(const RingOut& ring, uint64_t h0, in
 }
 
 constexpr int kMergeThreads = 256;
+constexpr int kMergeWaves = kMergeThreads / kWave;
 constexpr int kMergeR = 32;                        // pool entries per lane
 constexpr int kPoolMax = kMergeR * kWave;          // 2048
-constexpr int kMaxRepair = 16;                     // slices one repair redoes
+constexpr int kMaxRepair = 32;                     // slices one repair redoes one by one
 constexpr int kRepairR = 6;                        // repair pool entries per lane
 constexpr int kRepairPool = kRepairR * kWave;      // 384 >= k + one slice
+constexpr int kFloorRounds = 3;                    // pool refills above a raised floor
 
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
     const uint32_t lo = static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), m, kWave));
@@ -1131,26 +1146,55 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
     return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
-// pre-activation of latent j without the bias: plain fp32 dot product of
-// the packed dictionary row with the token row
-__device__ __forceinline__ float latent_dot(const uint16_t* __restrict__ Wp,
-                                            const uint16_t* __restrict__ hrow, int32_t j,
-                                            int32_t d, int32_t n_mt) {
-    const uint4* P = reinterpret_cast<const uint4*>(Wp);
-    const uint4* hr = reinterpret_cast<const uint4*>(hrow);
-    float acc = 0.0f;
-#pragma unroll 4
-    for (int32_t p = 0; p < d / 8; ++p) {
-        const uint4 wv = P[packed_piece(j, p * 8, n_mt)], hv = hr[p];
-        const uint32_t ww[4] = {wv.x, wv.y, wv.z, wv.w};
+// The pre-activation without bias of latent 256*mt + threadIdx.x for one
+// token: a plain fp32 dot product of the packed dictionary row with the
+// token row, the whole workgroup computing the 256 latents of slice mt
+// together.  The slice's K chunks of 64 (32 KB contiguous each in the
+// packed layout) are read with coalesced 16-byte loads: thread tid reads
+// pieces tid + 256 w (w = 0..7), elements 16 s + 8 g .. + 7 (s = tid >> 6,
+// g = (tid >> 5) & 1) of latent 32 w + (tid & 31), and keeps one partial
+// sum per latent; the 8 partials of a latent are added in a fixed order,
+// in pairs across lanes and then through LDS (part: 4 * 256 floats).
+__device__ __forceinline__ float slice_dot(const uint16_t* __restrict__ Wp,
+                                           const uint16_t* __restrict__ hrow, int32_t mt,
+                                           int32_t n_mt, int32_t d, float* part) {
+    const int tid = threadIdx.x;
+    const int sg = tid >> 5;  // 2 s + g
+    const uint4* P = reinterpret_cast<const uint4*>(Wp) + static_cast<int64_t>(mt) * 2048 + tid;
+    const int64_t stride = static_cast<int64_t>(n_mt) * 2048;  // pieces per K chunk
+    const uint4* hr = reinterpret_cast<const uint4*>(hrow) + sg;
+    float acc[8];
+#pragma unroll
+    for (int w = 0; w < 8; ++w) acc[w] = 0.0f;
+    const int nK = d / 64;
+#pragma unroll 1
+    for (int kc = 0; kc < nK; ++kc) {
+        const uint4 hv = hr[kc * 8];
+        uint4 wv[8];
+#pragma unroll
+        for (int w = 0; w < 8; ++w) wv[w] = P[kc * stride + w * 256];
         const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            acc = fmaf(lo_bf16(ww[e]), lo_bf16(hw[e]), acc);
-            acc = fmaf(hi_bf16(ww[e]), hi_bf16(hw[e]), acc);
+        for (int w = 0; w < 8; ++w) {
+            const uint32_t ww[4] = {wv[w].x, wv[w].y, wv[w].z, wv[w].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                acc[w] = fmaf(lo_bf16(ww[e]), lo_bf16(hw[e]), acc[w]);
+                acc[w] = fmaf(hi_bf16(ww[e]), hi_bf16(hw[e]), acc[w]);
+            }
         }
     }
-    return acc;
+    // lanes r and r + 32 hold the two halves g of one latent's elements
+    const int s = tid >> 6;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+        const float both = acc[w] + __shfl_xor(acc[w], 32, kWave);
+        if ((tid & 32) == 0) part[s * kBM + 32 * w + (tid & 31)] = both;
+    }
+    __syncthreads();
+    const float dot = (part[tid] + part[kBM + tid]) + (part[2 * kBM + tid] + part[3 * kBM + tid]);
+    __syncthreads();  // part is free for the next slice
+    return dot;
 }
 
 // One workgroup per subscribed token.  Every thread gathers the candidates
@@ -1159,8 +1203,11 @@ __device__ __forceinline__ float latent_dot(const uint16_t* __restrict__ Wp,
 // over the workgroup places them in an LDS pool, the workgroup selects the
 // k best of it (radix select) and wave 0 checks the certificate; a failed
 // check is repaired by the whole workgroup; wave 0 then writes each winner
-// at its rank.
-__global__ void __launch_bounds__(kMergeThreads)
+// at its rank.  When the candidates exceed the pool, the k-th best of the
+// first kPoolMax of them is a lower bound of the k-th best of all: the pool
+// is filled again with the candidates at or above it (a little below, so
+// that a repair finds what it needs), up to kFloorRounds times.
+__global__ void __launch_bounds__(kMergeThreads) __attribute__((amdgpu_waves_per_eu(5)))
 sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ tile_cnt,
                  const float* __restrict__ tile_tau, int32_t n_mt, int32_t cap,
                  const int32_t* __restrict__ app_count, const int32_t* __restrict__ tok_list,
@@ -1173,10 +1220,11 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
     __shared__ uint32_t K2[kWave];  // the selected k entries (k <= 64)
     __shared__ int32_t I2[kWave];
     __shared__ int hist_s[2][256];  // radix-select digit counts (two rounds in flight)
-    __shared__ uint64_t cmin_s[kMergeThreads / kWave], cmax_s[kMergeThreads / kWave];
+    __shared__ float part_s[4 * kBM];  // partial sums of a slice recompute
+    __shared__ uint64_t cmin_s[kMergeWaves], cmax_s[kMergeWaves];
     __shared__ int dig_s, gt_s, hb_s, sel_n_s;
-    __shared__ int scan_s[kMergeThreads / kWave];
-    __shared__ uint32_t tmax_s[kMergeThreads / kWave];
+    __shared__ int scan_s[kMergeWaves];
+    __shared__ uint32_t tmax_s[kMergeWaves];
     __shared__ int pool_n_s, nfail_s, fix_s;
     __shared__ uint32_t floor_s, sel_tau_s;
     __shared__ int fail_s[kMaxRepair];
@@ -1206,113 +1254,120 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
     const int cnt = *app_count;
     if (n >= cnt) return;  // uniform: no token, no ring row, no ticket
 
-    int total = 0;
+    // Gather: the candidates with key >= floor, in slice order, into the pool
+    // (the first kPoolMax of them; the rest are counted only).  Returns their
+    // number; tau_tiles receives the largest slice threshold.
     uint32_t tau_tiles = 0;
-    for (int t0 = 0; t0 < n_mt; t0 += kMergeThreads) {
-        const int tl = t0 + tid;
-        const bool own = tl < n_mt;
-        const int64_t row = row0 + (own ? tl : 0);
-        // count, threshold and the first 8 pairs of the slice, in one round
-        // (a slice holds about 2-3 candidates; more are fetched below)
-        const uint4* src = reinterpret_cast<const uint4*>(cand + row * cap);
-        uint4 v[4];
-        int c;
-        uint32_t tk;
-        if (t0 == 0) {
+    auto gather = [&](uint32_t floor) __attribute__((always_inline)) {
+        int total = 0;
+        for (int t0 = 0; t0 < n_mt; t0 += kMergeThreads) {
+            const int tl = t0 + tid;
+            const bool own = tl < n_mt;
+            const int64_t row = row0 + (own ? tl : 0);
+            // count, threshold and the first 8 pairs of the slice, in one round
+            // (a slice holds about 2-3 candidates; more are fetched below)
+            const uint4* src = reinterpret_cast<const uint4*>(cand + row * cap);
+            uint4 v[4];
+            int c;
+            uint32_t tk;
+            if (t0 == 0 && floor == 0) {
 #pragma unroll
-            for (int u = 0; u < 4; ++u) v[u] = v0[u];
-            c = c0;
-            tk = own ? f32_key(tf0) : 0u;
-        } else {
+                for (int u = 0; u < 4; ++u) v[u] = v0[u];
+                c = c0;
+                tk = own ? f32_key(tf0) : 0u;
+            } else {
 #pragma unroll
-            for (int u = 0; u < 4; ++u) v[u] = src[min(u, last)];
-            c = own ? tile_cnt[row] : 0;
-            tk = own ? f32_key(tile_tau[row]) : 0u;
-        }
-        // workgroup prefix of the counts
-        int incl = c;
-#pragma unroll
-        for (int off = 1; off < kWave; off <<= 1) {
-            const int y = __shfl_up(incl, off, kWave);
-            if (lane >= off) incl += y;
-        }
-        uint32_t tm = tk;
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1)
-            tm = max(tm, static_cast<uint32_t>(__shfl_xor(static_cast<int>(tm), off, kWave)));
-        __syncthreads();  // scan_s / tmax_s reuse
-        if (lane == kWave - 1) scan_s[wave] = incl;
-        if (lane == 0) tmax_s[wave] = tm;
-        __syncthreads();
-        int base = total, round = 0;
-#pragma unroll
-        for (int w = 0; w < kMergeThreads / kWave; ++w) {
-            base += (w < wave) ? scan_s[w] : 0;
-            round += scan_s[w];
-            tau_tiles = max(tau_tiles, tmax_s[w]);
-        }
-        const int pos = base + incl - c;
-        const int end = total + round;
-        total = end;
-        if (end > kPoolMax) continue;  // uniform: the pool overflows, recompute below
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int q = 2 * u;
-            if (q < c) {
-                K[pos + q] = f32_key(__uint_as_float(v[u].x));
-                I[pos + q] = static_cast<int32_t>(v[u].y);
+                for (int u = 0; u < 4; ++u) v[u] = src[min(u, last)];
+                c = own ? tile_cnt[row] : 0;
+                tk = own ? f32_key(tile_tau[row]) : 0u;
             }
-            if (q + 1 < c) {
-                K[pos + q + 1] = f32_key(__uint_as_float(v[u].z));
-                I[pos + q + 1] = static_cast<int32_t>(v[u].w);
-            }
-        }
-        // slices with more than 8 candidates (rare): the rest of the block
-        for (int q0 = 8; q0 < c; q0 += 8) {
+            // with a floor, only the candidates at or above it are kept
+            int kept = c;
+            if (floor != 0) {  // uniform
+                kept = 0;
+                for (int q0 = 0; q0 < c; q0 += 8) {
+                    uint4 x[4];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) v[u] = src[min(q0 / 2 + u, last)];
+                    for (int u = 0; u < 4; ++u) x[u] = q0 == 0 ? v[u] : src[min(q0 / 2 + u, last)];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int q = q0 + 2 * u;
-                if (q < c) {
-                    K[pos + q] = f32_key(__uint_as_float(v[u].x));
-                    I[pos + q] = static_cast<int32_t>(v[u].y);
-                }
-                if (q + 1 < c) {
-                    K[pos + q + 1] = f32_key(__uint_as_float(v[u].z));
-                    I[pos + q + 1] = static_cast<int32_t>(v[u].w);
+                    for (int u = 0; u < 4; ++u) {
+                        const int q = q0 + 2 * u;
+                        kept += (q < c && f32_key(__uint_as_float(x[u].x)) >= floor) ? 1 : 0;
+                        kept += (q + 1 < c && f32_key(__uint_as_float(x[u].z)) >= floor) ? 1 : 0;
+                    }
                 }
             }
+            // workgroup prefix of the kept counts
+            int incl = kept;
+#pragma unroll
+            for (int off = 1; off < kWave; off <<= 1) {
+                const int y = __shfl_up(incl, off, kWave);
+                if (lane >= off) incl += y;
+            }
+            uint32_t tm = tk;
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1)
+                tm = max(tm, static_cast<uint32_t>(__shfl_xor(static_cast<int>(tm), off, kWave)));
+            __syncthreads();  // scan_s / tmax_s reuse
+            if (lane == kWave - 1) scan_s[wave] = incl;
+            if (lane == 0) tmax_s[wave] = tm;
+            __syncthreads();
+            int base = total, round = 0;
+#pragma unroll
+            for (int w = 0; w < kMergeWaves; ++w) {
+                base += (w < wave) ? scan_s[w] : 0;
+                round += scan_s[w];
+                tau_tiles = max(tau_tiles, tmax_s[w]);
+            }
+            int pos = base + incl - kept;
+            total += round;
+            if (pos >= kPoolMax) continue;  // nothing of this slice fits
+            // the entries of this slice, in order (the first kPoolMax overall)
+            for (int q0 = 0; q0 < c; q0 += 8) {
+                uint4 x[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) x[u] = q0 == 0 ? v[u] : src[min(q0 / 2 + u, last)];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int q = q0 + 2 * u;
+                    const uint32_t ka = f32_key(__uint_as_float(x[u].x));
+                    const uint32_t kb = f32_key(__uint_as_float(x[u].z));
+                    if (q < c && ka >= floor) {
+                        if (pos < kPoolMax) {
+                            K[pos] = ka;
+                            I[pos] = static_cast<int32_t>(x[u].y);
+                        }
+                        ++pos;
+                    }
+                    if (q + 1 < c && kb >= floor) {
+                        if (pos < kPoolMax) {
+                            K[pos] = kb;
+                            I[pos] = static_cast<int32_t>(x[u].w);
+                        }
+                        ++pos;
+                    }
+                }
+            }
         }
-    }
-    __syncthreads();
-    // readback ring (optional): each workgroup with a token reads the head
-    // before it takes a ticket; the one drawing the last ticket advances it
-    // (read here, after the gather's loads, so that no wait for those waits
-    // for this one)
-    uint64_t h0 = 0;
-    if (ring.slots && tid == 0)
-        h0 = __hip_atomic_load(&ring.head[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    // Selection: a radix select over the pool by the whole workgroup.  An
-    // entry's rank is its 64-bit composite (key, ~latent), so the order key
-    // descending, latent ascending has no ties and exactly k entries lie at
-    // or above the k-th composite.  Starting at the 8-bit digit that holds
-    // the highest bit in which the pool's composites differ, each round
-    // counts (LDS atomics) the digits of the entries that match the prefix
-    // found so far, and wave 0 finds the digit that holds the k-th entry;
-    // the rounds end as soon as that digit's whole bin is needed.  The k
-    // entries at or above the prefix then go to wave 0.  The pool itself is
-    // left as it was (the repair below reads it).
-    uint32_t wk = 0;
-    int32_t wi = 0x7FFFFFFF;
-    const bool fits = total <= kPoolMax && total >= k;  // uniform
-    if (fits) {
-        // composite of pool entry i (read from LDS where needed)
-        auto comp = [&](int i) __attribute__((always_inline)) {
-            return (static_cast<uint64_t>(K[i]) << 32) | static_cast<uint32_t>(~I[i]);
-        };
+        return total;
+    };
+
+    // Radix select of the k-th best pool entry (entries 0 .. np - 1, np >= k)
+    // by the whole workgroup.  An entry's rank is its 64-bit composite
+    // (key, ~latent), so the order key descending, latent ascending has no
+    // ties and exactly k entries lie at or above the k-th composite.
+    // Starting at the 8-bit digit that holds the highest bit in which the
+    // composites differ, each round counts (LDS atomics) the digits of the
+    // entries that match the prefix found so far, and wave 0 finds the digit
+    // that holds the k-th entry; the rounds end as soon as that digit's whole
+    // bin is needed.  Returns the prefix (the k best are the entries whose
+    // composite >> *shift_out is >= prefix >> *shift_out).
+    auto comp = [&](int i) __attribute__((always_inline)) {
+        return (static_cast<uint64_t>(K[i]) << 32) | static_cast<uint32_t>(~I[i]);
+    };
+    auto radix_kth = [&](int np, int* shift_out) __attribute__((always_inline)) {
         uint64_t cmin = ~0ull, cmax = 0ull;
-        for (int i = tid; i < total; i += kMergeThreads) {
+        for (int i = tid; i < np; i += kMergeThreads) {
             const uint64_t c = comp(i);
             cmin = min(cmin, c);
             cmax = max(cmax, c);
@@ -1322,16 +1377,16 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
             cmin = min(cmin, shfl_xor_u64(cmin, off));
             cmax = max(cmax, shfl_xor_u64(cmax, off));
         }
+        __syncthreads();  // hist_s and the reduction slots are free
         hist_s[0][tid] = 0;
         hist_s[1][tid] = 0;
         if (lane == 0) {
             cmin_s[wave] = cmin;
             cmax_s[wave] = cmax;
         }
-        if (tid == 0) sel_n_s = 0;
         __syncthreads();
 #pragma unroll
-        for (int w = 0; w < kMergeThreads / kWave; ++w) {
+        for (int w = 0; w < kMergeWaves; ++w) {
             cmin = min(cmin, cmin_s[w]);
             cmax = max(cmax, cmax_s[w]);
         }
@@ -1343,7 +1398,7 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
         for (int round = 0;; ++round) {
             int* hc = hist_s[round & 1];
             const uint64_t hi = shift < 56 ? prefix >> (shift + 8) : 0ull;
-            for (int i = tid; i < total; i += kMergeThreads) {
+            for (int i = tid; i < np; i += kMergeThreads) {
                 const uint64_t c = comp(i);
                 if (shift >= 56 || (c >> (shift + 8)) == hi)
                     atomicAdd(&hc[static_cast<int>(c >> shift) & 255], 1);
@@ -1383,6 +1438,50 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
             if (hb == need || shift == 0) break;  // uniform
             shift -= 8;
         }
+        *shift_out = shift;
+        return prefix;
+    };
+
+    // Gather, then selection of the k best of the pool (the pool itself is
+    // left as it was: the repair below reads it).  While the candidates
+    // overflow the pool, the k-th best of its first kPoolMax entries gives
+    // the floor of a refill (one gather and one radix select serve every
+    // round).
+    uint32_t wk = 0;
+    int32_t wi = 0x7FFFFFFF;
+    uint32_t floor_key = 0;
+    int total = 0;
+    bool fits = false;
+    uint64_t h0 = 0;
+    for (int fr = 0;; ++fr) {
+        total = gather(floor_key);
+        __syncthreads();  // the pool is written
+        // readback ring (optional): each workgroup with a token reads the
+        // head before it takes a ticket; the one drawing the last ticket
+        // advances it (read here, after the gather's loads, so that no wait
+        // for those waits for this one)
+        if (fr == 0 && ring.slots && tid == 0)
+            h0 = __hip_atomic_load(&ring.head[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const bool refill = total > kPoolMax && fr < kFloorRounds;  // uniform
+        fits = total <= kPoolMax && total >= k;
+        if (!refill && !fits) break;
+        if (tid == 0) sel_n_s = 0;
+        int shift;
+        const uint64_t prefix = radix_kth(refill ? kPoolMax : total, &shift);
+        if (refill) {
+            // the k-th key is >= the prefix's key bits (the bits below its
+            // last digit are zero); step a little below it, as the repair's
+            // floor does
+            const float fv = key_f32(static_cast<uint32_t>(prefix >> 32));
+            const uint32_t fl = f32_key(fv - fabsf(fv) * 0x1p-11f);
+            if (fl <= floor_key) {  // uniform: no progress (ties at the floor)
+                fits = false;
+                break;
+            }
+            floor_key = fl;
+            __syncthreads();  // every read of the pool is done
+            continue;
+        }
         const uint64_t cut = prefix >> shift;
         for (int i = tid; i < total; i += kMergeThreads) {
             const uint64_t c = comp(i);
@@ -1399,7 +1498,9 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
             wk = K2[lane];
             wi = I2[lane];
         }
+        break;
     }
+    __syncthreads();
     if (wave == 0) {
         // the k-th key: the smallest of the selected
         uint32_t tau = lane < k ? wk : 0xFFFFFFFFu;
@@ -1414,16 +1515,16 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
     }
     __syncthreads();
     if (fix_s != 0) {  // uniform
-        // Repair: whole slices are recomputed exactly (an fp32 dot product
-        // per latent, one latent per thread).  The pool is cut down to what
-        // can still reach the top k, then after every slice wave 0 keeps the
-        // k best of the pool and that slice's values above the floor (at most
-        // kRepairPool entries), raising the floor to the k-th.  After a
-        // failed certificate only the slices whose threshold lies above the
-        // k-th selected value are redone and the pool keeps its other entries
-        // at or above that value; when the pool was unusable, more than
-        // kMaxRepair slices failed or too many entries are kept, every slice
-        // is redone from an empty pool.
+        // Repair: whole slices are recomputed exactly (fp32 dot products,
+        // the workgroup streaming each slice once).  The pool is cut down to
+        // what can still reach the top k, then after every slice wave 0
+        // keeps the k best of the pool and that slice's values above the
+        // floor (at most kRepairPool entries), raising the floor to the k-th.
+        // After a failed certificate only the slices whose threshold lies
+        // above the k-th selected value are redone and the pool keeps its
+        // other entries at or above that value; when the pool was unusable,
+        // more than kMaxRepair slices failed or too many entries are kept,
+        // every slice is redone from an empty pool.
         const uint16_t* hrow = h + static_cast<int64_t>(t) * d;
         const uint32_t st = sel_tau_s;
         bool all = fix_s == 2;
@@ -1444,11 +1545,12 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
             const uint32_t fl = f32_key(tv - fabsf(tv) * 0x1p-12f);
             const int nf = nfail_s;
             int out = 0;
-            for (int b0 = 0; b0 < total; b0 += kWave) {
+            const int np = min(total, kPoolMax);
+            for (int b0 = 0; b0 < np; b0 += kWave) {
                 const int i = b0 + lane;
-                const uint32_t kk = i < total ? K[i] : 0u;
-                const int32_t ii = i < total ? I[i] : 0;
-                bool keep = i < total && kk >= fl;
+                const uint32_t kk = i < np ? K[i] : 0u;
+                const int32_t ii = i < np ? I[i] : 0;
+                bool keep = i < np && kk >= fl;
                 for (int f = 0; f < nf; ++f) keep = keep && ii / kBM != fail_s[f];
                 const uint64_t bal = wave_ballot(keep);
                 wave_sync();  // this round's reads come before its writes
@@ -1477,8 +1579,10 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
             }
             const int n_rep = pass == 1 ? n_mt : nfail_s;
             for (int q = 0; q < n_rep; ++q) {
-                const int32_t j = (pass == 1 ? q : fail_s[q]) * kBM + tid;
-                const uint32_t key = f32_key(latent_dot(Wp, hrow, j, d, n_mt) + c_fold[j]);
+                const int32_t mtq = pass == 1 ? q : fail_s[q];
+                const int32_t j = mtq * kBM + tid;
+                const float dot = slice_dot(Wp, hrow, mtq, n_mt, d, part_s);
+                const uint32_t key = f32_key(dot + c_fold[j]);
                 if (key >= floor_s) {
                     const int pos = atomicAdd(&pool_n_s, 1);
                     K[pos] = key;

@@ -831,3 +831,50 @@ def test_encode_with_strong_latents_per_token(px, T):
     _check_encode(wl, sae, hb, idx, val, np.arange(T))
     for t in range(T):
         assert set(picks[t].tolist()) <= set(idx[t].tolist())
+
+
+@pytest.mark.parametrize("T", [64, 1100])
+def test_encode_candidate_pool_overflow(px, T):
+    """Every 256-latent slice holds a cluster of 7 latents about 4 stdev
+    above its others for every token (rows along one direction the tokens
+    share), so each slice's first threshold guess keeps about 7 candidates:
+    with m=131072 (512 slices) a token's candidates far exceed the merge's
+    2048-entry pool.  The merge refills its pool above the k-th best of the
+    first 2048 (the candidate counts read from the workspace show the
+    overflow), and the top-k must still match the oracle on every token.
+    64 token slots run the decode kernel, 1100 the prefill GEMM."""
+    d, m, k = 256, 131072, 32
+    wl = synth.make("c3", d=d, m=m, k=k, T=T, n_sub=T, n_outliers=0)
+    sae = wl.layers[0].saes[0]
+    Wf = bf16_f64(sae.W_enc).reshape(m, d)
+    u = bf16_f64(synth.normal_bf16("test/overflow/u", (d,), 1.0))
+    u /= np.linalg.norm(u)
+    lat = np.arange(m)
+    cl = (lat % 256) < 7
+    # other latents: pre ~ N(0, 5) with the shift below; cluster: 9 to 9.9
+    gamma = (4.5 + 0.45 * synth.uniform01("test/overflow/scale", m)) / np.sqrt(d)
+    Wf[cl] = gamma[cl][:, None] * u[None, :]
+    sae.W_enc = to_bf16_bits(Wf)
+    h = bf16_f64(wl.layers[0].h) + 2.0 * np.sqrt(d) * u[None, :]
+    hb = to_bf16_bits(h)
+    rt, _ = gpu_route(px, wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    hd = dev_bits(hb)
+    W = px.xmix_sae_pack_encoder(dev_bits(sae.W_enc))
+    be, bd = dev_bits(sae.b_enc), dev_bits(sae.b_dec)
+    c = torch.empty(m, dtype=torch.float32, device="cuda")
+    px.xmix_sae_fold_bias(W, be, bd, c)
+    idx = torch.full((T, k), -7, dtype=torch.int32, device="cuda")
+    val = torch.zeros((T, k), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(px.sae_encode_workspace(T, d, m, k), dtype=torch.uint8, device="cuda")
+    px.xmix_sae_encode_candidates(hd, rt, sae.bit, W, be, bd, c, k, ws)
+    torch.cuda.synchronize()
+    # workspace (white box): folded bias (m fp32, rounded up to 256 bytes),
+    # candidate pairs [T][n_mt][cap] (8 bytes each), counts [T][n_mt] int32
+    n_mt, cap = m // 256, 8
+    fold = (m * 4 + 255) // 256 * 256
+    cnt_off = fold + T * n_mt * cap * 8
+    counts = ws[cnt_off:cnt_off + T * n_mt * 4].cpu().numpy().view(np.int32).reshape(T, n_mt)
+    assert counts.max() <= cap and counts.sum(axis=1).min() > 2048
+    px.xmix_sae_merge_topk(hd, rt, sae.bit, W, c, k, idx, val, ws)
+    torch.cuda.synchronize()
+    _check_encode(wl, sae, hb, idx.cpu().numpy(), torch_bits(val), np.arange(T))
