@@ -22,7 +22,7 @@
 
 namespace xmix {
 
-constexpr int kProbeThreads = 256;
+constexpr int kProbeThreads = 512;  // the fused probe + steering pass slices rows the same way
 constexpr int kProbeWaves = kProbeThreads / kWave;
 
 // The request whose span [cu[r], cu[r+1]) holds token t, or -1: with cu

@@ -6,8 +6,10 @@
 // rounded once.  The arithmetic and its order are those of the separate
 // probe and steering kernels (same slicing, same per-thread accumulation,
 // same reductions), so the results are bit-identical to a token-mode probe
-// call followed by a steering call.  One workgroup per token slot; a row
-// with neither kind of bit returns after reading its mask word.
+// call followed by a steering call.  One workgroup of 512 threads per
+// token slot (a 4096-wide bf16 row is one slice per thread, so every load
+// of the pass goes out at once); a row with neither kind of bit returns
+// after reading its mask word.
 //
 // With r_tvalid given, the kernel also builds the step's routing (in place
 // of a route-build launch): each workgroup computes its token's mask
@@ -20,7 +22,7 @@
 
 namespace xmix {
 
-constexpr int kFuseThreads = 256;
+constexpr int kFuseThreads = 512;  // a 4096-wide bf16 row is one 16-byte slice per thread
 constexpr int kFuseWaves = kFuseThreads / kWave;
 
 template <bool BF16, int MAXP>
@@ -38,6 +40,7 @@ steer_probe_kernel(void* __restrict__ h, int32_t d, int32_t T_max,
     __shared__ int32_t list_s[kRouteMaxT];
     __shared__ int32_t rtot_s[kFuseWaves];
     const int32_t t = blockIdx.x;
+    const int32_t rq = req[t];  // loaded beside the mask (alpha's row depends on it)
     uint32_t mask;
     if (r_tvalid) {  // uniform
         uint32_t err = 0;
@@ -61,7 +64,7 @@ steer_probe_kernel(void* __restrict__ h, int32_t d, int32_t T_max,
     for (int s = 0; s < n_steer; ++s) ss |= ((mask >> sbits.bit[s]) & 1u) << s;
     for (int p = 0; p < n_probe; ++p) sp |= ((mask >> pbits.bit[p]) & 1u) << p;
     if ((ss | sp) == 0) return;
-    const float* a_row = ss ? alpha + static_cast<int64_t>(req[t]) * n_steer : alpha;
+    const float* a_row = ss ? alpha + static_cast<int64_t>(rq) * n_steer : alpha;
 
     constexpr int EPV = BF16 ? 8 : 4;  // elements per 16-byte vector
     const int32_t nvec = d / EPV;
