@@ -101,7 +101,10 @@ typedef struct {
  *                                head[1]: internal, must be zero when the
  *                                ring is created; every call leaves it zero.
  * A reader that consumed up to row r can read rows [r, head[0]); if
- * head[0] - r > capacity, the oldest rows were overwritten. */
+ * head[0] - r > capacity, the oldest rows were overwritten.  A call's rows
+ * and its head update are visible to work ordered after the call (later
+ * work on its stream, or after a synchronisation with it); a reader running
+ * concurrently with the call must not rely on head[0]. */
 typedef struct {
     uint8_t *slots;
     uint64_t *head;

@@ -61,7 +61,8 @@ compact_kernel(Segments segs, const int32_t* __restrict__ app_count,
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        __threadfence();
+        // no fence: the rows and the head are read by work ordered after the
+        // kernel, which its completion makes visible
         const uint64_t ticket = atomicAdd(reinterpret_cast<unsigned long long*>(&head[1]), 1ull);
         if (ticket == static_cast<uint64_t>(n_active) - 1u) {
             __atomic_store_n(&head[0], h0 + static_cast<uint64_t>(cnt), __ATOMIC_RELAXED);

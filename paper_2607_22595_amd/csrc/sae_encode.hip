@@ -1121,9 +1121,10 @@ struct RingOut {
 // The workgroup's ticket; the last of the `cnt` workgroups that hold a token
 // advances the head by `cnt` (each read the head before its ticket) and
 // resets the counter.  Workgroups without a token take no ticket, so a step
-// with no subscriber costs no atomics.
+// with no subscriber costs no atomics.  No fence before the ticket: the rows
+// and the head are read by work ordered after the kernel, which its
+// completion makes visible.
 __device__ __forceinline__ void ring_ticket(const RingOut& ring, uint64_t h0, int cnt) {
-    __threadfence();
     const uint64_t ticket = atomicAdd(reinterpret_cast<unsigned long long*>(&ring.head[1]), 1ull);
     if (ticket == static_cast<uint64_t>(cnt) - 1u) {
         __atomic_store_n(&ring.head[0], h0 + static_cast<uint64_t>(cnt), __ATOMIC_RELAXED);
@@ -1140,10 +1141,58 @@ constexpr int kRepairR = 6;                        // repair pool entries per la
 constexpr int kRepairPool = kRepairR * kWave;      // 384 >= k + one slice
 constexpr int kFloorRounds = 3;                    // pool refills above a raised floor
 
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
-    const uint32_t lo = static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), m, kWave));
-    const uint32_t hi = static_cast<uint32_t>(__shfl_xor(static_cast<int>(v >> 32), m, kWave));
+// Wave-wide scans and reductions on DPP lane moves (every lane active):
+// within each row of 16 lanes, then across the four rows (row_bcast for the
+// scan, lane reads for the reductions, whose results are uniform).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ int dpp_rows(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xF, false);
+}
+constexpr int kDppMirror = 0x140;
+// inclusive prefix sum over the lanes: row_shr 1, 2, 4, 8 inside each row
+// (a lane with no source adds 0), then row_bcast:15 adds row 0's total to
+// row 1 and row 2's to row 3, and row_bcast:31 the total of rows 0-1 to
+// rows 2 and 3
+__device__ __forceinline__ int wave_incl_sum(int v) {
+    v += dpp_rows<0x111, 0xF>(v);
+    v += dpp_rows<0x112, 0xF>(v);
+    v += dpp_rows<0x114, 0xF>(v);
+    v += dpp_rows<0x118, 0xF>(v);
+    v += dpp_rows<0x142, 0xA>(v);
+    v += dpp_rows<0x143, 0xC>(v);
+    return v;
+}
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t v) {
+    const uint32_t lo = static_cast<uint32_t>(dpp_i<CTRL>(static_cast<int>(v)));
+    const uint32_t hi = static_cast<uint32_t>(dpp_i<CTRL>(static_cast<int>(v >> 32)));
     return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int l) {
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(v), l);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(v >> 32), l);
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+template <bool MAX>
+__device__ __forceinline__ uint32_t wave_minmax_u32(uint32_t v) {
+    auto op = [](uint32_t a, uint32_t b) { return MAX ? max(a, b) : min(a, b); };
+    v = op(v, static_cast<uint32_t>(dpp_i<kDppXor1>(static_cast<int>(v))));
+    v = op(v, static_cast<uint32_t>(dpp_i<kDppXor2>(static_cast<int>(v))));
+    v = op(v, static_cast<uint32_t>(dpp_i<kDppHalfMirror>(static_cast<int>(v))));
+    v = op(v, static_cast<uint32_t>(dpp_i<kDppMirror>(static_cast<int>(v))));
+    const int iv = static_cast<int>(v);
+    return op(op(__builtin_amdgcn_readlane(iv, 0), __builtin_amdgcn_readlane(iv, 16)),
+              op(__builtin_amdgcn_readlane(iv, 32), __builtin_amdgcn_readlane(iv, 48)));
+}
+template <bool MAX>
+__device__ __forceinline__ uint64_t wave_minmax_u64(uint64_t v) {
+    auto op = [](uint64_t a, uint64_t b) { return MAX ? max(a, b) : min(a, b); };
+    v = op(v, dpp_u64<kDppXor1>(v));
+    v = op(v, dpp_u64<kDppXor2>(v));
+    v = op(v, dpp_u64<kDppHalfMirror>(v));
+    v = op(v, dpp_u64<kDppMirror>(v));
+    return op(op(readlane_u64(v, 0), readlane_u64(v, 16)),
+              op(readlane_u64(v, 32), readlane_u64(v, 48)));
 }
 
 // The pre-activation without bias of latent 256*mt + threadIdx.x for one
@@ -1207,7 +1256,7 @@ __device__ __forceinline__ float slice_dot(const uint16_t* __restrict__ Wp,
 // first kPoolMax of them is a lower bound of the k-th best of all: the pool
 // is filled again with the candidates at or above it (a little below, so
 // that a repair finds what it needs), up to kFloorRounds times.
-__global__ void __launch_bounds__(kMergeThreads) __attribute__((amdgpu_waves_per_eu(5)))
+__global__ void __launch_bounds__(kMergeThreads) __attribute__((amdgpu_waves_per_eu(4)))
 sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ tile_cnt,
                  const float* __restrict__ tile_tau, int32_t n_mt, int32_t cap,
                  const int32_t* __restrict__ app_count, const int32_t* __restrict__ tok_list,
@@ -1217,16 +1266,16 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
                  RingOut ring) {
     __shared__ uint32_t K[kPoolMax + kWave];
     __shared__ int32_t I[kPoolMax + kWave];
-    __shared__ uint32_t K2[kWave];  // the selected k entries (k <= 64)
-    __shared__ int32_t I2[kWave];
-    __shared__ int hist_s[2][256];  // radix-select digit counts (two rounds in flight)
+    __shared__ __align__(16) uint32_t K2[kWave];  // the selected k entries (k <= 64)
+    __shared__ __align__(16) int32_t I2[kWave];
+    __shared__ __align__(16) int hist_s[3][256];  // radix digit counts, 3 rounds in flight
     __shared__ float part_s[4 * kBM];  // partial sums of a slice recompute
     __shared__ uint64_t cmin_s[kMergeWaves], cmax_s[kMergeWaves];
-    __shared__ int dig_s, gt_s, hb_s, sel_n_s;
-    __shared__ int scan_s[kMergeWaves];
-    __shared__ uint32_t tmax_s[kMergeWaves];
-    __shared__ int pool_n_s, nfail_s, fix_s;
-    __shared__ uint32_t floor_s, sel_tau_s;
+    __shared__ int sel_n_s;
+    __shared__ int scan_s[2][kMergeWaves];  // gather rounds alternate between the two
+    __shared__ uint32_t tmax_s[2][kMergeWaves];
+    __shared__ int pool_n_s, nfail_s;
+    __shared__ uint32_t floor_s;
     __shared__ int fail_s[kMaxRepair];
     const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
     const int n = blockIdx.x;
@@ -1250,16 +1299,26 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
             tf0 = tile_tau[row];
         }
     }
+    // readback ring (optional): each workgroup with a token reads the head
+    // before it takes a ticket; the one drawing the last ticket advances it.
+    // Read with the loads above (after them, so that no wait for those
+    // waits for this one); the head was last written by an earlier call.
+    uint64_t h0 = 0;
+    if (ring.slots && tid == 0) h0 = ring.head[0];
     const int32_t t = tok_list[n];
     const int cnt = *app_count;
     if (n >= cnt) return;  // uniform: no token, no ring row, no ticket
+    if (tid == 0) nfail_s = 0;  // read after the gather's barriers
 
     // Gather: the candidates with key >= floor, in slice order, into the pool
     // (the first kPoolMax of them; the rest are counted only).  Returns their
-    // number; tau_tiles receives the largest slice threshold.
+    // number; tau_tiles receives the largest slice threshold, and each
+    // wave's smallest and largest pool composite go to cmin_s / cmax_s (read
+    // after the caller's barrier, with the first radix histogram cleared).
     uint32_t tau_tiles = 0;
     auto gather = [&](uint32_t floor) __attribute__((always_inline)) {
         int total = 0;
+        uint64_t cmn = ~0ull, cmx = 0ull;
         for (int t0 = 0; t0 < n_mt; t0 += kMergeThreads) {
             const int tl = t0 + tid;
             const bool own = tl < n_mt;
@@ -1297,27 +1356,20 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
                     }
                 }
             }
-            // workgroup prefix of the kept counts
-            int incl = kept;
-#pragma unroll
-            for (int off = 1; off < kWave; off <<= 1) {
-                const int y = __shfl_up(incl, off, kWave);
-                if (lane >= off) incl += y;
-            }
-            uint32_t tm = tk;
-#pragma unroll
-            for (int off = 32; off >= 1; off >>= 1)
-                tm = max(tm, static_cast<uint32_t>(__shfl_xor(static_cast<int>(tm), off, kWave)));
-            __syncthreads();  // scan_s / tmax_s reuse
-            if (lane == kWave - 1) scan_s[wave] = incl;
-            if (lane == 0) tmax_s[wave] = tm;
+            // workgroup prefix of the kept counts (the slots of a round were
+            // last read before the previous round's barrier)
+            const int incl = wave_incl_sum(kept);
+            const uint32_t tm = wave_minmax_u32<true>(tk);
+            const int par = (t0 / kMergeThreads) & 1;
+            if (lane == kWave - 1) scan_s[par][wave] = incl;
+            if (lane == 0) tmax_s[par][wave] = tm;
             __syncthreads();
             int base = total, round = 0;
 #pragma unroll
             for (int w = 0; w < kMergeWaves; ++w) {
-                base += (w < wave) ? scan_s[w] : 0;
-                round += scan_s[w];
-                tau_tiles = max(tau_tiles, tmax_s[w]);
+                base += (w < wave) ? scan_s[par][w] : 0;
+                round += scan_s[par][w];
+                tau_tiles = max(tau_tiles, tmax_s[par][w]);
             }
             int pos = base + incl - kept;
             total += round;
@@ -1336,6 +1388,9 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
                         if (pos < kPoolMax) {
                             K[pos] = ka;
                             I[pos] = static_cast<int32_t>(x[u].y);
+                            const uint64_t cc = (static_cast<uint64_t>(ka) << 32) | ~x[u].y;
+                            cmn = min(cmn, cc);
+                            cmx = max(cmx, cc);
                         }
                         ++pos;
                     }
@@ -1343,12 +1398,22 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
                         if (pos < kPoolMax) {
                             K[pos] = kb;
                             I[pos] = static_cast<int32_t>(x[u].w);
+                            const uint64_t cc = (static_cast<uint64_t>(kb) << 32) | ~x[u].w;
+                            cmn = min(cmn, cc);
+                            cmx = max(cmx, cc);
                         }
                         ++pos;
                     }
                 }
             }
         }
+        cmn = wave_minmax_u64<false>(cmn);
+        cmx = wave_minmax_u64<true>(cmx);
+        if (lane == 0) {
+            cmin_s[wave] = cmn;
+            cmax_s[wave] = cmx;
+        }
+        hist_s[0][tid] = 0;
         return total;
     };
 
@@ -1357,36 +1422,21 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
     // (key, ~latent), so the order key descending, latent ascending has no
     // ties and exactly k entries lie at or above the k-th composite.
     // Starting at the 8-bit digit that holds the highest bit in which the
-    // composites differ, each round counts (LDS atomics) the digits of the
-    // entries that match the prefix found so far, and wave 0 finds the digit
-    // that holds the k-th entry; the rounds end as soon as that digit's whole
-    // bin is needed.  Returns the prefix (the k best are the entries whose
-    // composite >> *shift_out is >= prefix >> *shift_out).
+    // composites differ (from the gather's smallest and largest), each round
+    // counts (LDS atomics) the digits of the entries that match the prefix
+    // found so far, and every wave finds the digit that holds the k-th entry
+    // from the same counts (one barrier per round; the three count buffers
+    // rotate, so a buffer is cleared two barriers after its last read); the
+    // rounds end as soon as that digit's whole bin is needed.  Returns the
+    // prefix (the k best are the entries whose composite >> *shift_out is
+    // >= prefix >> *shift_out).
     auto comp = [&](int i) __attribute__((always_inline)) {
         return (static_cast<uint64_t>(K[i]) << 32) | static_cast<uint32_t>(~I[i]);
     };
     auto radix_kth = [&](int np, int* shift_out) __attribute__((always_inline)) {
-        uint64_t cmin = ~0ull, cmax = 0ull;
-        for (int i = tid; i < np; i += kMergeThreads) {
-            const uint64_t c = comp(i);
-            cmin = min(cmin, c);
-            cmax = max(cmax, c);
-        }
+        uint64_t cmin = cmin_s[0], cmax = cmax_s[0];
 #pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) {
-            cmin = min(cmin, shfl_xor_u64(cmin, off));
-            cmax = max(cmax, shfl_xor_u64(cmax, off));
-        }
-        __syncthreads();  // hist_s and the reduction slots are free
-        hist_s[0][tid] = 0;
-        hist_s[1][tid] = 0;
-        if (lane == 0) {
-            cmin_s[wave] = cmin;
-            cmax_s[wave] = cmax;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int w = 0; w < kMergeWaves; ++w) {
+        for (int w = 1; w < kMergeWaves; ++w) {
             cmin = min(cmin, cmin_s[w]);
             cmax = max(cmax, cmax_s[w]);
         }
@@ -1396,43 +1446,40 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
         uint64_t prefix = shift < 56 ? cmin & ~((1ull << (shift + 8)) - 1ull) : 0ull;
         int need = k;
         for (int round = 0;; ++round) {
-            int* hc = hist_s[round & 1];
+            int* hc = hist_s[round % 3];
             const uint64_t hi = shift < 56 ? prefix >> (shift + 8) : 0ull;
             for (int i = tid; i < np; i += kMergeThreads) {
                 const uint64_t c = comp(i);
                 if (shift >= 56 || (c >> (shift + 8)) == hi)
                     atomicAdd(&hc[static_cast<int>(c >> shift) & 255], 1);
             }
-            // the other buffer was last read before the previous round's
-            // second barrier
-            hist_s[(round + 1) & 1][tid] = 0;
+            // for the next round; its last reads (two rounds ago) came
+            // before the previous round's barrier
+            hist_s[(round + 1) % 3][tid] = 0;
             __syncthreads();
-            if (wave == 0) {
-                int h4[4], ls = 0;
+            const int4 h4v = reinterpret_cast<const int4*>(hc)[lane];  // bins 4 lane .. + 3
+            const int h4[4] = {h4v.x, h4v.y, h4v.z, h4v.w};
+            const int ls = (h4[0] + h4[1]) + (h4[2] + h4[3]);
+            const int incl = wave_incl_sum(ls);
+            // entries in the bins of every higher lane
+            int above = __builtin_amdgcn_readlane(incl, kWave - 1) - incl, dl = 0, gl = 0, hl = 0;
+            bool found = false;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    h4[j] = hc[4 * lane + j];
-                    ls += h4[j];
+            for (int j = 3; j >= 0; --j) {
+                if (above < need && need <= above + h4[j]) {
+                    dl = 4 * lane + j;
+                    gl = above;
+                    hl = h4[j];
+                    found = true;
                 }
-                int sfx = ls;  // entries in this lane's bins and every higher lane's
-#pragma unroll
-                for (int off = 1; off < kWave; off <<= 1) {
-                    const int y = __shfl_down(sfx, off, kWave);
-                    if (lane + off < kWave) sfx += y;
-                }
-                int above = sfx - ls;
-#pragma unroll
-                for (int j = 3; j >= 0; --j) {
-                    if (above < need && need <= above + h4[j]) {
-                        dig_s = 4 * lane + j;
-                        gt_s = above;
-                        hb_s = h4[j];
-                    }
-                    above += h4[j];
-                }
+                above += h4[j];
             }
-            __syncthreads();
-            const int D = dig_s, gt = gt_s, hb = hb_s;
+            // exactly one bin holds the need-th entry
+            const uint64_t fb = wave_ballot(found);
+            const int src = fb ? __ffsll(static_cast<long long>(fb)) - 1 : 0;
+            const int D = __builtin_amdgcn_readlane(dl, src),
+                      gt = __builtin_amdgcn_readlane(gl, src),
+                      hb = __builtin_amdgcn_readlane(hl, src);
             need -= gt;
             prefix |= static_cast<uint64_t>(D) << shift;
             if (hb == need || shift == 0) break;  // uniform
@@ -1452,16 +1499,9 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
     uint32_t floor_key = 0;
     int total = 0;
     bool fits = false;
-    uint64_t h0 = 0;
     for (int fr = 0;; ++fr) {
         total = gather(floor_key);
         __syncthreads();  // the pool is written
-        // readback ring (optional): each workgroup with a token reads the
-        // head before it takes a ticket; the one drawing the last ticket
-        // advances it (read here, after the gather's loads, so that no wait
-        // for those waits for this one)
-        if (fr == 0 && ring.slots && tid == 0)
-            h0 = __hip_atomic_load(&ring.head[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const bool refill = total > kPoolMax && fr < kFloorRounds;  // uniform
         fits = total <= kPoolMax && total >= k;
         if (!refill && !fits) break;
@@ -1494,27 +1534,17 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
             }
         }
         __syncthreads();
-        if (wave == 0 && lane < k) {
+        if (lane < k) {
             wk = K2[lane];
             wi = I2[lane];
         }
         break;
     }
-    __syncthreads();
-    if (wave == 0) {
-        // the k-th key: the smallest of the selected
-        uint32_t tau = lane < k ? wk : 0xFFFFFFFFu;
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1)
-            tau = min(tau, static_cast<uint32_t>(__shfl_xor(static_cast<int>(tau), off, kWave)));
-        if (lane == 0) {
-            sel_tau_s = tau;
-            fix_s = !fits ? 2 : (tau_tiles <= tau ? 0 : 1);
-            nfail_s = 0;
-        }
-    }
-    __syncthreads();
-    if (fix_s != 0) {  // uniform
+    // every wave: the k-th key (the smallest of the selected) and whether
+    // the selection stands (0), fails its certificate (1) or was not made (2)
+    const uint32_t sel_tau = wave_minmax_u32<false>(lane < k ? wk : 0xFFFFFFFFu);
+    const int fix = !fits ? 2 : (tau_tiles <= sel_tau ? 0 : 1);
+    if (fix != 0) {  // uniform
         // Repair: whole slices are recomputed exactly (fp32 dot products,
         // the workgroup streaming each slice once).  The pool is cut down to
         // what can still reach the top k, then after every slice wave 0
@@ -1526,8 +1556,8 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
         // more than kMaxRepair slices failed or too many entries are kept,
         // every slice is redone from an empty pool.
         const uint16_t* hrow = h + static_cast<int64_t>(t) * d;
-        const uint32_t st = sel_tau_s;
-        bool all = fix_s == 2;
+        const uint32_t st = sel_tau;
+        bool all = fix == 2;
         if (!all) {
             for (int tl = tid; tl < n_mt; tl += kMergeThreads) {
                 if (f32_key(tile_tau[row0 + tl]) > st) {
