@@ -379,26 +379,33 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
 
     // With r_req given, the kernel also builds the step's routing (in place
     // of a route-build launch): every workgroup builds its app's token list
-    // in LDS; workgroup a < n_apps publishes app a's list and count, and
-    // workgroup 0 the token masks and the error word.
+    // in LDS from the routing inputs staged there (in the space of the K
+    // loop's token chunks); workgroup a < n_apps publishes app a's list and
+    // count, and workgroup 0 the token masks and the error word.
     const int32_t* tl = tok_list;
     int cnt = 0;
     if (r_req) {  // uniform
+        static_assert(sizeof(lds_main) >= (kRouteMaxT + kStageSubMax) * 4, "staging fits");
+        int32_t* req_s = reinterpret_cast<int32_t*>(lds_main);
+        uint32_t* sub_s = reinterpret_cast<uint32_t*>(lds_main) + kRouteMaxT;
+        stage_route<kEncThreads>(r_req, r_Tmax, r_sub, r_Rmax, req_s, sub_s);
         uint32_t err = 0;
         const int32_t tv = clamp_t_valid(*r_tvalid, r_Tmax, err);
         const uint32_t keep = r_napps >= 32 ? 0xFFFFFFFFu : ((1u << r_napps) - 1u);
         const int own = blockIdx.x;
         uint32_t* masks = own == 0 ? r_mask : nullptr;
+        __syncthreads();  // the staged inputs
         if (own < r_napps && own != r_bit) {
-            const int32_t n = build_token_list<kEncThreads>(r_req, tv, r_sub, r_Rmax, keep, own,
-                                                            r_Tmax, list_s, rtot_s, masks, err);
+            const int32_t n = build_token_list<kEncThreads>(req_s, tv, sub_s, r_sub, r_Rmax, keep,
+                                                            own, r_Tmax, list_s, rtot_s, masks,
+                                                            err);
             masks = nullptr;
             publish_token_list<kEncThreads>(list_s, n, r_Tmax,
                                             r_lists + static_cast<int64_t>(own) * r_Tmax,
                                             r_count + own);
             __syncthreads();  // list_s is rebuilt below
         }
-        cnt = build_token_list<kEncThreads>(r_req, tv, r_sub, r_Rmax, keep, r_bit, r_Tmax,
+        cnt = build_token_list<kEncThreads>(req_s, tv, sub_s, r_sub, r_Rmax, keep, r_bit, r_Tmax,
                                             list_s, rtot_s, masks, err);
         if (own == r_bit)
             publish_token_list<kEncThreads>(list_s, cnt, r_Tmax,

@@ -12,9 +12,10 @@
 // after reading its mask word.
 //
 // With r_tvalid given, the kernel also builds the step's routing (in place
-// of a route-build launch): each workgroup computes its token's mask
-// itself and writes it, and workgroup a < n_apps publishes app a's token
-// list and count (workgroup 0 also the error word).
+// of a route-build launch): n_apps more workgroups, dispatched first, each
+// build one app's token list from the routing inputs staged in LDS and
+// publish it with its count (the first also the error word), and each token
+// workgroup computes its token's mask itself and writes it.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "launch.hpp"
@@ -37,25 +38,33 @@ steer_probe_kernel(void* __restrict__ h, int32_t d, int32_t T_max,
                    uint32_t* __restrict__ r_mask, int32_t* __restrict__ r_count,
                    int32_t* __restrict__ r_lists, uint32_t* __restrict__ r_err) {
     __shared__ float red[kFuseWaves][MAXP];
-    __shared__ int32_t list_s[kRouteMaxT];
-    __shared__ int32_t rtot_s[kFuseWaves];
-    const int32_t t = blockIdx.x;
-    const int32_t rq = req[t];  // loaded beside the mask (alpha's row depends on it)
-    uint32_t mask;
-    if (r_tvalid) {  // uniform
+    const int n_list = r_tvalid ? r_napps : 0;  // route-list workgroups
+    if (static_cast<int>(blockIdx.x) < n_list) {  // uniform
+        __shared__ int32_t list_s[kRouteMaxT];
+        __shared__ int32_t rtot_s[kFuseWaves];
+        __shared__ int32_t req_s[kRouteMaxT];
+        __shared__ uint32_t sub_s[kStageSubMax];
+        const int a = blockIdx.x;
+        stage_route<kFuseThreads>(req, T_max, r_sub, r_Rmax, req_s, sub_s);
         uint32_t err = 0;
         const int32_t tv = clamp_t_valid(*r_tvalid, T_max, err);
         const uint32_t keep = r_napps >= 32 ? 0xFFFFFFFFu : ((1u << r_napps) - 1u);
-        if (t < r_napps) {
-            const int32_t n = build_token_list<kFuseThreads>(req, tv, r_sub, r_Rmax, keep, t,
-                                                             T_max, list_s, rtot_s, nullptr, err);
-            publish_token_list<kFuseThreads>(list_s, n, T_max,
-                                             r_lists + static_cast<int64_t>(t) * T_max,
-                                             r_count + t);
-            if (t == 0) publish_error(err, r_err);  // its pass saw every slot
-        }
+        __syncthreads();  // the staged inputs
+        const int32_t n = build_token_list<kFuseThreads>(req_s, tv, sub_s, r_sub, r_Rmax, keep, a,
+                                                         T_max, list_s, rtot_s, nullptr, err);
+        publish_token_list<kFuseThreads>(list_s, n, T_max,
+                                         r_lists + static_cast<int64_t>(a) * T_max, r_count + a);
+        if (a == 0) publish_error(err, r_err);  // its pass saw every slot
+        return;
+    }
+    const int32_t t = static_cast<int32_t>(blockIdx.x) - n_list;
+    const int32_t rq = req[t];  // loaded beside the mask (alpha's row depends on it)
+    uint32_t mask;
+    if (r_tvalid) {  // uniform
         uint32_t unused = 0;
-        mask = slot_mask(req, t, tv, r_sub, r_Rmax, keep, unused);
+        const int32_t tv = clamp_t_valid(*r_tvalid, T_max, unused);
+        const uint32_t keep = r_napps >= 32 ? 0xFFFFFFFFu : ((1u << r_napps) - 1u);
+        mask = request_mask(rq, t, tv, r_sub, r_Rmax, keep, unused);
         if (threadIdx.x == 0) r_mask[t] = mask;
     } else {
         mask = tok_mask[t];
@@ -172,7 +181,7 @@ static hipError_t launch_steer_probe_t(void* h, int32_t d, int32_t T_max,
                                        const float* b, const BitList& pbits, int32_t n_probe,
                                        float* logit, float* score, const RouteIn& r,
                                        hipStream_t stream) {
-    dim3 g(T_max), blk(kFuseThreads);
+    dim3 g(T_max + (r.T_valid ? r.n_apps : 0)), blk(kFuseThreads);
     if (n_probe <= 4)
         hipLaunchKernelGGL((steer_probe_kernel<BF16, 4>), g, blk, 0, stream, h, d, T_max,
                            tok_mask, req, vecs, sbits, alpha, n_steer, w, b, pbits, n_probe,
