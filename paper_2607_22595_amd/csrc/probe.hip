@@ -2,7 +2,7 @@
 //
 // Token pass: one workgroup per token slot reads the row once in 16-byte
 // slices and accumulates one partial dot product per subscribed probe in
-// registers; partials are reduced with a fixed butterfly inside each wave
+// registers; partials are reduced with fixed DPP moves inside each wave
 // and a fixed-order sum over the waves (bit-reproducible, no atomics).
 //
 // Mean pooling is a segmented reduction in two launches: the token pass
@@ -140,7 +140,7 @@ probe_token_kernel(const void* __restrict__ h, int32_t d, int32_t T_max,
 
 // One workgroup per request: pooled logit of every probe whose bit the
 // request carries.  Threads sum strided tokens of the span in order, then a
-// fixed butterfly and a fixed-order sum over the waves combine them.
+// fixed DPP pattern and a fixed-order sum over the waves combine them.
 __global__ void __launch_bounds__(kProbeThreads)
 probe_pool_kernel(const float* __restrict__ dots, int32_t T_max,
                   const uint32_t* __restrict__ tok_mask, const int32_t* __restrict__ cu,

@@ -162,17 +162,7 @@ sae_fold_kernel(const uint16_t* __restrict__ Wp, const uint16_t* __restrict__ b_
 // spread over every bank.
 constexpr int kSelStride = 260;  // floats per token row
 
-// DPP lane moves inside groups of 8 lanes (quad_perm [1,0,3,2] and
-// [2,3,0,1], row_half_mirror, row_shr:n; every source lane is active)
-template <int CTRL>
-__device__ __forceinline__ int dpp_i(int v) {
-    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
-}
-template <int CTRL>
-__device__ __forceinline__ float dpp_f(float v) {
-    return __int_as_float(dpp_i<CTRL>(__float_as_int(v)));
-}
-constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141;
+// Reductions inside groups of 8 lanes on DPP moves (quad_perm, row_half_mirror)
 __device__ __forceinline__ float sum8(float v) {
     v += dpp_f<kDppXor1>(v);
     v += dpp_f<kDppXor2>(v);
@@ -1155,7 +1145,6 @@ template <int CTRL, int ROWS>
 __device__ __forceinline__ int dpp_rows(int v) {
     return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xF, false);
 }
-constexpr int kDppMirror = 0x140;
 // inclusive prefix sum over the lanes: row_shr 1, 2, 4, 8 inside each row
 // (a lane with no source adds 0), then row_bcast:15 adds row 0's total to
 // row 1 and row 2's to row 3, and row_bcast:31 the total of rows 0-1 to

@@ -11,6 +11,7 @@
 #include "common.hpp"
 #include "kernels.hpp"
 #include "launch.hpp"
+#include "steer_add.hpp"
 
 namespace xmix {
 
@@ -45,21 +46,7 @@ steer_kernel(void* __restrict__ h, int32_t d, const uint32_t* __restrict__ tok_m
                 acc[e] = __uint_as_float(hw[e]);
             }
         }
-        for (uint32_t rest = sel; rest; rest &= rest - 1) {
-            const int s = __builtin_ctz(rest);
-            const double a = a_row[s];
-            const uint4 vv = V[static_cast<int64_t>(s) * nvec + i];
-            const uint32_t vw[4] = {vv.x, vv.y, vv.z, vv.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                if constexpr (BF16) {
-                    acc[2 * e] = fma(a, static_cast<double>(lo_bf16(vw[e])), acc[2 * e]);
-                    acc[2 * e + 1] = fma(a, static_cast<double>(hi_bf16(vw[e])), acc[2 * e + 1]);
-                } else {
-                    acc[e] = fma(a, static_cast<double>(__uint_as_float(vw[e])), acc[e]);
-                }
-            }
-        }
+        steer_accumulate<BF16>(acc, sel, a_row, V, nvec, i);
         uint4 out;
         if constexpr (BF16) {
             out.x = pack_bf16_from_f64(acc[0], acc[1]);

@@ -20,6 +20,7 @@
 #include "kernels.hpp"
 #include "launch.hpp"
 #include "route_list.hpp"
+#include "steer_add.hpp"
 
 namespace xmix {
 
@@ -120,22 +121,7 @@ steer_probe_kernel(void* __restrict__ h, int32_t d, int32_t T_max,
             double acc[EPV];
 #pragma unroll
             for (int e = 0; e < EPV; ++e) acc[e] = x[e];
-            for (uint32_t rest = ss; rest; rest &= rest - 1) {
-                const int s = __builtin_ctz(rest);
-                const double a = a_row[s];
-                const uint4 vv = V[static_cast<int64_t>(s) * nvec + i];
-                const uint32_t vw[4] = {vv.x, vv.y, vv.z, vv.w};
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    if constexpr (BF16) {
-                        acc[2 * e] = fma(a, static_cast<double>(lo_bf16(vw[e])), acc[2 * e]);
-                        acc[2 * e + 1] =
-                            fma(a, static_cast<double>(hi_bf16(vw[e])), acc[2 * e + 1]);
-                    } else {
-                        acc[e] = fma(a, static_cast<double>(__uint_as_float(vw[e])), acc[e]);
-                    }
-                }
-            }
+            steer_accumulate<BF16>(acc, ss, a_row, V, nvec, i);
             uint4 out;
             if constexpr (BF16) {
                 out.x = pack_bf16_from_f64(acc[0], acc[1]);
