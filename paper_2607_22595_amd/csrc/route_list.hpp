@@ -38,11 +38,14 @@ __device__ __forceinline__ uint32_t request_mask(int32_t r, int32_t t, int32_t t
 // into req_s (T_max <= kRouteMaxT) and, when R_max <= kStageSubMax, the
 // request table into sub_s; every global load is issued before the first
 // wait, so the staging costs one memory round trip.  The caller places a
-// barrier between this and the first build.
+// barrier between this and the first build.  Returns whether a request this
+// thread staged subscribes to an app of `bits` (true when the table was too
+// large to stage): no token can carry those bits unless some thread saw one.
 template <int THREADS>
-__device__ __forceinline__ void stage_route(const int32_t* __restrict__ req, int32_t T_max,
+__device__ __forceinline__ bool stage_route(const int32_t* __restrict__ req, int32_t T_max,
                                             const uint32_t* __restrict__ sub, int32_t R_max,
-                                            int32_t* req_s, uint32_t* sub_s) {
+                                            int32_t* req_s, uint32_t* sub_s,
+                                            uint32_t bits = 0u) {
     constexpr int kT = (kRouteMaxT + THREADS - 1) / THREADS;
     constexpr int kR = (kStageSubMax + THREADS - 1) / THREADS;
     const int tid = threadIdx.x;
@@ -62,9 +65,13 @@ __device__ __forceinline__ void stage_route(const int32_t* __restrict__ req, int
 #pragma unroll
     for (int j = 0; j < kT; ++j)
         if (tid + j * THREADS < T_max) req_s[tid + j * THREADS] = rv[j];
+    bool seen = !fits;
 #pragma unroll
-    for (int j = 0; j < kR; ++j)
+    for (int j = 0; j < kR; ++j) {
         if (fits && tid + j * THREADS < R_max) sub_s[tid + j * THREADS] = sv[j];
+        seen = seen || (sv[j] & bits) != 0u;
+    }
+    return seen;
 }
 
 // slot_mask on the staged inputs (the request table from global memory when

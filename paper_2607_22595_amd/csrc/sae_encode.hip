@@ -365,26 +365,105 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     static_assert(kBN * kSelStride / 4 >= 2 * kBN * 8, "token chunks fit");
     __shared__ int32_t list_s[kRouteMaxT];    // the app's token list (in-kernel route build)
     __shared__ int32_t rtot_s[kEncWaves];
+    __shared__ int32_t seen_s[kEncWaves];
     uint4 (*xs)[kBN * 8] = reinterpret_cast<uint4 (*)[kBN * 8]>(lds_main);
+
+    // Tile order.  Few token tiles (decode): latent tile fastest, so the
+    // workgroups of the first token tile, the ones with live tokens, are
+    // dispatched first and spread over every CU (interleaving them with
+    // tiles past the live count would leave every other CU idle).
+    // Many token tiles (prefill): launch slot L runs on XCD L % 8; XCD x
+    // owns the latent tiles [x*M8, (x+1)*M8) and walks them in blocks of 8
+    // token tiles x 4 latent tiles, 32 consecutive slots per block, token
+    // blocks fastest.  The 32 workgroups of a block run together on the
+    // XCD's 32 CUs, so each K chunk of 8 token tiles and 4 dictionary
+    // slices is fetched into the XCD's L2 once and read by 4 and 8
+    // workgroups; consecutive blocks reuse the same 4 slices.
+    const int L = blockIdx.x;
+    int nt, mt;
+    bool live;  // the tile exists (its tokens are counted below)
+    if (n_nt <= kLatentFastTiles) {
+        nt = L / n_mt;
+        mt = L % n_mt;
+        live = nt < n_nt;
+    } else {
+        const int xcd = L % 8, slot = L / 8;
+        const int m8 = (n_mt + 7) / 8;              // latent tiles per XCD
+        const int nbt = (n_nt + kBlkTok - 1) / kBlkTok;
+        const int b = slot / (kBlkTok * kBlkLat), p = slot % (kBlkTok * kBlkLat);
+        const int bt = b % nbt, bl = b / nbt;
+        const int lt = kBlkLat * bl + p / kBlkTok;
+        nt = kBlkTok * bt + p % kBlkTok;
+        mt = xcd * m8 + lt;
+        live = nt < n_nt && lt < m8;
+    }
+    live = live && mt < n_mt;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 5, j32 = lane & 31;
+    const int nK = d / kBK;  // a multiple of 4 (d % 256 == 0)
+
+    // operand A: this wave's 32 latents of the packed slice
+    const uint4* wbase = reinterpret_cast<const uint4*>(W) + static_cast<int64_t>(mt) * 2048 +
+                         wave * 256 + lane;
+    const int64_t wstride = static_cast<int64_t>(n_mt) * 2048;  // pieces per K chunk
+    uint4 wa0[4], wa1[4], wa2[4], wa3[4];   // W ring: 4 chunks, 3 in flight
+    // The dictionary is read once per launch: nontemporal loads stream it
+    // past the caches (about 4 % faster than cached loads at 65536 x 4096).
+    auto load_w = [&](uint4 (&a)[4], int kc) {
+        kc = min(kc, nK - 1);  // past the end: re-read the last chunk, unused
+        const u32x4_t* p = reinterpret_cast<const u32x4_t*>(wbase + kc * wstride);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            const u32x4_t v = __builtin_nontemporal_load(p + s * 64);
+            a[s] = make_uint4(v.x, v.y, v.z, v.w);
+        }
+    };
+    // folded bias of this lane's 16 latents, fetched with the first chunks
+    float cfv[16];
+    auto load_bias = [&]() {
+        const float* cf = c_fold + mt * kBM + 32 * wave + 4 * g;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) cfv[r] = cf[8 * (r / 4) + (r % 4)];
+    };
 
     // With r_req given, the kernel also builds the step's routing (in place
     // of a route-build launch): every workgroup builds its app's token list
     // in LDS from the routing inputs staged there (in the space of the K
     // loop's token chunks); workgroup a < n_apps publishes app a's list and
-    // count, and workgroup 0 the token masks and the error word.
+    // count, and workgroup 0 the token masks and the error word.  A
+    // workgroup of the first token tile starts its first dictionary chunks
+    // as soon as the staged table shows a request subscribed to the app, so
+    // that the stream runs while the list is built (without a subscriber it
+    // reads nothing).
     const int32_t* tl = tok_list;
     int cnt = 0;
+    bool w_issued = false;
     if (r_req) {  // uniform
         static_assert(sizeof(lds_main) >= (kRouteMaxT + kStageSubMax) * 4, "staging fits");
         int32_t* req_s = reinterpret_cast<int32_t*>(lds_main);
         uint32_t* sub_s = reinterpret_cast<uint32_t*>(lds_main) + kRouteMaxT;
-        stage_route<kEncThreads>(r_req, r_Tmax, r_sub, r_Rmax, req_s, sub_s);
+        const bool seen = stage_route<kEncThreads>(r_req, r_Tmax, r_sub, r_Rmax, req_s, sub_s,
+                                                   1u << r_bit);
+        const uint64_t seen_b = wave_ballot(seen);
+        if (lane == 0) seen_s[wave] = seen_b != 0;
         uint32_t err = 0;
         const int32_t tv = clamp_t_valid(*r_tvalid, r_Tmax, err);
         const uint32_t keep = r_napps >= 32 ? 0xFFFFFFFFu : ((1u << r_napps) - 1u);
         const int own = blockIdx.x;
         uint32_t* masks = own == 0 ? r_mask : nullptr;
         __syncthreads();  // the staged inputs
+        bool any = false;
+#pragma unroll
+        for (int w = 0; w < kEncWaves; ++w) any = any || seen_s[w] != 0;
+        if (live && nt == 0 && any) {  // uniform
+            load_w(wa0, 0);
+            load_w(wa1, 1);
+            load_w(wa2, 2);
+            load_bias();
+            w_issued = true;
+        }
         if (own < r_napps && own != r_bit) {
             const int32_t n = build_token_list<kEncThreads>(req_s, tv, sub_s, r_sub, r_Rmax, keep,
                                                             own, r_Tmax, list_s, rtot_s, masks,
@@ -406,49 +485,10 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     } else {
         cnt = *app_count;
     }
-
-    // Tile order.  Few token tiles (decode): latent tile fastest, so the
-    // workgroups of the first token tile, the ones with live tokens, are
-    // dispatched first and spread over every CU (interleaving them with
-    // tiles past the live count would leave every other CU idle).
-    // Many token tiles (prefill): launch slot L runs on XCD L % 8; XCD x
-    // owns the latent tiles [x*M8, (x+1)*M8) and walks them in blocks of 8
-    // token tiles x 4 latent tiles, 32 consecutive slots per block, token
-    // blocks fastest.  The 32 workgroups of a block run together on the
-    // XCD's 32 CUs, so each K chunk of 8 token tiles and 4 dictionary
-    // slices is fetched into the XCD's L2 once and read by 4 and 8
-    // workgroups; consecutive blocks reuse the same 4 slices.
-    const int L = blockIdx.x;
-    int nt, mt;
-    if (n_nt <= kLatentFastTiles) {
-        nt = L / n_mt;
-        mt = L % n_mt;
-        if (nt >= n_nt) return;
-    } else {
-        const int xcd = L % 8, slot = L / 8;
-        const int m8 = (n_mt + 7) / 8;              // latent tiles per XCD
-        const int nbt = (n_nt + kBlkTok - 1) / kBlkTok;
-        const int b = slot / (kBlkTok * kBlkLat), p = slot % (kBlkTok * kBlkLat);
-        const int bt = b % nbt, bl = b / nbt;
-        const int lt = kBlkLat * bl + p / kBlkTok;
-        nt = kBlkTok * bt + p % kBlkTok;
-        if (nt >= n_nt || lt >= m8) return;
-        mt = xcd * m8 + lt;
-    }
-    if (mt >= n_mt) return;
+    if (!live) return;
     const int n0 = nt * kBN;
     if (n0 >= cnt) return;
     const int ntok = min(kBN, cnt - n0);
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
-    const int g = lane >> 5, j32 = lane & 31;
-    const int nK = d / kBK;  // a multiple of 4 (d % 256 == 0)
-
-    // operand A: this wave's 32 latents of the packed slice
-    const uint4* wbase = reinterpret_cast<const uint4*>(W) + static_cast<int64_t>(mt) * 2048 +
-                         wave * 256 + lane;
-    const int64_t wstride = static_cast<int64_t>(n_mt) * 2048;  // pieces per K chunk
 
     // operand B: gathered token rows; padding rows read a valid row and are
     // zeroed when written to LDS
@@ -463,13 +503,7 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
         xrow[p] = h + static_cast<int64_t>(tl[n0 + (ok ? n : 0)]) * d + 8 * xc;
     }
 
-    // folded bias of this lane's 16 latents, fetched before the K loop
-    float cfv[16];
-    {
-        const float* cf = c_fold + mt * kBM + 32 * wave + 4 * g;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) cfv[r] = cf[8 * (r / 4) + (r % 4)];
-    }
+    if (!w_issued) load_bias();
 
     f32x16_t acc[4];
     // the accumulators start from the folded bias
@@ -478,20 +512,7 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[b][r] = cfv[r];
 
-    uint4 wa0[4], wa1[4], wa2[4], wa3[4];   // W ring: 4 chunks, 3 in flight
     uint4 xv0[2], xv1[2];                   // token ring: 2 chunks in flight
-
-    // The dictionary is read once per launch: nontemporal loads stream it
-    // past the caches (about 4 % faster than cached loads at 65536 x 4096).
-    auto load_w = [&](uint4 (&a)[4], int kc) {
-        kc = min(kc, nK - 1);  // past the end: re-read the last chunk, unused
-        const u32x4_t* p = reinterpret_cast<const u32x4_t*>(wbase + kc * wstride);
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            const u32x4_t v = __builtin_nontemporal_load(p + s * 64);
-            a[s] = make_uint4(v.x, v.y, v.z, v.w);
-        }
-    };
     auto load_x = [&](uint4 (&xv)[2], int kc) {
         kc = min(kc, nK - 1);
 #pragma unroll
@@ -539,9 +560,11 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
 
     load_x(xv0, 0);
     load_x(xv1, 1);
-    load_w(wa0, 0);
-    load_w(wa1, 1);
-    load_w(wa2, 2);
+    if (!w_issued) {
+        load_w(wa0, 0);
+        load_w(wa1, 1);
+        load_w(wa2, 2);
+    }
     store_x(xv0, 0);
     for (int kc = 0; kc < nK; kc += 4) {
         step(kc + 0, wa0, wa3, xv0, xv1);
