@@ -276,23 +276,33 @@ __device__ __forceinline__ void select_slices(const float* const (&vrow)[NT], in
         lo[t] = -INFINITY;
         hi[t] = INFINITY;
     }
+    // m[t]: this lane's latents at or above tau[t], one bit each; the count
+    // is its population, so the emission below reuses the last round's masks
+    uint32_t m[NT];
+    auto masks = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            uint32_t b = 0;
+#pragma unroll
+            for (int i = 0; i < 32; ++i) b |= (x[t][i] >= tau[t] ? 1u : 0u) << i;
+            m[t] = b;
+        }
+    };
+    bool settled = false;
     for (int it = 0; it < kRefineIters; ++it) {
+        masks();
         int c[NT];
         bool bad[NT], any = false;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            int k = 0;
-#pragma unroll
-            for (int i = 0; i < 32; ++i) k += x[t][i] >= tau[t] ? 1 : 0;
-            c[t] = k;
-        }
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            c[t] = isum8(c[t]);
+            c[t] = isum8(__popc(m[t]));
             bad[t] = valid[t] && (c[t] > cap || c[t] < lo_cnt);
             any = any || bad[t];
         }
-        if (!wave_ballot(any)) break;  // uniform
+        if (!wave_ballot(any)) {  // uniform
+            settled = true;
+            break;
+        }
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             if (!bad[t]) continue;
@@ -311,17 +321,11 @@ __device__ __forceinline__ void select_slices(const float* const (&vrow)[NT], in
             }
         }
     }
+    // out of rounds: the final thresholds were set after the last masks
+    if (!settled) masks();
     // emission: this lane's selected latents go to the slots after those of
     // the lanes before it in the token's group of 8
-    uint32_t m[NT];
     int base[NT], total[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        uint32_t b = 0;
-#pragma unroll
-        for (int i = 0; i < 32; ++i) b |= (x[t][i] >= tau[t] ? 1u : 0u) << i;
-        m[t] = b;
-    }
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
         const int cl = __popc(m[t]);
