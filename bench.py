@@ -220,7 +220,7 @@ def stage_times(torch, step, n, before=None, warm=3):
     return {k: round(float(np.mean(v)), 3) for k, v in acc.items()}
 
 
-def stage_times_graph(torch, step, n=10, before=None):
+def stage_times_graph(torch, step, n=10, before=None, rotate=None):
     """Per stage of a hook step: the GPU time (us) of one launch of that
     stage alone, from a graph of R back-to-back launches of it (the same
     arguments as in the step; the device state it reads is the one a full
@@ -229,7 +229,9 @@ def stage_times_graph(torch, step, n=10, before=None):
     step, launch of its kernels in the graph included; unlike events
     between eager launches, it does not depend on the host's enqueue rate
     for short kernels.  `before()` runs ahead of the full step (restore
-    copies)."""
+    copies).  rotate = (copies, set_copy): the encode stages' launches
+    cycle through the dictionary copies (R at least their number), so that
+    no launch finds its dictionary in a cache."""
     names = step.stage_names()
     if before is not None:
         before()
@@ -237,13 +239,22 @@ def stage_times_graph(torch, step, n=10, before=None):
     torch.cuda.synchronize()
     out = {}
     for name in names:
-        reps = 1
+        rot = rotate is not None and "encode" in name
+        reps = len(rotate[0]) if rot else 1
+
+        def launches():
+            for i in range(reps):
+                if rot:
+                    rotate[1](rotate[0][i % len(rotate[0])])
+                step.run(only=name)
+            if rot:
+                rotate[1](rotate[0][0])
         for _ in range(2):
-            g = graph_of(torch, lambda: step.run(only=name, repeat=reps))
+            g = graph_of(torch, launches)
             g.replay()
             ms = time_replays(torch, g.replay, n) / reps
             del g
-            if reps > 1 or ms > 0.2:
+            if reps >= 20 or ms > 0.2:
                 break
             reps = 20
         out[name] = round(ms * 1e3, 3)
@@ -280,7 +291,7 @@ def timed_sae_step(torch, step, steps, warmup, n_stage):
     stages = stage_times(torch, step, n_stage,
                          before=lambda i: set_copy(copies[i % len(copies)]))
     set_copy(copies[0])
-    stages["graph"] = stage_times_graph(torch, step)
+    stages["graph"] = stage_times_graph(torch, step, rotate=(copies, set_copy))
     return ms_step, stats, stages, multi
 
 
@@ -347,7 +358,11 @@ def run_decode(torch, synth, HookStep, args):
     s = wl.layers[0].saes[0]
     n_sub = int(np.count_nonzero(wl.sub & 1))
     enc_bytes = s.m * wl.d * 2 + s.m * 4 + n_sub * wl.d * 2   # W_enc + folded bias + tokens
-    ms_enc = stages["L0/sae0/route+encode"] * 1e-3
+    # the encode kernel's launch duration: graphs of back-to-back launches
+    # (each on the next dictionary copy), the closest a HIP event gets to
+    # the kernel's own duration; the eager figure adds the dispatch gaps
+    ms_enc = stages["graph"]["L0/sae0/route+encode"] * 1e-3
+    ms_enc_eager = stages["L0/sae0/route+encode"] * 1e-3
     achieved = enc_bytes / (ms_enc * 1e-3) / 1e9
     out = {
         "metric": "hooked tokens/sec per layer + % HBM/MFMA roofline (decode & prefill shapes)",
@@ -369,10 +384,11 @@ def run_decode(torch, synth, HookStep, args):
                                                "in the same launch)",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic("decode"),
-                     "ms_per_launch": ms_enc, "launches_timed": n_stage,
-                     "algorithmic_bytes": enc_bytes,
-                     "timing": "HIP events on the step's stream around the encode stage, "
-                               "back-to-back eager steps, dictionary copies rotating"},
+                     "ms_per_launch": ms_enc, "algorithmic_bytes": enc_bytes,
+                     "timing": "HIP events on the step's stream around graphs of back-to-back "
+                               "launches of the encode stage, each launch on the next "
+                               "dictionary copy",
+                     "eager_ms_per_launch": ms_enc_eager, "eager_launches_timed": n_stage},
         "settle_s": SETTLE_S,
     }
     out["step_stats"] = stats
@@ -555,18 +571,27 @@ def time_step_graph(torch, step, args):
 
 def run_steer_probe(torch, synth, HookStep, args):
     """The 4-layer decode step of steering and probe apps (d=4096, T=R=256,
-    bits 0-3 steer, bits 4-7 probe), captured as one graph.  Hot: replays
-    back to back, so each step finds its rows in the caches as a layer does
-    right after the model wrote them.  Cold: before each timed step a 512 MiB
+    bits 0-3 steer, bits 4-7 probe).  Hot: graphs of STEPS_PER_GRAPH
+    consecutive steps (as the decode step's timing does) replayed back to
+    back, so each step finds its rows in the caches as a layer does right
+    after the model wrote them; also a graph of one step, whose replays each
+    pay a graph launch.  Cold: before each timed one-step graph a 512 MiB
     write evicts the caches (outside the timed interval)."""
     log("timing the 4-layer steering + probe decode step (c2)")
     wl = synth.make("c2")
     step = HookStep(wl)
     g = graph_of(torch, step.run)
-    settle(torch, g.replay, 0.1)
+
+    def steps():
+        for _ in range(STEPS_PER_GRAPH):
+            step.run()
+    gm = graph_of(torch, steps)
+    settle(torch, gm.replay, 0.1)
     for _ in range(args.warmup):
-        g.replay()
-    ms = time_replays(torch, g.replay, args.steps)
+        gm.replay()
+    n_rep = max(1, args.steps // STEPS_PER_GRAPH)
+    ms = time_replays(torch, gm.replay, n_rep) / STEPS_PER_GRAPH
+    ms_single = time_replays(torch, g.replay, args.steps)
     flush = torch.empty(512 * 2 ** 20, dtype=torch.uint8, device="cuda")
     cold = []
     for _ in range(max(20, args.steps // 4)):
@@ -582,6 +607,8 @@ def run_steer_probe(torch, synth, HookStep, args):
     res = {"workload": "decode steering + probe step, 4 hooked layers, d=4096 T=R=256, "
                        "4 steering + 4 probe apps, subscriptions Bernoulli(0.3)",
            "us_per_step": ms * 1e3, "us_per_layer": ms * 1e3 / len(wl.layers),
+           "steps_per_graph": STEPS_PER_GRAPH,
+           "one_step_graph_us_per_step": ms_single * 1e3,
            "cold_us_per_step": ms_cold * 1e3,
            "value": wl.T_valid * len(wl.layers) / (ms * 1e-3), "unit": "hooked tokens/s per layer",
            "hbm_bytes": step.hbm_bytes(),
@@ -589,7 +616,7 @@ def run_steer_probe(torch, synth, HookStep, args):
     res["conditional_us"] = time_conditional(torch, step, wl, args)
     log("timing parameter updates on the step graph")
     res["step_graph"] = time_step_graph(torch, step, args)
-    del step, g
+    del step, g, gm
     torch.cuda.empty_cache()
     return res, wl
 
@@ -641,7 +668,8 @@ def run_prefill(torch, synth, HookStep, args):
                                                   max(2, args.warmup // 10), args.prefill_steps)
     s4 = wl4.layers[0].saes[0]
     flops = 2.0 * wl4.T_valid * s4.m * wl4.d
-    ms4_enc = stages4["L0/sae0/encode"] * 1e-3
+    ms4_enc = stages4["graph"]["L0/sae0/encode"] * 1e-3
+    ms4_enc_eager = stages4["L0/sae0/encode"] * 1e-3
     tf = flops / (ms4_enc * 1e-3) / 1e12
     res = {
         "workload": "prefill hook step: route + 4 token probes + 4 pooled probes + SAE "
@@ -652,8 +680,10 @@ def run_prefill(torch, synth, HookStep, args):
                      "kernel": "sae_xstage_kernel + sae_gemm_kernel (encode GEMM)",
                      "achieved": tf, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": tf / MFMA_BF16_PEAK_TFLOPS, "ms_per_launch": ms4_enc,
-                     "timing": "HIP events on the step's stream around the encode stage, "
-                               "back-to-back eager steps, dictionary copies rotating",
+                     "timing": "HIP events on the step's stream around graphs of back-to-back "
+                               "launches of the encode stage, each launch on the next "
+                               "dictionary copy",
+                     "eager_ms_per_launch": ms4_enc_eager,
                      "algorithmic_flops": flops,
                      "traffic": measured_traffic("prefill")},
         "step_stats": stats4, "stages_us": stages4.pop("graph"), "stages_eager_us": stages4}
