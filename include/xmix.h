@@ -425,6 +425,47 @@ xmix_status xmix_sae_merge_topk_ring(const uint16_t *h, int32_t d, const xmix_ro
                                      int32_t layer_id, int32_t app_id, const xmix_ring *ring,
                                      void *stream);
 
+/* One SAE app of a batched encode: the per-app arguments of
+ * xmix_sae_encode_topk (ring == NULL) or xmix_sae_encode_topk_ring (ring
+ * set, rows with the given app_id), with the same requirements. */
+typedef struct {
+    int32_t app_bit;
+    const xmix_sae_dict *dict;
+    const uint16_t *b_enc;  /* read only when c_fold is NULL */
+    const uint16_t *b_dec;
+    const float *c_fold;    /* may be NULL: folded into ws first */
+    int32_t k;
+    int32_t *idx_out;       /* [T_max, k] */
+    uint16_t *val_out;      /* [T_max, k] */
+    void *ws;               /* this app's own workspace */
+    size_t ws_bytes;
+    const xmix_ring *ring;  /* NULL: no readback */
+    int32_t app_id;
+} xmix_sae_app;
+
+/* The SAE apps of one hook (Sec. 4.2, several apps composed at one layer)
+ * encoded together: results identical to one xmix_sae_encode_topk (or
+ * _ring) call per app, in any order (every app reads h as given).  At
+ * decode shapes (T_max <= 1024) the candidates of up to 8 apps come from one
+ * launch whose apps' tiles follow each other (a CU that finishes its slice
+ * of one app takes a slice of the next) and their merges from one more, so
+ * the apps pay two launches together; larger batches run the apps one after
+ * the other.  req_of_token [T_max] is required when an app has a ring.
+ * Host array `apps` [n_sae], 1 <= n_sae <= 32. */
+xmix_status xmix_sae_encode_topk_multi(const uint16_t *h, int32_t d, const xmix_route *rt,
+                                       int32_t n_sae, const xmix_sae_app *apps,
+                                       const int32_t *req_of_token, int32_t layer_id,
+                                       void *stream);
+/* The same with the step's routing built by the first launch (as
+ * xmix_route_sae_encode_candidates does): results identical to
+ * xmix_route_build followed by xmix_sae_encode_topk_multi. */
+xmix_status xmix_route_sae_encode_topk_multi(const int32_t *req_of_token,
+                                             const int32_t *T_valid, const uint32_t *sub_mask,
+                                             int32_t R_max, const xmix_route *rt,
+                                             uint32_t *err_word, const uint16_t *h, int32_t d,
+                                             int32_t n_sae, const xmix_sae_app *apps,
+                                             int32_t layer_id, void *stream);
+
 /* One-time repack of a row-major encoder dictionary W_enc [m, d] (bf16)
  * into the tiled layout the encode kernels stream (same bytes, permuted),
  * written to W_packed (device, m * d bf16, caller-owned, not overlapping
@@ -459,6 +500,29 @@ xmix_status xmix_sae_clamp_decode(uint16_t *h, int32_t d, const xmix_route *rt,
                                   const uint16_t *W_dec, int32_t m,
                                   const int32_t *clamp_ids, const float *clamp_vals,
                                   int32_t n_clamp, float *delta_out, void *stream);
+
+/* One clamp app of a batched clamp-decode: the per-app arguments of
+ * xmix_sae_clamp_decode, with the same requirements. */
+typedef struct {
+    int32_t app_bit;
+    const int32_t *idx;
+    const uint16_t *val;
+    int32_t k;
+    const uint16_t *W_dec;
+    int32_t m;
+    const int32_t *clamp_ids;
+    const float *clamp_vals;
+    int32_t n_clamp;
+    float *delta_out;  /* may be NULL */
+} xmix_sae_clamp_app;
+
+/* Several clamp apps of one hook in one launch: h ends identical to one
+ * xmix_sae_clamp_decode call per app in the order of `apps` (each app's
+ * delta rounded in as that call rounds it; a token's row is read and written
+ * once).  Host array `apps` [n], 1 <= n <= 32. */
+xmix_status xmix_sae_clamp_decode_multi(uint16_t *h, int32_t d, const xmix_route *rt,
+                                        int32_t n, const xmix_sae_clamp_app *apps,
+                                        void *stream);
 
 /* ----------------------------------------------------- readback compaction
  * Buffer-mediated readback (Sec. 1; Sec. 4.2 "State and dataflow"): the

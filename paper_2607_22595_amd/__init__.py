@@ -58,6 +58,20 @@ class XmixSaeDict(ctypes.Structure):
 
 _vp, _i32, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
 _dp = ctypes.POINTER(XmixSaeDict)
+
+
+class XmixSaeApp(ctypes.Structure):
+    _fields_ = [("app_bit", _i32), ("dict", _dp), ("b_enc", _vp), ("b_dec", _vp),
+                ("c_fold", _vp), ("k", _i32), ("idx_out", _vp), ("val_out", _vp), ("ws", _vp),
+                ("ws_bytes", _sz), ("ring", ctypes.POINTER(XmixRing)), ("app_id", _i32)]
+
+
+class XmixSaeClampApp(ctypes.Structure):
+    _fields_ = [("app_bit", _i32), ("idx", _vp), ("val", _vp), ("k", _i32), ("W_dec", _vp),
+                ("m", _i32), ("clamp_ids", _vp), ("clamp_vals", _vp), ("n_clamp", _i32),
+                ("delta_out", _vp)]
+
+
 _st = ctypes.c_int
 _sigs = {
     "xmix_status_string": ([_st], ctypes.c_char_p),
@@ -101,6 +115,13 @@ _sigs = {
     "xmix_sae_merge_topk_ring": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _dp, _vp, _i32,
                                   _vp, _vp, _vp, _sz, _vp, _i32, _i32,
                                   ctypes.POINTER(XmixRing), _vp], _st),
+    "xmix_sae_encode_topk_multi": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32,
+                                    ctypes.POINTER(XmixSaeApp), _vp, _i32, _vp], _st),
+    "xmix_route_sae_encode_topk_multi": ([_vp, _vp, _vp, _i32, ctypes.POINTER(XmixRoute), _vp,
+                                          _vp, _i32, _i32, ctypes.POINTER(XmixSaeApp), _i32,
+                                          _vp], _st),
+    "xmix_sae_clamp_decode_multi": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32,
+                                     ctypes.POINTER(XmixSaeClampApp), _vp], _st),
     "xmix_sae_pack_encoder": ([_vp, _i32, _i32, _vp, _dp, _vp], _st),
     "xmix_sae_fold_bias": ([_dp, _vp, _vp, _vp, _vp], _st),
     "xmix_sae_clamp_decode": ([_vp, _i32, ctypes.POINTER(XmixRoute), _i32, _vp, _vp, _i32, _vp,
@@ -532,6 +553,77 @@ def xmix_sae_clamp_decode(h, route: Route, app_bit: int, idx, val, W_dec, clamp_
     _check("xmix_sae_clamp_decode", _lib.xmix_sae_clamp_decode(
         _ptr(h), d, ctypes.byref(route.struct), app_bit, _ptr(idx), _ptr(val), k, _ptr(W_dec), m,
         _ptr(clamp_ids), _ptr(clamp_vals), clamp_ids.numel(), _ptr(delta_out), _stream(stream)))
+
+
+class SaeApp:
+    """One SAE app of a batched encode: the per-app arguments of
+    xmix_sae_encode_topk (ring None) or xmix_sae_encode_topk_ring."""
+
+    def __init__(self, app_bit: int, W: SaeDict, b_enc, b_dec, c_fold, k: int, idx_out,
+                 val_out, ws, ring: Optional[Ring] = None, app_id: Optional[int] = None):
+        self.app_bit, self.W, self.b_enc, self.b_dec, self.c_fold = app_bit, _dict(W), b_enc, \
+            b_dec, c_fold
+        self.k, self.idx_out, self.val_out, self.ws, self.ring = k, idx_out, val_out, ws, ring
+        self.app_id = app_bit if app_id is None else app_id
+
+    def struct(self, T_max: int) -> XmixSaeApp:
+        assert self.idx_out.dtype == torch.int32 and self.idx_out.shape == (T_max, self.k)
+        assert self.val_out.dtype == torch.bfloat16 and self.val_out.shape == (T_max, self.k)
+        return XmixSaeApp(self.app_bit, ctypes.pointer(self.W.struct), _ptr(self.b_enc),
+                          _ptr(self.b_dec), _ptr(self.c_fold), self.k, _ptr(self.idx_out),
+                          _ptr(self.val_out), _ptr(self.ws),
+                          self.ws.numel() * self.ws.element_size(),
+                          ctypes.pointer(self.ring.struct) if self.ring is not None else None,
+                          self.app_id)
+
+
+def _sae_apps(apps: Sequence[SaeApp], T_max: int):
+    arr = (XmixSaeApp * len(apps))(*[a.struct(T_max) for a in apps])
+    return arr
+
+
+def xmix_sae_encode_topk_multi(h, route: Route, apps: Sequence[SaeApp], req_of_token=None,
+                               layer_id: int = 0, stream=None):
+    """The SAE apps of one hook encoded together (results identical to one
+    xmix_sae_encode_topk or _ring call per app)."""
+    T_max, d = h.shape
+    assert h.dtype == torch.bfloat16
+    arr = _sae_apps(apps, T_max)
+    _check("xmix_sae_encode_topk_multi", _lib.xmix_sae_encode_topk_multi(
+        _ptr(h), d, ctypes.byref(route.struct), len(apps), arr, _ptr(req_of_token), layer_id,
+        _stream(stream)))
+
+
+def xmix_route_sae_encode_topk_multi(req_of_token, T_valid, sub_mask, route: Route, err_word, h,
+                                     apps: Sequence[SaeApp], layer_id: int = 0, stream=None):
+    """The batched encode with the step's routing built by its first launch."""
+    T_max, d = h.shape
+    assert T_max == route.T_max and h.dtype == torch.bfloat16
+    arr = _sae_apps(apps, T_max)
+    _check("xmix_route_sae_encode_topk_multi", _lib.xmix_route_sae_encode_topk_multi(
+        _ptr(req_of_token), _ptr(T_valid), _ptr(sub_mask), sub_mask.numel(),
+        ctypes.byref(route.struct), _ptr(err_word), _ptr(h), d, len(apps), arr, layer_id,
+        _stream(stream)))
+
+
+def xmix_sae_clamp_decode_multi(h, route: Route, apps: Sequence[tuple], stream=None):
+    """apps: (app_bit, idx, val, W_dec, clamp_ids, clamp_vals[, delta_out]) per
+    clamp app, applied in this order (h ends as after one
+    xmix_sae_clamp_decode call per app)."""
+    T_max, d = h.shape
+    assert h.dtype == torch.bfloat16
+    items = []
+    for a in apps:
+        bit, idx, val, W_dec, ids, vals = a[:6]
+        delta = a[6] if len(a) > 6 else None
+        assert W_dec.dtype == torch.bfloat16 and ids.dtype == torch.int32
+        assert vals.dtype == torch.float32
+        items.append(XmixSaeClampApp(bit, _ptr(idx), _ptr(val), idx.shape[1], _ptr(W_dec),
+                                     W_dec.shape[0], _ptr(ids), _ptr(vals), ids.numel(),
+                                     _ptr(delta)))
+    arr = (XmixSaeClampApp * len(items))(*items)
+    _check("xmix_sae_clamp_decode_multi", _lib.xmix_sae_clamp_decode_multi(
+        _ptr(h), d, ctypes.byref(route.struct), len(items), arr, _stream(stream)))
 
 
 def xmix_readback_compact(segments: Sequence[torch.Tensor], route: Route, app_bit: int,

@@ -394,6 +394,94 @@ xmix_status xmix_sae_encode_topk(const uint16_t* h, int32_t d, const xmix_route*
                                ws_bytes, stream);
 }
 
+}  // extern "C"
+
+namespace {
+
+bool ring_ok(const xmix_ring* ring, int32_t k) {
+    return ring->slots && ring->head && ring->capacity >= 1 && ring->row_bytes == 16 + 6 * k &&
+           (reinterpret_cast<uintptr_t>(ring->slots) & 3u) == 0 &&
+           (reinterpret_cast<uintptr_t>(ring->head) & 7u) == 0;
+}
+
+// The batched encode: every app is checked before anything is launched;
+// apps without a folded bias get it folded into their workspace first.
+xmix_status encode_multi(const uint16_t* h, int32_t d, const xmix_route* rt, int32_t n,
+                         const xmix_sae_app* apps, const int32_t* req_of_token,
+                         int32_t layer_id, hipStream_t s, const RouteIn* route) {
+    if (!apps || n < 1 || n > XMIX_MAX_APPS || !route_ok(rt)) return XMIX_E_INVAL;
+    SaeAppIn in[XMIX_MAX_APPS];
+    MergeRing rings[XMIX_MAX_APPS];
+    float* fold[XMIX_MAX_APPS] = {};
+    for (int32_t i = 0; i < n; ++i) {
+        const xmix_sae_app& a = apps[i];
+        if (!a.idx_out || !a.val_out) return XMIX_E_INVAL;
+        if (!a.c_fold && (!a.b_enc || !a.b_dec || !aligned16(a.b_dec))) return XMIX_E_INVAL;
+        if (a.ring && (!req_of_token || !ring_ok(a.ring, a.k))) return XMIX_E_INVAL;
+        void* cand;
+        const xmix_status st =
+            encode_args(h, d, rt, a.app_bit, a.dict, a.k, a.ws, a.ws_bytes, &fold[i], &cand);
+        if (st != XMIX_OK) return st;
+        if (a.ring) {
+            rings[i] = MergeRing{a.ring->slots, a.ring->head, a.ring->capacity,
+                                 a.ring->row_bytes, req_of_token, layer_id, a.app_id};
+        }
+        in[i] = SaeAppIn{rt->app_count + a.app_bit, app_list(rt, a.app_bit), a.dict->pieces,
+                         a.c_fold ? a.c_fold : fold[i], a.dict->m, a.k, a.app_bit, cand,
+                         a.idx_out, a.val_out, a.ring ? &rings[i] : nullptr};
+    }
+    for (int32_t i = 0; i < n; ++i) {
+        const xmix_sae_app& a = apps[i];
+        if (!a.c_fold && launch_sae_fold(a.dict->pieces, a.b_enc, a.b_dec, a.dict->m, d, fold[i],
+                                         s) != hipSuccess)
+            return XMIX_E_LAUNCH;
+    }
+    if (sae_multi_supported(rt->T_max))
+        return launched(launch_sae_encode_multi(h, d, rt->T_max, n, in, s, route));
+    for (int32_t i = 0; i < n; ++i) {  // many token slots: one app after the other
+        const SaeAppIn& a = in[i];
+        if (launch_sae_candidates(h, d, rt->T_max, a.app_count, a.tok_list, a.W, a.c_fold, a.m,
+                                  a.k, a.cand, s, i == 0 ? route : nullptr) != hipSuccess ||
+            launch_sae_merge(h, d, rt->T_max, a.app_count, a.tok_list, a.W, a.c_fold, a.m, a.k,
+                             a.idx_out, a.val_out, a.cand, a.ring, s) != hipSuccess)
+            return XMIX_E_LAUNCH;
+    }
+    return XMIX_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+xmix_status xmix_sae_encode_topk_multi(const uint16_t* h, int32_t d, const xmix_route* rt,
+                                       int32_t n_sae, const xmix_sae_app* apps,
+                                       const int32_t* req_of_token, int32_t layer_id,
+                                       void* stream) {
+    return encode_multi(h, d, rt, n_sae, apps, req_of_token, layer_id, as_stream(stream),
+                        nullptr);
+}
+
+xmix_status xmix_route_sae_encode_topk_multi(const int32_t* req_of_token,
+                                             const int32_t* T_valid, const uint32_t* sub_mask,
+                                             int32_t R_max, const xmix_route* rt,
+                                             uint32_t* err_word, const uint16_t* h, int32_t d,
+                                             int32_t n_sae, const xmix_sae_app* apps,
+                                             int32_t layer_id, void* stream) {
+    if (!req_of_token || !T_valid || !sub_mask || !err_word || R_max < 1 || !route_ok(rt))
+        return XMIX_E_INVAL;
+    RouteIn r;
+    r.req = req_of_token;
+    r.T_valid = T_valid;
+    r.sub = sub_mask;
+    r.R_max = R_max;
+    r.n_apps = rt->n_apps;
+    r.tok_mask = rt->tok_mask;
+    r.app_count = rt->app_count;
+    r.app_tokens = rt->app_tokens;
+    r.err_word = err_word;
+    return encode_multi(h, d, rt, n_sae, apps, req_of_token, layer_id, as_stream(stream), &r);
+}
+
 xmix_status xmix_sae_clamp_decode(uint16_t* h, int32_t d, const xmix_route* rt,
                                   int32_t app_bit, const int32_t* idx, const uint16_t* val,
                                   int32_t k, const uint16_t* W_dec, int32_t m,
@@ -409,6 +497,25 @@ xmix_status xmix_sae_clamp_decode(uint16_t* h, int32_t d, const xmix_route* rt,
     return launched(launch_clamp_decode(h, d, rt->app_count + app_bit, app_list(rt, app_bit),
                                         rt->T_max, idx, val, k, W_dec, m, clamp_ids, clamp_vals,
                                         n_clamp, delta_out, as_stream(stream)));
+}
+
+xmix_status xmix_sae_clamp_decode_multi(uint16_t* h, int32_t d, const xmix_route* rt, int32_t n,
+                                        const xmix_sae_clamp_app* apps, void* stream) {
+    if (!h || !apps || n < 1 || n > XMIX_MAX_APPS || !route_ok(rt)) return XMIX_E_INVAL;
+    if (d < 8 || d % 8 != 0 || !aligned16(h)) return XMIX_E_INVAL;
+    ClampAppIn in[XMIX_MAX_APPS];
+    for (int32_t i = 0; i < n; ++i) {
+        const xmix_sae_clamp_app& a = apps[i];
+        if (!a.idx || !a.val || !a.W_dec || !a.clamp_ids || !a.clamp_vals) return XMIX_E_INVAL;
+        if (a.app_bit < 0 || a.app_bit >= rt->n_apps) return XMIX_E_INVAL;
+        if (a.m < 1 || a.k < 1 || a.k > XMIX_MAX_TOPK) return XMIX_E_INVAL;
+        if (a.n_clamp < 1 || a.n_clamp > XMIX_MAX_CLAMP) return XMIX_E_INVAL;
+        if (!aligned16(a.W_dec) || (a.delta_out && !aligned16(a.delta_out))) return XMIX_E_INVAL;
+        in[i] = ClampAppIn{a.idx, a.val, a.W_dec, a.clamp_ids, a.clamp_vals, a.delta_out,
+                           a.k, a.m, a.n_clamp, a.app_bit};
+    }
+    return launched(launch_clamp_multi(h, d, rt->T_max, rt->tok_mask, n, in,
+                                       as_stream(stream)));
 }
 
 xmix_status xmix_readback_compact(const void* const* seg_rows, const int32_t* seg_bytes,

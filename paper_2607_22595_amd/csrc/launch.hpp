@@ -45,6 +45,8 @@ hipError_t launch_sae_pack(const uint16_t* W_enc, int32_t m, int32_t d, uint16_t
                            hipStream_t stream);
 hipError_t launch_sae_fold(const uint16_t* W_enc, const uint16_t* b_enc, const uint16_t* b_dec,
                            int32_t m, int32_t d, float* c_fold, hipStream_t stream);
+constexpr int kMultiMax = 8;  // SAE apps per batched launch
+
 // Routing inputs and outputs for an encode launch that also builds the
 // step's routing (see xmix_route_sae_encode_candidates).
 struct RouteIn {
@@ -82,12 +84,45 @@ hipError_t launch_sae_merge(const uint16_t* h, int32_t d, int32_t T_max,
                             const uint16_t* W_enc, const float* c_fold, int32_t m, int32_t k,
                             int32_t* idx_out, uint16_t* val_out, void* cand,
                             const MergeRing* ring, hipStream_t stream);
+// One SAE app of a batched encode: its list, dictionary, folded bias,
+// candidate area, outputs and optional ring.
+struct SaeAppIn {
+    const int32_t* app_count;
+    const int32_t* tok_list;
+    const uint16_t* W;
+    const float* c_fold;
+    int32_t m, k, bit;
+    void* cand;
+    int32_t* idx_out;
+    uint16_t* val_out;
+    const MergeRing* ring;
+};
+// The candidates of up to kMultiMax apps in one launch, then their merges in
+// one launch (decode shapes: T_max < the prefill threshold).
+hipError_t launch_sae_encode_multi(const uint16_t* h, int32_t d, int32_t T_max, int32_t n,
+                                   const SaeAppIn* apps, hipStream_t stream,
+                                   const RouteIn* route = nullptr);
+bool sae_multi_supported(int32_t T_max);
 
 hipError_t launch_clamp_decode(uint16_t* h, int32_t d, const int32_t* app_count,
                                const int32_t* tok_list, int32_t T_max, const int32_t* idx,
                                const uint16_t* val, int32_t k, const uint16_t* W_dec, int32_t m,
                                const int32_t* clamp_ids, const float* clamp_vals,
                                int32_t n_clamp, float* delta_out, hipStream_t stream);
+// One clamp app of a batched clamp-decode.
+struct ClampAppIn {
+    const int32_t* idx;
+    const uint16_t* val;
+    const uint16_t* W_dec;
+    const int32_t* clamp_ids;
+    const float* clamp_vals;
+    float* delta_out;
+    int32_t k, m, n_clamp, bit;
+};
+// Up to kMultiMax clamp apps in one launch, one workgroup per token slot,
+// the apps applied to each row in the given order.
+hipError_t launch_clamp_multi(uint16_t* h, int32_t d, int32_t T_max, const uint32_t* tok_mask,
+                              int32_t n, const ClampAppIn* apps, hipStream_t stream);
 
 struct Segments {
     const uint8_t* ptr[4];

@@ -45,6 +45,7 @@
 // to the 8 XCDs, so consecutive tiles of one XCD share a dictionary slice in
 // that XCD's L2.
 #include <math.h>
+#include <string.h>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -353,17 +354,18 @@ __device__ __forceinline__ void select_slices(const float* const (&vrow)[NT], in
 }
 
 // ---------------------------------------------- GEMM + candidate emission
-__global__ void __launch_bounds__(kEncThreads, 1)
-sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
-                  const int32_t* __restrict__ app_count, const int32_t* __restrict__ tok_list,
-                  const uint16_t* __restrict__ W, const float* __restrict__ c_fold,
-                  int32_t n_mt, int32_t n_nt, float z_guess, int32_t lo_cnt, int32_t cap,
-                  uint2* __restrict__ cand, int32_t* __restrict__ tile_cnt,
-                  float* __restrict__ tile_tau, const int32_t* __restrict__ r_req,
-                  const int32_t* __restrict__ r_tvalid, const uint32_t* __restrict__ r_sub,
-                  int32_t r_Rmax, int32_t r_Tmax, int32_t r_napps, int32_t r_bit,
-                  uint32_t* __restrict__ r_mask, int32_t* __restrict__ r_count,
-                  int32_t* __restrict__ r_lists, uint32_t* __restrict__ r_err) {
+// One workgroup's tile: L is the tile's launch slot within its app's grid,
+// own the workgroup's index in the launch (its route-publishing duty).
+__device__ __forceinline__ void stream_tile(
+    int L, int own, const uint16_t* __restrict__ h, int32_t d,
+    const int32_t* __restrict__ app_count, const int32_t* __restrict__ tok_list,
+    const uint16_t* __restrict__ W, const float* __restrict__ c_fold, int32_t n_mt, int32_t n_nt,
+    float z_guess, int32_t lo_cnt, int32_t cap, uint2* __restrict__ cand,
+    int32_t* __restrict__ tile_cnt, float* __restrict__ tile_tau,
+    const int32_t* __restrict__ r_req, const int32_t* __restrict__ r_tvalid,
+    const uint32_t* __restrict__ r_sub, int32_t r_Rmax, int32_t r_Tmax, int32_t r_napps,
+    int32_t r_bit, uint32_t* __restrict__ r_mask, int32_t* __restrict__ r_count,
+    int32_t* __restrict__ r_lists, uint32_t* __restrict__ r_err) {
     // K loop: two 16 KiB token chunks; epilogue: the tile's 128 token rows
     __shared__ uint4 lds_main[kBN * kSelStride / 4];
     static_assert(kBN * kSelStride / 4 >= 2 * kBN * 8, "token chunks fit");
@@ -372,10 +374,10 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     __shared__ int32_t seen_s[kEncWaves];
     uint4 (*xs)[kBN * 8] = reinterpret_cast<uint4 (*)[kBN * 8]>(lds_main);
 
-    // Tile order.  Few token tiles (decode): latent tile fastest, so the
-    // workgroups of the first token tile, the ones with live tokens, are
-    // dispatched first and spread over every CU (interleaving them with
-    // tiles past the live count would leave every other CU idle).
+    // Tile order.  Few token tiles (decode): one workgroup per latent tile,
+    // which takes the live token tiles of its slice in turn (no workgroup
+    // is launched for a tile past the live count; the first tile, the one
+    // every live token count reaches, spreads over every CU).
     // Many token tiles (prefill): launch slot L runs on XCD L % 8; XCD x
     // owns the latent tiles [x*M8, (x+1)*M8) and walks them in blocks of 8
     // token tiles x 4 latent tiles, 32 consecutive slots per block, token
@@ -383,7 +385,6 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     // XCD's 32 CUs, so each K chunk of 8 token tiles and 4 dictionary
     // slices is fetched into the XCD's L2 once and read by 4 and 8
     // workgroups; consecutive blocks reuse the same 4 slices.
-    const int L = blockIdx.x;
     int nt, mt;
     bool live;  // the tile exists (its tokens are counted below)
     if (n_nt <= kLatentFastTiles) {
@@ -455,12 +456,14 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
         uint32_t err = 0;
         const int32_t tv = clamp_t_valid(*r_tvalid, r_Tmax, err);
         const uint32_t keep = r_napps >= 32 ? 0xFFFFFFFFu : ((1u << r_napps) - 1u);
-        const int own = blockIdx.x;
         uint32_t* masks = own == 0 ? r_mask : nullptr;
         __syncthreads();  // the staged inputs
         bool any = false;
 #pragma unroll
         for (int w = 0; w < kEncWaves; ++w) any = any || seen_s[w] != 0;
+        // no request subscribes to the app: no token is listed, and a
+        // workgroup with nothing to publish is done
+        if (!any && own >= r_napps) return;  // uniform
         if (live && nt == 0 && any) {  // uniform
             load_w(wa0, 0);
             load_w(wa1, 1);
@@ -489,33 +492,15 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     } else {
         cnt = *app_count;
     }
-    if (!live) return;
-    const int n0 = nt * kBN;
-    if (n0 >= cnt) return;
-    const int ntok = min(kBN, cnt - n0);
+    if (!live || nt * kBN >= cnt) return;
+    if (!w_issued) load_bias();  // the slice's bias serves every token tile
 
     // operand B: gathered token rows; padding rows read a valid row and are
     // zeroed when written to LDS
     const int xr = tid >> 3, xc = tid & 7;
     const uint16_t* xrow[2];
     uint32_t xmask[2];
-#pragma unroll
-    for (int p = 0; p < 2; ++p) {
-        const int n = xr + 64 * p;
-        const bool ok = n < ntok;
-        xmask[p] = ok ? 0xFFFFFFFFu : 0u;
-        xrow[p] = h + static_cast<int64_t>(tl[n0 + (ok ? n : 0)]) * d + 8 * xc;
-    }
-
-    if (!w_issued) load_bias();
-
     f32x16_t acc[4];
-    // the accumulators start from the folded bias
-#pragma unroll
-    for (int b = 0; b < 4; ++b)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[b][r] = cfv[r];
-
     uint4 xv0[2], xv1[2];                   // token ring: 2 chunks in flight
     auto load_x = [&](uint4 (&xv)[2], int kc) {
         kc = min(kc, nK - 1);
@@ -562,6 +547,24 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
         store_x(xstore, (kc + 1) & 1);
     };
 
+    const bool tiles_in_turn = n_nt <= kLatentFastTiles;
+    for (;; ++nt) {
+    const int n0 = nt * kBN;
+    if (n0 >= cnt) return;
+    const int ntok = min(kBN, cnt - n0);
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+        const int n = xr + 64 * p;
+        const bool ok = n < ntok;
+        xmask[p] = ok ? 0xFFFFFFFFu : 0u;
+        xrow[p] = h + static_cast<int64_t>(tl[n0 + (ok ? n : 0)]) * d + 8 * xc;
+    }
+    // the accumulators start from the folded bias
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[b][r] = cfv[r];
+
     load_x(xv0, 0);
     load_x(xv1, 1);
     if (!w_issued) {
@@ -569,6 +572,7 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
         load_w(wa1, 1);
         load_w(wa2, 2);
     }
+    w_issued = false;
     store_x(xv0, 0);
     for (int kc = 0; kc < nK; kc += 4) {
         step(kc + 0, wa0, wa3, xv0, xv1);
@@ -604,6 +608,61 @@ sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
     int32_t* const co[2] = {tile_cnt + row0, tile_cnt + row1};
     float* const to[2] = {tile_tau + row0, tile_tau + row1};
     select_slices<true, 2>(vr, q, ok, z_guess, lo_cnt, cap, mt * kBM, dst, co, to);
+    if (!tiles_in_turn || nt + 1 >= n_nt) return;
+    __syncthreads();  // the tile rows are read before the next tile's token chunks land
+    }
+}
+
+__global__ void __launch_bounds__(kEncThreads, 1)
+sae_stream_kernel(const uint16_t* __restrict__ h, int32_t d,
+                  const int32_t* __restrict__ app_count, const int32_t* __restrict__ tok_list,
+                  const uint16_t* __restrict__ W, const float* __restrict__ c_fold,
+                  int32_t n_mt, int32_t n_nt, float z_guess, int32_t lo_cnt, int32_t cap,
+                  uint2* __restrict__ cand, int32_t* __restrict__ tile_cnt,
+                  float* __restrict__ tile_tau, const int32_t* __restrict__ r_req,
+                  const int32_t* __restrict__ r_tvalid, const uint32_t* __restrict__ r_sub,
+                  int32_t r_Rmax, int32_t r_Tmax, int32_t r_napps, int32_t r_bit,
+                  uint32_t* __restrict__ r_mask, int32_t* __restrict__ r_count,
+                  int32_t* __restrict__ r_lists, uint32_t* __restrict__ r_err) {
+    stream_tile(blockIdx.x, blockIdx.x, h, d, app_count, tok_list, W, c_fold, n_mt, n_nt,
+                z_guess, lo_cnt, cap, cand, tile_cnt, tile_tau, r_req, r_tvalid, r_sub, r_Rmax,
+                r_Tmax, r_napps, r_bit, r_mask, r_count, r_lists, r_err);
+}
+
+// Several SAE apps of one hook in one launch: the apps' grids follow each
+// other (app i owns launch slots [grid0[i], grid0[i + 1])), so a CU that
+// finishes its slice of one app takes a slice of the next, and the step
+// pays one launch for every app's candidates.
+struct EncApp {
+    const int32_t* app_count;
+    const int32_t* tok_list;
+    const uint16_t* W;
+    const float* c_fold;
+    uint2* cand;
+    int32_t* tile_cnt;
+    float* tile_tau;
+    int32_t n_mt, lo_cnt, cap, bit, grid0;
+    float z;
+};
+struct EncApps {
+    EncApp a[kMultiMax];
+    int32_t n, grid_end;
+};
+
+__global__ void __launch_bounds__(kEncThreads, 1)
+sae_stream_multi_kernel(const uint16_t* __restrict__ h, int32_t d, int32_t n_nt, EncApps apps,
+                        const int32_t* __restrict__ r_req, const int32_t* __restrict__ r_tvalid,
+                        const uint32_t* __restrict__ r_sub, int32_t r_Rmax, int32_t r_Tmax,
+                        int32_t r_napps, uint32_t* __restrict__ r_mask,
+                        int32_t* __restrict__ r_count, int32_t* __restrict__ r_lists,
+                        uint32_t* __restrict__ r_err) {
+    const int g = blockIdx.x;
+    int i = 0;
+    for (int j = 1; j < apps.n; ++j) i = g >= apps.a[j].grid0 ? j : i;  // uniform
+    const EncApp& a = apps.a[i];
+    stream_tile(g - a.grid0, g, h, d, a.app_count, a.tok_list, a.W, a.c_fold, a.n_mt, n_nt, a.z,
+                a.lo_cnt, a.cap, a.cand, a.tile_cnt, a.tile_tau, r_req, r_tvalid, r_sub, r_Rmax,
+                r_Tmax, r_napps, a.bit, r_mask, r_count, r_lists, r_err);
 }
 
 // ------------------------------------------ prefill GEMM + candidate emission
@@ -1278,15 +1337,15 @@ __device__ __forceinline__ float slice_dot(const uint16_t* __restrict__ Wp,
 // at its rank.  When the candidates exceed the pool, the k-th best of the
 // first kPoolMax of them is a lower bound of the k-th best of all: the pool
 // is filled again with the candidates at or above it (a little below, so
-// that a repair finds what it needs), up to kFloorRounds times.
-__global__ void __launch_bounds__(kMergeThreads) __attribute__((amdgpu_waves_per_eu(4)))
-sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ tile_cnt,
-                 const float* __restrict__ tile_tau, int32_t n_mt, int32_t cap,
-                 const int32_t* __restrict__ app_count, const int32_t* __restrict__ tok_list,
-                 int32_t k, const uint16_t* __restrict__ h, int32_t d,
-                 const uint16_t* __restrict__ Wp, const float* __restrict__ c_fold,
-                 int32_t* __restrict__ idx_out, uint16_t* __restrict__ val_out,
-                 RingOut ring) {
+// that a repair finds what it needs), up to kFloorRounds times.  n: the
+// workgroup's slot of the app's token list.
+__device__ __forceinline__ void merge_token(
+    int n, const uint2* __restrict__ cand, const int32_t* __restrict__ tile_cnt,
+    const float* __restrict__ tile_tau, int32_t n_mt, int32_t cap,
+    const int32_t* __restrict__ app_count, const int32_t* __restrict__ tok_list, int32_t k,
+    const uint16_t* __restrict__ h, int32_t d, const uint16_t* __restrict__ Wp,
+    const float* __restrict__ c_fold, int32_t* __restrict__ idx_out,
+    uint16_t* __restrict__ val_out, const RingOut& ring) {
     __shared__ uint32_t K[kPoolMax + kWave];
     __shared__ int32_t I[kPoolMax + kWave];
     __shared__ __align__(16) uint32_t K2[kWave];  // the selected k entries (k <= 64)
@@ -1301,7 +1360,6 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
     __shared__ uint32_t floor_s;
     __shared__ int fail_s[kMaxRepair];
     const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
-    const int n = blockIdx.x;
     const int64_t row0 = static_cast<int64_t>(n) * n_mt;
     // The first round of the gather below does not depend on the token
     // count: its loads go out before the count is read (the slot's area
@@ -1718,9 +1776,49 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
     }
 }
 
+__global__ void __launch_bounds__(kMergeThreads) __attribute__((amdgpu_waves_per_eu(4)))
+sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ tile_cnt,
+                 const float* __restrict__ tile_tau, int32_t n_mt, int32_t cap,
+                 const int32_t* __restrict__ app_count, const int32_t* __restrict__ tok_list,
+                 int32_t k, const uint16_t* __restrict__ h, int32_t d,
+                 const uint16_t* __restrict__ Wp, const float* __restrict__ c_fold,
+                 int32_t* __restrict__ idx_out, uint16_t* __restrict__ val_out,
+                 RingOut ring) {
+    merge_token(blockIdx.x, cand, tile_cnt, tile_tau, n_mt, cap, app_count, tok_list, k, h, d,
+                Wp, c_fold, idx_out, val_out, ring);
+}
+
+// Several SAE apps' merges in one launch: workgroup a * T_max + n takes
+// slot n of app a's list.
+struct MergeApp {
+    const uint2* cand;
+    const int32_t* tile_cnt;
+    const float* tile_tau;
+    const int32_t* app_count;
+    const int32_t* tok_list;
+    const uint16_t* Wp;
+    const float* c_fold;
+    int32_t* idx_out;
+    uint16_t* val_out;
+    RingOut ring;
+    int32_t n_mt, cap, k;
+};
+struct MergeApps {
+    MergeApp a[kMultiMax];
+};
+
+__global__ void __launch_bounds__(kMergeThreads) __attribute__((amdgpu_waves_per_eu(4)))
+sae_merge_multi_kernel(const uint16_t* __restrict__ h, int32_t d, int32_t T_max,
+                       MergeApps apps) {
+    const int i = blockIdx.x / T_max, n = blockIdx.x % T_max;
+    const MergeApp& a = apps.a[i];
+    merge_token(n, a.cand, a.tile_cnt, a.tile_tau, a.n_mt, a.cap, a.app_count, a.tok_list, a.k,
+                h, d, a.Wp, a.c_fold, a.idx_out, a.val_out, a.ring);
+}
+
 // ------------------------------------------------------------------ launch
 static int enc_grid(int32_t n_mt, int32_t n_nt) {
-    if (n_nt <= kLatentFastTiles) return n_mt * n_nt;
+    if (n_nt <= kLatentFastTiles) return n_mt;  // one workgroup per slice, tiles in turn
     const int m8 = (n_mt + 7) / 8;
     const int nbt = (n_nt + kBlkTok - 1) / kBlkTok;
     const int nbl = (m8 + kBlkLat - 1) / kBlkLat;
@@ -1875,6 +1973,68 @@ hipError_t launch_sae_merge(const uint16_t* h, int32_t d, int32_t T_max,
     return hipGetLastError();
 }
 
+bool sae_multi_supported(int32_t T_max) { return T_max < kPrefillMinT; }
+
+hipError_t launch_sae_encode_multi(const uint16_t* h, int32_t d, int32_t T_max, int32_t n,
+                                   const SaeAppIn* apps, hipStream_t stream,
+                                   const RouteIn* route) {
+    const int32_t n_nt = (T_max + kBN - 1) / kBN;
+    for (int32_t c0 = 0; c0 < n; c0 += kMultiMax) {
+        const int32_t nc = n - c0 < kMultiMax ? n - c0 : kMultiMax;
+        EncApps ea;
+        MergeApps ma;
+        memset(&ea, 0, sizeof(ea));
+        memset(&ma, 0, sizeof(ma));
+        int32_t grid = 0;
+        for (int32_t i = 0; i < nc; ++i) {
+            const SaeAppIn& in = apps[c0 + i];
+            const int32_t n_mt = in.m / kBM;
+            const EmitPlan e = emit_plan(in.m, in.k);
+            const CandArea a = cand_area(in.cand, T_max, n_mt, e.cap);
+            ea.a[i] = EncApp{in.app_count, in.tok_list, in.W, in.c_fold, a.cand, a.cnt, a.tau,
+                             n_mt, e.lo, e.cap, in.bit, grid, e.z};
+            grid += enc_grid(n_mt, n_nt);
+            RingOut r{};
+            if (in.ring) {
+                r.slots = in.ring->slots;
+                r.head = in.ring->head;
+                r.capacity = in.ring->capacity;
+                r.row_bytes = in.ring->row_bytes;
+                r.req = in.ring->req;
+                r.layer_id = in.ring->layer_id;
+                r.app_id = in.ring->app_id;
+            }
+            ma.a[i] = MergeApp{a.cand, a.cnt, a.tau, in.app_count, in.tok_list, in.W, in.c_fold,
+                               in.idx_out, in.val_out, r, n_mt, e.cap, in.k};
+        }
+        ea.n = nc;
+        ea.grid_end = grid;
+        // the first launch builds the routing when the batch fits its LDS list
+        // and its grid has a workgroup for every app to publish
+        const RouteIn* ri = c0 == 0 ? route : nullptr;
+        if (ri && (T_max > kRouteMaxT || grid < ri->n_apps)) {
+            const hipError_t r = launch_route_build(ri->req, ri->T_valid, ri->sub, ri->R_max,
+                                                    T_max, ri->n_apps, ri->tok_mask,
+                                                    ri->app_count, ri->app_tokens,
+                                                    ri->err_word, stream);
+            if (r != hipSuccess) return r;
+            ri = nullptr;
+        }
+        const RouteIn none{};
+        const RouteIn& rr = ri ? *ri : none;
+        hipLaunchKernelGGL(sae_stream_multi_kernel, dim3(grid), dim3(kEncThreads), 0, stream, h,
+                           d, n_nt, ea, rr.req, rr.T_valid, rr.sub, rr.R_max, T_max, rr.n_apps,
+                           rr.tok_mask, rr.app_count, rr.app_tokens, rr.err_word);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(sae_merge_multi_kernel, dim3(nc * T_max), dim3(kMergeThreads), 0,
+                           stream, h, d, T_max, ma);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 void add_sae_kernels(std::vector<KernelInfo>& t) {
     t.push_back(kernel_info(sae_pack_kernel));
     t.push_back(kernel_info(sae_fold_kernel));
@@ -1882,6 +2042,8 @@ void add_sae_kernels(std::vector<KernelInfo>& t) {
     t.push_back(kernel_info(sae_xstage_kernel));
     t.push_back(kernel_info(sae_gemm_kernel));
     t.push_back(kernel_info(sae_merge_kernel));
+    t.push_back(kernel_info(sae_stream_multi_kernel));
+    t.push_back(kernel_info(sae_merge_multi_kernel));
 }
 
 }  // namespace xmix

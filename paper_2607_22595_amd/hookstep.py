@@ -31,13 +31,14 @@ from typing import List, Optional
 import numpy as np
 import torch
 
-from . import (XMIX_PROBE_LAST, XMIX_PROBE_MEAN, XMIX_PROBE_TOKEN, Ring, Route, SaeDict,
+from . import (XMIX_PROBE_LAST, XMIX_PROBE_MEAN, XMIX_PROBE_TOKEN, Ring, Route, SaeApp, SaeDict,
                probe_workspace, sae_encode_workspace, xmix_probe_score, xmix_readback_compact,
-               xmix_route_build, xmix_sae_clamp_decode, xmix_sae_encode_candidates,
-               xmix_sae_encode_topk, xmix_sae_encode_topk_ring, xmix_sae_fold_bias,
-               xmix_route_sae_encode_candidates, xmix_route_steer_probe, xmix_sae_merge_topk,
-               xmix_sae_merge_topk_ring, xmix_sae_pack_encoder, xmix_steer_apply,
-               xmix_steer_probe)
+               xmix_route_build, xmix_route_sae_encode_topk_multi, xmix_sae_clamp_decode,
+               xmix_sae_clamp_decode_multi, xmix_sae_encode_candidates,
+               xmix_sae_encode_topk, xmix_sae_encode_topk_multi, xmix_sae_encode_topk_ring,
+               xmix_sae_fold_bias, xmix_route_sae_encode_candidates, xmix_route_steer_probe,
+               xmix_sae_merge_topk, xmix_sae_merge_topk_ring, xmix_sae_pack_encoder,
+               xmix_steer_apply, xmix_steer_probe)
 
 
 def to_device_bits(a: np.ndarray, device) -> torch.Tensor:
@@ -95,9 +96,15 @@ class _Layer:
 
 class HookStep:
     def __init__(self, wl, device="cuda", fold_bias: bool = True, fuse_readback: bool = True,
-                 fuse_steer_probe: bool = True, fuse_route: bool = True):
+                 fuse_steer_probe: bool = True, fuse_route: bool = True,
+                 batch_saes: bool = True):
         dev = torch.device(device)
         self.wl = wl
+        # a layer's SAE apps encoded by one batched call and clamped by
+        # another (two launches for every app's candidates and merges, one
+        # for every app's clamp) instead of two launches per app and one per
+        # clamp; the results are the per-app calls' bit for bit
+        self.batch_saes = batch_saes
         self.fuse_readback = fuse_readback
         self.fuse_steer_probe = fuse_steer_probe
         self.fuse_route = fuse_route
@@ -213,7 +220,22 @@ class HookStep:
                       lambda p=p, lay=lay: xmix_probe_score(
                           lay.h, self.route, p.w, p.b, p.bits, p.mode, p.logit, p.score,
                           cu_seqlens=self.cu, ws=p.ws, stream=stream))
-            for i, s in enumerate(lay.saes):
+            batched = (self.batch_saes and len(lay.saes) > 1
+                       and (self.fuse_readback or all(s.ring is None for s in lay.saes)))
+            if batched:
+                apps = [SaeApp(s.bit, s.W_enc, s.b_enc, s.b_dec, s.c_fold, s.k, s.idx, s.val,
+                               s.ws, s.ring if self.fuse_readback else None, s.bit)
+                        for s in lay.saes]
+                if route_in_encode and li == 0:
+                    issue(f"L{li}/saes/route+encode",
+                          lambda lay=lay, apps=apps: xmix_route_sae_encode_topk_multi(
+                              self.req, self.T_valid, self.sub, self.route, self.err, lay.h,
+                              apps, lay.layer_id, stream))
+                else:
+                    issue(f"L{li}/saes/encode",
+                          lambda lay=lay, apps=apps: xmix_sae_encode_topk_multi(
+                              lay.h, self.route, apps, self.req, lay.layer_id, stream))
+            for i, s in enumerate(lay.saes if not batched else []):
                 routed = route_in_encode and li == 0 and i == 0
                 name = f"L{li}/sae{s.bit}"
                 if split or routed:
@@ -260,8 +282,15 @@ class HookStep:
             elif lay.steer_v is not None:
                 issue(f"L{li}/steer", lambda lay=lay: xmix_steer_apply(
                     lay.h, self.route, self.req, lay.steer_v, lay.steer_bits, self.alpha, stream))
-            for s in lay.saes:
-                if s.W_dec is not None:
+            clampers = [s for s in lay.saes if s.W_dec is not None]
+            if self.batch_saes and len(clampers) > 1:
+                issue(f"L{li}/saes/clamp",
+                      lambda lay=lay, cs=clampers: xmix_sae_clamp_decode_multi(
+                          lay.h, self.route,
+                          [(s.bit, s.idx, s.val, s.W_dec, s.clamp_ids, s.clamp_vals) for s in cs],
+                          stream))
+            else:
+                for s in clampers:
                     issue(f"L{li}/sae{s.bit}/clamp",
                           lambda s=s, lay=lay: xmix_sae_clamp_decode(
                               lay.h, self.route, s.bit, s.idx, s.val, s.W_dec, s.clamp_ids,

@@ -175,3 +175,46 @@ def test_ceiling_library_exports_its_header():
     # invalid arguments are rejected before any device call
     assert lib.xmix_ceiling_read(None, ctypes.c_uint64(16), None, None) == 1
     assert lib.xmix_ceiling_mfma(0, None, None, None) == 1
+
+
+def test_batched_calls_check_every_app_on_the_host(lib):
+    """Fake (never dereferenced) device addresses: the batched encode and
+    clamp refuse a bad count, and an app the per-app call would refuse,
+    before anything is launched."""
+    import paper_2607_22595_amd as px
+    A = 0x100000
+    rt = px.XmixRoute(0x10000, 0x20000, 0x30000, 256, 4)
+    good = px.XmixSaeDict(A, 65536, 4096, px.XMIX_SAE_DICT_TILED)
+    bad = px.XmixSaeDict(A, 65536, 4096, 0)
+
+    def app(bit=0, dct=good, k=64, ws_bytes=1 << 40, ring=None):
+        return px.XmixSaeApp(bit, ctypes.pointer(dct), A, A, A, k, A, A, A, ws_bytes, ring, bit)
+
+    enc = lib.xmix_sae_encode_topk_multi
+    enc.restype = ctypes.c_int
+    enc.argtypes = None
+
+    def call(apps, n=None):
+        arr = (px.XmixSaeApp * max(1, len(apps)))(*apps)
+        return enc(ctypes.c_void_p(A), 4096, ctypes.byref(rt), len(apps) if n is None else n,
+                   arr, ctypes.c_void_p(A), 0, None)
+    assert call([app()], n=0) == 1
+    assert call([app()] * 33) == 1                    # more than 32 apps
+    assert call([app(), app(1, dct=bad)]) == 1         # a dictionary without its tag
+    assert call([app(), app(bit=4)]) == 1              # bit outside the route's apps
+    assert call([app(), app(k=65)]) == 1
+    assert call([app(), app(ws_bytes=16)]) == 3        # workspace too small
+    ring = px.XmixRing(A, A, 8, 16 + 6 * 64)
+    arr = (px.XmixSaeApp * 1)(app(ring=ctypes.pointer(ring)))
+    assert enc(ctypes.c_void_p(A), 4096, ctypes.byref(rt), 1, arr, None, 0, None) == 1  # no req
+    clamp = lib.xmix_sae_clamp_decode_multi
+    clamp.restype = ctypes.c_int
+    clamp.argtypes = None
+
+    def capp(bit=0, k=64, n_clamp=4):
+        return px.XmixSaeClampApp(bit, A, A, k, A, 65536, A, A, n_clamp, None)
+    carr = (px.XmixSaeClampApp * 2)(capp(), capp(n_clamp=17))
+    assert clamp(ctypes.c_void_p(A), 4096, ctypes.byref(rt), 2, carr, None) == 1
+    carr = (px.XmixSaeClampApp * 2)(capp(), capp(bit=7))
+    assert clamp(ctypes.c_void_p(A), 4096, ctypes.byref(rt), 2, carr, None) == 1
+    assert clamp(ctypes.c_void_p(A), 4096, ctypes.byref(rt), 0, carr, None) == 1

@@ -1,0 +1,246 @@
+"""The batched SAE calls of one hook against one call per app.
+
+xmix_sae_encode_topk_multi (and its routed form) must give every app the
+same indices, values and ring rows, bit for bit, as one xmix_sae_encode_topk
+or xmix_sae_encode_topk_ring call per app; xmix_sae_clamp_decode_multi must
+leave h (and each delta) exactly as one xmix_sae_clamp_decode call per app
+in the same order.  One app of each batch is also checked against the
+oracle, so the comparison is not between two wrong answers."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from parity import check_topk, torch_bits
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def px():
+    import paper_2607_22595_amd as px
+    return px
+
+
+def dev_bits(a):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
+
+
+def dev_i32(a):
+    a = np.asarray(a)
+    if a.dtype == np.uint32:
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int32)).cuda()
+    return torch.from_numpy(np.ascontiguousarray(a, np.int32)).cuda()
+
+
+def route_inputs(wl):
+    return (dev_i32(wl.req), torch.tensor([wl.T_valid], dtype=torch.int32, device="cuda"),
+            dev_i32(np.asarray(wl.sub, np.uint32)))
+
+
+def gpu_route(px, wl):
+    rt = px.Route(wl.T_max, wl.n_apps)
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    req, tv, sub = route_inputs(wl)
+    px.xmix_route_build(req, tv, sub, rt, err)
+    return rt, err
+
+
+class Apps:
+    """Device buffers of a workload's SAE apps: packed dictionaries, folded
+    biases (every other app without one, so the batched call folds it),
+    outputs, workspaces and, on every third app, a ring."""
+
+    def __init__(self, px, wl, fold_every=2, ring_every=3):
+        self.px, self.wl = px, wl
+        self.items = []
+        for i, s in enumerate(wl.layers[0].saes):
+            W = px.xmix_sae_pack_encoder(dev_bits(s.W_enc))
+            be, bd = dev_bits(s.b_enc), dev_bits(s.b_dec)
+            c = None
+            if i % fold_every == 0:
+                c = torch.empty(s.m, dtype=torch.float32, device="cuda")
+                px.xmix_sae_fold_bias(W, be, bd, c)
+            ws = torch.empty(px.sae_encode_workspace(wl.T_max, wl.d, s.m, s.k),
+                             dtype=torch.uint8, device="cuda")
+            ring = px.Ring(97, 16 + 6 * s.k) if i % ring_every == 1 else None
+            self.items.append(dict(s=s, W=W, be=be, bd=bd, c=c, ws=ws, ring=ring))
+        self.reset()
+
+    def reset(self):
+        for it in self.items:
+            k = it["s"].k
+            it["idx"] = torch.full((self.wl.T_max, k), -7, dtype=torch.int32, device="cuda")
+            it["val"] = torch.zeros((self.wl.T_max, k), dtype=torch.bfloat16, device="cuda")
+            if it["ring"] is not None:
+                it["ring"].slots.zero_()
+                it["ring"].head.fill_(5)  # a head that is not at a slot boundary
+                it["ring"].head[1] = 0
+
+    def multi_apps(self):
+        return [self.px.SaeApp(it["s"].bit, it["W"], it["be"], it["bd"], it["c"], it["s"].k,
+                               it["idx"], it["val"], it["ws"], it["ring"], 100 + it["s"].bit)
+                for it in self.items]
+
+    def one_call_per_app(self, h, rt, req):
+        for it in self.items:
+            s = it["s"]
+            if it["ring"] is None:
+                self.px.xmix_sae_encode_topk(h, rt, s.bit, it["W"], it["be"], it["bd"], it["c"],
+                                             s.k, it["idx"], it["val"], it["ws"])
+            else:
+                self.px.xmix_sae_encode_topk_ring(h, rt, s.bit, it["W"], it["be"], it["bd"],
+                                                  it["c"], s.k, it["idx"], it["val"], it["ws"],
+                                                  req, 3, 100 + s.bit, it["ring"])
+
+    def results(self):
+        torch.cuda.synchronize()
+        out = []
+        for it in self.items:
+            r = it["ring"]
+            out.append((it["idx"].cpu().numpy(), torch_bits(it["val"]),
+                        None if r is None else (r.slots.cpu().numpy(), r.head.cpu().numpy())))
+        return out
+
+
+def assert_same(a, b):
+    for (i1, v1, r1), (i2, v2, r2) in zip(a, b):
+        assert np.array_equal(i1, i2)
+        assert np.array_equal(v1, v2)
+        assert (r1 is None) == (r2 is None)
+        if r1 is not None:
+            assert np.array_equal(r1[0], r2[0]) and np.array_equal(r1[1], r2[1])
+
+
+def small_c5(T=256, n_clamp_apps=10, m=4096, seed=3):
+    # 4 steering, 2 probe and n_clamp_apps SAE apps; two dictionary sizes
+    return synth.make("c5", d=1024, T=T, m=m, k=32, p=0.3, n_steer=4, n_probe=2,
+                      n_clamp_apps=n_clamp_apps, seed=seed)
+
+
+@pytest.mark.parametrize("n_apps", [3, 10])
+def test_encode_multi_matches_one_call_per_app(px, n_apps):
+    """3 apps: one batched launch; 10 apps: two (at most 8 per launch)."""
+    wl = small_c5(n_clamp_apps=n_apps)
+    rt, err = gpu_route(px, wl)
+    h = dev_bits(wl.layers[0].h)
+    req = dev_i32(wl.req)
+    apps = Apps(px, wl)
+    apps.one_call_per_app(h, rt, req)
+    ref = apps.results()
+    apps.reset()
+    px.xmix_sae_encode_topk_multi(h, rt, apps.multi_apps(), req, 3)
+    assert_same(apps.results(), ref)
+    # one app against the oracle
+    tm, cnt, lists, _ = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    s = wl.layers[0].saes[-1]
+    toks = lists[s.bit, :cnt[s.bit]][:24]
+    idx_ref, _, _, pre = oracle.sae_encode(wl.layers[0].h, toks, s.W_enc, s.b_enc, s.b_dec, s.k,
+                                           want_pre=True)
+    idx, val, _ = ref[-1]
+    for q, t in enumerate(toks):
+        check_topk(idx[t], val[t], idx_ref[q], pre[q], s.k)
+    # tokens without the app's bit are not written
+    for it, (idx, _, _) in zip(apps.items, ref):
+        b = it["s"].bit
+        off = np.setdiff1d(np.arange(wl.T_max), lists[b, :cnt[b]])
+        assert np.all(idx[off] == -7)
+
+
+def test_routed_encode_multi_matches_route_build_then_multi(px):
+    wl = small_c5(n_clamp_apps=5, seed=4)
+    rt, err = gpu_route(px, wl)
+    h = dev_bits(wl.layers[0].h)
+    req, tv, sub = route_inputs(wl)
+    apps = Apps(px, wl)
+    px.xmix_sae_encode_topk_multi(h, rt, apps.multi_apps(), req, 3)
+    ref = apps.results()
+    ref_route = (rt.tok_mask.cpu().numpy(), rt.app_count.cpu().numpy(),
+                 rt.app_tokens.cpu().numpy(), err.cpu().numpy())
+    apps.reset()
+    rt2 = px.Route(wl.T_max, wl.n_apps)
+    rt2.tok_mask.fill_(-1)
+    rt2.app_count.fill_(-1)
+    rt2.app_tokens.fill_(-3)
+    err2 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    px.xmix_route_sae_encode_topk_multi(req, tv, sub, rt2, err2, h, apps.multi_apps(), 3)
+    assert_same(apps.results(), ref)
+    got_route = (rt2.tok_mask.cpu().numpy(), rt2.app_count.cpu().numpy(),
+                 rt2.app_tokens.cpu().numpy(), err2.cpu().numpy())
+    for a, b in zip(got_route, ref_route):
+        assert np.array_equal(a, b)
+
+
+def test_encode_multi_with_dictionaries_of_two_sizes(px):
+    """Apps whose tiles differ in number follow each other in one launch."""
+    wl = small_c5(n_clamp_apps=4, seed=5)
+    big = small_c5(n_clamp_apps=4, m=8192, seed=6)
+    saes = wl.layers[0].saes
+    saes[1], saes[3] = big.layers[0].saes[1], big.layers[0].saes[3]
+    rt, _ = gpu_route(px, wl)
+    h = dev_bits(wl.layers[0].h)
+    req = dev_i32(wl.req)
+    apps = Apps(px, wl)
+    apps.one_call_per_app(h, rt, req)
+    ref = apps.results()
+    apps.reset()
+    px.xmix_sae_encode_topk_multi(h, rt, apps.multi_apps(), req, 3)
+    assert_same(apps.results(), ref)
+
+
+def test_encode_multi_prefill_shape_runs_apps_in_turn(px):
+    """From 1025 token slots the apps run one after the other (the GEMM
+    path); the results are those of one call per app."""
+    wl = small_c5(T=1100, n_clamp_apps=2, seed=7)
+    rt, _ = gpu_route(px, wl)
+    h = dev_bits(wl.layers[0].h)
+    req = dev_i32(wl.req)
+    apps = Apps(px, wl)
+    apps.one_call_per_app(h, rt, req)
+    ref = apps.results()
+    apps.reset()
+    px.xmix_sae_encode_topk_multi(h, rt, apps.multi_apps(), req, 3)
+    assert_same(apps.results(), ref)
+
+
+def test_clamp_multi_matches_one_call_per_app(px):
+    wl = small_c5(n_clamp_apps=10, seed=8)
+    rt, _ = gpu_route(px, wl)
+    h0 = dev_bits(wl.layers[0].h)
+    req = dev_i32(wl.req)
+    apps = Apps(px, wl, ring_every=10 ** 6)
+    px.xmix_sae_encode_topk_multi(h0, rt, apps.multi_apps(), req, 3)
+    torch.cuda.synchronize()
+    clamp = []
+    for i, it in enumerate(apps.items):
+        s = it["s"]
+        ids = dev_i32(s.clamp_ids)
+        vals = torch.from_numpy(np.asarray(s.clamp_vals, np.float32) * (1 + i)).cuda()
+        clamp.append((s.bit, it["idx"], it["val"], dev_bits(s.W_dec), ids, vals))
+    # reference: one call per app, in order, each with its own delta
+    h_ref = h0.clone()
+    d_ref = [torch.zeros((wl.T_max, wl.d), dtype=torch.float32, device="cuda") for _ in clamp]
+    for c, dref in zip(clamp, d_ref):
+        px.xmix_sae_clamp_decode(h_ref, rt, *c, delta_out=dref)
+    h = h0.clone()
+    d_got = [torch.zeros_like(x) for x in d_ref]
+    px.xmix_sae_clamp_decode_multi(h, rt, [c + (dg,) for c, dg in zip(clamp, d_got)])
+    torch.cuda.synchronize()
+    assert np.array_equal(torch_bits(h), torch_bits(h_ref))
+    for a, b in zip(d_got, d_ref):
+        assert torch.equal(a, b)
+    # rows of tokens with no clamp app are untouched
+    tm, _, _, _ = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    bits = sum(1 << c[0] for c in clamp)
+    untouched = (tm & np.uint32(bits)) == 0
+    assert np.array_equal(torch_bits(h)[untouched], wl.layers[0].h[untouched])
+    # the order of the apps matters only through the roundings: the reverse
+    # order, one call per app, matches the batched call in reverse order
+    h_rev_ref = h0.clone()
+    for c in reversed(clamp):
+        px.xmix_sae_clamp_decode(h_rev_ref, rt, *c)
+    h_rev = h0.clone()
+    px.xmix_sae_clamp_decode_multi(h_rev, rt, list(reversed(clamp)))
+    torch.cuda.synchronize()
+    assert np.array_equal(torch_bits(h_rev), torch_bits(h_rev_ref))
