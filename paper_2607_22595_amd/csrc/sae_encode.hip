@@ -47,6 +47,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <atomic>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "launch.hpp"
@@ -354,146 +356,68 @@ __device__ __forceinline__ void select_slices(const float* const (&vrow)[NT], in
 }
 
 // ---------------------------------------------- GEMM + candidate emission
-// One workgroup's tile: L is the tile's launch slot within its app's grid,
-// own the workgroup's index in the launch (its route-publishing duty).
-__device__ __forceinline__ void stream_tile(
-    int L, int own, const uint16_t* __restrict__ h, int32_t d,
-    const int32_t* __restrict__ app_count, const int32_t* __restrict__ tok_list,
-    const uint16_t* __restrict__ W, const float* __restrict__ c_fold, int32_t n_mt, int32_t n_nt,
-    float z_guess, int32_t lo_cnt, int32_t cap, uint2* __restrict__ cand,
-    int32_t* __restrict__ tile_cnt, float* __restrict__ tile_tau,
-    const int32_t* __restrict__ r_req, const int32_t* __restrict__ r_tvalid,
-    const uint32_t* __restrict__ r_sub, int32_t r_Rmax, int32_t r_Tmax, int32_t r_napps,
-    int32_t r_bit, uint32_t* __restrict__ r_mask, int32_t* __restrict__ r_count,
-    int32_t* __restrict__ r_lists, uint32_t* __restrict__ r_err) {
-    // K loop: two 16 KiB token chunks; epilogue: the tile's 128 token rows
-    __shared__ uint4 lds_main[kBN * kSelStride / 4];
-    static_assert(kBN * kSelStride / 4 >= 2 * kBN * 8, "token chunks fit");
-    __shared__ int32_t list_s[kRouteMaxT];    // the app's token list (in-kernel route build)
-    __shared__ int32_t rtot_s[kEncWaves];
-    __shared__ int32_t seen_s[kEncWaves];
-    uint4 (*xs)[kBN * 8] = reinterpret_cast<uint4 (*)[kBN * 8]>(lds_main);
-
-    // Tile order.  Few token tiles (decode): one workgroup per latent tile,
-    // which takes the live token tiles of its slice in turn (no workgroup
-    // is launched for a tile past the live count; the first tile, the one
-    // every live token count reaches, spreads over every CU).
-    // Many token tiles (prefill): launch slot L runs on XCD L % 8; XCD x
-    // owns the latent tiles [x*M8, (x+1)*M8) and walks them in blocks of 8
-    // token tiles x 4 latent tiles, 32 consecutive slots per block, token
-    // blocks fastest.  The 32 workgroups of a block run together on the
-    // XCD's 32 CUs, so each K chunk of 8 token tiles and 4 dictionary
-    // slices is fetched into the XCD's L2 once and read by 4 and 8
-    // workgroups; consecutive blocks reuse the same 4 slices.
-    int nt, mt;
-    bool live;  // the tile exists (its tokens are counted below)
-    if (n_nt <= kLatentFastTiles) {
-        nt = L / n_mt;
-        mt = L % n_mt;
-        live = nt < n_nt;
-    } else {
-        const int xcd = L % 8, slot = L / 8;
-        const int m8 = (n_mt + 7) / 8;              // latent tiles per XCD
-        const int nbt = (n_nt + kBlkTok - 1) / kBlkTok;
-        const int b = slot / (kBlkTok * kBlkLat), p = slot % (kBlkTok * kBlkLat);
-        const int bt = b % nbt, bl = b / nbt;
-        const int lt = kBlkLat * bl + p / kBlkTok;
-        nt = kBlkTok * bt + p % kBlkTok;
-        mt = xcd * m8 + lt;
-        live = nt < n_nt && lt < m8;
+// The dictionary stream of one workgroup: the first piece of a slice's K
+// chunk 0, and the pieces from one K chunk to the next (both the same for
+// every lane; each lane adds its own offset when it loads).
+struct SliceSrc {
+    const uint4* base;
+    int64_t stride;
+};
+__device__ __forceinline__ SliceSrc slice_src(const uint16_t* W, int32_t n_mt, int mt) {
+    return {reinterpret_cast<const uint4*>(W) + static_cast<int64_t>(mt) * 2048,
+            static_cast<int64_t>(n_mt) * 2048};
+}
+// operand A of one K chunk at p: this wave's 32 latents of the packed
+// slice.  The dictionary is read once per launch: nontemporal loads stream
+// it past the caches (about 4 % faster than cached loads at 65536 x 4096).
+__device__ __forceinline__ void load_chunk(uint4 (&a)[4], const uint4* p) {
+    const uint32_t off = threadIdx.x & 511;  // wave * 256 + lane: pieces 4 x 64 apart
+    const u32x4_t* q = reinterpret_cast<const u32x4_t*>(p) + ((off >> 6) * 256 + (off & 63));
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        const u32x4_t v = __builtin_nontemporal_load(q + s * 64);
+        a[s] = make_uint4(v.x, v.y, v.z, v.w);
     }
-    live = live && mt < n_mt;
+}
+// the folded bias of this lane's 16 latents of slice mt
+__device__ __forceinline__ void load_bias(float (&cfv)[16], const float* c_fold, int mt) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const float* cf = c_fold + mt * kBM + 32 * wave + 4 * (lane >> 5);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) cfv[r] = cf[8 * (r / 4) + (r % 4)];
+}
 
+// Where one app's slices put their candidates, and how they select them.
+struct SliceSink {
+    uint2* cand;
+    int32_t* tile_cnt;
+    float* tile_tau;
+    int32_t n_mt, lo_cnt, cap;
+    float z;
+};
+
+// The GEMM and candidate emission of latent slice mt over the token tiles
+// nt, nt + 1, ... of the app's list tl[0, cnt) (only tile nt unless
+// in_turn); the caller has checked nt * kBN < cnt.  On entry wa0..wa2 hold
+// the slice's K chunks 0-2 and cfv its folded bias when `issued`.  The K
+// loop fetches three chunks ahead; past the slice's last chunk it fetches
+// the first chunks of what runs next: the same slice again for the next
+// token tile, else slice `nxt` when has_nxt (then also its bias from
+// nxt_cf, after this tile's selection), else nothing new (the last chunk
+// again, unused).  Returns has_nxt: whether wa0..wa2 and cfv now hold nxt's
+// first chunks and bias.  lds_main is the workgroup's token-chunk and
+// selection space.
+__device__ __forceinline__ bool slice_tiles(
+    uint4* lds_main, const uint16_t* __restrict__ h, int32_t d, const int32_t* tl, int cnt,
+    int nt, bool in_turn, int mt, const SliceSrc cur, const SliceSink sink, bool issued,
+    const SliceSrc nxt, bool has_nxt, int nxt_mt, const float* __restrict__ nxt_cf,
+    const float* __restrict__ c_fold, uint4 (&wa0)[4], uint4 (&wa1)[4], uint4 (&wa2)[4],
+    uint4 (&wa3)[4], float (&cfv)[16]) {
+    uint4 (*xs)[kBN * 8] = reinterpret_cast<uint4 (*)[kBN * 8]>(lds_main);
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 5, j32 = lane & 31;
     const int nK = d / kBK;  // a multiple of 4 (d % 256 == 0)
-
-    // operand A: this wave's 32 latents of the packed slice
-    const uint4* wbase = reinterpret_cast<const uint4*>(W) + static_cast<int64_t>(mt) * 2048 +
-                         wave * 256 + lane;
-    const int64_t wstride = static_cast<int64_t>(n_mt) * 2048;  // pieces per K chunk
-    uint4 wa0[4], wa1[4], wa2[4], wa3[4];   // W ring: 4 chunks, 3 in flight
-    // The dictionary is read once per launch: nontemporal loads stream it
-    // past the caches (about 4 % faster than cached loads at 65536 x 4096).
-    auto load_w = [&](uint4 (&a)[4], int kc) {
-        kc = min(kc, nK - 1);  // past the end: re-read the last chunk, unused
-        const u32x4_t* p = reinterpret_cast<const u32x4_t*>(wbase + kc * wstride);
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            const u32x4_t v = __builtin_nontemporal_load(p + s * 64);
-            a[s] = make_uint4(v.x, v.y, v.z, v.w);
-        }
-    };
-    // folded bias of this lane's 16 latents, fetched with the first chunks
-    float cfv[16];
-    auto load_bias = [&]() {
-        const float* cf = c_fold + mt * kBM + 32 * wave + 4 * g;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) cfv[r] = cf[8 * (r / 4) + (r % 4)];
-    };
-
-    // With r_req given, the kernel also builds the step's routing (in place
-    // of a route-build launch): every workgroup builds its app's token list
-    // in LDS from the routing inputs staged there (in the space of the K
-    // loop's token chunks); workgroup a < n_apps publishes app a's list and
-    // count, and workgroup 0 the token masks and the error word.  A
-    // workgroup of the first token tile starts its first dictionary chunks
-    // as soon as the staged table shows a request subscribed to the app, so
-    // that the stream runs while the list is built (without a subscriber it
-    // reads nothing).
-    const int32_t* tl = tok_list;
-    int cnt = 0;
-    bool w_issued = false;
-    if (r_req) {  // uniform
-        static_assert(sizeof(lds_main) >= (kRouteMaxT + kStageSubMax) * 4, "staging fits");
-        int32_t* req_s = reinterpret_cast<int32_t*>(lds_main);
-        uint32_t* sub_s = reinterpret_cast<uint32_t*>(lds_main) + kRouteMaxT;
-        const bool seen = stage_route<kEncThreads>(r_req, r_Tmax, r_sub, r_Rmax, req_s, sub_s,
-                                                   1u << r_bit);
-        const uint64_t seen_b = wave_ballot(seen);
-        if (lane == 0) seen_s[wave] = seen_b != 0;
-        uint32_t err = 0;
-        const int32_t tv = clamp_t_valid(*r_tvalid, r_Tmax, err);
-        const uint32_t keep = r_napps >= 32 ? 0xFFFFFFFFu : ((1u << r_napps) - 1u);
-        uint32_t* masks = own == 0 ? r_mask : nullptr;
-        __syncthreads();  // the staged inputs
-        bool any = false;
-#pragma unroll
-        for (int w = 0; w < kEncWaves; ++w) any = any || seen_s[w] != 0;
-        // no request subscribes to the app: no token is listed, and a
-        // workgroup with nothing to publish is done
-        if (!any && own >= r_napps) return;  // uniform
-        if (live && nt == 0 && any) {  // uniform
-            load_w(wa0, 0);
-            load_w(wa1, 1);
-            load_w(wa2, 2);
-            load_bias();
-            w_issued = true;
-        }
-        if (own < r_napps && own != r_bit) {
-            const int32_t n = build_token_list<kEncThreads>(req_s, tv, sub_s, r_sub, r_Rmax, keep,
-                                                            own, r_Tmax, list_s, rtot_s, masks,
-                                                            err);
-            masks = nullptr;
-            publish_token_list<kEncThreads>(list_s, n, r_Tmax,
-                                            r_lists + static_cast<int64_t>(own) * r_Tmax,
-                                            r_count + own);
-            __syncthreads();  // list_s is rebuilt below
-        }
-        cnt = build_token_list<kEncThreads>(req_s, tv, sub_s, r_sub, r_Rmax, keep, r_bit, r_Tmax,
-                                            list_s, rtot_s, masks, err);
-        if (own == r_bit)
-            publish_token_list<kEncThreads>(list_s, cnt, r_Tmax,
-                                            r_lists + static_cast<int64_t>(r_bit) * r_Tmax,
-                                            r_count + r_bit);
-        if (own == 0) publish_error(err, r_err);
-        tl = list_s;
-    } else {
-        cnt = *app_count;
-    }
-    if (!live || nt * kBN >= cnt) return;
-    if (!w_issued) load_bias();  // the slice's bias serves every token tile
 
     // operand B: gathered token rows; padding rows read a valid row and are
     // zeroed when written to LDS
@@ -534,83 +458,231 @@ __device__ __forceinline__ void stream_tile(
         }
     };
     // One K chunk (branch-free): issue the token chunk two ahead and the W
-    // chunk three ahead, multiply the current chunk, then publish the next
-    // token chunk to the other LDS buffer.  Loads are issued oldest-needed
-    // first, so the in-order vmcnt wait for the next token chunk never
-    // waits on a W prefetch.
-    auto step = [&](int kc, const uint4 (&cur)[4], uint4 (&wnext)[4], uint4 (&xload)[2],
-                    const uint4 (&xstore)[2]) {
+    // chunk three ahead (at wp), multiply the current chunk, then publish
+    // the next token chunk to the other LDS buffer.  Loads are issued
+    // oldest-needed first, so the in-order vmcnt wait for the next token
+    // chunk never waits on a W prefetch.
+    auto step = [&](int kc, const uint4 (&cur_w)[4], uint4 (&wnext)[4], const uint4* wp,
+                    uint4 (&xload)[2], const uint4 (&xstore)[2]) {
         load_x(xload, kc + 2);
-        load_w(wnext, kc + 3);
+        __builtin_amdgcn_sched_barrier(0);  // keep the token loads ahead of the W loads
+        load_chunk(wnext, wp);
         __syncthreads();
-        compute(cur, kc & 1);
+        compute(cur_w, kc & 1);
         store_x(xstore, (kc + 1) & 1);
+        __builtin_amdgcn_sched_barrier(0);
     };
 
-    const bool tiles_in_turn = n_nt <= kLatentFastTiles;
+    if (!issued) load_bias(cfv, c_fold, mt);  // the slice's bias serves every token tile
     for (;; ++nt) {
-    const int n0 = nt * kBN;
-    if (n0 >= cnt) return;
-    const int ntok = min(kBN, cnt - n0);
+        const int n0 = nt * kBN;
+        const int ntok = min(kBN, cnt - n0);
+        const bool last = !in_turn || n0 + kBN >= cnt;
+        // the stream past this slice's last chunk: the next token tile's
+        // first chunks, nxt's, or the last chunk again (unused)
+        const uint4* after = !last ? cur.base : has_nxt ? nxt.base : cur.base + (nK - 1) * cur.stride;
+        const int64_t after_stride = !last ? cur.stride : has_nxt ? nxt.stride : 0;
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
-        const int n = xr + 64 * p;
-        const bool ok = n < ntok;
-        xmask[p] = ok ? 0xFFFFFFFFu : 0u;
-        xrow[p] = h + static_cast<int64_t>(tl[n0 + (ok ? n : 0)]) * d + 8 * xc;
-    }
-    // the accumulators start from the folded bias
+        for (int p = 0; p < 2; ++p) {
+            const int n = xr + 64 * p;
+            const bool ok = n < ntok;
+            xmask[p] = ok ? 0xFFFFFFFFu : 0u;
+            xrow[p] = h + static_cast<int64_t>(tl[n0 + (ok ? n : 0)]) * d + 8 * xc;
+        }
+        // the accumulators start from the folded bias
 #pragma unroll
-    for (int b = 0; b < 4; ++b)
+        for (int b = 0; b < 4; ++b)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[b][r] = cfv[r];
+            for (int r = 0; r < 16; ++r) acc[b][r] = cfv[r];
 
-    load_x(xv0, 0);
-    load_x(xv1, 1);
-    if (!w_issued) {
-        load_w(wa0, 0);
-        load_w(wa1, 1);
-        load_w(wa2, 2);
-    }
-    w_issued = false;
-    store_x(xv0, 0);
-    for (int kc = 0; kc < nK; kc += 4) {
-        step(kc + 0, wa0, wa3, xv0, xv1);
-        step(kc + 1, wa1, wa0, xv1, xv0);
-        step(kc + 2, wa2, wa1, xv0, xv1);
-        step(kc + 3, wa3, wa2, xv1, xv0);
-    }
+        load_x(xv0, 0);
+        load_x(xv1, 1);
+        if (!issued) {
+            load_chunk(wa0, cur.base);
+            load_chunk(wa1, cur.base + cur.stride);
+            load_chunk(wa2, cur.base + 2 * cur.stride);
+        }
+        store_x(xv0, 0);
+        // four chunks per round (the W registers rotate); the last round
+        // fetches what follows the slice
+        auto round4 = [&](int kc, const uint4* p0, const uint4* p1, const uint4* p2,
+                          const uint4* p3) {
+            step(kc + 0, wa0, wa3, p0, xv0, xv1);
+            step(kc + 1, wa1, wa0, p1, xv1, xv0);
+            step(kc + 2, wa2, wa1, p2, xv0, xv1);
+            step(kc + 3, wa3, wa2, p3, xv1, xv0);
+        };
+        const uint4* wp = cur.base + 3 * cur.stride;
+        const int64_t ws = cur.stride;
+        if (nK > 4) {
+            // The first round runs apart from the loop: its loads follow the
+            // prologue's (whose W chunks may have been issued long before),
+            // while every round of the loop follows a round.  So the loop's
+            // waits count only a round's loads, and a step waits for its
+            // token chunk without waiting for the W chunk issued a step ago.
+            round4(0, wp, wp + ws, wp + 2 * ws, wp + 3 * ws);
+            wp += 4 * ws;
+            for (int kc = 4; kc < nK - 4; kc += 4) {
+                round4(kc, wp, wp + ws, wp + 2 * ws, wp + 3 * ws);
+                wp += 4 * ws;
+            }
+        }
+        round4(nK - 4, wp, after, after + after_stride, after + 2 * after_stride);
+        // wa0..wa2 now hold the first three chunks of what runs next
+        issued = !last || has_nxt;
 
-    // ---------------------------------------------------------- epilogue
-    // acc[nb][r] holds latent 32*wave + 8*(r/4) + 4*g + r%4 of token
-    // 32*nb + j32 (the 32x32 MFMA output layout).  Every lane writes its
-    // values to the tile's 128 token rows in LDS; then wave w selects for
-    // rows 16w .. 16w + 15, eight lanes per row, two rows per lane.
-    __syncthreads();  // every wave is done with the token chunks
-    float* V = reinterpret_cast<float*>(lds_main);
+        // ------------------------------------------------------ epilogue
+        // acc[nb][r] holds latent 32*wave + 8*(r/4) + 4*g + r%4 of token
+        // 32*nb + j32 (the 32x32 MFMA output layout).  Every lane writes its
+        // values to the tile's 128 token rows in LDS; then wave w selects for
+        // rows 16w .. 16w + 15, eight lanes per row, two rows per lane.
+        __syncthreads();  // every wave is done with the token chunks
+        float* V = reinterpret_cast<float*>(lds_main);
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb) {
-        float* rowp = V + (32 * nb + j32) * kSelStride + 32 * wave + 4 * g;
+        for (int nb = 0; nb < 4; ++nb) {
+            float* rowp = V + (32 * nb + j32) * kSelStride + 32 * wave + 4 * g;
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-            *reinterpret_cast<float4*>(rowp + 8 * j) =
-                make_float4(acc[nb][4 * j], acc[nb][4 * j + 1], acc[nb][4 * j + 2],
-                            acc[nb][4 * j + 3]);
+            for (int j = 0; j < 4; ++j)
+                *reinterpret_cast<float4*>(rowp + 8 * j) =
+                    make_float4(acc[nb][4 * j], acc[nb][4 * j + 1], acc[nb][4 * j + 2],
+                                acc[nb][4 * j + 3]);
+        }
+        __syncthreads();
+        const int q = lane & 7;
+        const int r0 = 16 * wave + (lane >> 3), r1 = r0 + 8;
+        const int64_t row0 = static_cast<int64_t>(n0 + r0) * sink.n_mt + mt;
+        const int64_t row1 = static_cast<int64_t>(n0 + r1) * sink.n_mt + mt;
+        const float* const vr[2] = {V + r0 * kSelStride, V + r1 * kSelStride};
+        const bool ok[2] = {r0 < ntok, r1 < ntok};
+        uint2* const dst[2] = {sink.cand + row0 * sink.cap, sink.cand + row1 * sink.cap};
+        int32_t* const co[2] = {sink.tile_cnt + row0, sink.tile_cnt + row1};
+        float* const to[2] = {sink.tile_tau + row0, sink.tile_tau + row1};
+        select_slices<true, 2>(vr, q, ok, sink.z, sink.lo_cnt, sink.cap, mt * kBM, dst, co, to);
+        if (last) {
+            if (has_nxt && nxt_cf) load_bias(cfv, nxt_cf, nxt_mt);
+            return has_nxt;
+        }
+        __syncthreads();  // the tile rows are read before the next tile's token chunks land
     }
-    __syncthreads();
-    const int q = lane & 7;
-    const int r0 = 16 * wave + (lane >> 3), r1 = r0 + 8;
-    const int64_t row0 = static_cast<int64_t>(n0 + r0) * n_mt + mt;
-    const int64_t row1 = static_cast<int64_t>(n0 + r1) * n_mt + mt;
-    const float* const vr[2] = {V + r0 * kSelStride, V + r1 * kSelStride};
-    const bool ok[2] = {r0 < ntok, r1 < ntok};
-    uint2* const dst[2] = {cand + row0 * cap, cand + row1 * cap};
-    int32_t* const co[2] = {tile_cnt + row0, tile_cnt + row1};
-    float* const to[2] = {tile_tau + row0, tile_tau + row1};
-    select_slices<true, 2>(vr, q, ok, z_guess, lo_cnt, cap, mt * kBM, dst, co, to);
-    if (!tiles_in_turn || nt + 1 >= n_nt) return;
-    __syncthreads();  // the tile rows are read before the next tile's token chunks land
+}
+
+// One workgroup's tile: L is the tile's launch slot within its app's grid,
+// own the workgroup's index in the launch (its route-publishing duty).
+__device__ __forceinline__ void stream_tile(
+    int L, int own, const uint16_t* __restrict__ h, int32_t d,
+    const int32_t* __restrict__ app_count, const int32_t* __restrict__ tok_list,
+    const uint16_t* __restrict__ W, const float* __restrict__ c_fold, int32_t n_mt, int32_t n_nt,
+    float z_guess, int32_t lo_cnt, int32_t cap, uint2* __restrict__ cand,
+    int32_t* __restrict__ tile_cnt, float* __restrict__ tile_tau,
+    const int32_t* __restrict__ r_req, const int32_t* __restrict__ r_tvalid,
+    const uint32_t* __restrict__ r_sub, int32_t r_Rmax, int32_t r_Tmax, int32_t r_napps,
+    int32_t r_bit, uint32_t* __restrict__ r_mask, int32_t* __restrict__ r_count,
+    int32_t* __restrict__ r_lists, uint32_t* __restrict__ r_err) {
+    // K loop: two 16 KiB token chunks; epilogue: the tile's 128 token rows
+    __shared__ uint4 lds_main[kBN * kSelStride / 4];
+    static_assert(kBN * kSelStride / 4 >= 2 * kBN * 8, "token chunks fit");
+    __shared__ int32_t list_s[kRouteMaxT];    // the app's token list (in-kernel route build)
+    __shared__ int32_t rtot_s[kEncWaves];
+    __shared__ int32_t seen_s[kEncWaves];
+
+    // Tile order.  Few token tiles (decode): one workgroup per latent tile,
+    // which takes the live token tiles of its slice in turn (no workgroup
+    // is launched for a tile past the live count; the first tile, the one
+    // every live token count reaches, spreads over every CU).
+    // Many token tiles (prefill): launch slot L runs on XCD L % 8; XCD x
+    // owns the latent tiles [x*M8, (x+1)*M8) and walks them in blocks of 8
+    // token tiles x 4 latent tiles, 32 consecutive slots per block, token
+    // blocks fastest.  The 32 workgroups of a block run together on the
+    // XCD's 32 CUs, so each K chunk of 8 token tiles and 4 dictionary
+    // slices is fetched into the XCD's L2 once and read by 4 and 8
+    // workgroups; consecutive blocks reuse the same 4 slices.
+    int nt, mt;
+    bool live;  // the tile exists (its tokens are counted below)
+    if (n_nt <= kLatentFastTiles) {
+        nt = L / n_mt;
+        mt = L % n_mt;
+        live = nt < n_nt;
+    } else {
+        const int xcd = L % 8, slot = L / 8;
+        const int m8 = (n_mt + 7) / 8;              // latent tiles per XCD
+        const int nbt = (n_nt + kBlkTok - 1) / kBlkTok;
+        const int b = slot / (kBlkTok * kBlkLat), p = slot % (kBlkTok * kBlkLat);
+        const int bt = b % nbt, bl = b / nbt;
+        const int lt = kBlkLat * bl + p / kBlkTok;
+        nt = kBlkTok * bt + p % kBlkTok;
+        mt = xcd * m8 + lt;
+        live = nt < n_nt && lt < m8;
     }
+    live = live && mt < n_mt;
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const SliceSrc src = slice_src(W, n_mt, mt);
+    uint4 wa0[4], wa1[4], wa2[4], wa3[4];   // W ring: 4 chunks, 3 in flight
+    float cfv[16];
+
+    // With r_req given, the kernel also builds the step's routing (in place
+    // of a route-build launch): every workgroup builds its app's token list
+    // in LDS from the routing inputs staged there (in the space of the K
+    // loop's token chunks); workgroup a < n_apps publishes app a's list and
+    // count, and workgroup 0 the token masks and the error word.  A
+    // workgroup of the first token tile starts its first dictionary chunks
+    // as soon as the staged table shows a request subscribed to the app, so
+    // that the stream runs while the list is built (without a subscriber it
+    // reads nothing).
+    const int32_t* tl = tok_list;
+    int cnt = 0;
+    bool w_issued = false;
+    if (r_req) {  // uniform
+        static_assert(sizeof(lds_main) >= (kRouteMaxT + kStageSubMax) * 4, "staging fits");
+        int32_t* req_s = reinterpret_cast<int32_t*>(lds_main);
+        uint32_t* sub_s = reinterpret_cast<uint32_t*>(lds_main) + kRouteMaxT;
+        const bool seen = stage_route<kEncThreads>(r_req, r_Tmax, r_sub, r_Rmax, req_s, sub_s,
+                                                   1u << r_bit);
+        const uint64_t seen_b = wave_ballot(seen);
+        if (lane == 0) seen_s[wave] = seen_b != 0;
+        uint32_t err = 0;
+        const int32_t tv = clamp_t_valid(*r_tvalid, r_Tmax, err);
+        const uint32_t keep = r_napps >= 32 ? 0xFFFFFFFFu : ((1u << r_napps) - 1u);
+        uint32_t* masks = own == 0 ? r_mask : nullptr;
+        __syncthreads();  // the staged inputs
+        bool any = false;
+#pragma unroll
+        for (int w = 0; w < kEncWaves; ++w) any = any || seen_s[w] != 0;
+        // no request subscribes to the app: no token is listed, and a
+        // workgroup with nothing to publish is done
+        if (!any && own >= r_napps) return;  // uniform
+        if (live && nt == 0 && any) {  // uniform
+            load_chunk(wa0, src.base);
+            load_chunk(wa1, src.base + src.stride);
+            load_chunk(wa2, src.base + 2 * src.stride);
+            load_bias(cfv, c_fold, mt);
+            w_issued = true;
+        }
+        if (own < r_napps && own != r_bit) {
+            const int32_t n = build_token_list<kEncThreads>(req_s, tv, sub_s, r_sub, r_Rmax, keep,
+                                                            own, r_Tmax, list_s, rtot_s, masks,
+                                                            err);
+            masks = nullptr;
+            publish_token_list<kEncThreads>(list_s, n, r_Tmax,
+                                            r_lists + static_cast<int64_t>(own) * r_Tmax,
+                                            r_count + own);
+            __syncthreads();  // list_s is rebuilt below
+        }
+        cnt = build_token_list<kEncThreads>(req_s, tv, sub_s, r_sub, r_Rmax, keep, r_bit, r_Tmax,
+                                            list_s, rtot_s, masks, err);
+        if (own == r_bit)
+            publish_token_list<kEncThreads>(list_s, cnt, r_Tmax,
+                                            r_lists + static_cast<int64_t>(r_bit) * r_Tmax,
+                                            r_count + r_bit);
+        if (own == 0) publish_error(err, r_err);
+        tl = list_s;
+    } else {
+        cnt = *app_count;
+    }
+    if (!live || nt * kBN >= cnt) return;
+    const SliceSink sink{cand, tile_cnt, tile_tau, n_mt, lo_cnt, cap, z_guess};
+    slice_tiles(lds_main, h, d, tl, cnt, nt, n_nt <= kLatentFastTiles, mt, src, sink, w_issued,
+                src, false, 0, nullptr, c_fold, wa0, wa1, wa2, wa3, cfv);
 }
 
 __global__ void __launch_bounds__(kEncThreads, 1)
@@ -663,6 +735,119 @@ sae_stream_multi_kernel(const uint16_t* __restrict__ h, int32_t d, int32_t n_nt,
     stream_tile(g - a.grid0, g, h, d, a.app_count, a.tok_list, a.W, a.c_fold, a.n_mt, n_nt, a.z,
                 a.lo_cnt, a.cap, a.cand, a.tile_cnt, a.tile_tau, r_req, r_tvalid, r_sub, r_Rmax,
                 r_Tmax, r_napps, a.bit, r_mask, r_count, r_lists, r_err);
+}
+
+// The same batch with few token tiles, on a persistent grid: workgroup w
+// runs slices w, w + G, w + 2G, ... of the apps' slices laid end to end (G
+// the grid, at most one workgroup per CU), each over its app's live token
+// tiles in turn, and skips the slices of an app without a token.  The
+// routing inputs are staged once per workgroup, in LDS of their own; the
+// dictionary stream runs on from one slice into the next, so the next
+// slice's first chunks load while this one's candidates are selected.
+__global__ void __launch_bounds__(kEncThreads, 1)
+sae_stream_apps_kernel(const uint16_t* __restrict__ h, int32_t d, EncApps apps,
+                       const int32_t* __restrict__ r_req, const int32_t* __restrict__ r_tvalid,
+                       const uint32_t* __restrict__ r_sub, int32_t r_Rmax, int32_t r_Tmax,
+                       int32_t r_napps, uint32_t* __restrict__ r_mask,
+                       int32_t* __restrict__ r_count, int32_t* __restrict__ r_lists,
+                       uint32_t* __restrict__ r_err) {
+    __shared__ uint4 lds_main[kBN * kSelStride / 4];
+    __shared__ int32_t list_s[kRouteMaxT];
+    __shared__ int32_t rtot_s[kEncWaves];
+    __shared__ int32_t stage_s[kRouteMaxT + kStageSubMax];
+    __shared__ uint32_t bits_s;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int own = blockIdx.x, G = gridDim.x, U = apps.grid_end;
+
+    // the batch's apps with at least one token (bit i for apps.a[i])
+    uint32_t live = 0;
+    int32_t* req_s = stage_s;
+    uint32_t* sub_s = reinterpret_cast<uint32_t*>(stage_s + kRouteMaxT);
+    int32_t tv = 0;
+    uint32_t keep = 0;
+    if (r_req) {  // uniform
+        if (tid == 0) bits_s = 0u;
+        stage_route<kEncThreads>(r_req, r_Tmax, r_sub, r_Rmax, req_s, sub_s);
+        uint32_t err = 0;
+        tv = clamp_t_valid(*r_tvalid, r_Tmax, err);
+        keep = r_napps >= 32 ? 0xFFFFFFFFu : ((1u << r_napps) - 1u);
+        __syncthreads();  // the staged inputs
+        // every app bit some token slot carries
+        uint32_t any = 0u;
+        for (int32_t t = tid; t < r_Tmax; t += kEncThreads)
+            any |= slot_mask_staged(req_s, t, tv, sub_s, r_sub, r_Rmax, keep, err);
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) any |= __shfl_xor(any, off, kWave);
+        if (lane == 0 && any != 0u) atomicOr(&bits_s, any);
+        if (own < r_napps) {
+            const int32_t n = build_token_list<kEncThreads>(
+                req_s, tv, sub_s, r_sub, r_Rmax, keep, own, r_Tmax, list_s, rtot_s,
+                own == 0 ? r_mask : nullptr, err);
+            publish_token_list<kEncThreads>(list_s, n, r_Tmax,
+                                            r_lists + static_cast<int64_t>(own) * r_Tmax,
+                                            r_count + own);
+        }
+        if (own == 0) publish_error(err, r_err);
+        __syncthreads();  // bits_s complete; list_s free
+        const uint32_t bits = bits_s;
+        for (int i = 0; i < apps.n; ++i) live |= ((bits >> apps.a[i].bit) & 1u) << i;
+    } else {
+        for (int i = 0; i < apps.n; ++i) live |= (*apps.a[i].app_count > 0 ? 1u : 0u) << i;
+    }
+
+    auto app_of = [&](int u) {
+        int i = 0;
+        for (int j = 1; j < apps.n; ++j) i = u >= apps.a[j].grid0 ? j : i;
+        return i;
+    };
+    // the first of u, u + G, ... whose app has a token (U if none)
+    auto live_from = [&](int u) {
+        for (; u < U; u += G)
+            if ((live >> app_of(u)) & 1u) break;
+        return u;
+    };
+    int u = live_from(own);
+    if (u >= U) return;  // uniform
+    int i = app_of(u);
+    int mt = u - apps.a[i].grid0;
+    SliceSrc src = slice_src(apps.a[i].W, apps.a[i].n_mt, mt);
+    uint4 wa0[4], wa1[4], wa2[4], wa3[4];
+    float cfv[16];
+    load_chunk(wa0, src.base);
+    load_chunk(wa1, src.base + src.stride);
+    load_chunk(wa2, src.base + 2 * src.stride);
+    load_bias(cfv, apps.a[i].c_fold, mt);
+    int list_app = -1, cnt = 0;
+    const int32_t* tl = nullptr;
+    for (;;) {
+        const EncApp& a = apps.a[i];
+        if (i != list_app) {  // uniform
+            if (r_req) {
+                uint32_t e = 0;
+                cnt = build_token_list<kEncThreads>(req_s, tv, sub_s, r_sub, r_Rmax, keep, a.bit,
+                                                    r_Tmax, list_s, rtot_s, nullptr, e);
+                tl = list_s;
+            } else {
+                cnt = *a.app_count;
+                tl = a.tok_list;
+            }
+            list_app = i;
+        }
+        const int un = live_from(u + G);
+        const bool has_nxt = un < U;
+        const int in = has_nxt ? app_of(un) : i;
+        const int mtn = has_nxt ? un - apps.a[in].grid0 : mt;
+        const SliceSrc nsrc = has_nxt ? slice_src(apps.a[in].W, apps.a[in].n_mt, mtn) : src;
+        const SliceSink sink{a.cand, a.tile_cnt, a.tile_tau, a.n_mt, a.lo_cnt, a.cap, a.z};
+        slice_tiles(lds_main, h, d, tl, cnt, 0, true, mt, src, sink, true, nsrc, has_nxt, mtn,
+                    apps.a[in].c_fold, a.c_fold, wa0, wa1, wa2, wa3, cfv);
+        if (!has_nxt) return;
+        __syncthreads();  // the tile rows and list_s are read before they are rewritten
+        u = un;
+        i = in;
+        mt = mtn;
+        src = nsrc;
+    }
 }
 
 // ------------------------------------------ prefill GEMM + candidate emission
@@ -1788,8 +1973,7 @@ sae_merge_kernel(const uint2* __restrict__ cand, const int32_t* __restrict__ til
                 Wp, c_fold, idx_out, val_out, ring);
 }
 
-// Several SAE apps' merges in one launch: workgroup a * T_max + n takes
-// slot n of app a's list.
+// One app's merge inputs and outputs in a batched launch.
 struct MergeApp {
     const uint2* cand;
     const int32_t* tile_cnt;
@@ -1807,13 +1991,31 @@ struct MergeApps {
     MergeApp a[kMultiMax];
 };
 
+// The merges of a batch of apps on a persistent grid: the pairs (app, slot
+// of its token list) of every app's listed tokens, app by app, are dealt to
+// the workgroups in turn, so a slot past its app's count costs nothing (no
+// workgroup, no gather) and an empty batch costs one read of the counts.
 __global__ void __launch_bounds__(kMergeThreads) __attribute__((amdgpu_waves_per_eu(4)))
-sae_merge_multi_kernel(const uint16_t* __restrict__ h, int32_t d, int32_t T_max,
-                       MergeApps apps) {
-    const int i = blockIdx.x / T_max, n = blockIdx.x % T_max;
-    const MergeApp& a = apps.a[i];
-    merge_token(n, a.cand, a.tile_cnt, a.tile_tau, a.n_mt, a.cap, a.app_count, a.tok_list, a.k,
-                h, d, a.Wp, a.c_fold, a.idx_out, a.val_out, a.ring);
+sae_merge_apps_kernel(const uint16_t* __restrict__ h, int32_t d, int32_t T_max, int32_t n_apps,
+                      MergeApps apps) {
+    __shared__ int32_t cnt_s[kMultiMax];
+    for (int i = 0; i < n_apps; ++i)
+        if (threadIdx.x == i) cnt_s[i] = min(max(*apps.a[i].app_count, 0), T_max);
+    __syncthreads();
+    int32_t start[kMultiMax + 1];
+    start[0] = 0;
+#pragma unroll
+    for (int i = 0; i < kMultiMax; ++i) start[i + 1] = start[i] + (i < n_apps ? cnt_s[i] : 0);
+    const int32_t P = start[kMultiMax];
+    for (int32_t p = blockIdx.x; p < P; p += gridDim.x) {  // uniform
+        int i = 0;
+#pragma unroll
+        for (int j = 1; j < kMultiMax; ++j) i = j < n_apps && p >= start[j] ? j : i;
+        const MergeApp& a = apps.a[i];
+        merge_token(p - start[i], a.cand, a.tile_cnt, a.tile_tau, a.n_mt, a.cap, a.app_count,
+                    a.tok_list, a.k, h, d, a.Wp, a.c_fold, a.idx_out, a.val_out, a.ring);
+        __syncthreads();  // the token's LDS is read before the next token's gather
+    }
 }
 
 // ------------------------------------------------------------------ launch
@@ -1975,6 +2177,24 @@ hipError_t launch_sae_merge(const uint16_t* h, int32_t d, int32_t T_max,
 
 bool sae_multi_supported(int32_t T_max) { return T_max < kPrefillMinT; }
 
+// CUs of the current device (256 if the query fails), looked up once per device.
+static int32_t cu_count() {
+    constexpr int kDevs = 64;
+    static std::atomic<int32_t> cache[kDevs];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kDevs) return 256;
+    int32_t n = cache[dev].load(std::memory_order_relaxed);
+    if (n <= 0) {
+        int v = 0;
+        n = hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+                    v > 0
+                ? v
+                : 256;
+        cache[dev].store(n, std::memory_order_relaxed);
+    }
+    return n;
+}
+
 hipError_t launch_sae_encode_multi(const uint16_t* h, int32_t d, int32_t T_max, int32_t n,
                                    const SaeAppIn* apps, hipStream_t stream,
                                    const RouteIn* route) {
@@ -2022,13 +2242,24 @@ hipError_t launch_sae_encode_multi(const uint16_t* h, int32_t d, int32_t T_max, 
         }
         const RouteIn none{};
         const RouteIn& rr = ri ? *ri : none;
-        hipLaunchKernelGGL(sae_stream_multi_kernel, dim3(grid), dim3(kEncThreads), 0, stream, h,
-                           d, n_nt, ea, rr.req, rr.T_valid, rr.sub, rr.R_max, T_max, rr.n_apps,
-                           rr.tok_mask, rr.app_count, rr.app_tokens, rr.err_word);
+        if (n_nt <= kLatentFastTiles) {
+            // persistent: one workgroup per CU (and one per app to publish)
+            int32_t g = grid < cu_count() ? grid : cu_count();
+            if (ri && g < ri->n_apps) g = ri->n_apps;
+            hipLaunchKernelGGL(sae_stream_apps_kernel, dim3(g), dim3(kEncThreads), 0, stream, h,
+                               d, ea, rr.req, rr.T_valid, rr.sub, rr.R_max, T_max, rr.n_apps,
+                               rr.tok_mask, rr.app_count, rr.app_tokens, rr.err_word);
+        } else {
+            hipLaunchKernelGGL(sae_stream_multi_kernel, dim3(grid), dim3(kEncThreads), 0, stream,
+                               h, d, n_nt, ea, rr.req, rr.T_valid, rr.sub, rr.R_max, T_max,
+                               rr.n_apps, rr.tok_mask, rr.app_count, rr.app_tokens, rr.err_word);
+        }
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(sae_merge_multi_kernel, dim3(nc * T_max), dim3(kMergeThreads), 0,
-                           stream, h, d, T_max, ma);
+        // persistent merges: up to four workgroups per CU
+        const int32_t mg = nc * T_max < 4 * cu_count() ? nc * T_max : 4 * cu_count();
+        hipLaunchKernelGGL(sae_merge_apps_kernel, dim3(mg), dim3(kMergeThreads), 0, stream, h, d,
+                           T_max, nc, ma);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -2043,7 +2274,8 @@ void add_sae_kernels(std::vector<KernelInfo>& t) {
     t.push_back(kernel_info(sae_gemm_kernel));
     t.push_back(kernel_info(sae_merge_kernel));
     t.push_back(kernel_info(sae_stream_multi_kernel));
-    t.push_back(kernel_info(sae_merge_multi_kernel));
+    t.push_back(kernel_info(sae_merge_apps_kernel));
+    t.push_back(kernel_info(sae_stream_apps_kernel));
 }
 
 }  // namespace xmix

@@ -244,3 +244,62 @@ def test_clamp_multi_matches_one_call_per_app(px):
     px.xmix_sae_clamp_decode_multi(h_rev, rt, list(reversed(clamp)))
     torch.cuda.synchronize()
     assert np.array_equal(torch_bits(h_rev), torch_bits(h_rev_ref))
+
+
+def test_encode_multi_workgroups_run_many_slices_and_skip_empty_apps(px):
+    """Eight apps of 256 slices each on the persistent grid: every
+    workgroup runs several slices, one after the other, over up to four
+    token tiles each, and two apps without a subscriber are skipped."""
+    wl = small_c5(T=512, n_clamp_apps=8, m=65536, seed=9)
+    wl.sub = (wl.sub | np.uint32(0xFF << 6)).astype(np.uint32)  # every request: every SAE
+    saes = wl.layers[0].saes
+    for s in (saes[2], saes[5]):
+        wl.sub &= ~np.uint32(1 << s.bit)
+    sparse = saes[6].bit  # one app with few tokens: one token tile
+    wl.sub[np.arange(len(wl.sub)) % 7 != 0] &= ~np.uint32(1 << sparse)
+    rt, _ = gpu_route(px, wl)
+    h = dev_bits(wl.layers[0].h)
+    req = dev_i32(wl.req)
+    apps = Apps(px, wl)
+    apps.one_call_per_app(h, rt, req)
+    ref = apps.results()
+    apps.reset()
+    px.xmix_sae_encode_topk_multi(h, rt, apps.multi_apps(), req, 3)
+    got = apps.results()
+    assert_same(got, ref)
+    # the routed form as well
+    apps.reset()
+    rt2 = px.Route(wl.T_max, wl.n_apps)
+    err2 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    r, tv, sb = route_inputs(wl)
+    px.xmix_route_sae_encode_topk_multi(r, tv, sb, rt2, err2, h, apps.multi_apps(), 3)
+    assert_same(apps.results(), ref)
+    assert np.array_equal(rt2.app_count.cpu().numpy(), rt.app_count.cpu().numpy())
+    tm, cnt, lists, _ = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    assert cnt[saes[2].bit] == 0 and cnt[saes[5].bit] == 0 and cnt[saes[0].bit] == 512
+    # the empty apps' outputs are untouched
+    for j in (2, 5):
+        assert np.all(got[j][0] == -7)
+    # tokens of every token tile of one app against the oracle
+    s = saes[3]
+    toks = lists[s.bit, :cnt[s.bit]][[0, 127, 128, 300, 383, 384, 511]]
+    idx_ref, _, _, pre = oracle.sae_encode(wl.layers[0].h, toks, s.W_enc, s.b_enc, s.b_dec, s.k,
+                                           want_pre=True)
+    idx, val, _ = got[3]
+    for q, t in enumerate(toks):
+        check_topk(idx[t], val[t], idx_ref[q], pre[q], s.k)
+
+
+def test_encode_multi_between_decode_and_prefill_shapes(px):
+    """513 to 1024 token slots: the batched launch over the apps' blocked
+    tile grids (neither the persistent grid nor the prefill GEMM)."""
+    wl = small_c5(T=700, n_clamp_apps=3, seed=10)
+    rt, _ = gpu_route(px, wl)
+    h = dev_bits(wl.layers[0].h)
+    req = dev_i32(wl.req)
+    apps = Apps(px, wl)
+    apps.one_call_per_app(h, rt, req)
+    ref = apps.results()
+    apps.reset()
+    px.xmix_sae_encode_topk_multi(h, rt, apps.multi_apps(), req, 3)
+    assert_same(apps.results(), ref)
