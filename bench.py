@@ -743,7 +743,11 @@ def run_repair(torch, synth, HookStep, args):
              ("c3 20 tied slices", {}, 20, 5),
              ("c3 every slice tied", {}, 256, 3),
              ("prefill GEMM, 1100 tokens, strong latents", {"T": 1100, "n_sub": 1100,
-                                                            "m": 131072, "k": 32}, "strong", 5)]
+                                                            "m": 131072, "k": 32}, "strong", 5),
+             ("prefill GEMM, 1100 tokens, 10 tied slices", {"T": 1100, "n_sub": 1100,
+                                                            "m": 131072, "k": 32}, 10, 5),
+             ("prefill GEMM, 1100 tokens, every slice tied", {"T": 1100, "n_sub": 1100,
+                                                              "m": 131072, "k": 32}, 512, 3)]
     res = {}
     for name, kw, kind, n in cases:
         wl = synth.make("c3", ring_capacity=0, **kw)

@@ -350,7 +350,9 @@ __device__ __forceinline__ void select_slices(const float* const (&vrow)[NT], in
         }
         if (q == 0) {
             *cnt_out[t] = min(total[t], cap);
-            *tau_out[t] = tau[t];
+            // nothing at or above tau: the next value above the slice's
+            // maximum bounds its values as well, and tighter
+            *tau_out[t] = TRIM && mx[t] < tau[t] ? key_f32(f32_key(mx[t]) + 1u) : tau[t];
         }
     }
 }
@@ -1145,7 +1147,7 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
         }
     }
     __syncthreads();
-    float tau[4], lo_b[4], hi_b[4];
+    float tau[4], lo_b[4], hi_b[4], mxv[4];
     uint32_t m0[4], m1[4];  // bit i: value i >= tau (m1: value 32 + i)
     bool bad[4];
 #pragma unroll
@@ -1155,6 +1157,7 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
         const float mu = s1 * (1.0f / 256.0f);
         const float sd = sqrtf(fmaxf(s2 * (1.0f / 256.0f) - mu * mu, 0.0f));
         const float mx = fmaxf(red3[0][n], red3[1][n]);
+        mxv[nb] = mx;
         // a strong latent (above mean + 5 stdev, such as a feature clamped
         // high at an earlier layer) would lift the guess for its whole
         // slice: the guess leaves the slice's largest value out then (the
@@ -1254,7 +1257,10 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
                 ++slot;
             }
         }
-        if (n < ntok && wm == 0 && g == 0) tile_tau[row] = tau[nb];
+        // nothing at or above tau: the next value above the slice's maximum
+        // bounds its values as well, and tighter
+        if (n < ntok && wm == 0 && g == 0)
+            tile_tau[row] = mxv[nb] < tau[nb] ? key_f32(f32_key(mxv[nb]) + 1u) : tau[nb];
         // the wave's reads of this buffer precede these stores in its LDS queue
         if (nb < 2) park_group(nb + 2);
     }
@@ -1404,7 +1410,6 @@ constexpr int kMergeThreads = 256;
 constexpr int kMergeWaves = kMergeThreads / kWave;
 constexpr int kMergeR = 32;                        // pool entries per lane
 constexpr int kPoolMax = kMergeR * kWave;          // 2048
-constexpr int kMaxRepair = 32;                     // slices one repair redoes one by one
 constexpr int kRepairR = 6;                        // repair pool entries per lane
 constexpr int kRepairPool = kRepairR * kWave;      // 384 >= k + one slice
 constexpr int kFloorRounds = 3;                    // pool refills above a raised floor
@@ -1541,9 +1546,9 @@ __device__ __forceinline__ void merge_token(
     __shared__ int sel_n_s;
     __shared__ int scan_s[2][kMergeWaves];  // gather rounds alternate between the two
     __shared__ uint32_t tmax_s[2][kMergeWaves];
-    __shared__ int pool_n_s, nfail_s;
+    __shared__ int pool_n_s;
     __shared__ uint32_t floor_s;
-    __shared__ int fail_s[kMaxRepair];
+    __shared__ uint64_t rbest_s[kMergeWaves], kth_s;  // repair: next slice, k-th composite
     const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
     const int64_t row0 = static_cast<int64_t>(n) * n_mt;
     // The first round of the gather below does not depend on the token
@@ -1574,7 +1579,6 @@ __device__ __forceinline__ void merge_token(
     const int32_t t = tok_list[n];
     const int cnt = *app_count;
     if (n >= cnt) return;  // uniform: no token, no ring row, no ticket
-    if (tid == 0) nfail_s = 0;  // read after the gather's barriers
 
     // Gather: the candidates with key >= floor, in slice order, into the pool
     // (the first kPoolMax of them; the rest are counted only).  Returns their
@@ -1812,42 +1816,35 @@ __device__ __forceinline__ void merge_token(
     const int fix = !fits ? 2 : (tau_tiles <= sel_tau ? 0 : 1);
     if (fix != 0) {  // uniform
         // Repair: whole slices are recomputed exactly (fp32 dot products,
-        // the workgroup streaming each slice once).  The pool is cut down to
-        // what can still reach the top k, then after every slice wave 0
-        // keeps the k best of the pool and that slice's values above the
-        // floor (at most kRepairPool entries), raising the floor to the k-th.
-        // After a failed certificate only the slices whose threshold lies
-        // above the k-th selected value are redone and the pool keeps its
-        // other entries at or above that value; when the pool was unusable,
-        // more than kMaxRepair slices failed or too many entries are kept,
+        // the workgroup streaming each slice once).  A slice hides only
+        // values below its threshold, none of them at a latent below its
+        // first: that composite bound says whether it can hide a winner.
+        // The pool is cut down to what can still reach the top k; then the
+        // slices are redone in descending order of their bound, each one's
+        // pool entries replaced by its recomputed values above the floor,
+        // wave 0 keeping the k best (at most kRepairPool entries) and raising
+        // the floor and the k-th composite; the first slice whose bound lies
+        // at or below the k-th composite ends the repair, since no later one
+        // can hold a winner.  So tied or crowded slices cost the slices that
+        // hold the top k, not every slice.  When the pool misses candidates
+        // (more than kPoolMax after the refills) or keeps too many entries,
         // every slice is redone from an empty pool.
         const uint16_t* hrow = h + static_cast<int64_t>(t) * d;
-        const uint32_t st = sel_tau;
-        bool all = fix == 2;
-        if (!all) {
-            for (int tl = tid; tl < n_mt; tl += kMergeThreads) {
-                if (f32_key(tile_tau[row0 + tl]) > st) {
-                    const int q = atomicAdd(&nfail_s, 1);
-                    if (q < kMaxRepair) fail_s[q] = tl;
-                }
-            }
-            __syncthreads();
-            all = nfail_s > kMaxRepair;
-        }
-        if (!all && wave == 0) {
-            // a little below the k-th value, so that a value whose recomputed
-            // rounding differs from the GEMM's still enters
-            const float tv = key_f32(st);
-            const uint32_t fl = f32_key(tv - fabsf(tv) * 0x1p-12f);
-            const int nf = nfail_s;
+        // the k-th selected composite (0: no selection yet)
+        uint64_t kth = fix == 1 ? wave_minmax_u64<false>(
+                                      lane < k ? (static_cast<uint64_t>(wk) << 32) |
+                                                     static_cast<uint32_t>(~wi)
+                                               : ~0ull)
+                                : 0ull;
+        // pool entries of slice q leave the pool (wave 0; q < 0: none), the
+        // others from `fl` up stay
+        auto cut_pool = [&](int np, uint32_t fl, int q) __attribute__((always_inline)) {
             int out = 0;
-            const int np = min(total, kPoolMax);
             for (int b0 = 0; b0 < np; b0 += kWave) {
                 const int i = b0 + lane;
                 const uint32_t kk = i < np ? K[i] : 0u;
                 const int32_t ii = i < np ? I[i] : 0;
-                bool keep = i < np && kk >= fl;
-                for (int f = 0; f < nf; ++f) keep = keep && ii / kBM != fail_s[f];
+                const bool keep = i < np && kk >= fl && ii / kBM != q;
                 const uint64_t bal = wave_ballot(keep);
                 wave_sync();  // this round's reads come before its writes
                 if (keep) {
@@ -1857,6 +1854,19 @@ __device__ __forceinline__ void merge_token(
                 out += __popcll(bal);
             }
             wave_sync();
+            return out;
+        };
+        bool all = total > kPoolMax;  // uniform: the pool misses candidates
+        if (!all && wave == 0) {
+            // with a selection, a little below its k-th value, so that a
+            // value whose recomputed rounding differs from the GEMM's still
+            // enters; without one, the whole pool
+            uint32_t fl = 0u;
+            if (fix == 1) {
+                const float tv = key_f32(sel_tau);
+                fl = f32_key(tv - fabsf(tv) * 0x1p-12f);
+            }
+            const int out = cut_pool(total, fl, -1);
             if (lane == 0) {
                 pool_n_s = out;
                 floor_s = fl;
@@ -1864,20 +1874,92 @@ __device__ __forceinline__ void merge_token(
         }
         __syncthreads();
         if (!all && pool_n_s > kRepairPool - kBM) all = true;
-        for (int pass = all ? 1 : 0; pass < 2; ++pass) {
-            __syncthreads();  // every thread has read the pool size
-            if (pass == 1) {
-                if (tid == 0) {
-                    pool_n_s = 0;
-                    floor_s = 0u;
+        if (!all) {
+            uint64_t prev = ~0ull;  // the slices with bounds below it are left
+            for (;;) {
+                uint64_t best = 0ull;
+                for (int q = tid; q < n_mt; q += kMergeThreads) {
+                    const uint32_t tk = f32_key(tile_tau[row0 + q]);
+                    const uint64_t bq = tk == 0u ? 0ull
+                                                 : (static_cast<uint64_t>(tk - 1u) << 32) |
+                                                       static_cast<uint32_t>(~(q * kBM));
+                    if (bq < prev) best = max(best, bq);
+                }
+                best = wave_minmax_u64<true>(best);
+                if (lane == 0) rbest_s[wave] = best;
+                __syncthreads();
+                best = max(max(rbest_s[0], rbest_s[1]), max(rbest_s[2], rbest_s[3]));
+                if (best <= kth) break;  // uniform: no slice left can hold a winner
+                prev = best;
+                const int32_t q = static_cast<int32_t>(~static_cast<uint32_t>(best)) / kBM;
+                if (wave == 0) {
+                    const int out = cut_pool(pool_n_s, 0u, q);
+                    if (lane == 0) pool_n_s = out;
                 }
                 __syncthreads();
+                const int32_t j = q * kBM + tid;
+                const float dot = slice_dot(Wp, hrow, q, n_mt, d, part_s);
+                const uint32_t key = f32_key(dot + c_fold[j]);
+                if (key >= floor_s) {
+                    const int pos = atomicAdd(&pool_n_s, 1);
+                    K[pos] = key;
+                    I[pos] = j;
+                }
+                __syncthreads();
+                const int pn = pool_n_s;
+                __syncthreads();  // every thread has read the pool size
+                if (pn >= k) {
+                    if (wave == 0) {
+                        uint32_t tk, a;
+                        int32_t b;
+                        if (pn > k) {
+                            wave_select_take<kRepairR>(K, I, pn, k, K + kPoolMax, I + kPoolMax,
+                                                       &tk, &a, &b);
+                            if (lane < k) {
+                                K[lane] = a;
+                                I[lane] = b;
+                            }
+                        } else {
+                            a = lane < k ? K[lane] : 0xFFFFFFFFu;
+                            b = lane < k ? I[lane] : 0;
+                            tk = wave_minmax_u32<false>(a);
+                        }
+                        const uint64_t kc = wave_minmax_u64<false>(
+                            lane < k ? (static_cast<uint64_t>(a) << 32) | static_cast<uint32_t>(~b)
+                                     : ~0ull);
+                        if (lane == 0) {
+                            pool_n_s = k;
+                            floor_s = max(floor_s, tk);
+                            kth_s = kc;
+                        }
+                    }
+                    __syncthreads();
+                    kth = kth_s;
+                }
             }
-            const int n_rep = pass == 1 ? n_mt : nfail_s;
-            for (int q = 0; q < n_rep; ++q) {
-                const int32_t mtq = pass == 1 ? q : fail_s[q];
-                const int32_t j = mtq * kBM + tid;
-                const float dot = slice_dot(Wp, hrow, mtq, n_mt, d, part_s);
+            // the pool holds the k best unless no slice was redone after the cut
+            const int pn = pool_n_s;
+            if (pn > k && wave == 0) {
+                uint32_t tk, a;
+                int32_t b;
+                wave_select_take<kRepairR>(K, I, pn, k, K + kPoolMax, I + kPoolMax, &tk, &a, &b);
+                if (lane < k) {
+                    K[lane] = a;
+                    I[lane] = b;
+                }
+            }
+            all = pn < k;  // (rounding) redo every slice
+        }
+        if (all) {  // uniform
+            __syncthreads();  // every thread has read the pool size
+            if (tid == 0) {
+                pool_n_s = 0;
+                floor_s = 0u;
+            }
+            __syncthreads();
+            for (int q = 0; q < n_mt; ++q) {
+                const int32_t j = q * kBM + tid;
+                const float dot = slice_dot(Wp, hrow, q, n_mt, d, part_s);
                 const uint32_t key = f32_key(dot + c_fold[j]);
                 if (key >= floor_s) {
                     const int pos = atomicAdd(&pool_n_s, 1);
@@ -1905,7 +1987,6 @@ __device__ __forceinline__ void merge_token(
                     __syncthreads();
                 }
             }
-            if (pool_n_s >= k) break;  // else (rounding) redo every slice
         }
         if (wave == 0) {
             wk = lane < k ? K[lane] : 0u;

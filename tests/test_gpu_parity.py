@@ -786,12 +786,12 @@ def test_encode_repair_of_tied_slices(px, n_tied, T):
     """n_tied slices whose 256 pre-activations are all exactly 40 (zero
     dictionary rows, bias 40), far above every other latent.  No threshold
     splits a tie, so these slices emit nothing and fail the certificate.
-    10: the merge recomputes them one by one and its pool overflows on the
-    way (compaction to the k best); 20: more than it repairs slice by
-    slice, so every slice is recomputed; 64: nothing is emitted at all.
-    The k lowest latents of the tie win.  With 1100 token slots the prefill
-    GEMM runs, whose threshold search on a tied slice uses every refinement
-    round and then gives up."""
+    The merge redoes slices in the order of their bounds: the first tied
+    slice gives the k winners, and every other tied slice, bounded by the
+    same value at higher latents, cannot beat them (64: nothing is emitted
+    at all, the pool starts empty).  The k lowest latents of the tie win.
+    With 1100 token slots the prefill GEMM runs, whose threshold search on
+    a tied slice uses every refinement round and then gives up."""
     d, m, k = 256, 16384, 64
     wl = synth.make("c3", d=d, m=m, k=k, T=T, n_sub=T)
     sae = wl.layers[0].saes[0]
@@ -806,6 +806,51 @@ def test_encode_repair_of_tied_slices(px, n_tied, T):
     first = 256 * int(slices[0])
     for t in range(T):
         assert sorted(idx[t].tolist()) == list(range(first, first + k))
+        assert np.all(bf16_f64(val[t]) == 40.0)
+
+
+@pytest.mark.parametrize("T", [6, 1100])
+def test_encode_repair_takes_the_highest_bound_first(px, T):
+    """Ten tied slices at different levels (zero rows; the i-th tied slice
+    has bias 40 + 2i), so the highest tie sits in the last of them: the
+    merge must redo that slice first and stop there.  Its k lowest latents
+    win with value 58."""
+    d, m, k = 256, 16384, 64
+    wl = synth.make("c3", d=d, m=m, k=k, T=T, n_sub=T)
+    sae = wl.layers[0].saes[0]
+    W, b = sae.W_enc.copy(), sae.b_enc.copy()
+    slices = 1 + 3 * np.arange(10)
+    for i, s in enumerate(slices):
+        W[256 * s:256 * (s + 1)] = 0
+        b[256 * s:256 * (s + 1)] = to_bf16_bits(np.full(256, 40.0 + 2 * i))
+    sae.W_enc, sae.b_enc = W, b
+    rt, idx, val = _encode(px, wl, sae, wl.layers[0].h)
+    _check_encode(wl, sae, wl.layers[0].h, idx, val, np.arange(T))
+    first = 256 * int(slices[-1])
+    for t in range(T):
+        assert sorted(idx[t].tolist()) == list(range(first, first + k))
+        assert np.all(bf16_f64(val[t]) == 58.0)
+
+
+@pytest.mark.parametrize("T", [6, 1100])
+def test_encode_repair_winners_over_two_tied_slices(px, T):
+    """Three slices each hold 32 latents tied at 40 (zero rows, bias 40) far
+    above the rest, with k = 64: the repair needs the first two slices (32
+    winners each) and must not take the third's, which lose on the latent
+    index."""
+    d, m, k = 256, 16384, 64
+    wl = synth.make("c3", d=d, m=m, k=k, T=T, n_sub=T)
+    sae = wl.layers[0].saes[0]
+    W, b = sae.W_enc.copy(), sae.b_enc.copy()
+    for s in (2, 5, 9):
+        W[256 * s:256 * s + 32] = 0
+        b[256 * s:256 * s + 32] = 0x4220  # 40.0
+    sae.W_enc, sae.b_enc = W, b
+    rt, idx, val = _encode(px, wl, sae, wl.layers[0].h)
+    _check_encode(wl, sae, wl.layers[0].h, idx, val, np.arange(T))
+    want = list(range(512, 544)) + list(range(1280, 1312))
+    for t in range(T):
+        assert sorted(idx[t].tolist()) == want
         assert np.all(bf16_f64(val[t]) == 40.0)
 
 
