@@ -361,10 +361,12 @@ xmix_status xmix_sae_encode_topk_noalloc(const uint16_t *h, int32_t d, const xmi
  *               The top-k of the kept latents is the top-k of all m
  *               latents when its k-th value is >= every slice's tau (a
  *               latent left out lies below its slice's tau); otherwise the
- *               merge recomputes the slices that can hide a winner (those
- *               whose tau lies above the k-th selected value) and selects
- *               again (same result, slower; it happens only when the
- *               winners crowd into a few slices).
+ *               merge recomputes slices in descending order of that bound
+ *               until no slice left can hide a winner (same result, slower;
+ *               it happens only when the winners crowd into a few slices
+ *               or tie across whole slices).  A slice with nothing at or
+ *               above its tau keeps, as its tau, the next value above its
+ *               largest pre-activation.
  * The same certificate lets a dictionary be split across devices by latent
  * slices: exchange the kept candidates and thresholds, then merge. */
 xmix_status xmix_sae_encode_candidates(const uint16_t *h, int32_t d, const xmix_route *rt,

@@ -32,8 +32,10 @@
 // all m latents whenever the k-th selected value is >= every tile's tau,
 // because a latent that was not emitted lies below its tile's tau.  When
 // that certificate fails (only for inputs whose best latents crowd into a
-// few tiles), the workgroup recomputes the failing tiles' 256
-// pre-activations with plain fp32 dot products and selects again.  The
+// few tiles or tie across whole tiles), the workgroup recomputes tiles'
+// 256 pre-activations with plain fp32 dot products, in descending order of
+// the bound each tile's tau sets on its left-out values, until no tile left
+// can hold a winner.  The
 // decode kernel's first threshold guess leaves a tile's strongest values
 // out of the statistics (above mean + 5 stdev), so that a few strong
 // latents, such as features clamped high by a steering app, do not lift it:
