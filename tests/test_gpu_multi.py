@@ -303,3 +303,57 @@ def test_encode_multi_between_decode_and_prefill_shapes(px):
     apps.reset()
     px.xmix_sae_encode_topk_multi(h, rt, apps.multi_apps(), req, 3)
     assert_same(apps.results(), ref)
+
+
+def test_routed_encode_multi_publishes_the_routing_without_subscribers(px):
+    """No request subscribes to anything: the routed batched call still
+    publishes every app's (empty) list, count and mask, as the route build
+    does, and writes no output row."""
+    wl = small_c5(n_clamp_apps=4, seed=11)
+    wl.sub = np.zeros_like(wl.sub)
+    rt, err = gpu_route(px, wl)
+    ref = (rt.tok_mask.cpu().numpy(), rt.app_count.cpu().numpy(), rt.app_tokens.cpu().numpy(),
+           err.cpu().numpy())
+    h = dev_bits(wl.layers[0].h)
+    req, tv, sub = route_inputs(wl)
+    apps = Apps(px, wl)
+    rt2 = px.Route(wl.T_max, wl.n_apps)
+    rt2.tok_mask.fill_(-1)
+    rt2.app_count.fill_(-1)
+    rt2.app_tokens.fill_(-3)
+    err2 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    px.xmix_route_sae_encode_topk_multi(req, tv, sub, rt2, err2, h, apps.multi_apps(), 3)
+    got = (rt2.tok_mask.cpu().numpy(), rt2.app_count.cpu().numpy(),
+           rt2.app_tokens.cpu().numpy(), err2.cpu().numpy())
+    for a, b in zip(got, ref):
+        assert np.array_equal(a, b)
+    for idx, _, ring in apps.results():
+        assert np.all(idx == -7)
+        if ring is not None:
+            assert np.all(ring[0] == 0) and ring[1][0] == 5
+
+
+def test_routed_encode_multi_with_fewer_slices_than_apps(px):
+    """Three one-slice dictionaries (m = 256) among 9 apps: the persistent
+    grid has more workgroups than slices, so that every app's list is
+    published; the results are those of one call per app."""
+    wl = small_c5(n_clamp_apps=3, m=256, seed=12)
+    rt, err = gpu_route(px, wl)
+    h = dev_bits(wl.layers[0].h)
+    req, tv, sub = route_inputs(wl)
+    apps = Apps(px, wl)
+    apps.one_call_per_app(h, rt, req)
+    ref = apps.results()
+    ref_route = (rt.tok_mask.cpu().numpy(), rt.app_count.cpu().numpy(),
+                 rt.app_tokens.cpu().numpy(), err.cpu().numpy())
+    apps.reset()
+    rt2 = px.Route(wl.T_max, wl.n_apps)
+    rt2.app_count.fill_(-1)
+    rt2.app_tokens.fill_(-3)
+    err2 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    px.xmix_route_sae_encode_topk_multi(req, tv, sub, rt2, err2, h, apps.multi_apps(), 3)
+    assert_same(apps.results(), ref)
+    got = (rt2.tok_mask.cpu().numpy(), rt2.app_count.cpu().numpy(),
+           rt2.app_tokens.cpu().numpy(), err2.cpu().numpy())
+    for a, b in zip(got, ref_route):
+        assert np.array_equal(a, b)
