@@ -357,3 +357,45 @@ def test_routed_encode_multi_with_fewer_slices_than_apps(px):
            rt2.app_tokens.cpu().numpy(), err2.cpu().numpy())
     for a, b in zip(got, ref_route):
         assert np.array_equal(a, b)
+
+
+def test_routed_encode_multi_with_mixed_k_padding_and_t_valid(px):
+    """Apps with k = 8, 32 and 64 in one batch (each its own candidate cap
+    and threshold quantile), a padded slot, a request id out of range and
+    T_valid below T_max: the routed batched call matches the route build
+    followed by one call per app, error word included."""
+    wl = small_c5(T=300, n_clamp_apps=3, seed=13)
+    saes = wl.layers[0].saes
+    for s, k in zip(saes, (8, 32, 64)):
+        s.k = k
+    wl.req = wl.req.copy()
+    wl.req[5] = -1              # padding
+    wl.req[7] = wl.R_max + 3    # out of range: routes nowhere, flags the error word
+    wl.T_valid = 290
+    rt, err = gpu_route(px, wl)
+    assert int(err.item()) != 0
+    h = dev_bits(wl.layers[0].h)
+    req, tv, sub = route_inputs(wl)
+    apps = Apps(px, wl)
+    apps.one_call_per_app(h, rt, req)
+    ref = apps.results()
+    ref_route = (rt.tok_mask.cpu().numpy(), rt.app_count.cpu().numpy(),
+                 rt.app_tokens.cpu().numpy(), err.cpu().numpy())
+    apps.reset()
+    rt2 = px.Route(wl.T_max, wl.n_apps)
+    err2 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    px.xmix_route_sae_encode_topk_multi(req, tv, sub, rt2, err2, h, apps.multi_apps(), 3)
+    assert_same(apps.results(), ref)
+    got = (rt2.tok_mask.cpu().numpy(), rt2.app_count.cpu().numpy(),
+           rt2.app_tokens.cpu().numpy(), err2.cpu().numpy())
+    for a, b in zip(got, ref_route):
+        assert np.array_equal(a, b)
+    # the k = 64 app against the oracle
+    tm, cnt, lists, _ = oracle.route(wl.req, wl.T_valid, wl.sub, wl.n_apps)
+    s = saes[2]
+    toks = lists[s.bit, :cnt[s.bit]][::9]
+    idx_ref, _, _, pre = oracle.sae_encode(wl.layers[0].h, toks, s.W_enc, s.b_enc, s.b_dec, s.k,
+                                           want_pre=True)
+    idx, val, _ = ref[2]
+    for q, t in enumerate(toks):
+        check_topk(idx[t], val[t], idx_ref[q], pre[q], s.k)
