@@ -561,7 +561,10 @@ xmix_status xmix_readback_compact(const void *const *seg_rows, const int32_t *se
  * be made on the stream meanwhile.  stream must not be the null stream.
  *
  * xmix_graph_redirect: every pointer argument of those nodes that holds
- * `from` is set to `to` for all later launches (one
+ * `from` (also a pointer inside the app descriptors of the batched calls:
+ * dictionaries, biases, outputs, clamp values, rings) is set to `to` for all
+ * later launches; pointers into the middle of `from` (such as parts of a
+ * workspace) are not changed (one
  * hipGraphExecKernelNodeSetParams per affected node; the graph is neither
  * recaptured nor re-instantiated).  `to` must be a device buffer of the same
  * size and layout as `from`.  *n_args (optional) receives the number of

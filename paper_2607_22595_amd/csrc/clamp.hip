@@ -2,6 +2,7 @@
 // one app, fp32 accumulation and one RNE rounding.  Only the n_clamp decoder
 // rows are read; the dense m x d decode is never formed.  One workgroup per
 // slot of the app's token list (slots past the live count return at once).
+#include <stddef.h>
 #include <string.h>
 
 #include "common.hpp"
@@ -190,6 +191,23 @@ hipError_t launch_clamp_decode(uint16_t* h, int32_t d, const int32_t* app_count,
                        n_clamp, delta_out);
     return hipGetLastError();
 }
+
+// Where the batched descriptor holds device pointers (for the graph
+// executor's redirection).
+template <>
+struct ArgPointers<ClampApps> {
+    static std::vector<uint16_t> offsets() {
+        std::vector<uint16_t> o;
+        for (int i = 0; i < kMultiMax; ++i)
+            for (const size_t f : {offsetof(ClampAppIn, idx), offsetof(ClampAppIn, val),
+                                   offsetof(ClampAppIn, W_dec), offsetof(ClampAppIn, clamp_ids),
+                                   offsetof(ClampAppIn, clamp_vals),
+                                   offsetof(ClampAppIn, delta_out)})
+                o.push_back(
+                    static_cast<uint16_t>(offsetof(ClampApps, a) + i * sizeof(ClampAppIn) + f));
+        return o;
+    }
+};
 
 void add_clamp_kernels(std::vector<KernelInfo>& t) {
     t.push_back(kernel_info(clamp_decode_kernel));

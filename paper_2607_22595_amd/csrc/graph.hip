@@ -7,7 +7,8 @@
 // captured graph and keeps, for every kernel node launched by this library,
 // the node handle and a copy of its argument bytes, decoded with the
 // argument layout of that kernel (kernels.hpp).  xmix_graph_redirect then
-// points every pointer argument that holds one device buffer at another,
+// points every pointer argument that holds one device buffer at another
+// (also the pointers inside the batched calls' app descriptors),
 // through hipGraphExecKernelNodeSetParams on the affected nodes only: no
 // recapture and no re-instantiation.  This is the node-update path; the
 // library's own design keeps per-step values in device memory, which needs
@@ -143,13 +144,15 @@ xmix_status xmix_graph_redirect(xmix_graph* g, const void* from, const void* to,
     for (xmix_graph::Node& rec : g->nodes) {
         bool hit = false;
         for (size_t i = 0; i < rec.info->size.size(); ++i) {
-            if (!rec.info->is_ptr[i]) continue;
-            void* v;
-            memcpy(&v, rec.bytes.data() + rec.offset[i], sizeof(v));
-            if (v != from) continue;
-            memcpy(rec.bytes.data() + rec.offset[i], &to, sizeof(to));
-            hit = true;
-            ++count;
+            for (const uint16_t at : rec.info->ptr_at[i]) {  // pointers, also inside structs
+                uint8_t* where = rec.bytes.data() + rec.offset[i] + at;
+                void* v;
+                memcpy(&v, where, sizeof(v));
+                if (v != from) continue;
+                memcpy(where, &to, sizeof(to));
+                hit = true;
+                ++count;
+            }
         }
         if (!hit) continue;
         args.resize(rec.info->size.size());

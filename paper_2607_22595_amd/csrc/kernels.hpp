@@ -12,9 +12,20 @@
 namespace xmix {
 
 struct KernelInfo {
-    const void* func;             // the address hipLaunchKernelGGL records
-    std::vector<uint16_t> size;   // bytes of each argument, in order
-    std::vector<uint8_t> is_ptr;  // 1 for a pointer argument
+    const void* func;                           // the address hipLaunchKernelGGL records
+    std::vector<uint16_t> size;                 // bytes of each argument, in order
+    std::vector<std::vector<uint16_t>> ptr_at;  // device pointers inside each argument
+};
+
+// Byte offsets of the device pointers inside an argument of type T: the
+// argument itself when it is a pointer, none otherwise.  A struct passed by
+// value that holds pointers (the batched calls' app descriptors) lists them
+// in a specialization beside its definition, before its kernels' table.
+template <typename T>
+struct ArgPointers {
+    static std::vector<uint16_t> offsets() {
+        return std::is_pointer<T>::value ? std::vector<uint16_t>{0} : std::vector<uint16_t>{};
+    }
 };
 
 // Top-level qualifiers (const, __restrict__) are not part of a function
@@ -23,7 +34,7 @@ template <typename... A>
 KernelInfo kernel_info(void (*f)(A...)) {
     return KernelInfo{reinterpret_cast<const void*>(f),
                       {static_cast<uint16_t>(sizeof(A))...},
-                      {static_cast<uint8_t>(std::is_pointer<A>::value)...}};
+                      {ArgPointers<A>::offsets()...}};
 }
 
 // One per kernel source: appends the kernels that file launches.

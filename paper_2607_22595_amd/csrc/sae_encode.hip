@@ -47,6 +47,7 @@
 // to the 8 XCDs, so consecutive tiles of one XCD share a dictionary slice in
 // that XCD's L2.
 #include <math.h>
+#include <stddef.h>
 #include <string.h>
 
 #include <atomic>
@@ -2348,6 +2349,46 @@ hipError_t launch_sae_encode_multi(const uint16_t* h, int32_t d, int32_t T_max, 
     }
     return hipSuccess;
 }
+
+// Where the by-value descriptors hold device pointers (for the graph
+// executor's redirection).
+template <>
+struct ArgPointers<RingOut> {
+    static std::vector<uint16_t> offsets() {
+        return {offsetof(RingOut, slots), offsetof(RingOut, head), offsetof(RingOut, req)};
+    }
+};
+template <>
+struct ArgPointers<EncApps> {
+    static std::vector<uint16_t> offsets() {
+        std::vector<uint16_t> o;
+        for (int i = 0; i < kMultiMax; ++i)
+            for (const size_t f : {offsetof(EncApp, app_count), offsetof(EncApp, tok_list),
+                                   offsetof(EncApp, W), offsetof(EncApp, c_fold),
+                                   offsetof(EncApp, cand), offsetof(EncApp, tile_cnt),
+                                   offsetof(EncApp, tile_tau)})
+                o.push_back(static_cast<uint16_t>(offsetof(EncApps, a) + i * sizeof(EncApp) + f));
+        return o;
+    }
+};
+template <>
+struct ArgPointers<MergeApps> {
+    static std::vector<uint16_t> offsets() {
+        std::vector<uint16_t> o;
+        for (int i = 0; i < kMultiMax; ++i) {
+            const size_t b = offsetof(MergeApps, a) + i * sizeof(MergeApp);
+            for (const size_t f : {offsetof(MergeApp, cand), offsetof(MergeApp, tile_cnt),
+                                   offsetof(MergeApp, tile_tau), offsetof(MergeApp, app_count),
+                                   offsetof(MergeApp, tok_list), offsetof(MergeApp, Wp),
+                                   offsetof(MergeApp, c_fold), offsetof(MergeApp, idx_out),
+                                   offsetof(MergeApp, val_out)})
+                o.push_back(static_cast<uint16_t>(b + f));
+            for (const uint16_t f : ArgPointers<RingOut>::offsets())
+                o.push_back(static_cast<uint16_t>(b + offsetof(MergeApp, ring) + f));
+        }
+        return o;
+    }
+};
 
 void add_sae_kernels(std::vector<KernelInfo>& t) {
     t.push_back(kernel_info(sae_pack_kernel));

@@ -207,3 +207,73 @@ def test_decode_sae_step_graph_with_routing_in_the_encode():
     finally:
         torch.cuda.synchronize()
         g.close()
+
+
+def test_redirect_reaches_buffers_inside_batched_calls():
+    """A layer with three clamp SAEs runs as one batched encode and one
+    batched clamp, whose app descriptors hold the buffers: redirecting one
+    app's clamp values changes one argument (the batched clamp), and one
+    app's dictionary two (the batched encode and merge); each replay equals
+    an eager run with the new buffer, and the graph goes back."""
+    import paper_2607_22595_amd as px
+    from paper_2607_22595_amd.hookstep import HookStep
+    wl = synth.make("c5", d=512, T=160, m=1024, k=16, n_steer=2, n_probe=1, n_clamp_apps=3,
+                    seed=21)
+    step = HookStep(wl)
+    saes = step.layers[0].saes
+
+    def snap():
+        torch.cuda.synchronize()
+        return [torch_bits(step.layers[0].h).copy()] + \
+            [x for s in saes for x in (s.idx.cpu().numpy(), torch_bits(s.val))]
+
+    def eager():
+        step.reset()
+        step.run()
+        return snap()
+
+    def same(a, b):
+        return all(np.array_equal(x, y) for x, y in zip(a, b))
+
+    ref0 = eager()
+    stream = torch.cuda.Stream()
+    g = px.Graph(lambda: step.run(stream), stream)
+
+    def replay():
+        step.reset()
+        torch.cuda.synchronize()
+        g.launch()
+        g.stream.synchronize()
+        return snap()
+
+    try:
+        assert same(replay(), ref0)
+        s1 = saes[1]
+        vals0 = s1.clamp_vals
+        vals1 = (vals0 * -1.5 + 3.0).contiguous()
+        assert g.redirect(vals0, vals1) == 1
+        got = replay()
+        s1.clamp_vals = vals1
+        try:
+            ref = eager()
+        finally:
+            s1.clamp_vals = vals0
+        assert same(got, ref) and not same(got, ref0)
+        assert g.redirect(vals1, vals0) == 1
+        # app 2's dictionary swapped for a copy of app 0's (same shape)
+        s2 = saes[2]
+        W0 = s2.W_enc
+        W1 = saes[0].W_enc.clone()
+        assert g.redirect(W0.packed, W1.packed) == 2
+        got = replay()
+        s2.W_enc = W1
+        try:
+            ref = eager()
+        finally:
+            s2.W_enc = W0
+        assert same(got, ref) and not same(got, ref0)
+        assert g.redirect(W1.packed, W0.packed) == 2
+        assert same(replay(), ref0)
+    finally:
+        torch.cuda.synchronize()
+        g.close()
