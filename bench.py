@@ -731,6 +731,30 @@ def _tied_slices(wl, n_tied):
     s.W_enc, s.b_enc = W, b
 
 
+def _tied_candidates(synth, wl, rows=8):
+    """In every 256-latent slice, `rows` identical dictionary rows along one
+    direction the tokens share (zero bias), so that every slice emits that
+    many candidates of exactly the same value far above the rest: with
+    m=131072 a token's candidates overflow the merge's pool with ties."""
+    s = wl.layers[0].saes[0]
+    d = wl.d
+    u = synth.bf16_bits_to_f32(synth.normal_bf16("bench/tied_pool/u", (d,), 1.0)).astype(np.float64)
+    u /= np.linalg.norm(u)
+    row = (10.0 / np.sqrt(d)) * u
+    W, b = s.W_enc.copy(), s.b_enc.copy()
+    tied = (np.arange(s.m) % 256) < rows
+    W[tied] = _to_bf16(row)[None, :]
+    b[tied] = 0
+    s.W_enc, s.b_enc = W, b
+    h = synth.bf16_bits_to_f32(wl.layers[0].h).astype(np.float64) + 3.0 * np.sqrt(d) * u[None, :]
+    wl.layers[0].h = _to_bf16(h)
+
+
+def _to_bf16(x):
+    u = np.asarray(x, np.float64).astype(np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)  # RNE
+
+
 def run_repair(torch, synth, HookStep, args):
     """The merge's repair path on inputs built to defeat the candidate
     thresholds, at the decode SAE shape (c3) and with the prefill GEMM
@@ -747,12 +771,16 @@ def run_repair(torch, synth, HookStep, args):
              ("prefill GEMM, 1100 tokens, 10 tied slices", {"T": 1100, "n_sub": 1100,
                                                             "m": 131072, "k": 32}, 10, 5),
              ("prefill GEMM, 1100 tokens, every slice tied", {"T": 1100, "n_sub": 1100,
-                                                              "m": 131072, "k": 32}, 512, 3)]
+                                                              "m": 131072, "k": 32}, 512, 3),
+             ("prefill GEMM, 1100 tokens, 4096 tied candidates per token",
+              {"T": 1100, "n_sub": 1100, "m": 131072, "k": 32, "n_outliers": 0}, "tied_pool", 3)]
     res = {}
     for name, kw, kind, n in cases:
         wl = synth.make("c3", ring_capacity=0, **kw)
         if kind == "strong":
             _strong_latents(synth, wl)
+        elif kind == "tied_pool":
+            _tied_candidates(synth, wl)
         elif kind is not None:
             _tied_slices(wl, kind)
         step = HookStep(wl)

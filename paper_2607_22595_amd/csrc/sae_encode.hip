@@ -1530,8 +1530,9 @@ __device__ __forceinline__ float slice_dot(const uint16_t* __restrict__ Wp,
 // at its rank.  When the candidates exceed the pool, the k-th best of the
 // first kPoolMax of them is a lower bound of the k-th best of all: the pool
 // is filled again with the candidates at or above it (a little below, so
-// that a repair finds what it needs), up to kFloorRounds times.  n: the
-// workgroup's slot of the app's token list.
+// that a repair finds what it needs; when exact ties leave that value floor
+// where it was, the k-th composite (value, latent) itself), up to
+// kFloorRounds times.  n: the workgroup's slot of the app's token list.
 __device__ __forceinline__ void merge_token(
     int n, const uint2* __restrict__ cand, const int32_t* __restrict__ tile_cnt,
     const float* __restrict__ tile_tau, int32_t n_mt, int32_t cap,
@@ -1583,13 +1584,14 @@ __device__ __forceinline__ void merge_token(
     const int cnt = *app_count;
     if (n >= cnt) return;  // uniform: no token, no ring row, no ticket
 
-    // Gather: the candidates with key >= floor, in slice order, into the pool
+    // Gather: the candidates whose composite (key, ~latent) is >= floor, in
+    // slice order, into the pool
     // (the first kPoolMax of them; the rest are counted only).  Returns their
     // number; tau_tiles receives the largest slice threshold, and each
     // wave's smallest and largest pool composite go to cmin_s / cmax_s (read
     // after the caller's barrier, with the first radix histogram cleared).
     uint32_t tau_tiles = 0;
-    auto gather = [&](uint32_t floor) __attribute__((always_inline)) {
+    auto gather = [&](uint64_t floor) __attribute__((always_inline)) {
         int total = 0;
         uint64_t cmn = ~0ull, cmx = 0ull;
         for (int t0 = 0; t0 < n_mt; t0 += kMergeThreads) {
@@ -1624,8 +1626,14 @@ __device__ __forceinline__ void merge_token(
 #pragma unroll
                     for (int u = 0; u < 4; ++u) {
                         const int q = q0 + 2 * u;
-                        kept += (q < c && f32_key(__uint_as_float(x[u].x)) >= floor) ? 1 : 0;
-                        kept += (q + 1 < c && f32_key(__uint_as_float(x[u].z)) >= floor) ? 1 : 0;
+                        const uint64_t ca =
+                            (static_cast<uint64_t>(f32_key(__uint_as_float(x[u].x))) << 32) |
+                            ~x[u].y;
+                        const uint64_t cb =
+                            (static_cast<uint64_t>(f32_key(__uint_as_float(x[u].z))) << 32) |
+                            ~x[u].w;
+                        kept += (q < c && ca >= floor) ? 1 : 0;
+                        kept += (q + 1 < c && cb >= floor) ? 1 : 0;
                     }
                 }
             }
@@ -1657,7 +1665,7 @@ __device__ __forceinline__ void merge_token(
                     const int q = q0 + 2 * u;
                     const uint32_t ka = f32_key(__uint_as_float(x[u].x));
                     const uint32_t kb = f32_key(__uint_as_float(x[u].z));
-                    if (q < c && ka >= floor) {
+                    if (q < c && ((static_cast<uint64_t>(ka) << 32) | ~x[u].y) >= floor) {
                         if (pos < kPoolMax) {
                             K[pos] = ka;
                             I[pos] = static_cast<int32_t>(x[u].y);
@@ -1667,7 +1675,7 @@ __device__ __forceinline__ void merge_token(
                         }
                         ++pos;
                     }
-                    if (q + 1 < c && kb >= floor) {
+                    if (q + 1 < c && ((static_cast<uint64_t>(kb) << 32) | ~x[u].w) >= floor) {
                         if (pos < kPoolMax) {
                             K[pos] = kb;
                             I[pos] = static_cast<int32_t>(x[u].w);
@@ -1769,11 +1777,11 @@ __device__ __forceinline__ void merge_token(
     // round).
     uint32_t wk = 0;
     int32_t wi = 0x7FFFFFFF;
-    uint32_t floor_key = 0;
+    uint64_t floor_c = 0;  // composite floor of the refills
     int total = 0;
     bool fits = false;
     for (int fr = 0;; ++fr) {
-        total = gather(floor_key);
+        total = gather(floor_c);
         __syncthreads();  // the pool is written
         const bool refill = total > kPoolMax && fr < kFloorRounds;  // uniform
         fits = total <= kPoolMax && total >= k;
@@ -1786,12 +1794,18 @@ __device__ __forceinline__ void merge_token(
             // last digit are zero); step a little below it, as the repair's
             // floor does
             const float fv = key_f32(static_cast<uint32_t>(prefix >> 32));
-            const uint32_t fl = f32_key(fv - fabsf(fv) * 0x1p-11f);
-            if (fl <= floor_key) {  // uniform: no progress (ties at the floor)
-                fits = false;
-                break;
+            uint64_t fl = static_cast<uint64_t>(f32_key(fv - fabsf(fv) * 0x1p-11f)) << 32;
+            if (fl <= floor_c) {
+                // no progress on the value (exact ties at the floor): the
+                // k-th composite of the first kPoolMax itself, with exactly k
+                // of them at or above it (the latent breaks the ties)
+                fl = prefix;
+                if (fl <= floor_c) {  // uniform: no progress at all
+                    fits = false;
+                    break;
+                }
             }
-            floor_key = fl;
+            floor_c = fl;
             __syncthreads();  // every read of the pool is done
             continue;
         }

@@ -879,6 +879,35 @@ def test_encode_with_strong_latents_per_token(px, T):
 
 
 @pytest.mark.parametrize("T", [64, 1100])
+def test_encode_pool_overflow_with_exact_ties(px, T):
+    """Every 256-latent slice holds 8 identical rows (one direction the
+    tokens share, one bias), so each slice emits 8 candidates of exactly the
+    same value far above the rest: 4096 tied candidates per token, twice the
+    merge's pool.  No refill floor on the value alone can cut them; the
+    floor on (value, latent) does, and the k lowest tied latents (slices 0-3)
+    win.  64 token slots run the decode kernel, 1100 the prefill GEMM."""
+    d, m, k = 256, 131072, 32
+    wl = synth.make("c3", d=d, m=m, k=k, T=T, n_sub=T, n_outliers=0)
+    sae = wl.layers[0].saes[0]
+    Wf = bf16_f64(sae.W_enc).reshape(m, d)
+    b = sae.b_enc.copy()
+    u = bf16_f64(synth.normal_bf16("test/overflow_ties/u", (d,), 1.0))
+    u /= np.linalg.norm(u)
+    tied = (np.arange(m) % 256) < 8
+    Wf[tied] = (10.0 / np.sqrt(d)) * u[None, :]
+    b[tied] = 0
+    sae.W_enc, sae.b_enc = to_bf16_bits(Wf), b
+    h = bf16_f64(wl.layers[0].h) + 3.0 * np.sqrt(d) * u[None, :]
+    hb = to_bf16_bits(h)
+    rt, idx, val = _encode(px, wl, sae, hb)
+    _check_encode(wl, sae, hb, idx, val, np.arange(T))
+    want = [256 * s + j for s in range(4) for j in range(8)]
+    for t in range(T):
+        assert sorted(idx[t].tolist()) == want
+        assert len(set(val[t].tolist())) == 1
+
+
+@pytest.mark.parametrize("T", [64, 1100])
 def test_encode_candidate_pool_overflow(px, T):
     """Every 256-latent slice holds a cluster of 7 latents about 4 stdev
     above its others for every token (rows along one direction the tokens
