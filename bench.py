@@ -750,6 +750,25 @@ def _tied_candidates(synth, wl, rows=8):
     wl.layers[0].h = _to_bf16(h)
 
 
+def _heavy_tailed(torch, synth, wl, alpha=1.5, cap=200.0):
+    """Dictionary rows scaled by Pareto(alpha) factors (capped): a token's
+    pre-activations over the latents become a scale mixture of normals with
+    a power-law tail, which the first threshold guess (a slice's mean and
+    stdev) misjudges: slices with a large factor overshoot the window and
+    refine, the others keep few candidates."""
+    s = wl.layers[0].saes[0]
+    u = synth.uniform01("bench/heavy/scale", s.m)
+    f = np.minimum((1.0 - u) ** (-1.0 / alpha), cap)
+    W = s.W_enc.reshape(s.m, -1).copy()
+    fs = torch.from_numpy(f.astype(np.float32))
+    for r0 in range(0, s.m, 8192):  # in row blocks, to bound host memory
+        blk = torch.from_numpy(W[r0:r0 + 8192].view(np.int16)).view(torch.bfloat16)
+        # bf16 x fp32 is exact in fp32's 24 bits; one RNE rounding to bf16
+        out = (blk.float() * fs[r0:r0 + 8192, None]).to(torch.bfloat16)
+        W[r0:r0 + 8192] = out.view(torch.int16).numpy().view(np.uint16)
+    s.W_enc = W.reshape(s.W_enc.shape)
+
+
 def _to_bf16(x):
     u = np.asarray(x, np.float64).astype(np.float32).view(np.uint32).astype(np.uint64)
     return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)  # RNE
@@ -766,12 +785,15 @@ def run_repair(torch, synth, HookStep, args):
              ("c3 10 tied slices", {}, 10, 10),
              ("c3 20 tied slices", {}, 20, 5),
              ("c3 every slice tied", {}, 256, 3),
+             ("c3 heavy-tailed rows (Pareto 1.5 scales)", {}, "heavy", 10),
              ("prefill GEMM, 1100 tokens, strong latents", {"T": 1100, "n_sub": 1100,
                                                             "m": 131072, "k": 32}, "strong", 5),
              ("prefill GEMM, 1100 tokens, 10 tied slices", {"T": 1100, "n_sub": 1100,
                                                             "m": 131072, "k": 32}, 10, 5),
              ("prefill GEMM, 1100 tokens, every slice tied", {"T": 1100, "n_sub": 1100,
                                                               "m": 131072, "k": 32}, 512, 3),
+             ("prefill GEMM, 1100 tokens, heavy-tailed rows (Pareto 1.5 scales)",
+              {"T": 1100, "n_sub": 1100, "m": 131072, "k": 32}, "heavy", 5),
              ("prefill GEMM, 1100 tokens, 4096 tied candidates per token",
               {"T": 1100, "n_sub": 1100, "m": 131072, "k": 32, "n_outliers": 0}, "tied_pool", 3)]
     res = {}
@@ -781,6 +803,8 @@ def run_repair(torch, synth, HookStep, args):
             _strong_latents(synth, wl)
         elif kind == "tied_pool":
             _tied_candidates(synth, wl)
+        elif kind == "heavy":
+            _heavy_tailed(torch, synth, wl)
         elif kind is not None:
             _tied_slices(wl, kind)
         step = HookStep(wl)

@@ -356,17 +356,18 @@ xmix_status xmix_sae_encode_topk_noalloc(const uint16_t *h, int32_t d, const xmi
  *   candidates: the GEMM; for every 256-latent slice of the dictionary and
  *               every subscribed token, a threshold tau is chosen from the
  *               slice's own values and every latent with pre >= tau is kept
- *               in the workspace together with tau;
+ *               in the workspace together with the slice's bound, a value
+ *               at most tau that every latent it does not keep lies below
+ *               (up to 1024 token slots the next value above the largest
+ *               one it does not keep);
  *   merge:      the exact top-k per token, written to idx_out / val_out.
  *               The top-k of the kept latents is the top-k of all m
- *               latents when its k-th value is >= every slice's tau (a
- *               latent left out lies below its slice's tau); otherwise the
- *               merge recomputes slices in descending order of that bound
- *               until no slice left can hide a winner (same result, slower;
- *               it happens only when the winners crowd into a few slices
- *               or tie across whole slices).  A slice with nothing at or
- *               above its tau keeps, as its tau, the next value above its
- *               largest pre-activation.
+ *               latents when its k-th value is >= every slice's bound (a
+ *               latent left out lies below its slice's bound); otherwise
+ *               the merge recomputes slices in descending order of that
+ *               bound until no slice left can hide a winner (same result,
+ *               slower; it happens only when the winners crowd into a few
+ *               slices or tie across whole slices).
  * The same certificate lets a dictionary be split across devices by latent
  * slices: exchange the kept candidates and thresholds, then merge. */
 xmix_status xmix_sae_encode_candidates(const uint16_t *h, int32_t d, const xmix_route *rt,

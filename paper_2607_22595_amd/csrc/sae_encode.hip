@@ -17,8 +17,11 @@
 // Epilogue, per token of the tile: a threshold tau is chosen so that the
 // number of latents with pre >= tau lies in a small window (first guess
 // mean + z * stdev of the tile's 256 values, then bisection on the value if
-// needed); every latent with pre >= tau is emitted as a candidate, and tau
-// and the count are recorded for the tile.  This costs O(1) work per value.
+// needed); every latent with pre >= tau is emitted as a candidate, and the
+// count and the tile's bound are recorded: a value that every latent left
+// out lies below (the decode kernels: the next value above the largest one
+// left out; the prefill GEMM: tau, or the next value above the tile's
+// maximum when nothing is emitted).  This costs O(1) work per value.
 // The decode kernel writes the tile to LDS token-major, and eight lanes of
 // one wave select for each token with no barrier or LDS atomic between the
 // waves.  The prefill kernel (one wave per SIMD, values in accumulator
@@ -29,18 +32,18 @@
 // Stage 2 (sae_merge_kernel): one workgroup per subscribed token gathers the
 // candidates of all tiles and selects the exact top-k of that pool (a radix
 // select over (value, latent) composites, ties to the lower latent).  The result is the exact top-k of
-// all m latents whenever the k-th selected value is >= every tile's tau,
-// because a latent that was not emitted lies below its tile's tau.  When
+// all m latents whenever the k-th selected value is >= every tile's bound,
+// because a latent that was not emitted lies below its tile's bound.  When
 // that certificate fails (only for inputs whose best latents crowd into a
 // few tiles or tie across whole tiles), the workgroup recomputes tiles'
 // 256 pre-activations with plain fp32 dot products, in descending order of
-// the bound each tile's tau sets on its left-out values, until no tile left
-// can hold a winner.  The
-// decode kernel's first threshold guess leaves a tile's strongest values
-// out of the statistics (above mean + 5 stdev), so that a few strong
-// latents, such as features clamped high by a steering app, do not lift it:
-// with a decode dictionary's ratio of k to m the certificate has little
-// slack.  The prefill kernel keeps the plain statistics (a GEMM epilogue
+// their bounds, until no tile left can hold a winner.  The
+// decode kernel's first threshold guess leaves a tile's outlying values
+// out of the statistics (beyond mean +- 5 stdev), so that a few strong
+// latents, such as features clamped high by a steering app, or rows of a
+// much larger norm than the others, do not lift it: with a decode
+// dictionary's ratio of k to m the certificate has little slack.  The
+// prefill kernel keeps the plain statistics (a GEMM epilogue
 // pays for every extra pass, and the repair covers the rare failure).
 //
 // The workgroup-to-tile map is XCD-aware: launch slots are dealt round-robin
@@ -70,9 +73,10 @@ constexpr int kEncWaves = 8;
 constexpr int kEncThreads = kEncWaves * kWave;
 constexpr int kRefineIters = 24;
 constexpr int kMaxCap = 64;  // most candidate pairs one slice may emit
-// Values above mean + kTrimZ * stdev of a tile's 256 pre-activations are left
-// out of the statistics behind the decode kernel's first threshold guess
-// (one strong latent would otherwise raise the guess for its whole tile).
+// Values beyond mean +- kTrimZ * stdev of a tile's 256 pre-activations are
+// left out of the statistics behind the decode kernel's first threshold
+// guess (one strong latent, or one of a large norm on either side, would
+// otherwise raise the guess for its whole tile).
 constexpr float kTrimZ = 5.0f;
 constexpr int kLatentFastTiles = 4;  // token tiles up to which the latent tile runs fastest
 constexpr int kBlkTok = 8;           // prefill block: token tiles
@@ -200,12 +204,12 @@ __device__ __forceinline__ int excl_scan8(int v, int q) {
 // threshold tau with lo_cnt <= count(pre >= tau) <= cap (first guess
 // mean + z * stdev of the 256 values, then bisection on the value), and
 // every latent with pre >= tau written to dst[t][0 .. count) as (fp32 bits,
-// latent), with the count and tau beside it.  vrow[t]: token t's LDS row;
-// q = lane & 7 takes latents [32q, 32q + 32); lat0: the slice's first
+// latent), with the count and the slice's bound beside it.  vrow[t]: token
+// t's LDS row; q = lane & 7 takes latents [32q, 32q + 32); lat0: the slice's first
 // latent.  Every lane of the wave calls it (the cross-lane steps are
 // wave-wide); the lanes of a token with valid[t] == false take part in them
-// and write nothing.  With TRIM, the values above mean + 5 stdev are left
-// out of the statistics behind the first guess (a few strong latents would
+// and write nothing.  With TRIM, the values beyond mean +- 5 stdev are left
+// out of the statistics behind the first guess (a few outlying latents would
 // otherwise lift it for the whole slice).
 template <bool TRIM, int NT>
 __device__ __forceinline__ void select_slices(const float* const (&vrow)[NT], int q,
@@ -226,45 +230,54 @@ __device__ __forceinline__ void select_slices(const float* const (&vrow)[NT], in
             x[t][4 * i + 3] = v.w;
         }
     }
-    float tau[NT], s1[NT], s2[NT], mx[NT], mu[NT], sd[NT];
+    float tau[NT], s1[NT], s2[NT], mx[NT], mn[NT], mu[NT], sd[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-        float a = 0.0f, b = 0.0f, c = -INFINITY;
+        float a = 0.0f, b = 0.0f, c = -INFINITY, e = INFINITY;
 #pragma unroll
         for (int i = 0; i < 32; ++i) {
             a += x[t][i];
             b = fmaf(x[t][i], x[t][i], b);
-            if (TRIM) c = fmaxf(c, x[t][i]);
+            if (TRIM) {
+                c = fmaxf(c, x[t][i]);
+                e = fminf(e, x[t][i]);
+            }
         }
         s1[t] = a;
         s2[t] = b;
         mx[t] = c;
+        mn[t] = e;
     }
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
         s1[t] = sum8(s1[t]);
         s2[t] = sum8(s2[t]);
-        if (TRIM) mx[t] = max8(mx[t]);
+        if (TRIM) {
+            mx[t] = max8(mx[t]);
+            mn[t] = -max8(-mn[t]);
+        }
         mu[t] = s1[t] * (1.0f / kBM);
         sd[t] = sqrtf(fmaxf(s2[t] * (1.0f / kBM) - mu[t] * mu[t], 0.0f));
         tau[t] = mu[t] + z * sd[t];
     }
     if (TRIM) {
+        // values more than kTrimZ stdev from the mean on either side: a large
+        // value lifts the mean and the spread, a large negative one the spread
         bool trim[NT], any = false;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            trim[t] = valid[t] && mx[t] > mu[t] + kTrimZ * sd[t];
+            trim[t] = valid[t] && (mx[t] > mu[t] + kTrimZ * sd[t] || mn[t] < mu[t] - kTrimZ * sd[t]);
             any = any || trim[t];
         }
         if (wave_ballot(any)) {  // uniform
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
-                const float cut = mu[t] + kTrimZ * sd[t];
+                const float cut = mu[t] + kTrimZ * sd[t], cut_lo = mu[t] - kTrimZ * sd[t];
                 float e1 = 0.0f, e2 = 0.0f;
                 int ne = 0;
 #pragma unroll
                 for (int i = 0; i < 32; ++i) {
-                    const bool o = x[t][i] > cut;
+                    const bool o = x[t][i] > cut || x[t][i] < cut_lo;
                     ne += o ? 1 : 0;
                     e1 += o ? x[t][i] : 0.0f;
                     e2 = fmaf(o ? x[t][i] : 0.0f, x[t][i], e2);
@@ -331,12 +344,19 @@ __device__ __forceinline__ void select_slices(const float* const (&vrow)[NT], in
     if (!settled) masks();
     // emission: this lane's selected latents go to the slots after those of
     // the lanes before it in the token's group of 8
+    // nk[t]: the largest of the token's values that are not kept (NaN never
+    // counts: it compares below everything)
     int base[NT], total[NT];
+    float nk[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
         const int cl = __popc(m[t]);
         base[t] = excl_scan8(cl, q);
         total[t] = isum8(cl);
+        float l = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 32; ++i) l = fmaxf(l, x[t][i] >= tau[t] ? -INFINITY : x[t][i]);
+        nk[t] = max8(l);
     }
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
@@ -353,9 +373,10 @@ __device__ __forceinline__ void select_slices(const float* const (&vrow)[NT], in
         }
         if (q == 0) {
             *cnt_out[t] = min(total[t], cap);
-            // nothing at or above tau: the next value above the slice's
-            // maximum bounds its values as well, and tighter
-            *tau_out[t] = TRIM && mx[t] < tau[t] ? key_f32(f32_key(mx[t]) + 1u) : tau[t];
+            // the slice's bound: the next value above the largest one it
+            // does not keep (at most tau, and the tightest bound there is;
+            // with nothing kept, the next value above its maximum)
+            *tau_out[t] = key_f32(f32_key(nk[t]) + 1u);
         }
     }
 }
@@ -1260,8 +1281,8 @@ sae_gemm_kernel(const uint16_t* __restrict__ xs_g, int32_t d, int32_t n_pad,
                 ++slot;
             }
         }
-        // nothing at or above tau: the next value above the slice's maximum
-        // bounds its values as well, and tighter
+        // the slice's bound: tau, or with nothing at or above it the next
+        // value above the slice's maximum (the tighter of the two)
         if (n < ntok && wm == 0 && g == 0)
             tile_tau[row] = mxv[nb] < tau[nb] ? key_f32(f32_key(mxv[nb]) + 1u) : tau[nb];
         // the wave's reads of this buffer precede these stores in its LDS queue
@@ -1587,7 +1608,7 @@ __device__ __forceinline__ void merge_token(
     // Gather: the candidates whose composite (key, ~latent) is >= floor, in
     // slice order, into the pool
     // (the first kPoolMax of them; the rest are counted only).  Returns their
-    // number; tau_tiles receives the largest slice threshold, and each
+    // number; tau_tiles receives the largest slice bound, and each
     // wave's smallest and largest pool composite go to cmin_s / cmax_s (read
     // after the caller's barrier, with the first radix histogram cleared).
     uint32_t tau_tiles = 0;
