@@ -343,9 +343,9 @@ __device__ __forceinline__ void select_slices(const float* const (&vrow)[NT], in
     // out of rounds: the final thresholds were set after the last masks
     if (!settled) masks();
     // emission: this lane's selected latents go to the slots after those of
-    // the lanes before it in the token's group of 8
-    // nk[t]: the largest of the token's values that are not kept (NaN never
-    // counts: it compares below everything)
+    // the lanes before it in the token's group of 8; nk[t]: the largest of
+    // the token's values that are not kept (NaN never counts: it compares
+    // below everything)
     int base[NT], total[NT];
     float nk[NT];
 #pragma unroll
