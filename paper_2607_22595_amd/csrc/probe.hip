@@ -82,8 +82,18 @@ probe_token_kernel(const void* __restrict__ h, int32_t d, int32_t T_max,
 #pragma unroll
     for (int p = 0; p < MAXP; ++p) part[p] = 0.0f;
 
+    // weights fetched together with the row (the rest, for more than eight
+    // probes, when used)
+    constexpr int AP = MAXP < 8 ? MAXP : 8;
     for (int32_t i = threadIdx.x; i < nvec; i += kProbeThreads) {
+        // the row and the weights of the token's probes, all loaded before the
+        // first use, so that the slice waits for one memory round trip
         const uint4 hv = row[i];
+        uint4 wv[AP];
+#pragma unroll
+        for (int p = 0; p < AP; ++p)
+            wv[p] = ((sel >> p) & 1u) ? W[static_cast<int64_t>(p) * nvec + i]
+                                      : make_uint4(0u, 0u, 0u, 0u);
         const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w};
         float x[EPV];
 #pragma unroll
@@ -98,8 +108,8 @@ probe_token_kernel(const void* __restrict__ h, int32_t d, int32_t T_max,
 #pragma unroll
         for (int p = 0; p < MAXP; ++p) {
             if (!((sel >> p) & 1u)) continue;
-            const uint4 wv = W[static_cast<int64_t>(p) * nvec + i];
-            const uint32_t ww[4] = {wv.x, wv.y, wv.z, wv.w};
+            const uint4 w4 = p < AP ? wv[p < AP ? p : 0] : W[static_cast<int64_t>(p) * nvec + i];
+            const uint32_t ww[4] = {w4.x, w4.y, w4.z, w4.w};
             float acc = part[p];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {

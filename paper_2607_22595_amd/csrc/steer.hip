@@ -34,7 +34,12 @@ steer_kernel(void* __restrict__ h, int32_t d, const uint32_t* __restrict__ tok_m
     uint4* row = reinterpret_cast<uint4*>(h) + static_cast<int64_t>(t) * nvec;
     const uint4* V = reinterpret_cast<const uint4*>(vecs);
     for (int32_t i = threadIdx.x; i < nvec; i += kSteerThreads) {
+        // the row and the first four vectors with their alphas, loaded
+        // together (one memory round trip before the first add)
         const uint4 hv = row[i];
+        uint32_t rest = sel;
+        SteerGroup g0;
+        steer_fetch(g0, rest, a_row, V, nvec, i);
         const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w};
         double acc[EPV];
 #pragma unroll
@@ -46,7 +51,8 @@ steer_kernel(void* __restrict__ h, int32_t d, const uint32_t* __restrict__ tok_m
                 acc[e] = __uint_as_float(hw[e]);
             }
         }
-        steer_accumulate<BF16>(acc, sel, a_row, V, nvec, i);
+        steer_add_group<BF16>(acc, g0);
+        if (rest) steer_accumulate<BF16>(acc, rest, a_row, V, nvec, i);
         uint4 out;
         if constexpr (BF16) {
             out.x = pack_bf16_from_f64(acc[0], acc[1]);

@@ -85,8 +85,23 @@ steer_probe_kernel(void* __restrict__ h, int32_t d, int32_t T_max,
 #pragma unroll
     for (int p = 0; p < MAXP; ++p) part[p] = 0.0f;
 
+    // probe weights fetched together with the row (the rest, for more than
+    // eight probes, when used)
+    constexpr int AP = MAXP < 8 ? MAXP : 8;
     for (int32_t i = threadIdx.x; i < nvec; i += kFuseThreads) {
+        // Every load of the slice before its first use: the row, the weights
+        // of the token's probes and its first four steering vectors with
+        // their alphas, so that the slice waits for one memory round trip,
+        // not one per operand.
         const uint4 hv = row[i];
+        uint4 wv[AP];
+#pragma unroll
+        for (int p = 0; p < AP; ++p)
+            wv[p] = ((sp >> p) & 1u) ? W[static_cast<int64_t>(p) * nvec + i]
+                                     : make_uint4(0u, 0u, 0u, 0u);
+        uint32_t rest = ss;
+        SteerGroup g0;
+        steer_fetch(g0, rest, a_row, V, nvec, i);
         const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w};
         // probes, on the row as read
         float x[EPV];
@@ -102,8 +117,8 @@ steer_probe_kernel(void* __restrict__ h, int32_t d, int32_t T_max,
 #pragma unroll
         for (int p = 0; p < MAXP; ++p) {
             if (!((sp >> p) & 1u)) continue;
-            const uint4 wv = W[static_cast<int64_t>(p) * nvec + i];
-            const uint32_t ww[4] = {wv.x, wv.y, wv.z, wv.w};
+            const uint4 w4 = p < AP ? wv[p < AP ? p : 0] : W[static_cast<int64_t>(p) * nvec + i];
+            const uint32_t ww[4] = {w4.x, w4.y, w4.z, w4.w};
             float acc = part[p];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -116,12 +131,14 @@ steer_probe_kernel(void* __restrict__ h, int32_t d, int32_t T_max,
             }
             part[p] = acc;
         }
-        // steering, written back
+        // steering, written back: the first four vectors as fetched, then
+        // the rest (more than four steering apps) four at a time
         if (ss) {
             double acc[EPV];
 #pragma unroll
             for (int e = 0; e < EPV; ++e) acc[e] = x[e];
-            steer_accumulate<BF16>(acc, ss, a_row, V, nvec, i);
+            steer_add_group<BF16>(acc, g0);
+            if (rest) steer_accumulate<BF16>(acc, rest, a_row, V, nvec, i);
             uint4 out;
             if constexpr (BF16) {
                 out.x = pack_bf16_from_f64(acc[0], acc[1]);
