@@ -230,43 +230,41 @@ __device__ __forceinline__ void select_slices(const float* const (&vrow)[NT], in
             x[t][4 * i + 3] = v.w;
         }
     }
-    float tau[NT], s1[NT], s2[NT], mx[NT], mn[NT], mu[NT], sd[NT];
+    // ax[t]: the largest magnitude among the token's values
+    float tau[NT], s1[NT], s2[NT], ax[NT], mu[NT], sd[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-        float a = 0.0f, b = 0.0f, c = -INFINITY, e = INFINITY;
+        float a = 0.0f, b = 0.0f, c = 0.0f;
 #pragma unroll
         for (int i = 0; i < 32; ++i) {
             a += x[t][i];
             b = fmaf(x[t][i], x[t][i], b);
-            if (TRIM) {
-                c = fmaxf(c, x[t][i]);
-                e = fminf(e, x[t][i]);
-            }
+            if (TRIM) c = fmaxf(c, fabsf(x[t][i]));
         }
         s1[t] = a;
         s2[t] = b;
-        mx[t] = c;
-        mn[t] = e;
+        ax[t] = c;
     }
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
         s1[t] = sum8(s1[t]);
         s2[t] = sum8(s2[t]);
-        if (TRIM) {
-            mx[t] = max8(mx[t]);
-            mn[t] = -max8(-mn[t]);
-        }
+        if (TRIM) ax[t] = max8(ax[t]);
         mu[t] = s1[t] * (1.0f / kBM);
         sd[t] = sqrtf(fmaxf(s2[t] * (1.0f / kBM) - mu[t] * mu[t], 0.0f));
         tau[t] = mu[t] + z * sd[t];
     }
     if (TRIM) {
         // values more than kTrimZ stdev from the mean on either side: a large
-        // value lifts the mean and the spread, a large negative one the spread
+        // value lifts the mean and the spread, a large negative one the
+        // spread.  A value that far out has a magnitude above
+        // kTrimZ * stdev - |mean|; the pass below leaves out exactly the
+        // values beyond the two cuts, so a token it finds none for keeps its
+        // guess.
         bool trim[NT], any = false;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            trim[t] = valid[t] && (mx[t] > mu[t] + kTrimZ * sd[t] || mn[t] < mu[t] - kTrimZ * sd[t]);
+            trim[t] = valid[t] && ax[t] + fabsf(mu[t]) > kTrimZ * sd[t];
             any = any || trim[t];
         }
         if (wave_ballot(any)) {  // uniform
