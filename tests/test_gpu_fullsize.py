@@ -68,8 +68,9 @@ def test_decode_8b_shape_four_layers(HookStep):
         _probe_outputs(step, wl, L, lay, tm)
 
 
-def test_decode_sae_with_ring(HookStep):
-    wl = synth.make("c3")
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_decode_sae_with_ring(HookStep, seed):
+    wl = synth.make("c3", seed=seed)
     step = HookStep(wl)
     L, lay = wl.layers[0], step.layers[0]
     s, sd = L.saes[0], lay.saes[0]
@@ -95,8 +96,9 @@ def test_decode_sae_with_ring(HookStep):
         check_topk(idx[t], val[t], idx_ref[q], pre[q], s.k)
 
 
-def test_prefill_sae_and_probes(HookStep):
-    wl = synth.make("c4")
+@pytest.mark.parametrize("seed", [0, 1])
+def test_prefill_sae_and_probes(HookStep, seed):
+    wl = synth.make("c4", seed=seed)
     step = HookStep(wl)
     step.run()
     torch.cuda.synchronize()
